@@ -1,0 +1,290 @@
+#!/usr/bin/env python3
+"""Benchmark of one simulation step of the invocation-distance memory manager
+on one MI355X: plan (distances + activation mask -> victims, loads, block
+table), evict (pack + device-to-host copy) and prefetch (host-to-device copy
++ unpack), on the 1,000-agent round-robin workload by default.
+
+Prints one JSON line.  ``value`` is evict+prefetch bytes moved per second of
+wall time over the timed steps (inputs -- the per-step distances and masks --
+already resident in HBM; the host link is part of the measured work).
+``roofline`` is the dominant copy kernel against HBM peak, ``dma`` the copies
+against the measured host-link bandwidth, ``plan_latency_us`` the plan call,
+and ``cpu_baseline`` the CPU oracle on a bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0         # MI355X HBM3E, published
+WORKLOAD_TEXT = {
+    "tiny": "64 agents, 2x2x64 fp16 KV in 16 KiB pages, pool of 16 agents, 10% active/step",
+    "roundrobin": "1,000 agents, 32x8x128 bf16 KV (128 KiB/token) in 2 MiB pages of 64 x 32 KiB, "
+                  "prefix 512-2048 tokens, 40 GB pool, ~5% active/step round-robin, exact distances",
+    "bursty": "10,000 agents, 2 MiB KV pages, lognormal prefixes, 120 GB pool, clustered bursts of "
+              "1-3% per step, noisy distances",
+    "zipf_lora": "2,000 agents, rank-16 LoRA (80 MiB, 448 planes, 256 slots) + 512-token KV "
+                 "(30 GB pool), Zipf(1.1) activation 4%/step",
+    "diffusion": "50,000 agents, unified 160 GB pool of 512 KiB units (KV pages + LoRA), "
+                 "activation by messages on a degree-8 graph, noisy distances",
+}
+
+
+def kernel_source_hash():
+    p = os.path.join(ROOT, "paper_2601_21473_amd", "csrc", "ss_kernels.hip")
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="roundrobin", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--threshold", type=int, default=0xFFFFFFFF)
+    ap.add_argument("--budget", type=int, default=None)
+    ap.add_argument("--staging-mib", type=int, default=4096)
+    ap.add_argument("--ring", type=int, default=8)
+    ap.add_argument("--host-copies", type=int, default=128,
+                    help="distinct host copies shared round-robin by agents; 0 = one per agent")
+    ap.add_argument("--plan-steps", type=int, default=20)
+    ap.add_argument("--cpu-steps", type=int, default=2)
+    ap.add_argument("--cpu-agents", type=int, default=8)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-probe", action="store_true")
+    return ap.parse_args()
+
+
+def probes(torch, binding):
+    dev = torch.device("cuda", 0)
+    out = {}
+    n = 2 << 30
+    a = torch.empty(n, dtype=torch.uint8, device=dev)
+    b = torch.empty(n, dtype=torch.uint8, device=dev)
+    ms = binding.probe_copy(b.data_ptr(), a.data_ptr(), n, iters=10)
+    out["hbm_copy_GBps"] = 2 * n / ms / 1e6
+    del a, b
+    m = 1 << 30
+    h = torch.empty(2 * m, dtype=torch.uint8, pin_memory=True)
+    d = torch.empty(2 * m, dtype=torch.uint8, device=dev)
+    out["h2d_GBps"] = m / binding.probe_link(h.data_ptr(), d.data_ptr(), m, 0, 5) / 1e6
+    out["d2h_GBps"] = m / binding.probe_link(h.data_ptr(), d.data_ptr(), m, 1, 5) / 1e6
+    out["duplex_GBps"] = 2 * m / binding.probe_link(h.data_ptr(), d.data_ptr(), m, 2, 5) / 1e6
+    del h, d
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
+    """The CPU oracle on a bounded sample: the oracle plan for every agent on
+    steps [warmup, warmup + n_steps) (after replaying the earlier steps'
+    plans), and the oracle's numpy gather/scatter of the bytes of the first
+    ``n_agents_moved`` victims and loads of each sampled step through warm
+    buffers."""
+    from types import SimpleNamespace
+    from oracle import OraclePool, BytePool, apply_step_bytes
+    spec = trace.pools[0]
+    ub = spec.unit_bytes
+    opool = OraclePool(spec.capacity_units, spec.agent_units, ub)
+    for t in range(warmup):
+        opool.plan_step(trace.dist[t], trace.active[t], threshold, budget)
+    bp = BytePool(spec.capacity_units, spec.chunk_bytes)
+    s = spec.agent_units.astype(np.int64)
+    max_agent = int(s.max()) * ub
+    stage_out = np.ones(n_agents_moved * max_agent, dtype=np.uint8)
+    stage_in = np.ones(n_agents_moved * max_agent, dtype=np.uint8)
+    host = [np.ones(max_agent, dtype=np.uint8) for _ in range(2 * n_agents_moved)]
+    t_plan = t_move = 0.0
+    moved = 0
+    for t in range(warmup, warmup + n_steps):
+        t0 = time.perf_counter()
+        plan = opool.plan_step(trace.dist[t], trace.active[t], threshold, budget)
+        t_plan += time.perf_counter() - t0
+        V = plan.victims[:n_agents_moved]
+        Ld = plan.loads[:n_agents_moved]
+        nvu = int(s[V].sum())
+        nlu = int(s[Ld].sum())
+        sub = SimpleNamespace(victims=V, loads=Ld, victim_units=plan.victim_units[:nvu],
+                              load_units=plan.load_units[:nlu])
+        slot = {int(a): i for i, a in enumerate(list(V) + list(Ld))}
+        for u in np.concatenate([sub.victim_units, sub.load_units]):   # warm the pages
+            for c, plane in enumerate(bp.planes):
+                plane[u] = 1
+        t0 = time.perf_counter()
+        apply_step_bytes(bp, sub, s, lambda a: host[slot[a]][:s[a] * ub],
+                         lambda a, b: host[slot[a]][:len(b)].__setitem__(slice(None), b),
+                         staging_out=stage_out, staging_in=stage_in)
+        t_move += time.perf_counter() - t0
+        moved += (nvu + nlu) * ub
+    return {"value": moved / (t_plan + t_move) / 1e9, "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"steps {warmup}-{warmup + n_steps - 1} of the {trace.name} trace: oracle plan "
+                      f"of all {trace.n_agents} agents per step ({1e3 * t_plan / n_steps:.2f} ms/step) "
+                      f"+ numpy gather/scatter of the first {n_agents_moved} victims' and loads' "
+                      f"bytes ({moved / 1e9:.2f} GB in {t_move:.2f} s), single thread",
+            "host_threads_available": len(os.sched_getaffinity(0))}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import workloads as W
+    from paper_2601_21473_amd import binding
+    from paper_2601_21473_amd.memory import PoolMemory
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    binding.load()
+    trace = W.make_trace(args.workload, args.seed)
+    T_need = args.warmup + args.steps + args.plan_steps
+    if T_need > trace.n_steps:
+        sys.exit(f"warmup + steps + plan-steps = {T_need} exceeds the trace's {trace.n_steps} steps")
+    budget = args.budget
+    thr = args.threshold
+
+    probe = {} if args.no_probe else probes(torch, binding)
+
+    mems, pools = [], []
+    for spec in trace.pools:
+        host_slots = None if args.host_copies == 0 else args.host_copies
+        mem = PoolMemory(spec, args.staging_mib << 20, args.ring, host_slots=host_slots)
+        mems.append(mem)
+        pools.append(mem.make_pool(timing=True))
+    dev = torch.device("cuda", 0)
+    dist = torch.from_numpy(np.ascontiguousarray(trace.dist).view(np.int32)).to(dev)
+    act = torch.from_numpy(np.ascontiguousarray(trace.active)).to(dev)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def step(t):
+        plans = [p.plan_step(dist[t].data_ptr(), act[t].data_ptr(), thr, budget, stream)
+                 for p in pools]
+        for p in pools:
+            p.evict_pack(stream)
+        for p in pools:
+            p.prefetch_unpack(stream)
+        return plans
+
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+    for p in pools:
+        p.reset_stats()
+    moved = out_b = in_b = 0
+    step_wall = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        ts = time.perf_counter()
+        plans = step(args.warmup + k)
+        step_wall.append(time.perf_counter() - ts)
+        for pl in plans:
+            out_b += pl["bytes_out"]
+            in_b += pl["bytes_in"]
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    moved = out_b + in_b
+    stats = [p.stats() for p in pools]
+
+    # plan latency: each plan issued with the device idle
+    lat = []
+    for k in range(args.plan_steps):
+        torch.cuda.synchronize()
+        ts = time.perf_counter()
+        for p in pools:
+            p.plan_step(dist[args.warmup + args.steps + k].data_ptr(),
+                        act[args.warmup + args.steps + k].data_ptr(), thr, budget, stream)
+        lat.append(time.perf_counter() - ts)
+        for p in pools:
+            p.evict_pack(stream)
+        for p in pools:
+            p.prefetch_unpack(stream)
+    torch.cuda.synchronize()
+    plan_stats = [p.stats() for p in pools]
+    for p in pools:
+        p.close()
+
+    pack_ms = sum(s["pack_ms"] for s in stats)
+    unpack_ms = sum(s["unpack_ms"] for s in stats)
+    pack_b = sum(s["pack_bytes"] for s in stats)
+    unpack_b = sum(s["unpack_bytes"] for s in stats)
+    pack_n = sum(s["pack_launches"] for s in stats)
+    unpack_n = sum(s["unpack_launches"] for s in stats)
+    kern = {
+        "pack": {"launches": pack_n, "bytes_per_launch": 2 * pack_b / max(pack_n, 1),
+                 "avg_us": 1e3 * pack_ms / max(pack_n, 1),
+                 "GBps": 2 * pack_b / max(pack_ms, 1e-9) / 1e6},
+        "unpack": {"launches": unpack_n, "bytes_per_launch": 2 * unpack_b / max(unpack_n, 1),
+                   "avg_us": 1e3 * unpack_ms / max(unpack_n, 1),
+                   "GBps": 2 * unpack_b / max(unpack_ms, 1e-9) / 1e6},
+    }
+    dom = "pack" if pack_ms >= unpack_ms else "unpack"
+    traffic = None
+    pmc_path = os.path.join(ROOT, "profiles", f"{dom}_{args.workload}_pmc.json")
+    if os.path.exists(pmc_path):
+        pmc = json.load(open(pmc_path))
+        if pmc.get("kernel_source_sha256_16") == kernel_source_hash():
+            traffic = pmc.get("hbm_bytes_per_launch")
+    roofline = {"bound": "hbm", "kernel": f"k_copy<{dom}>", "achieved": kern[dom]["GBps"],
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": kern[dom]["GBps"] / HBM_PEAK_GBPS,
+                "traffic": traffic,
+                "algorithmic_bytes_per_launch": kern[dom]["bytes_per_launch"]}
+    d2h_b = sum(s["d2h_bytes"] for s in stats)
+    h2d_b = sum(s["h2d_bytes"] for s in stats)
+    d2h_ms = sum(s["d2h_ms"] for s in stats)
+    h2d_ms = sum(s["h2d_ms"] for s in stats)
+    dma = {"bytes_d2h": d2h_b, "bytes_h2d": h2d_b,
+           "d2h_GBps": d2h_b / max(d2h_ms, 1e-9) / 1e6, "h2d_GBps": h2d_b / max(h2d_ms, 1e-9) / 1e6,
+           "wall_GBps": moved / wall / 1e9}
+    if probe:
+        duplex = probe["duplex_GBps"] > 1.2 * max(probe["h2d_GBps"], probe["d2h_GBps"])
+        ideal = (max(out_b / probe["d2h_GBps"], in_b / probe["h2d_GBps"]) if duplex
+                 else out_b / probe["d2h_GBps"] + in_b / probe["h2d_GBps"]) / 1e9
+        dma["ideal_s"] = ideal
+        dma["frac_of_measured_link"] = ideal / wall
+        dma["duplex_overlap_measured"] = duplex
+    lat_us = np.array(lat) * 1e6
+    plan_gpu_ms = sum(s["plan_gpu_ms"] for s in plan_stats) - sum(s["plan_gpu_ms"] for s in stats)
+    plan = {"median": float(np.median(lat_us)), "p99": float(np.percentile(lat_us, 99)),
+            "gpu_kernels_us": 1e3 * plan_gpu_ms / max(args.plan_steps, 1)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(trace, args.warmup, args.cpu_steps, args.cpu_agents, thr, budget)
+
+    rec = {
+        "metric": "evict+prefetch GB/s per step (HBM and host-link % of peak); plan latency us/step",
+        "value": moved / wall / 1e9, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": 1e3 * wall / args.steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u8", "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {WORKLOAD_TEXT[args.workload]}",
+                   "seed": args.seed, "threshold": thr, "budget_units": budget,
+                   "staging_bytes": args.staging_mib << 20, "ring_slots": args.ring,
+                   "host_copies": ("one per agent" if args.host_copies == 0 else
+                                   f"{args.host_copies} shared round-robin"),
+                   "bytes_out": out_b, "bytes_in": in_b},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "dma": dma,
+        "plan_latency_us": plan,
+        "kernels": kern,
+        "probe": probe,
+        "step_wall_ms": {"median": 1e3 * float(np.median(step_wall)),
+                         "max": 1e3 * float(np.max(step_wall))},
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

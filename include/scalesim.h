@@ -1,0 +1,209 @@
+/*
+ * scalesim.h -- C ABI of the per-step hot path of an invocation-distance
+ * memory manager for agent-specific GPU memory (prefix KV pages, LoRA
+ * adapter slots) on one AMD Instinct MI355X (gfx950).
+ *
+ * The operations follow the paper's memory-module interface (ScaleSim,
+ * Appendix A, Table "agent-mem-interface"):
+ *   HandleReq(req, agentID)            -> the per-step activation mask;
+ *   Evict(size, agentDistances)        -> the demand half of ss_plan_step;
+ *   DispatchLoadTasks(agentDistances, threshold, budget)
+ *                                      -> the prefetch half of ss_plan_step;
+ *   Load(memObj, agentIDs, ...)        -> ss_prefetch_unpack;
+ * with eviction writing memory back to its host copy (Section 3.3,
+ * "Future reuse-aware eviction") -> ss_evict_pack.  One ss_pool is one
+ * registered memory module (Appendix A); several modules are several pools
+ * planned with the same distances and mask.
+ *
+ * Data model.  A pool has `capacity_units` physical units.  A unit is made of
+ * `n_planes` planes: the chunk of plane c of unit u lives at
+ *     plane_base[c] + u * chunk_bytes[c]          (device memory).
+ * Agent a owns agent_units[a] >= 1 units, logical units j = 0..s[a]-1, and
+ * a host copy of them at host_backing + host_off[a]: unit j, then plane c,
+ * each chunk contiguous (s[a] * unit_bytes bytes in all).
+ *
+ * Decision rules (each the reading of a passage; the CPU oracle applies the
+ * same ones):
+ *   d[a]   = 0 if a is active (Section 3.3, prefetch example), else the
+ *            caller's distance estimate (Section 3.2; only order matters);
+ *   key[a] = (d[a], a) compared lexicographically: ties go to the agent id;
+ *   demand = active agents not resident, loaded in id order; when the free
+ *            units cannot hold them, inactive residents are evicted largest
+ *            key first, shortest prefix that frees enough (Section 3.3);
+ *   prefetch = offloaded, inactive agents with distance < threshold, in
+ *            increasing key; each is taken if it fits into free units or into
+ *            units of further inactive residents with strictly larger
+ *            distance, and the total stays within the budget; the first one
+ *            that cannot be taken ends the prefetch (Section 3.3,
+ *            "Distance-guided proactive prefetch"; Appendix A,
+ *            DispatchLoadTasks);
+ *   units  = loads receive the units free before the step in ascending index,
+ *            then the units released by this step's victims in eviction
+ *            order, in load order and logical-unit order.
+ *
+ * Threading and streams.  A pool is used by one host thread at a time.  The
+ * library owns its internal HIP streams (all at the default priority).  Work
+ * of a call starts after the work the caller has queued on `stream` before
+ * the call; ss_prefetch_unpack makes `stream` wait for the whole step (both
+ * directions of the copy) before the caller's later work on it.
+ *
+ * Errors.  No C++ exception crosses this boundary.  Every call returns an
+ * ss_status; ss_last_error() gives a message for the calling thread.
+ * SS_ERR_ARG and SS_ERR_OVERCOMMIT leave the pool unchanged.  A HIP failure
+ * while moving data poisons the pool: every later call returns
+ * SS_ERR_POISONED (moves that were partly applied cannot be undone).
+ */
+#ifndef SCALESIM_H
+#define SCALESIM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ss_pool ss_pool;     /* opaque; ss_pool_create / ss_pool_destroy */
+typedef int32_t ss_status;
+
+#define SS_OK               0
+#define SS_ERR_ARG         (-1)     /* invalid argument; nothing changed            */
+#define SS_ERR_OVERCOMMIT  (-2)     /* active agents need more units than the pool  */
+#define SS_ERR_ORDER       (-3)     /* calls out of plan -> evict -> prefetch order */
+#define SS_ERR_HIP         (-4)     /* a HIP runtime call failed                     */
+#define SS_ERR_NOMEM       (-5)     /* the library could not allocate its metadata   */
+#define SS_ERR_POISONED    (-6)     /* an earlier HIP failure left the pool unusable */
+
+#define SS_NO_BUDGET       UINT64_MAX
+#define SS_NO_DISTANCE     0xFFFFFFFFu  /* "never activated again"; never < threshold */
+
+#define SS_FLAG_TIMING     1u       /* record HIP events around every copy launch   */
+
+typedef struct {
+    uint32_t        n_agents;       /* N >= 1, N < 2^31                                    */
+    uint64_t        capacity_units; /* U >= 1, U < 2^31                                    */
+    uint32_t        n_planes;       /* P >= 1                                              */
+    void* const*    plane_base;     /* [P] device pointers, plane c = U chunks (caller-owned) */
+    const uint64_t* chunk_bytes;    /* [P] bytes per chunk, multiples of 16, >= 16         */
+    const uint32_t* agent_units;    /* [N] units per agent, each >= 1 (copied)             */
+    void*           host_backing;   /* pinned host memory from hipHostMalloc (caller-owned) */
+    const uint64_t* host_off;       /* [N] byte offset of each agent's host copy (copied);
+                                       NULL = packed, agent after agent. Offsets may alias
+                                       (agents then share one host copy, as when one
+                                       physical adapter serves many logical ones).       */
+    uint64_t        host_bytes;     /* size of host_backing; every copy must fit           */
+    void*           dev_staging;    /* device buffer (caller-owned): first half stages
+                                       evictions, second half stages loads               */
+    uint64_t        staging_bytes;  /* each half is cut into ring_slots slots of whole units */
+    uint32_t        ring_slots;     /* >= 1 slots per direction                            */
+    int32_t         device;         /* HIP device ordinal                                  */
+    uint32_t        flags;          /* SS_FLAG_*                                           */
+} ss_pool_desc;
+
+typedef struct {
+    uint32_t threshold;             /* prefetch agents with distance < threshold (0 = off) */
+    uint64_t budget_units;          /* max prefetched units per step; SS_NO_BUDGET = none  */
+} ss_plan_params;
+
+typedef struct {
+    uint32_t        n_victims;      /* agents evicted this step                         */
+    uint32_t        n_loads;        /* agents loaded this step                          */
+    uint32_t        n_demand;       /* leading loads that are demand loads              */
+    uint32_t        n_demand_victims; /* leading victims evicted for demand             */
+    const uint32_t* victims;        /* [n_victims] host, eviction order; pool-owned,
+                                       valid until the next ss_plan_step               */
+    const uint32_t* loads;          /* [n_loads] host: demand loads by id, then prefetches */
+    uint64_t        units_out, units_in;
+    uint64_t        bytes_out, bytes_in;
+} ss_plan;
+
+typedef struct {                    /* cumulative since create or ss_reset_stats          */
+    uint64_t steps;
+    uint64_t pack_launches, unpack_launches;
+    uint64_t pack_bytes, unpack_bytes;     /* bytes moved (each read once, written once) */
+    double   pack_ms, unpack_ms;           /* sum of per-launch event durations         */
+    uint64_t d2h_bytes, h2d_bytes;
+    double   d2h_ms, h2d_ms;               /* per step: first to last copy on its stream */
+    double   plan_gpu_ms;                  /* event time of the plan kernels             */
+} ss_stats;
+
+/* Create a pool (Appendix A: register a memory module).  Validates every
+ * descriptor field, copies the host arrays, allocates the library's device
+ * metadata (block table, state, plan buffers; O(N + U + sum(s)) bytes) and its
+ * streams.  The pool starts empty.  Returns SS_ERR_ARG (message in
+ * ss_last_error) for an invalid descriptor, SS_ERR_HIP / SS_ERR_NOMEM on
+ * runtime failures; *out is set only on SS_OK. */
+ss_status ss_pool_create(const ss_pool_desc* desc, ss_pool** out);
+
+/* Wait for the pool's queued work and free what the library allocated.
+ * Caller-owned buffers are not touched.  NULL is ignored. */
+void ss_pool_destroy(ss_pool* pool);
+
+/* Plan one step (Section 3.3 and Appendix A, Evict + DispatchLoadTasks):
+ * turns distances and the activation mask into victims and loads and updates
+ * the block table.  `distances` [N] uint32 and `active` [N] uint8 (0/1) are
+ * DEVICE pointers read during the call's kernels.  The call returns after the
+ * plan is known on the host (one device-to-host readback); the block-table
+ * update continues on the device and is ordered before the copy kernels.
+ * Previous step's data movement is waited for on the device first.
+ * SS_ERR_OVERCOMMIT if the active agents need more than capacity_units
+ * (pool unchanged).  SS_ERR_ORDER if the previous step was not completed with
+ * ss_evict_pack and ss_prefetch_unpack. */
+ss_status ss_plan_step(ss_pool* pool, const uint32_t* distances, const uint8_t* active,
+                       const ss_plan_params* params, ss_plan* out, void* stream);
+
+/* Evict (Section 3.3: eviction writes the victims' memory back to host):
+ * packs the victims' units (victim, then logical unit, then plane) into the
+ * eviction staging ring with the pack kernel and copies each victim's bytes
+ * to its host copy with hipMemcpyAsync, ring slot by ring slot.  Returns once
+ * queued.  SS_ERR_ORDER unless called right after ss_plan_step. */
+ss_status ss_evict_pack(ss_pool* pool, void* stream);
+
+/* Load (Appendix A, Load(memObj, agentIDs, ...)): copies every loaded agent's
+ * host copy into the load staging ring with hipMemcpyAsync and scatters it
+ * into the agent's new units with the unpack kernel on a side stream.  A slot
+ * is unpacked only after the eviction has read every unit it overwrites, so
+ * the two directions overlap.  `stream` then waits for the whole step.
+ * SS_ERR_ORDER unless called right after ss_evict_pack. */
+ss_status ss_prefetch_unpack(ss_pool* pool, void* stream);
+
+/* The device block table in CSR form: agent a's logical unit j is physical
+ * unit (*d_units)[(*d_agent_off)[a] + j], or -1 when a is not resident.
+ * Pool-owned device memory, valid until ss_pool_destroy; current after the
+ * work of ss_plan_step has run on the device. */
+ss_status ss_block_table(ss_pool* pool, const int32_t** d_units, const uint64_t** d_agent_off);
+
+/* Copy agent's block-table row to host (synchronous).  *n = agent's units;
+ * SS_ERR_ARG if cap < *n or agent >= N. */
+ss_status ss_block_table_host(ss_pool* pool, uint32_t agent, int32_t* out, uint32_t cap,
+                              uint32_t* n);
+
+/* Copy the whole block table (sum of agent_units entries, agent after agent,
+ * -1 = not resident) to host (synchronous).  *n = entries; SS_ERR_ARG if
+ * cap < *n. */
+ss_status ss_block_table_host_all(ss_pool* pool, int32_t* out, uint64_t cap, uint64_t* n);
+
+/* Resident flags [N] (0/1) to host (synchronous). */
+ss_status ss_resident_host(ss_pool* pool, uint8_t* out);
+
+/* Timing counters (SS_FLAG_TIMING); waits for the pool's queued work. */
+ss_status ss_get_stats(ss_pool* pool, ss_stats* out);
+ss_status ss_reset_stats(ss_pool* pool);
+
+/* Measurement probes (not part of a step).  ss_probe_copy runs the library's
+ * copy loop as a plain device-to-device copy of `bytes` (multiple of 16) and
+ * returns its event time; ss_probe_link times `iters` hipMemcpyAsync copies of
+ * `bytes` between pinned host memory and device memory: dir 0 = host to
+ * device, 1 = device to host, 2 = both at once on two streams: host[0, bytes)
+ * to dev[0, bytes) and dev[bytes, 2 bytes) to host[bytes, 2 bytes), so both
+ * buffers must hold 2 * bytes; the time is for the pair. */
+ss_status ss_probe_copy(void* dst, const void* src, uint64_t bytes, int iters, float* ms_per_iter);
+ss_status ss_probe_link(void* host, void* dev, uint64_t bytes, int dir, int iters,
+                        float* ms_per_iter);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* ss_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SCALESIM_H */

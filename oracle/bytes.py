@@ -28,9 +28,12 @@ class BytePool:
         self.planes = [np.zeros((capacity_units, c), dtype=np.uint8) for c in self.chunk_bytes]
         self.unit_bytes = sum(self.chunk_bytes)
 
-    def gather(self, units) -> np.ndarray:
-        """Staging bytes of the given physical units, unit then plane order."""
-        out = np.empty((len(units), self.unit_bytes), dtype=np.uint8)
+    def gather(self, units, out=None) -> np.ndarray:
+        """Staging bytes of the given physical units, unit then plane order
+        (into ``out`` when given, a buffer of at least that many bytes)."""
+        n = len(units) * self.unit_bytes
+        out = (np.empty(n, dtype=np.uint8) if out is None else out[:n])
+        out = out.reshape(len(units), self.unit_bytes)
         off = 0
         for c, plane in enumerate(self.planes):
             out[:, off:off + self.chunk_bytes[c]] = plane[np.asarray(units, dtype=np.int64)]
@@ -46,19 +49,24 @@ class BytePool:
             off += self.chunk_bytes[c]
 
 
-def apply_step_bytes(bpool: BytePool, plan, agent_units, host_read, host_write):
+def apply_step_bytes(bpool: BytePool, plan, agent_units, host_read, host_write,
+                     staging_out=None, staging_in=None):
     """Move one step's bytes.
 
     ``host_write(agent, bytes)`` receives each victim's evicted bytes;
     ``host_read(agent)`` returns a loaded agent's host copy.  Returns the two
-    staging streams (evicted, loaded) for comparison."""
-    staging_out = bpool.gather(plan.victim_units)
+    staging streams (evicted, loaded) for comparison; ``staging_out`` and
+    ``staging_in`` are optional preallocated byte buffers for them."""
+    staging_out = bpool.gather(plan.victim_units, out=staging_out)
     pos = 0
     for v in plan.victims:
         k = int(agent_units[v]) * bpool.unit_bytes
         host_write(int(v), staging_out[pos:pos + k])
         pos += k
     parts = [np.asarray(host_read(int(a)), dtype=np.uint8) for a in plan.loads]
-    staging_in = (np.concatenate(parts) if parts else np.zeros(0, np.uint8))
+    n_in = sum(len(x) for x in parts)
+    staging_in = (np.empty(n_in, dtype=np.uint8) if staging_in is None else staging_in[:n_in])
+    if parts:
+        np.concatenate(parts, out=staging_in)
     bpool.scatter(plan.load_units, staging_in)
     return staging_out, staging_in

@@ -1,0 +1,237 @@
+"""ctypes binding of libscalesim (include/scalesim.h).
+
+Argument marshalling only: every step of the hot path runs in the library's
+HIP kernels and HIP copies.  Importing this module does not load the library;
+the first call does, and raises if ``libscalesim.so`` has not been built
+(``python -m paper_2601_21473_amd.build``).  There is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libscalesim.so")
+
+SS_OK = 0
+SS_ERR_ARG = -1
+SS_ERR_OVERCOMMIT = -2
+SS_ERR_ORDER = -3
+SS_ERR_HIP = -4
+SS_ERR_NOMEM = -5
+SS_ERR_POISONED = -6
+SS_NO_BUDGET = (1 << 64) - 1
+SS_NO_DISTANCE = 0xFFFFFFFF
+SS_FLAG_TIMING = 1
+
+EXPORTS = ["ss_pool_create", "ss_pool_destroy", "ss_plan_step", "ss_evict_pack",
+           "ss_prefetch_unpack", "ss_block_table", "ss_block_table_host", "ss_block_table_host_all", "ss_resident_host",
+           "ss_get_stats", "ss_reset_stats", "ss_probe_copy", "ss_probe_link", "ss_last_error"]
+
+
+class ss_pool_desc(C.Structure):
+    _fields_ = [("n_agents", C.c_uint32), ("capacity_units", C.c_uint64),
+                ("n_planes", C.c_uint32), ("plane_base", C.POINTER(C.c_void_p)),
+                ("chunk_bytes", C.POINTER(C.c_uint64)), ("agent_units", C.POINTER(C.c_uint32)),
+                ("host_backing", C.c_void_p), ("host_off", C.POINTER(C.c_uint64)),
+                ("host_bytes", C.c_uint64), ("dev_staging", C.c_void_p),
+                ("staging_bytes", C.c_uint64), ("ring_slots", C.c_uint32),
+                ("device", C.c_int32), ("flags", C.c_uint32)]
+
+
+class ss_plan_params(C.Structure):
+    _fields_ = [("threshold", C.c_uint32), ("budget_units", C.c_uint64)]
+
+
+class ss_plan(C.Structure):
+    _fields_ = [("n_victims", C.c_uint32), ("n_loads", C.c_uint32), ("n_demand", C.c_uint32),
+                ("n_demand_victims", C.c_uint32), ("victims", C.POINTER(C.c_uint32)),
+                ("loads", C.POINTER(C.c_uint32)), ("units_out", C.c_uint64),
+                ("units_in", C.c_uint64), ("bytes_out", C.c_uint64), ("bytes_in", C.c_uint64)]
+
+
+class ss_stats(C.Structure):
+    _fields_ = [("steps", C.c_uint64), ("pack_launches", C.c_uint64),
+                ("unpack_launches", C.c_uint64), ("pack_bytes", C.c_uint64),
+                ("unpack_bytes", C.c_uint64), ("pack_ms", C.c_double), ("unpack_ms", C.c_double),
+                ("d2h_bytes", C.c_uint64), ("h2d_bytes", C.c_uint64), ("d2h_ms", C.c_double),
+                ("h2d_ms", C.c_double), ("plan_gpu_ms", C.c_double)]
+
+
+class ScaleSimError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"scalesim status {status}: {msg}")
+        self.status = status
+
+
+class OvercommitError(ScaleSimError):
+    pass
+
+
+_lib = None
+
+
+def load():
+    """Load libscalesim.so and declare its signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run python -m paper_2601_21473_amd.build")
+    L = C.CDLL(LIB_PATH)
+    P = C.c_void_p
+    sig = {
+        "ss_pool_create": ([C.POINTER(ss_pool_desc), C.POINTER(P)], C.c_int32),
+        "ss_pool_destroy": ([P], None),
+        "ss_plan_step": ([P, P, P, C.POINTER(ss_plan_params), C.POINTER(ss_plan), P], C.c_int32),
+        "ss_evict_pack": ([P, P], C.c_int32),
+        "ss_prefetch_unpack": ([P, P], C.c_int32),
+        "ss_block_table": ([P, C.POINTER(P), C.POINTER(P)], C.c_int32),
+        "ss_block_table_host": ([P, C.c_uint32, C.POINTER(C.c_int32), C.c_uint32,
+                                 C.POINTER(C.c_uint32)], C.c_int32),
+        "ss_block_table_host_all": ([P, C.POINTER(C.c_int32), C.c_uint64,
+                                     C.POINTER(C.c_uint64)], C.c_int32),
+        "ss_resident_host": ([P, C.POINTER(C.c_uint8)], C.c_int32),
+        "ss_get_stats": ([P, C.POINTER(ss_stats)], C.c_int32),
+        "ss_reset_stats": ([P], C.c_int32),
+        "ss_probe_copy": ([P, P, C.c_uint64, C.c_int, C.POINTER(C.c_float)], C.c_int32),
+        "ss_probe_link": ([P, P, C.c_uint64, C.c_int, C.c_int, C.POINTER(C.c_float)], C.c_int32),
+        "ss_last_error": ([], C.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != SS_OK:
+        msg = load().ss_last_error().decode()
+        if status == SS_ERR_OVERCOMMIT:
+            raise OvercommitError(status, msg)
+        raise ScaleSimError(status, msg)
+
+
+def _u64(a):
+    return np.ascontiguousarray(a, dtype=np.uint64)
+
+
+class Pool:
+    """One memory module's pool (``ss_pool``).  Pointers are plain integers
+    (device addresses, pinned host addresses, hipStream_t handles)."""
+
+    def __init__(self, *, capacity_units, chunk_bytes, agent_units, plane_base, host_backing,
+                 host_bytes, dev_staging, staging_bytes, ring_slots, host_off=None, device=0,
+                 timing=False):
+        L = load()
+        self._chunk = _u64(chunk_bytes)
+        self._units = np.ascontiguousarray(agent_units, dtype=np.uint32)
+        self._bases = (C.c_void_p * len(plane_base))(*[int(b) for b in plane_base])
+        self._host_off = None if host_off is None else _u64(host_off)
+        self.n_agents = len(self._units)
+        d = ss_pool_desc()
+        d.n_agents = self.n_agents
+        d.capacity_units = int(capacity_units)
+        d.n_planes = len(self._chunk)
+        d.plane_base = self._bases
+        d.chunk_bytes = self._chunk.ctypes.data_as(C.POINTER(C.c_uint64))
+        d.agent_units = self._units.ctypes.data_as(C.POINTER(C.c_uint32))
+        d.host_backing = int(host_backing)
+        d.host_off = (None if self._host_off is None
+                      else self._host_off.ctypes.data_as(C.POINTER(C.c_uint64)))
+        d.host_bytes = int(host_bytes)
+        d.dev_staging = int(dev_staging)
+        d.staging_bytes = int(staging_bytes)
+        d.ring_slots = int(ring_slots)
+        d.device = int(device)
+        d.flags = SS_FLAG_TIMING if timing else 0
+        h = C.c_void_p()
+        _check(L.ss_pool_create(C.byref(d), C.byref(h)))
+        self._h = h
+        self.unit_bytes = int(self._chunk.sum())
+
+    def close(self):
+        if getattr(self, "_h", None):
+            load().ss_pool_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def plan_step(self, distances_ptr: int, active_ptr: int, threshold: int, budget=None,
+                  stream: int = 0):
+        """``ss_plan_step``; returns a dict with numpy copies of the plan."""
+        prm = ss_plan_params(int(threshold), SS_NO_BUDGET if budget is None else int(budget))
+        out = ss_plan()
+        _check(load().ss_plan_step(self._h, int(distances_ptr), int(active_ptr), C.byref(prm),
+                                   C.byref(out), int(stream) or None))
+        nv, nl = out.n_victims, out.n_loads
+        victims = (np.ctypeslib.as_array(out.victims, shape=(nv,)).copy() if nv
+                   else np.zeros(0, np.uint32))
+        loads = (np.ctypeslib.as_array(out.loads, shape=(nl,)).copy() if nl
+                 else np.zeros(0, np.uint32))
+        return {"victims": victims, "loads": loads, "n_demand": out.n_demand,
+                "n_demand_victims": out.n_demand_victims, "units_out": out.units_out,
+                "units_in": out.units_in, "bytes_out": out.bytes_out, "bytes_in": out.bytes_in}
+
+    def evict_pack(self, stream: int = 0):
+        _check(load().ss_evict_pack(self._h, int(stream) or None))
+
+    def prefetch_unpack(self, stream: int = 0):
+        _check(load().ss_prefetch_unpack(self._h, int(stream) or None))
+
+    def block_table(self):
+        """(device pointer of int32 units, device pointer of uint64 agent offsets)."""
+        u, o = C.c_void_p(), C.c_void_p()
+        _check(load().ss_block_table(self._h, C.byref(u), C.byref(o)))
+        return u.value, o.value
+
+    def block_table_host(self, agent: int) -> np.ndarray:
+        cap = int(self._units[agent])
+        buf = np.empty(cap, dtype=np.int32)
+        n = C.c_uint32()
+        _check(load().ss_block_table_host(self._h, int(agent),
+                                          buf.ctypes.data_as(C.POINTER(C.c_int32)), cap,
+                                          C.byref(n)))
+        return buf[: n.value]
+
+    def block_table_host_all(self) -> np.ndarray:
+        """The whole block table, agent after agent (-1 = not resident)."""
+        cap = int(self._units.astype(np.uint64).sum())
+        buf = np.empty(cap, dtype=np.int32)
+        n = C.c_uint64()
+        _check(load().ss_block_table_host_all(self._h, buf.ctypes.data_as(C.POINTER(C.c_int32)),
+                                              cap, C.byref(n)))
+        return buf[: n.value]
+
+    def resident_host(self) -> np.ndarray:
+        out = np.empty(self.n_agents, dtype=np.uint8)
+        _check(load().ss_resident_host(self._h, out.ctypes.data_as(C.POINTER(C.c_uint8))))
+        return out
+
+    def stats(self) -> dict:
+        s = ss_stats()
+        _check(load().ss_get_stats(self._h, C.byref(s)))
+        return {k: getattr(s, k) for k, _ in ss_stats._fields_}
+
+    def reset_stats(self):
+        _check(load().ss_reset_stats(self._h))
+
+
+def probe_copy(dst: int, src: int, nbytes: int, iters: int = 10) -> float:
+    ms = C.c_float()
+    _check(load().ss_probe_copy(int(dst), int(src), int(nbytes), int(iters), C.byref(ms)))
+    return ms.value
+
+
+def probe_link(host: int, dev: int, nbytes: int, direction: int, iters: int = 5) -> float:
+    ms = C.c_float()
+    _check(load().ss_probe_link(int(host), int(dev), int(nbytes), int(direction), int(iters),
+                                C.byref(ms)))
+    return ms.value

@@ -1,0 +1,119 @@
+// Declarations shared by the device kernels (ss_kernels.hip) and the host
+// library (ss_pool.hip).  Internal to libscalesim.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ss {
+
+typedef unsigned long long u64;
+
+// Per-step accumulators written by the classify kernel.  The plan-core
+// kernel consumes and re-zeroes them, so they are zero between steps.
+struct PlanCounters {
+    u64 sum_active;      // units of active agents
+    u64 sum_resident;    // units of resident agents
+    u64 sum_demand;      // units of active, non-resident agents
+    u64 sum_evictable;   // units of inactive, resident agents
+    u64 sum_cand;        // units of prefetch candidates
+    unsigned n_E, n_C, n_L, pad;
+};
+
+// Outcome of a plan, written by the plan-core kernel to device memory and to
+// a mapped pinned host mirror.
+struct PlanResult {
+    int status;                 // 0 ok, 1 overcommit (nothing changed)
+    unsigned n_victims, n_loads, n_demand, n_demand_victims, pad;
+    u64 units_out, units_in;
+    u64 free_before;            // free units before the step
+    u64 n_free_used;            // loads' units taken from the pre-step free units
+};
+
+// One wave-sized piece of a unit: `len` bytes of plane `plane`, starting at
+// `chunk_off` inside the plane's chunk and at `unit_off` inside the unit's
+// serialised bytes (planes concatenated in order).
+struct CopyItem {
+    unsigned plane;
+    unsigned len;
+    u64 chunk_off;
+    u64 unit_off;
+};
+
+struct PlanArgs {
+    const unsigned* dist;           // [N] caller distances (device)
+    const unsigned char* active;    // [N] caller mask (device)
+    unsigned char* resident;        // [N] state
+    const unsigned* units;          // [N] s[a]
+    unsigned n;
+    unsigned idbits;                // key = (d << idbits) | id
+    unsigned threshold;
+    unsigned pad0;
+    u64 budget;
+    u64 capacity;
+    PlanCounters* cnt;
+    u64* listE;                     // [N] unsorted keys from classify
+    u64* listC;
+    u64* listL;
+    u64* sortE;                     // [pow2 >= N] sorted keys (ascending), also global sort scratch
+    u64* sortC;
+    u64* sortL;
+    u64* prefE;                     // [N+1] prefix units over E in eviction (descending) order
+    u64* prefC;                     // [N+1] prefix units over selected candidates (ascending)
+    u64* loff;                      // [N+1] prefix units over loads
+    unsigned* victims;              // [N] device copy of the plan
+    unsigned* loads;                // [N]
+    const unsigned* occ;            // occupancy bitmap, bit u = unit u in use
+    unsigned occ_words;
+    unsigned pad1;
+    int* free_old;                  // [U] pre-step free units, ascending
+    PlanResult* res;                // device
+    PlanResult* res_host;           // mapped pinned host
+    unsigned* victims_host;         // mapped pinned host [N]
+    unsigned* loads_host;           // mapped pinned host [N]
+};
+
+struct BtArgs {
+    const PlanResult* res;
+    const unsigned* victims;
+    const unsigned* loads;
+    const unsigned* units;          // s[a]
+    const u64* agent_off;           // [N+1] block-table CSR offsets
+    int* bt;                        // [sum s]
+    unsigned* occ;
+    const u64* voff;                // = prefE: prefix units over victims
+    const u64* loff;
+    const int* free_old;
+    int* vunits;                    // [U] victims' old units, victim then j order
+    int* lunits;                    // [U] loads' new units, load then j order
+    u64 capacity;                   // U
+};
+
+struct CopyArgs {
+    const int* units_list;          // vunits (pack) or lunits (unpack)
+    u64 first;                      // first position in units_list
+    u64 count;                      // units in this launch
+    const CopyItem* items;
+    unsigned n_items;               // items per unit
+    unsigned pad;
+    const u64* plane_base;          // [P] device addresses
+    const u64* chunk_bytes;         // [P]
+    char* staging;                  // slot base
+    u64 unit_bytes;
+    u64 capacity;                   // U; unit ids outside [0, U) are skipped
+};
+
+constexpr int kCopyThreads = 256;                 // 4 waves, one item per wave
+constexpr int kCopyWavesPerBlock = kCopyThreads / 64;
+constexpr unsigned kItemBytes = 16384;            // max bytes per item
+constexpr int kCoreThreads = 1024;
+constexpr int kLdsKeys = 16384;                   // 128 KiB of u64 keys in LDS
+
+hipError_t launch_classify(const PlanArgs& a, hipStream_t st);
+hipError_t launch_plan_core(const PlanArgs& a, hipStream_t st);
+hipError_t launch_bt_update(const BtArgs& a, unsigned n_agents, hipStream_t st);
+hipError_t launch_pack(const CopyArgs& a, hipStream_t st);
+hipError_t launch_unpack(const CopyArgs& a, hipStream_t st);
+hipError_t launch_zero_u32(unsigned* p, u64 n, hipStream_t st);
+hipError_t launch_probe_copy(void* dst, const void* src, u64 bytes, hipStream_t st);
+
+}  // namespace ss

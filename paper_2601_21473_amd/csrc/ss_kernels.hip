@@ -1,0 +1,587 @@
+// Device kernels of the invocation-distance memory manager for gfx950.
+//
+// Plan (per step, Section 3.3 of the paper and its Appendix A interface):
+//   k_classify   one pass over the agents: distance of active agents forced
+//                to 0, 64-bit priority keys (d, id), classification into
+//                evictable residents / demand loads / prefetch candidates,
+//                wave64 ballot + mbcnt stream compaction of each class, and
+//                the unit sums the plan needs.
+//   k_plan_core  one workgroup of 1024 threads: LDS bitonic sorts, weighted
+//                radix select of the candidate prefix that can possibly fit,
+//                prefix sums, the prefetch acceptance rule in closed form,
+//                the victim count, the free-unit list, and the plan written
+//                to a mapped host mirror.
+//   k_bt_victims / k_bt_loads   block-table release and allocation.
+// Data movement:
+//   k_copy<pack>  gathers (pack) or scatters (unpack) whole units between the
+//                pool's planes and a contiguous staging slot, one wave per
+//                piece of at most 16 KiB, 16-byte non-temporal accesses.
+//
+// Nothing here is a dense contraction; all work is integer indexing and byte
+// movement, so there is no MFMA.
+#include "ss_internal.h"
+
+namespace ss {
+
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ unsigned lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ unsigned mbcnt(u64 mask) {
+    return __builtin_amdgcn_mbcnt_hi((unsigned)(mask >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((unsigned)mask, 0u));
+}
+
+__device__ __forceinline__ u64 wave_sum(u64 v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+__device__ __forceinline__ u64 wave_incl_scan(u64 v) {
+    const unsigned l = lane_id();
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        u64 t = __shfl_up(v, o);
+        if (l >= (unsigned)o) v += t;
+    }
+    return v;
+}
+
+// ---------------------------------------------------------------------------
+// k_classify
+// ---------------------------------------------------------------------------
+
+// Append `key` of every lane with `pred` to list[*counter ...]; one atomic per
+// wave, lane order inside the wave (the order between waves is arbitrary and
+// is removed by the sort that follows).
+__device__ __forceinline__ void wave_append(bool pred, u64 key, u64* list, unsigned* counter) {
+    const u64 mask = __ballot(pred);
+    if (mask == 0) return;                           // wave-uniform
+    unsigned base = 0;
+    if (lane_id() == 0) base = atomicAdd(counter, (unsigned)__popcll(mask));
+    base = __shfl(base, 0);
+    if (pred) list[base + mbcnt(mask)] = key;
+}
+
+__global__ void __launch_bounds__(256) k_classify(PlanArgs A) {
+    const unsigned a = blockIdx.x * 256u + threadIdx.x;
+    const bool valid = a < A.n;
+    unsigned D = 0;
+    bool act = false, res = false;
+    u64 s = 0;
+    if (valid) {
+        D = A.dist[a];
+        act = A.active[a] != 0;
+        res = A.resident[a] != 0;
+        s = A.units[a];
+    }
+    const u64 d = act ? 0ull : (u64)D;               // active agents: distance 0
+    const u64 key = (d << A.idbits) | a;
+    const bool isE = valid && res && !act;            // evictable resident
+    const bool isL = valid && act && !res;            // demand load
+    const bool isC = valid && !res && !act && D < A.threshold;   // prefetch candidate
+    wave_append(isE, key, A.listE, &A.cnt->n_E);
+    wave_append(isL, key, A.listL, &A.cnt->n_L);
+    wave_append(isC, key, A.listC, &A.cnt->n_C);
+    const u64 s_act = wave_sum(act ? s : 0);
+    const u64 s_res = wave_sum(res ? s : 0);
+    const u64 s_dem = wave_sum(isL ? s : 0);
+    const u64 s_evi = wave_sum(isE ? s : 0);
+    const u64 s_can = wave_sum(isC ? s : 0);
+    if (lane_id() == 0) {
+        if (s_act) atomicAdd(&A.cnt->sum_active, s_act);
+        if (s_res) atomicAdd(&A.cnt->sum_resident, s_res);
+        if (s_dem) atomicAdd(&A.cnt->sum_demand, s_dem);
+        if (s_evi) atomicAdd(&A.cnt->sum_evictable, s_evi);
+        if (s_can) atomicAdd(&A.cnt->sum_cand, s_can);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// k_plan_core helpers (blockDim.x == kCoreThreads)
+// ---------------------------------------------------------------------------
+
+struct CoreShared {
+    u64 wsum[kCoreThreads / 64 + 1];
+    u64 hist[256];
+    unsigned hcnt[256];
+    u64 scal[8];
+    unsigned uscal[8];
+};
+
+// Exclusive block scan of one value per thread; returns the prefix and sets
+// *total (same on every thread).
+__device__ u64 block_excl_scan(u64 v, CoreShared& S, u64* total) {
+    const unsigned w = threadIdx.x >> 6, l = lane_id();
+    const unsigned nw = blockDim.x >> 6;
+    const u64 inc = wave_incl_scan(v);
+    if (l == 63) S.wsum[w] = inc;
+    __syncthreads();
+    if (w == 0) {
+        u64 x = (l < nw) ? S.wsum[l] : 0;
+        u64 xi = wave_incl_scan(x);
+        if (l < nw) S.wsum[l] = xi - x;
+        if (l == nw - 1) S.wsum[nw] = xi;
+    }
+    __syncthreads();
+    const u64 r = inc - v + S.wsum[w];
+    *total = S.wsum[nw];
+    __syncthreads();
+    return r;
+}
+
+// out[0] = 0, out[i+1] = out[i] + f(i) for i < n.
+template <class F>
+__device__ void block_prefix(unsigned n, F f, u64* out, CoreShared& S) {
+    u64 carry = 0;
+    if (threadIdx.x == 0) out[0] = 0;
+    for (unsigned base = 0; base < n; base += blockDim.x) {
+        const unsigned i = base + threadIdx.x;
+        const u64 v = (i < n) ? f(i) : 0;
+        u64 tot;
+        const u64 ex = block_excl_scan(v, S, &tot);
+        if (i < n) out[i + 1] = carry + ex + v;
+        carry += tot;
+    }
+    __syncthreads();
+}
+
+__device__ __forceinline__ unsigned pow2ceil(unsigned n) {
+    unsigned p = 1;
+    while (p < n) p <<= 1;
+    return p;
+}
+
+// Ascending bitonic sort of buf[0..npad), npad a power of two.  buf is LDS or
+// (for lists larger than the LDS budget) global memory private to this block.
+__device__ void bitonic_asc(u64* buf, unsigned npad) {
+    for (unsigned k = 2; k <= npad; k <<= 1) {
+        for (unsigned j = k >> 1; j > 0; j >>= 1) {
+            for (unsigned t = threadIdx.x; t < (npad >> 1); t += blockDim.x) {
+                const unsigned i = ((t & ~(j - 1)) << 1) | (t & (j - 1));
+                const unsigned p = i | j;
+                const u64 a = buf[i], b = buf[p];
+                const bool asc = (i & k) == 0;
+                if ((a > b) == asc) {
+                    buf[i] = b;
+                    buf[p] = a;
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// Sort the keys src[i] < kstar (there are exactly m of them) ascending into
+// dst[0..m).  dst has room for pow2ceil(N) keys and doubles as the sort buffer
+// when m exceeds the LDS budget.
+__device__ void select_sort(const u64* src, unsigned n_src, u64 kstar, unsigned m,
+                            u64* dst, u64* lds, CoreShared& S) {
+    if (m == 0) return;
+    const unsigned npad = pow2ceil(m);
+    u64* buf = (npad <= (unsigned)kLdsKeys) ? lds : dst;
+    if (threadIdx.x == 0) S.uscal[7] = 0;
+    __syncthreads();
+    if (kstar == ~0ull) {
+        for (unsigned i = threadIdx.x; i < n_src; i += blockDim.x) buf[i] = src[i];
+    } else {
+        for (unsigned i = threadIdx.x; i < n_src; i += blockDim.x) {
+            const u64 k = src[i];
+            if (k < kstar) {
+                const unsigned pos = atomicAdd(&S.uscal[7], 1u);
+                if (pos < m) buf[pos] = k;
+            }
+        }
+    }
+    for (unsigned i = m + threadIdx.x; i < npad; i += blockDim.x) buf[i] = ~0ull;
+    __syncthreads();
+    bitonic_asc(buf, npad);
+    if (buf == lds) {
+        for (unsigned i = threadIdx.x; i < m; i += blockDim.x) dst[i] = lds[i];
+        __syncthreads();
+    }
+}
+
+// Weighted radix select over the candidate keys: the smallest key k* such that
+// the units of all candidates with key <= k* exceed `cap`.  Candidates with
+// key < k* are the only ones whose cumulative prefix can stay within `cap`.
+// Returns k* and the number of keys below it in *m.  Requires the total
+// weight to exceed cap.
+__device__ u64 weighted_select(const u64* keys, unsigned n, const unsigned* units, u64 idmask,
+                               u64 cap, CoreShared& S, unsigned* m_out) {
+    // highest set bit over all keys bounds the digits that can differ
+    u64 orv = 0;
+    for (unsigned i = threadIdx.x; i < n; i += blockDim.x) orv |= keys[i];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) orv |= __shfl_xor(orv, o);
+    if (threadIdx.x == 0) S.scal[0] = 0;
+    __syncthreads();
+    if (lane_id() == 0) atomicOr(&S.scal[0], orv);
+    __syncthreads();
+    orv = S.scal[0];
+    const int top = orv ? 63 - __clzll(orv) : 0;
+    int shift = (top / 8) * 8;
+    u64 prefix = 0, pmask = 0, below = 0;
+    unsigned below_cnt = 0;
+    for (; shift >= 0; shift -= 8) {
+        for (unsigned b = threadIdx.x; b < 256; b += blockDim.x) {
+            S.hist[b] = 0;
+            S.hcnt[b] = 0;
+        }
+        __syncthreads();
+        for (unsigned i = threadIdx.x; i < n; i += blockDim.x) {
+            const u64 k = keys[i];
+            if ((k & pmask) == prefix) {
+                const unsigned b = (unsigned)(k >> shift) & 255u;
+                atomicAdd(&S.hist[b], (u64)units[k & idmask]);
+                atomicAdd(&S.hcnt[b], 1u);
+            }
+        }
+        __syncthreads();
+        if (threadIdx.x < 64) {
+            // lane l owns bins 4l..4l+3
+            const unsigned l = threadIdx.x;
+            u64 w4 = 0;
+            unsigned c4 = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                w4 += S.hist[4 * l + q];
+                c4 += S.hcnt[4 * l + q];
+            }
+            const u64 wi = wave_incl_scan(w4);
+            const u64 ci = wave_incl_scan((u64)c4);
+            const u64 over = __ballot(below + wi > cap);
+            const unsigned L = over ? (unsigned)__ffsll((long long)over) - 1 : 63;
+            if (l == L) {
+                u64 acc = below + wi - w4;
+                unsigned cacc = below_cnt + (unsigned)(ci - c4);
+                unsigned bsel = 4 * l + 3;
+                for (int q = 0; q < 4; ++q) {
+                    const u64 h = S.hist[4 * l + q];
+                    if (acc + h > cap) {
+                        bsel = 4 * l + q;
+                        break;
+                    }
+                    acc += h;
+                    cacc += S.hcnt[4 * l + q];
+                }
+                S.scal[1] = acc;
+                S.uscal[0] = cacc;
+                S.uscal[1] = bsel;
+            }
+        }
+        __syncthreads();
+        below = S.scal[1];
+        below_cnt = S.uscal[0];
+        prefix |= (u64)S.uscal[1] << shift;
+        pmask |= 255ull << shift;
+        __syncthreads();
+    }
+    *m_out = below_cnt;
+    return prefix;
+}
+
+// ---------------------------------------------------------------------------
+// k_plan_core
+// ---------------------------------------------------------------------------
+
+__global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
+    __shared__ u64 lds[kLdsKeys];
+    __shared__ CoreShared S;
+    const unsigned tid = threadIdx.x;
+    const PlanCounters c = *A.cnt;
+    const u64 idmask = (1ull << A.idbits) - 1;
+    const unsigned* units = A.units;
+    __syncthreads();
+
+    if (c.sum_active > A.capacity) {                 // overcommit: change nothing
+        if (tid == 0) {
+            PlanResult r = {};
+            r.status = 1;
+            *A.res = r;
+            *A.res_host = r;
+            *A.cnt = PlanCounters{};
+        }
+        return;
+    }
+    const u64 free_before = A.capacity - c.sum_resident;
+    const unsigned nE = c.n_E, nL = c.n_L, nC = c.n_C;
+
+    // demand loads by id (their distance is 0, so key order is id order)
+    select_sort(A.listL, nL, ~0ull, nL, A.sortL, lds, S);
+    // evictable residents; eviction order is descending key = reversed array
+    select_sort(A.listE, nE, ~0ull, nE, A.sortE, lds, S);
+    const u64* sortE = A.sortE;
+    block_prefix(nE, [&](unsigned i) { return (u64)units[sortE[nE - 1 - i] & idmask]; },
+                 A.prefE, S);
+    block_prefix(nL, [&](unsigned i) { return (u64)units[A.sortL[i] & idmask]; }, A.loff, S);
+
+    // demand victims: shortest prefix of the eviction order covering `need`
+    if (tid == 0) {
+        const long long need = (long long)c.sum_demand - (long long)free_before;
+        unsigned n_d = 0;
+        if (need > 0) {
+            unsigned lo = 1, hi = nE;                // prefE[hi] >= need holds
+            while (lo < hi) {
+                const unsigned mid = (lo + hi) >> 1;
+                if ((long long)A.prefE[mid] >= need) hi = mid; else lo = mid + 1;
+            }
+            n_d = lo < nE ? lo : nE;
+        }
+        S.uscal[2] = n_d;
+    }
+    __syncthreads();
+    const unsigned n_d = S.uscal[2];
+    const u64 free1 = free_before + A.prefE[n_d] - c.sum_demand;
+    const u64 avail = free1 + (A.prefE[nE] - A.prefE[n_d]);
+    const u64 cap = A.budget < avail ? A.budget : avail;
+
+    // candidates whose cumulative units can stay within cap, sorted by key
+    unsigned m = nC;
+    u64 kstar = ~0ull;
+    if (c.sum_cand > cap) kstar = weighted_select(A.listC, nC, units, idmask, cap, S, &m);
+    select_sort(A.listC, nC, kstar, m, A.sortC, lds, S);
+    const u64* sortC = A.sortC;
+    block_prefix(m, [&](unsigned i) { return (u64)units[sortC[i] & idmask]; }, A.prefC, S);
+
+    // acceptance: S_i <= budget and S_i <= free1 + (units of the remaining
+    // evictable residents with distance strictly larger than d_i)
+    if (tid == 0) S.uscal[3] = m;
+    __syncthreads();
+    for (unsigned i = tid; i < m; i += blockDim.x) {
+        const u64 di = sortC[i] >> A.idbits;
+        const u64 Si = A.prefC[i + 1];
+        unsigned lo = 0, hi = nE;                    // first eviction index with d <= di
+        while (lo < hi) {
+            const unsigned mid = (lo + hi) >> 1;
+            if ((sortE[nE - 1 - mid] >> A.idbits) > di) lo = mid + 1; else hi = mid;
+        }
+        const u64 G = lo > n_d ? A.prefE[lo] - A.prefE[n_d] : 0;
+        const bool ok = Si <= A.budget && Si <= free1 + G;
+        if (!ok) atomicMin(&S.uscal[3], i);
+    }
+    __syncthreads();
+    const unsigned n_p = S.uscal[3];
+    if (tid == 0) {
+        unsigned n_v = n_d;
+        if (n_p > 0 && A.prefC[n_p] > free1) {
+            const u64 target = A.prefE[n_d] + (A.prefC[n_p] - free1);
+            unsigned lo = n_d + 1, hi = nE;
+            while (lo < hi) {
+                const unsigned mid = (lo + hi) >> 1;
+                if (A.prefE[mid] >= target) hi = mid; else lo = mid + 1;
+            }
+            n_v = lo < nE ? lo : nE;
+        }
+        S.uscal[4] = n_v;
+    }
+    __syncthreads();
+    const unsigned n_v = S.uscal[4];
+    const unsigned n_l = nL + n_p;
+    const u64 units_out = A.prefE[n_v];
+    const u64 units_in = c.sum_demand + A.prefC[n_p];
+
+    // plan lists, load offsets, residency
+    for (unsigned i = tid; i < n_v; i += blockDim.x) {
+        const unsigned v = (unsigned)(sortE[nE - 1 - i] & idmask);
+        A.victims[i] = v;
+        A.victims_host[i] = v;
+        A.resident[v] = 0;
+    }
+    for (unsigned i = tid; i < n_l; i += blockDim.x) {
+        const unsigned a = (unsigned)((i < nL ? A.sortL[i] : sortC[i - nL]) & idmask);
+        A.loads[i] = a;
+        A.loads_host[i] = a;
+        A.resident[a] = 1;
+        if (i >= nL) A.loff[i + 1] = c.sum_demand + A.prefC[i - nL + 1];
+    }
+
+    // pre-step free units in ascending order, as many as the loads can use
+    const u64 n_free_used = units_in < free_before ? units_in : free_before;
+    if (n_free_used > 0) {
+        const unsigned W = A.occ_words;
+        const unsigned per = (W + blockDim.x - 1) / blockDim.x;
+        const unsigned w0 = tid * per;
+        const unsigned w1 = min(W, w0 + per);
+        u64 cnt = 0;
+        for (unsigned w = w0; w < w1; ++w) cnt += __popc(~A.occ[w]);
+        u64 tot;
+        u64 pos = block_excl_scan(cnt, S, &tot);
+        for (unsigned w = w0; w < w1 && pos < n_free_used; ++w) {
+            unsigned bits = ~A.occ[w];
+            while (bits && pos < n_free_used) {
+                const unsigned b = __ffs(bits) - 1;
+                bits &= bits - 1;
+                A.free_old[pos++] = (int)(w * 32u + b);
+            }
+        }
+    }
+
+    __syncthreads();
+    if (tid == 0) {
+        PlanResult r = {};
+        r.status = 0;
+        r.n_victims = n_v;
+        r.n_loads = n_l;
+        r.n_demand = nL;
+        r.n_demand_victims = n_d;
+        r.units_out = units_out;
+        r.units_in = units_in;
+        r.free_before = free_before;
+        r.n_free_used = n_free_used;
+        *A.res = r;
+        *A.res_host = r;
+        *A.cnt = PlanCounters{};
+    }
+}
+
+// ---------------------------------------------------------------------------
+// block table
+// ---------------------------------------------------------------------------
+
+__global__ void __launch_bounds__(256) k_bt_victims(BtArgs B) {
+    if (B.res->status != 0) return;
+    const unsigned nv = B.res->n_victims;
+    for (unsigned i = blockIdx.x; i < nv; i += gridDim.x) {
+        const unsigned v = B.victims[i];
+        const u64 base = B.agent_off[v];
+        const unsigned s = B.units[v];
+        const u64 o = B.voff[i];
+        for (unsigned j = threadIdx.x; j < s; j += blockDim.x) {
+            const int u = B.bt[base + j];
+            B.vunits[o + j] = u;
+            B.bt[base + j] = -1;
+            if ((u64)(unsigned)u < B.capacity)
+                atomicAnd(&B.occ[(unsigned)u >> 5], ~(1u << ((unsigned)u & 31u)));
+        }
+    }
+}
+
+__global__ void __launch_bounds__(256) k_bt_loads(BtArgs B) {
+    if (B.res->status != 0) return;
+    const unsigned nl = B.res->n_loads;
+    const u64 nF = B.res->n_free_used;
+    for (unsigned i = blockIdx.x; i < nl; i += gridDim.x) {
+        const unsigned a = B.loads[i];
+        const u64 base = B.agent_off[a];
+        const unsigned s = B.units[a];
+        const u64 o = B.loff[i];
+        for (unsigned j = threadIdx.x; j < s; j += blockDim.x) {
+            const u64 q = o + j;
+            const int u = q < nF ? B.free_old[q] : B.vunits[q - nF];
+            B.bt[base + j] = u;
+            B.lunits[q] = u;
+            if ((u64)(unsigned)u < B.capacity)
+                atomicOr(&B.occ[(unsigned)u >> 5], 1u << ((unsigned)u & 31u));
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// pack / unpack
+// ---------------------------------------------------------------------------
+
+// One wave copies len bytes (multiple of 16, at most kItemBytes): lane l moves
+// the 16-byte words l, l+64, l+128, ...; eight words per lane are loaded
+// before any is stored so that each wave keeps 8 KiB in flight.
+__device__ __forceinline__ void wave_copy(char* dst, const char* src, unsigned len) {
+    const v4u* s = reinterpret_cast<const v4u*>(src);
+    v4u* d = reinterpret_cast<v4u*>(dst);
+    const unsigned n16 = len >> 4;
+    unsigned i = lane_id();
+    for (; i + 7 * 64 < n16; i += 8 * 64) {
+        v4u r[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) r[k] = __builtin_nontemporal_load(s + i + k * 64);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) __builtin_nontemporal_store(r[k], d + i + k * 64);
+    }
+    for (; i < n16; i += 64) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
+}
+
+template <bool kPack>
+__global__ void __launch_bounds__(kCopyThreads) k_copy(CopyArgs A) {
+    const u64 w = (u64)blockIdx.x * kCopyWavesPerBlock + (threadIdx.x >> 6);
+    const u64 total = A.count * A.n_items;
+    if (w >= total) return;
+    const u64 p = w / A.n_items;
+    const unsigned r = (unsigned)(w - p * A.n_items);
+    const u64 u = (u64)(unsigned)A.units_list[A.first + p];
+    if (u >= A.capacity) return;
+    const CopyItem it = A.items[r];
+    char* chunk = reinterpret_cast<char*>(A.plane_base[it.plane]) + u * A.chunk_bytes[it.plane] +
+                  it.chunk_off;
+    char* stage = A.staging + p * A.unit_bytes + it.unit_off;
+    if (kPack) wave_copy(stage, chunk, it.len);
+    else wave_copy(chunk, stage, it.len);
+}
+
+__global__ void __launch_bounds__(kCopyThreads) k_probe_copy(char* dst, const char* src, u64 bytes) {
+    const u64 w = (u64)blockIdx.x * kCopyWavesPerBlock + (threadIdx.x >> 6);
+    const u64 off = w * kItemBytes;
+    if (off >= bytes) return;
+    const u64 rem = bytes - off;
+    wave_copy(dst + off, src + off, rem < kItemBytes ? (unsigned)rem : kItemBytes);
+}
+
+__global__ void k_zero_u32(unsigned* p, u64 n) {
+    for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x)
+        p[i] = 0;
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+
+hipError_t launch_classify(const PlanArgs& a, hipStream_t st) {
+    const unsigned blocks = (a.n + 255) / 256;
+    hipLaunchKernelGGL(k_classify, dim3(blocks), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_plan_core(const PlanArgs& a, hipStream_t st) {
+    hipLaunchKernelGGL(k_plan_core, dim3(1), dim3(kCoreThreads), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_bt_update(const BtArgs& b, unsigned n_agents, hipStream_t st) {
+    const unsigned blocks = n_agents < 1024 ? n_agents : 1024;
+    hipLaunchKernelGGL(k_bt_victims, dim3(blocks), dim3(256), 0, st, b);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_bt_loads, dim3(blocks), dim3(256), 0, st, b);
+    return hipGetLastError();
+}
+
+static hipError_t launch_copy(const CopyArgs& a, hipStream_t st, bool pack) {
+    const u64 waves = a.count * a.n_items;
+    if (waves == 0) return hipSuccess;
+    const u64 blocks = (waves + kCopyWavesPerBlock - 1) / kCopyWavesPerBlock;
+    if (blocks > 0x7fffffffull) return hipErrorInvalidValue;
+    if (pack) hipLaunchKernelGGL(k_copy<true>, dim3((unsigned)blocks), dim3(kCopyThreads), 0, st, a);
+    else hipLaunchKernelGGL(k_copy<false>, dim3((unsigned)blocks), dim3(kCopyThreads), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack(const CopyArgs& a, hipStream_t st) { return launch_copy(a, st, true); }
+hipError_t launch_unpack(const CopyArgs& a, hipStream_t st) { return launch_copy(a, st, false); }
+
+hipError_t launch_zero_u32(unsigned* p, u64 n, hipStream_t st) {
+    if (n == 0) return hipSuccess;
+    u64 blocks = (n + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)blocks), dim3(256), 0, st, p, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_copy(void* dst, const void* src, u64 bytes, hipStream_t st) {
+    const u64 items = (bytes + kItemBytes - 1) / kItemBytes;
+    const u64 blocks = (items + kCopyWavesPerBlock - 1) / kCopyWavesPerBlock;
+    if (blocks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_probe_copy, dim3((unsigned)blocks), dim3(kCopyThreads), 0, st,
+                       static_cast<char*>(dst), static_cast<const char*>(src), bytes);
+    return hipGetLastError();
+}
+
+}  // namespace ss

@@ -1,0 +1,879 @@
+// Host side of libscalesim: the C ABI declared in include/scalesim.h.
+//
+// Streams (all created non-blocking at the default priority):
+//   plan    classify -> plan core -> block-table update
+//   pack    pack kernels, one per eviction ring slot
+//   d2h     hipMemcpyAsync of packed slots to the victims' host copies
+//   h2d     hipMemcpyAsync of the loads' host copies into load ring slots
+//   unpack  unpack kernels, one per load ring slot
+// Hazards ordered with events:
+//   * a pack slot is rewritten only after its previous D2H finished;
+//   * a load slot is refilled only after its previous unpack finished;
+//   * an unpack that writes units released by this step's victims waits for
+//     the pack that read them (loads take pre-step free units first, then the
+//     released units in eviction order, so this is one monotone dependency);
+//   * the next step's plan waits for all of this step's copies.
+#include "scalesim.h"
+#include "ss_internal.h"
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+using namespace ss;
+
+namespace {
+
+thread_local std::string g_err;
+
+ss_status set_err(ss_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+enum State { kIdle = 0, kPlanned = 1, kPacked = 2 };
+
+struct TimedPair {
+    hipEvent_t a = nullptr, b = nullptr;
+    u64 bytes = 0;
+};
+
+}  // namespace
+
+struct ss_pool {
+    int device = 0;
+    uint32_t N = 0;
+    u64 U = 0;
+    uint32_t P = 0;
+    u64 unit_bytes = 0;
+    uint32_t idbits = 1;
+    uint32_t flags = 0;
+    std::vector<u64> chunk_bytes;
+    std::vector<uint32_t> s;
+    std::vector<u64> host_off;
+    char* host = nullptr;
+    u64 host_bytes = 0;
+    char* stage_out = nullptr;
+    char* stage_in = nullptr;
+    uint32_t ring = 1;
+    u64 units_per_slot = 0;
+    u64 slot_bytes = 0;
+
+    // device metadata
+    unsigned* d_units = nullptr;
+    u64* d_agent_off = nullptr;
+    int* d_bt = nullptr;
+    unsigned char* d_resident = nullptr;
+    unsigned* d_occ = nullptr;
+    unsigned occ_words = 0;
+    PlanCounters* d_cnt = nullptr;
+    u64 *d_listE = nullptr, *d_listC = nullptr, *d_listL = nullptr;
+    u64 *d_sortE = nullptr, *d_sortC = nullptr, *d_sortL = nullptr;
+    u64 *d_prefE = nullptr, *d_prefC = nullptr, *d_loff = nullptr;
+    unsigned *d_victims = nullptr, *d_loads = nullptr;
+    int *d_vunits = nullptr, *d_lunits = nullptr, *d_free_old = nullptr;
+    PlanResult* d_res = nullptr;
+    CopyItem* d_items = nullptr;
+    unsigned n_items = 0;
+    u64* d_plane_base = nullptr;
+    u64* d_chunk_bytes = nullptr;
+
+    // mapped pinned host mirrors of the plan
+    PlanResult* h_res = nullptr;
+    unsigned* h_victims = nullptr;
+    unsigned* h_loads = nullptr;
+    PlanResult* h_res_dev = nullptr;
+    unsigned* h_victims_dev = nullptr;
+    unsigned* h_loads_dev = nullptr;
+
+    hipStream_t st_plan = nullptr, st_pack = nullptr, st_d2h = nullptr, st_h2d = nullptr,
+                st_unpack = nullptr;
+    hipEvent_t ev_planned = nullptr, ev_bt = nullptr, ev_caller = nullptr,
+               ev_d2h_done = nullptr, ev_unpack_done = nullptr;
+    std::vector<hipEvent_t> ev_packed;            // per eviction slot index in the step
+    std::vector<hipEvent_t> ev_out_free, ev_in_ready, ev_in_free;   // per ring slot
+
+    // timing (SS_FLAG_TIMING)
+    std::vector<TimedPair> t_pack, t_unpack;
+    size_t n_t_pack = 0, n_t_unpack = 0;
+    TimedPair t_d2h, t_h2d, t_plan;
+    bool t_d2h_used = false, t_h2d_used = false, t_plan_used = false;
+    ss_stats stats{};
+
+    // plan of the current step (host)
+    ss_plan plan{};
+    PlanResult res{};
+    std::vector<u64> voff, loff;
+
+    State state = kIdle;
+    bool poisoned = false;
+};
+
+namespace {
+
+struct DeviceGuard {
+    int prev = -1;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        if (prev != dev) (void)hipSetDevice(dev);
+    }
+    ~DeviceGuard() {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+ss_status hip_fail(ss_pool* p, hipError_t e, const char* what, bool poison) {
+    if (p && poison) p->poisoned = true;
+    return set_err(SS_ERR_HIP, "%s failed: %s", what, hipGetErrorString(e));
+}
+
+#define TRY_HIP(pool, expr, poison)                                              \
+    do {                                                                         \
+        hipError_t _e = (expr);                                                  \
+        if (_e != hipSuccess) return hip_fail((pool), _e, #expr, (poison));      \
+    } while (0)
+
+template <class T>
+hipError_t dalloc(T** p, size_t n) {
+    return hipMalloc(reinterpret_cast<void**>(p), std::max<size_t>(n, 1) * sizeof(T));
+}
+
+unsigned pow2ceil_u(unsigned n) {
+    unsigned p = 1;
+    while (p < n) p <<= 1;
+    return p;
+}
+
+void free_pool(ss_pool* p) {
+    if (!p) return;
+    DeviceGuard g(p->device);
+    hipStream_t sts[] = {p->st_plan, p->st_pack, p->st_d2h, p->st_h2d, p->st_unpack};
+    for (hipStream_t s : sts)
+        if (s) (void)hipStreamSynchronize(s);
+    void* dptrs[] = {p->d_units, p->d_agent_off, p->d_bt, p->d_resident, p->d_occ, p->d_cnt,
+                     p->d_listE, p->d_listC, p->d_listL, p->d_sortE, p->d_sortC, p->d_sortL,
+                     p->d_prefE, p->d_prefC, p->d_loff, p->d_victims, p->d_loads, p->d_vunits,
+                     p->d_lunits, p->d_free_old, p->d_res, p->d_items, p->d_plane_base,
+                     p->d_chunk_bytes};
+    for (void* d : dptrs)
+        if (d) (void)hipFree(d);
+    void* hptrs[] = {p->h_res, p->h_victims, p->h_loads};
+    for (void* h : hptrs)
+        if (h) (void)hipHostFree(h);
+    for (hipStream_t s : sts)
+        if (s) (void)hipStreamDestroy(s);
+    hipEvent_t evs[] = {p->ev_planned, p->ev_bt, p->ev_caller, p->ev_d2h_done, p->ev_unpack_done,
+                        p->t_d2h.a, p->t_d2h.b, p->t_h2d.a, p->t_h2d.b, p->t_plan.a, p->t_plan.b};
+    for (hipEvent_t e : evs)
+        if (e) (void)hipEventDestroy(e);
+    for (auto* v : {&p->ev_packed, &p->ev_out_free, &p->ev_in_ready, &p->ev_in_free})
+        for (hipEvent_t e : *v)
+            if (e) (void)hipEventDestroy(e);
+    for (auto* v : {&p->t_pack, &p->t_unpack})
+        for (auto& tp : *v) {
+            if (tp.a) (void)hipEventDestroy(tp.a);
+            if (tp.b) (void)hipEventDestroy(tp.b);
+        }
+    delete p;
+}
+
+hipError_t make_event(hipEvent_t* e, bool timing) {
+    return hipEventCreateWithFlags(e, timing ? hipEventDefault : hipEventDisableTiming);
+}
+
+hipError_t timed_pair(std::vector<TimedPair>& v, size_t idx, TimedPair** out) {
+    while (v.size() <= idx) {
+        TimedPair tp;
+        hipError_t e = make_event(&tp.a, true);
+        if (e != hipSuccess) return e;
+        e = make_event(&tp.b, true);
+        if (e != hipSuccess) return e;
+        v.push_back(tp);
+    }
+    *out = &v[idx];
+    return hipSuccess;
+}
+
+// Fold the previous step's event times into the stats.  Called only when that
+// step's work is known to have finished.
+void collect_timing(ss_pool* p) {
+    if (!(p->flags & SS_FLAG_TIMING)) return;
+    float ms = 0.f;
+    for (size_t i = 0; i < p->n_t_pack; ++i)
+        if (hipEventElapsedTime(&ms, p->t_pack[i].a, p->t_pack[i].b) == hipSuccess) {
+            p->stats.pack_ms += ms;
+            p->stats.pack_bytes += p->t_pack[i].bytes;
+            p->stats.pack_launches++;
+        }
+    for (size_t i = 0; i < p->n_t_unpack; ++i)
+        if (hipEventElapsedTime(&ms, p->t_unpack[i].a, p->t_unpack[i].b) == hipSuccess) {
+            p->stats.unpack_ms += ms;
+            p->stats.unpack_bytes += p->t_unpack[i].bytes;
+            p->stats.unpack_launches++;
+        }
+    if (p->t_d2h_used && hipEventElapsedTime(&ms, p->t_d2h.a, p->t_d2h.b) == hipSuccess) {
+        p->stats.d2h_ms += ms;
+        p->stats.d2h_bytes += p->t_d2h.bytes;
+    }
+    if (p->t_h2d_used && hipEventElapsedTime(&ms, p->t_h2d.a, p->t_h2d.b) == hipSuccess) {
+        p->stats.h2d_ms += ms;
+        p->stats.h2d_bytes += p->t_h2d.bytes;
+    }
+    if (p->t_plan_used && hipEventElapsedTime(&ms, p->t_plan.a, p->t_plan.b) == hipSuccess)
+        p->stats.plan_gpu_ms += ms;
+    p->n_t_pack = p->n_t_unpack = 0;
+    p->t_d2h_used = p->t_h2d_used = p->t_plan_used = false;
+}
+
+// True if [ptr, ptr + bytes) lies inside one allocation of device memory on
+// `device` (or managed memory).
+bool device_range_ok(const void* ptr, u64 bytes, int device) {
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, ptr) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    if (attr.type == hipMemoryTypeManaged) return true;
+    if (attr.type != hipMemoryTypeDevice || attr.device != device) return false;
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, const_cast<void*>(ptr)) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    const u64 off = reinterpret_cast<uintptr_t>(ptr) - reinterpret_cast<uintptr_t>(base);
+    return off <= size && bytes <= size - off;
+}
+
+// True if host_ptr is pinned (page-locked) host memory; when the runtime
+// reports the allocation's extent, [host_ptr, host_ptr + bytes) must fit in it.
+bool pinned_range_ok(const void* ptr, u64 bytes) {
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, ptr) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    if (attr.type != hipMemoryTypeHost) return false;
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, const_cast<void*>(ptr)) != hipSuccess) {
+        (void)hipGetLastError();
+        return true;
+    }
+    const u64 off = reinterpret_cast<uintptr_t>(ptr) - reinterpret_cast<uintptr_t>(base);
+    return off <= size && bytes <= size - off;
+}
+
+ss_status check_usable(ss_pool* p) {
+    if (!p) return set_err(SS_ERR_ARG, "pool is NULL");
+    if (p->poisoned) return set_err(SS_ERR_POISONED, "pool is poisoned by an earlier HIP failure");
+    return SS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ss_last_error(void) { return g_err.c_str(); }
+
+ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
+    if (!d || !out) return set_err(SS_ERR_ARG, "desc and out must not be NULL");
+    if (d->n_agents == 0 || d->n_agents >= (1u << 31))
+        return set_err(SS_ERR_ARG, "n_agents must be in [1, 2^31)");
+    if (d->capacity_units == 0 || d->capacity_units >= (1ull << 31))
+        return set_err(SS_ERR_ARG, "capacity_units must be in [1, 2^31)");
+    if (d->n_planes == 0 || !d->plane_base || !d->chunk_bytes || !d->agent_units)
+        return set_err(SS_ERR_ARG, "n_planes, plane_base, chunk_bytes and agent_units are required");
+    if (!d->host_backing) return set_err(SS_ERR_ARG, "host_backing is required");
+    if (!d->dev_staging) return set_err(SS_ERR_ARG, "dev_staging is required");
+    if (d->ring_slots == 0) return set_err(SS_ERR_ARG, "ring_slots must be >= 1");
+    if (d->flags & ~SS_FLAG_TIMING) return set_err(SS_ERR_ARG, "unknown flag bits");
+    u64 unit_bytes = 0;
+    for (uint32_t c = 0; c < d->n_planes; ++c) {
+        const u64 cb = d->chunk_bytes[c];
+        if (cb < 16 || cb % 16 != 0)
+            return set_err(SS_ERR_ARG, "chunk_bytes[%u] = %llu is not a positive multiple of 16", c,
+                           (unsigned long long)cb);
+        if (!d->plane_base[c]) return set_err(SS_ERR_ARG, "plane_base[%u] is NULL", c);
+        if (reinterpret_cast<uintptr_t>(d->plane_base[c]) % 16 != 0)
+            return set_err(SS_ERR_ARG, "plane_base[%u] is not 16-byte aligned", c);
+        unit_bytes += cb;
+    }
+    if (reinterpret_cast<uintptr_t>(d->dev_staging) % 16 != 0)
+        return set_err(SS_ERR_ARG, "dev_staging is not 16-byte aligned");
+    u64 total_units = 0;
+    for (uint32_t a = 0; a < d->n_agents; ++a) {
+        if (d->agent_units[a] == 0) return set_err(SS_ERR_ARG, "agent_units[%u] is 0", a);
+        total_units += d->agent_units[a];
+    }
+    if (total_units >= (1ull << 40)) return set_err(SS_ERR_ARG, "too many agent units");
+    const u64 half = (d->staging_bytes / 2) & ~15ull;    // second half 16-byte aligned
+    const u64 ups = half / d->ring_slots / unit_bytes;
+    if (ups == 0)
+        return set_err(SS_ERR_ARG, "staging_bytes %llu too small: each of 2 x %u slots needs >= %llu",
+                       (unsigned long long)d->staging_bytes, d->ring_slots,
+                       (unsigned long long)unit_bytes);
+
+    std::vector<u64> host_off(d->n_agents);
+    u64 acc = 0;
+    for (uint32_t a = 0; a < d->n_agents; ++a) {
+        const u64 off = d->host_off ? d->host_off[a] : acc;
+        const u64 len = (u64)d->agent_units[a] * unit_bytes;
+        if (off > d->host_bytes || len > d->host_bytes - off)
+            return set_err(SS_ERR_ARG, "host copy of agent %u [%llu, +%llu) exceeds host_bytes", a,
+                           (unsigned long long)off, (unsigned long long)len);
+        host_off[a] = off;
+        acc += len;
+    }
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || d->device < 0 || d->device >= ndev) {
+        (void)hipGetLastError();
+        return set_err(SS_ERR_ARG, "device %d not present", (int)d->device);
+    }
+
+    {
+        DeviceGuard g(d->device);
+        for (uint32_t c = 0; c < d->n_planes; ++c)
+            if (!device_range_ok(d->plane_base[c], d->capacity_units * d->chunk_bytes[c], d->device))
+                return set_err(SS_ERR_ARG, "plane %u: [plane_base, +capacity*chunk_bytes) is not "
+                                           "device memory of device %d", c, (int)d->device);
+        if (!device_range_ok(d->dev_staging, d->staging_bytes, d->device))
+            return set_err(SS_ERR_ARG, "dev_staging [0, staging_bytes) is not device memory");
+        if (!pinned_range_ok(d->host_backing, d->host_bytes))
+            return set_err(SS_ERR_ARG, "host_backing [0, host_bytes) is not pinned host memory");
+    }
+
+    ss_pool* p = new (std::nothrow) ss_pool();
+    if (!p) return set_err(SS_ERR_NOMEM, "out of host memory");
+    p->device = d->device;
+    p->N = d->n_agents;
+    p->U = d->capacity_units;
+    p->P = d->n_planes;
+    p->unit_bytes = unit_bytes;
+    p->flags = d->flags;
+    p->chunk_bytes.assign(d->chunk_bytes, d->chunk_bytes + d->n_planes);
+    p->s.assign(d->agent_units, d->agent_units + d->n_agents);
+    p->host_off = std::move(host_off);
+    p->host = static_cast<char*>(d->host_backing);
+    p->host_bytes = d->host_bytes;
+    p->ring = d->ring_slots;
+    p->units_per_slot = ups;
+    p->slot_bytes = ups * unit_bytes;
+    p->stage_out = static_cast<char*>(d->dev_staging);
+    p->stage_in = static_cast<char*>(d->dev_staging) + half;
+    while ((1ull << p->idbits) < p->N) p->idbits++;
+
+    DeviceGuard g(p->device);
+    hipError_t e = hipSuccess;
+#define CREATE_TRY(expr)                                          \
+    do {                                                          \
+        e = (expr);                                               \
+        if (e != hipSuccess) {                                    \
+            ss_status st = hip_fail(nullptr, e, #expr, false);    \
+            free_pool(p);                                         \
+            return st;                                            \
+        }                                                         \
+    } while (0)
+
+    const u64 N = p->N, U = p->U;
+    const unsigned npad = pow2ceil_u(p->N);
+    p->occ_words = (unsigned)((U + 31) / 32);
+    CREATE_TRY(dalloc(&p->d_units, N));
+    CREATE_TRY(dalloc(&p->d_agent_off, N + 1));
+    CREATE_TRY(dalloc(&p->d_bt, total_units));
+    CREATE_TRY(dalloc(&p->d_resident, N));
+    CREATE_TRY(dalloc(&p->d_occ, p->occ_words));
+    CREATE_TRY(dalloc(&p->d_cnt, 1));
+    CREATE_TRY(dalloc(&p->d_listE, N));
+    CREATE_TRY(dalloc(&p->d_listC, N));
+    CREATE_TRY(dalloc(&p->d_listL, N));
+    CREATE_TRY(dalloc(&p->d_sortE, npad));
+    CREATE_TRY(dalloc(&p->d_sortC, npad));
+    CREATE_TRY(dalloc(&p->d_sortL, npad));
+    CREATE_TRY(dalloc(&p->d_prefE, N + 1));
+    CREATE_TRY(dalloc(&p->d_prefC, N + 1));
+    CREATE_TRY(dalloc(&p->d_loff, N + 1));
+    CREATE_TRY(dalloc(&p->d_victims, N));
+    CREATE_TRY(dalloc(&p->d_loads, N));
+    CREATE_TRY(dalloc(&p->d_vunits, U));
+    CREATE_TRY(dalloc(&p->d_lunits, U));
+    CREATE_TRY(dalloc(&p->d_free_old, U));
+    CREATE_TRY(dalloc(&p->d_res, 1));
+    CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_res), sizeof(PlanResult),
+                             hipHostMallocMapped));
+    CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_victims), N * sizeof(unsigned),
+                             hipHostMallocMapped));
+    CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_loads), N * sizeof(unsigned),
+                             hipHostMallocMapped));
+    CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_res_dev), p->h_res, 0));
+    CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_victims_dev), p->h_victims, 0));
+    CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_loads_dev), p->h_loads, 0));
+
+    // copy items: pieces of at most kItemBytes, plane by plane
+    std::vector<CopyItem> items;
+    u64 plane_off = 0;
+    for (uint32_t c = 0; c < p->P; ++c) {
+        for (u64 off = 0; off < p->chunk_bytes[c]; off += kItemBytes) {
+            CopyItem it;
+            it.plane = c;
+            it.len = (unsigned)std::min<u64>(kItemBytes, p->chunk_bytes[c] - off);
+            it.chunk_off = off;
+            it.unit_off = plane_off + off;
+            items.push_back(it);
+        }
+        plane_off += p->chunk_bytes[c];
+    }
+    p->n_items = (unsigned)items.size();
+    CREATE_TRY(dalloc(&p->d_items, items.size()));
+    CREATE_TRY(dalloc(&p->d_plane_base, p->P));
+    CREATE_TRY(dalloc(&p->d_chunk_bytes, p->P));
+
+    std::vector<u64> agent_off(N + 1, 0);
+    for (u64 a = 0; a < N; ++a) agent_off[a + 1] = agent_off[a] + p->s[a];
+    std::vector<int> bt(total_units, -1);
+    std::vector<unsigned> occ(p->occ_words, 0u);
+    if (U % 32) occ.back() = ~((1u << (U % 32)) - 1u);       // units >= U never free
+    std::vector<u64> bases(p->P);
+    for (uint32_t c = 0; c < p->P; ++c) bases[c] = reinterpret_cast<u64>(d->plane_base[c]);
+    std::vector<unsigned char> zeros_n(N, 0);
+    PlanCounters zc{};
+    CREATE_TRY(hipMemcpy(p->d_units, p->s.data(), N * sizeof(unsigned), hipMemcpyHostToDevice));
+    CREATE_TRY(hipMemcpy(p->d_agent_off, agent_off.data(), (N + 1) * sizeof(u64),
+                         hipMemcpyHostToDevice));
+    CREATE_TRY(hipMemcpy(p->d_bt, bt.data(), total_units * sizeof(int), hipMemcpyHostToDevice));
+    CREATE_TRY(hipMemcpy(p->d_occ, occ.data(), occ.size() * sizeof(unsigned), hipMemcpyHostToDevice));
+    CREATE_TRY(hipMemcpy(p->d_resident, zeros_n.data(), N, hipMemcpyHostToDevice));
+    CREATE_TRY(hipMemcpy(p->d_cnt, &zc, sizeof zc, hipMemcpyHostToDevice));
+    CREATE_TRY(hipMemcpy(p->d_items, items.data(), items.size() * sizeof(CopyItem),
+                         hipMemcpyHostToDevice));
+    CREATE_TRY(hipMemcpy(p->d_plane_base, bases.data(), p->P * sizeof(u64), hipMemcpyHostToDevice));
+    CREATE_TRY(hipMemcpy(p->d_chunk_bytes, p->chunk_bytes.data(), p->P * sizeof(u64),
+                         hipMemcpyHostToDevice));
+
+    for (hipStream_t* s : {&p->st_plan, &p->st_pack, &p->st_d2h, &p->st_h2d, &p->st_unpack})
+        CREATE_TRY(hipStreamCreateWithFlags(s, hipStreamNonBlocking));
+    for (hipEvent_t* ev : {&p->ev_planned, &p->ev_bt, &p->ev_caller, &p->ev_d2h_done,
+                           &p->ev_unpack_done})
+        CREATE_TRY(make_event(ev, false));
+    for (auto* v : {&p->ev_out_free, &p->ev_in_ready, &p->ev_in_free}) {
+        v->resize(p->ring, nullptr);
+        for (auto& ev : *v) {
+            CREATE_TRY(make_event(&ev, false));
+            CREATE_TRY(hipEventRecord(ev, p->st_plan));
+        }
+    }
+    if (p->flags & SS_FLAG_TIMING)
+        for (TimedPair* tp : {&p->t_d2h, &p->t_h2d, &p->t_plan}) {
+            CREATE_TRY(make_event(&tp->a, true));
+            CREATE_TRY(make_event(&tp->b, true));
+        }
+    CREATE_TRY(hipEventRecord(p->ev_d2h_done, p->st_plan));
+    CREATE_TRY(hipEventRecord(p->ev_unpack_done, p->st_plan));
+    CREATE_TRY(hipStreamSynchronize(p->st_plan));
+#undef CREATE_TRY
+    *out = p;
+    return SS_OK;
+}
+
+void ss_pool_destroy(ss_pool* p) { free_pool(p); }
+
+ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* active,
+                       const ss_plan_params* params, ss_plan* out, void* stream) {
+    ss_status st = check_usable(p);
+    if (st) return st;
+    if (!distances || !active || !params || !out)
+        return set_err(SS_ERR_ARG, "distances, active, params and out are required");
+    if (p->state != kIdle)
+        return set_err(SS_ERR_ORDER, "previous step not finished: call ss_evict_pack and "
+                                     "ss_prefetch_unpack before the next ss_plan_step");
+    DeviceGuard g(p->device);
+    if (!device_range_ok(distances, (u64)p->N * 4, p->device) ||
+        !device_range_ok(active, (u64)p->N, p->device))
+        return set_err(SS_ERR_ARG, "distances [N] and active [N] must be device memory of "
+                                   "device %d", p->device);
+    hipStream_t caller = static_cast<hipStream_t>(stream);
+
+    TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_plan, p->ev_caller, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_plan, p->ev_d2h_done, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_plan, p->ev_unpack_done, 0), true);
+
+    PlanArgs A{};
+    A.dist = distances;
+    A.active = active;
+    A.resident = p->d_resident;
+    A.units = p->d_units;
+    A.n = p->N;
+    A.idbits = p->idbits;
+    A.threshold = params->threshold;
+    A.budget = params->budget_units;
+    A.capacity = p->U;
+    A.cnt = p->d_cnt;
+    A.listE = p->d_listE;
+    A.listC = p->d_listC;
+    A.listL = p->d_listL;
+    A.sortE = p->d_sortE;
+    A.sortC = p->d_sortC;
+    A.sortL = p->d_sortL;
+    A.prefE = p->d_prefE;
+    A.prefC = p->d_prefC;
+    A.loff = p->d_loff;
+    A.victims = p->d_victims;
+    A.loads = p->d_loads;
+    A.occ = p->d_occ;
+    A.occ_words = p->occ_words;
+    A.free_old = p->d_free_old;
+    A.res = p->d_res;
+    A.res_host = p->h_res_dev;
+    A.victims_host = p->h_victims_dev;
+    A.loads_host = p->h_loads_dev;
+
+    const bool timing = p->flags & SS_FLAG_TIMING;
+    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.a, p->st_plan), true);
+    TRY_HIP(p, launch_classify(A, p->st_plan), true);
+    TRY_HIP(p, launch_plan_core(A, p->st_plan), true);
+    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.b, p->st_plan), true);
+    TRY_HIP(p, hipEventRecord(p->ev_planned, p->st_plan), true);
+
+    BtArgs B{};
+    B.res = p->d_res;
+    B.victims = p->d_victims;
+    B.loads = p->d_loads;
+    B.units = p->d_units;
+    B.agent_off = p->d_agent_off;
+    B.bt = p->d_bt;
+    B.occ = p->d_occ;
+    B.voff = p->d_prefE;
+    B.loff = p->d_loff;
+    B.free_old = p->d_free_old;
+    B.vunits = p->d_vunits;
+    B.lunits = p->d_lunits;
+    B.capacity = p->U;
+    TRY_HIP(p, launch_bt_update(B, p->N, p->st_plan), true);
+    TRY_HIP(p, hipEventRecord(p->ev_bt, p->st_plan), true);
+
+    TRY_HIP(p, hipEventSynchronize(p->ev_planned), true);
+    // the previous step finished before the plan kernels ran
+    collect_timing(p);
+    if (timing) p->t_plan_used = true;
+
+    const PlanResult r = *p->h_res;
+    if (r.status == 1) {
+        return set_err(SS_ERR_OVERCOMMIT, "active agents need more than %llu units",
+                       (unsigned long long)p->U);
+    }
+    p->res = r;
+    p->voff.resize(r.n_victims + 1);
+    p->loff.resize(r.n_loads + 1);
+    p->voff[0] = 0;
+    for (unsigned i = 0; i < r.n_victims; ++i) p->voff[i + 1] = p->voff[i] + p->s[p->h_victims[i]];
+    p->loff[0] = 0;
+    for (unsigned i = 0; i < r.n_loads; ++i) p->loff[i + 1] = p->loff[i] + p->s[p->h_loads[i]];
+
+    ss_plan& pl = p->plan;
+    pl.n_victims = r.n_victims;
+    pl.n_loads = r.n_loads;
+    pl.n_demand = r.n_demand;
+    pl.n_demand_victims = r.n_demand_victims;
+    pl.victims = p->h_victims;
+    pl.loads = p->h_loads;
+    pl.units_out = r.units_out;
+    pl.units_in = r.units_in;
+    pl.bytes_out = r.units_out * p->unit_bytes;
+    pl.bytes_in = r.units_in * p->unit_bytes;
+    *out = pl;
+    p->state = kPlanned;
+    p->stats.steps++;
+    return SS_OK;
+}
+
+ss_status ss_evict_pack(ss_pool* p, void* stream) {
+    ss_status st = check_usable(p);
+    if (st) return st;
+    if (p->state != kPlanned) return set_err(SS_ERR_ORDER, "ss_evict_pack must follow ss_plan_step");
+    DeviceGuard g(p->device);
+    hipStream_t caller = static_cast<hipStream_t>(stream);
+    const bool timing = p->flags & SS_FLAG_TIMING;
+    TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_pack, p->ev_caller, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_pack, p->ev_bt, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_d2h, p->ev_caller, 0), true);
+
+    const u64 total = p->res.units_out;
+    const u64 ups = p->units_per_slot;
+    const u64 nslots = (total + ups - 1) / ups;
+    while (p->ev_packed.size() < nslots) {
+        hipEvent_t ev;
+        TRY_HIP(p, make_event(&ev, false), true);
+        p->ev_packed.push_back(ev);
+    }
+    CopyArgs C{};
+    C.units_list = p->d_vunits;
+    C.items = p->d_items;
+    C.n_items = p->n_items;
+    C.plane_base = p->d_plane_base;
+    C.chunk_bytes = p->d_chunk_bytes;
+    C.unit_bytes = p->unit_bytes;
+    C.capacity = p->U;
+    size_t vi = 0;
+    for (u64 k = 0; k < nslots; ++k) {
+        const unsigned r = (unsigned)(k % p->ring);
+        const u64 p0 = k * ups, p1 = std::min(total, p0 + ups);
+        char* slot = p->stage_out + (u64)r * p->slot_bytes;
+        TRY_HIP(p, hipStreamWaitEvent(p->st_pack, p->ev_out_free[r], 0), true);
+        C.first = p0;
+        C.count = p1 - p0;
+        C.staging = slot;
+        TimedPair* tp = nullptr;
+        if (timing) {
+            TRY_HIP(p, timed_pair(p->t_pack, p->n_t_pack, &tp), true);
+            p->n_t_pack++;
+            tp->bytes = (p1 - p0) * p->unit_bytes;
+            TRY_HIP(p, hipEventRecord(tp->a, p->st_pack), true);
+        }
+        TRY_HIP(p, launch_pack(C, p->st_pack), true);
+        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_pack), true);
+        TRY_HIP(p, hipEventRecord(p->ev_packed[k], p->st_pack), true);
+        TRY_HIP(p, hipStreamWaitEvent(p->st_d2h, p->ev_packed[k], 0), true);
+        if (timing && k == 0) {
+            TRY_HIP(p, hipEventRecord(p->t_d2h.a, p->st_d2h), true);
+            p->t_d2h_used = true;
+            p->t_d2h.bytes = total * p->unit_bytes;
+        }
+        // each victim's bytes inside [p0, p1) go to its host copy
+        while (vi < p->res.n_victims && p->voff[vi + 1] <= p0) vi++;
+        for (size_t i = vi; i < p->res.n_victims && p->voff[i] < p1; ++i) {
+            const u64 lo = std::max(p0, p->voff[i]), hi = std::min(p1, p->voff[i + 1]);
+            const unsigned v = p->h_victims[i];
+            char* dst = p->host + p->host_off[v] + (lo - p->voff[i]) * p->unit_bytes;
+            const char* src = slot + (lo - p0) * p->unit_bytes;
+            TRY_HIP(p, hipMemcpyAsync(dst, src, (hi - lo) * p->unit_bytes, hipMemcpyDeviceToHost,
+                                      p->st_d2h), true);
+        }
+        TRY_HIP(p, hipEventRecord(p->ev_out_free[r], p->st_d2h), true);
+    }
+    if (timing && nslots > 0) TRY_HIP(p, hipEventRecord(p->t_d2h.b, p->st_d2h), true);
+    TRY_HIP(p, hipEventRecord(p->ev_d2h_done, p->st_d2h), true);
+    p->state = kPacked;
+    return SS_OK;
+}
+
+ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
+    ss_status st = check_usable(p);
+    if (st) return st;
+    if (p->state != kPacked)
+        return set_err(SS_ERR_ORDER, "ss_prefetch_unpack must follow ss_evict_pack");
+    DeviceGuard g(p->device);
+    hipStream_t caller = static_cast<hipStream_t>(stream);
+    const bool timing = p->flags & SS_FLAG_TIMING;
+    TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_h2d, p->ev_caller, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_unpack, p->ev_caller, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_unpack, p->ev_bt, 0), true);
+
+    const u64 total = p->res.units_in;
+    const u64 ups = p->units_per_slot;
+    const u64 nslots = (total + ups - 1) / ups;
+    const u64 nF = p->res.n_free_used;
+    CopyArgs C{};
+    C.units_list = p->d_lunits;
+    C.items = p->d_items;
+    C.n_items = p->n_items;
+    C.plane_base = p->d_plane_base;
+    C.chunk_bytes = p->d_chunk_bytes;
+    C.unit_bytes = p->unit_bytes;
+    C.capacity = p->U;
+    size_t li = 0;
+    for (u64 k = 0; k < nslots; ++k) {
+        const unsigned r = (unsigned)(k % p->ring);
+        const u64 q0 = k * ups, q1 = std::min(total, q0 + ups);
+        char* slot = p->stage_in + (u64)r * p->slot_bytes;
+        TRY_HIP(p, hipStreamWaitEvent(p->st_h2d, p->ev_in_free[r], 0), true);
+        if (timing && k == 0) {
+            TRY_HIP(p, hipEventRecord(p->t_h2d.a, p->st_h2d), true);
+            p->t_h2d_used = true;
+            p->t_h2d.bytes = total * p->unit_bytes;
+        }
+        while (li < p->res.n_loads && p->loff[li + 1] <= q0) li++;
+        for (size_t i = li; i < p->res.n_loads && p->loff[i] < q1; ++i) {
+            const u64 lo = std::max(q0, p->loff[i]), hi = std::min(q1, p->loff[i + 1]);
+            const unsigned a = p->h_loads[i];
+            const char* src = p->host + p->host_off[a] + (lo - p->loff[i]) * p->unit_bytes;
+            char* dst = slot + (lo - q0) * p->unit_bytes;
+            TRY_HIP(p, hipMemcpyAsync(dst, src, (hi - lo) * p->unit_bytes, hipMemcpyHostToDevice,
+                                      p->st_h2d), true);
+        }
+        TRY_HIP(p, hipEventRecord(p->ev_in_ready[r], p->st_h2d), true);
+        TRY_HIP(p, hipStreamWaitEvent(p->st_unpack, p->ev_in_ready[r], 0), true);
+        // units released by victims are overwritten only after the pack read them
+        const u64 last = q1 - 1;
+        if (last >= nF) {
+            const u64 kv = (last - nF) / ups;
+            TRY_HIP(p, hipStreamWaitEvent(p->st_unpack, p->ev_packed[kv], 0), true);
+        }
+        C.first = q0;
+        C.count = q1 - q0;
+        C.staging = slot;
+        TimedPair* tp = nullptr;
+        if (timing) {
+            TRY_HIP(p, timed_pair(p->t_unpack, p->n_t_unpack, &tp), true);
+            p->n_t_unpack++;
+            tp->bytes = (q1 - q0) * p->unit_bytes;
+            TRY_HIP(p, hipEventRecord(tp->a, p->st_unpack), true);
+        }
+        TRY_HIP(p, launch_unpack(C, p->st_unpack), true);
+        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_unpack), true);
+        TRY_HIP(p, hipEventRecord(p->ev_in_free[r], p->st_unpack), true);
+    }
+    if (timing && nslots > 0) TRY_HIP(p, hipEventRecord(p->t_h2d.b, p->st_h2d), true);
+    TRY_HIP(p, hipEventRecord(p->ev_unpack_done, p->st_unpack), true);
+    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_unpack_done, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_d2h_done, 0), true);
+    p->state = kIdle;
+    return SS_OK;
+}
+
+ss_status ss_block_table(ss_pool* p, const int32_t** d_units, const uint64_t** d_agent_off) {
+    if (!p || !d_units || !d_agent_off) return set_err(SS_ERR_ARG, "NULL argument");
+    *d_units = p->d_bt;
+    *d_agent_off = reinterpret_cast<const uint64_t*>(p->d_agent_off);
+    return SS_OK;
+}
+
+ss_status ss_block_table_host(ss_pool* p, uint32_t agent, int32_t* out, uint32_t cap, uint32_t* n) {
+    ss_status st = check_usable(p);
+    if (st) return st;
+    if (!out || !n || agent >= p->N) return set_err(SS_ERR_ARG, "bad agent or NULL output");
+    const uint32_t s = p->s[agent];
+    *n = s;
+    if (cap < s) return set_err(SS_ERR_ARG, "cap %u < %u units", cap, s);
+    DeviceGuard g(p->device);
+    u64 off = 0;
+    for (uint32_t a = 0; a < agent; ++a) off += p->s[a];
+    TRY_HIP(p, hipStreamSynchronize(p->st_plan), false);
+    TRY_HIP(p, hipMemcpy(out, p->d_bt + off, s * sizeof(int32_t), hipMemcpyDeviceToHost), false);
+    return SS_OK;
+}
+
+ss_status ss_block_table_host_all(ss_pool* p, int32_t* out, uint64_t cap, uint64_t* n) {
+    ss_status st = check_usable(p);
+    if (st) return st;
+    if (!out || !n) return set_err(SS_ERR_ARG, "NULL output");
+    u64 total = 0;
+    for (uint32_t a = 0; a < p->N; ++a) total += p->s[a];
+    *n = total;
+    if (cap < total) return set_err(SS_ERR_ARG, "cap %llu < %llu entries", (unsigned long long)cap,
+                                    (unsigned long long)total);
+    DeviceGuard g(p->device);
+    TRY_HIP(p, hipStreamSynchronize(p->st_plan), false);
+    TRY_HIP(p, hipMemcpy(out, p->d_bt, total * sizeof(int32_t), hipMemcpyDeviceToHost), false);
+    return SS_OK;
+}
+
+ss_status ss_resident_host(ss_pool* p, uint8_t* out) {
+    ss_status st = check_usable(p);
+    if (st) return st;
+    if (!out) return set_err(SS_ERR_ARG, "NULL output");
+    DeviceGuard g(p->device);
+    TRY_HIP(p, hipStreamSynchronize(p->st_plan), false);
+    TRY_HIP(p, hipMemcpy(out, p->d_resident, p->N, hipMemcpyDeviceToHost), false);
+    return SS_OK;
+}
+
+ss_status ss_get_stats(ss_pool* p, ss_stats* out) {
+    if (!p || !out) return set_err(SS_ERR_ARG, "NULL argument");
+    DeviceGuard g(p->device);
+    for (hipStream_t s : {p->st_plan, p->st_pack, p->st_d2h, p->st_h2d, p->st_unpack})
+        TRY_HIP(p, hipStreamSynchronize(s), false);
+    collect_timing(p);
+    *out = p->stats;
+    return SS_OK;
+}
+
+ss_status ss_reset_stats(ss_pool* p) {
+    if (!p) return set_err(SS_ERR_ARG, "NULL pool");
+    DeviceGuard g(p->device);
+    for (hipStream_t s : {p->st_plan, p->st_pack, p->st_d2h, p->st_h2d, p->st_unpack})
+        TRY_HIP(p, hipStreamSynchronize(s), false);
+    collect_timing(p);
+    p->stats = ss_stats{};
+    return SS_OK;
+}
+
+ss_status ss_probe_copy(void* dst, const void* src, uint64_t bytes, int iters, float* ms) {
+    if (!dst || !src || !ms || iters < 1 || bytes == 0 || bytes % 16)
+        return set_err(SS_ERR_ARG, "bad probe arguments");
+    hipEvent_t a, b;
+    TRY_HIP(nullptr, make_event(&a, true), false);
+    TRY_HIP(nullptr, make_event(&b, true), false);
+    hipStream_t s;
+    TRY_HIP(nullptr, hipStreamCreateWithFlags(&s, hipStreamNonBlocking), false);
+    hipError_t e = launch_probe_copy(dst, src, bytes, s);                 // warm-up
+    if (e == hipSuccess) e = hipEventRecord(a, s);
+    for (int i = 0; i < iters && e == hipSuccess; ++i) e = launch_probe_copy(dst, src, bytes, s);
+    if (e == hipSuccess) e = hipEventRecord(b, s);
+    if (e == hipSuccess) e = hipEventSynchronize(b);
+    float t = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, a, b);
+    (void)hipStreamDestroy(s);
+    (void)hipEventDestroy(a);
+    (void)hipEventDestroy(b);
+    if (e != hipSuccess) return hip_fail(nullptr, e, "probe copy", false);
+    *ms = t / iters;
+    return SS_OK;
+}
+
+ss_status ss_probe_link(void* host, void* dev, uint64_t bytes, int dir, int iters, float* ms) {
+    if (!host || !dev || !ms || iters < 1 || bytes == 0 || dir < 0 || dir > 2)
+        return set_err(SS_ERR_ARG, "bad probe arguments");
+    hipEvent_t a, b, c;
+    hipStream_t s1, s2;
+    TRY_HIP(nullptr, make_event(&a, true), false);
+    TRY_HIP(nullptr, make_event(&b, true), false);
+    TRY_HIP(nullptr, make_event(&c, false), false);
+    TRY_HIP(nullptr, hipStreamCreateWithFlags(&s1, hipStreamNonBlocking), false);
+    TRY_HIP(nullptr, hipStreamCreateWithFlags(&s2, hipStreamNonBlocking), false);
+    char* h = static_cast<char*>(host);
+    char* d = static_cast<char*>(dev);
+    hipError_t e = hipSuccess;
+    auto issue = [&](hipStream_t st, int which) {
+        if (which == 0) return hipMemcpyAsync(d, h, bytes, hipMemcpyHostToDevice, st);
+        return hipMemcpyAsync(h + (dir == 2 ? bytes : 0), d + (dir == 2 ? bytes : 0), bytes,
+                              hipMemcpyDeviceToHost, st);
+    };
+    for (int w = 0; w < 2 && e == hipSuccess; ++w) {               // warm-up, then timed
+        if (e == hipSuccess) e = hipEventRecord(a, s1);
+        if (e == hipSuccess) e = hipStreamWaitEvent(s2, a, 0);
+        for (int i = 0; i < (w ? iters : 1) && e == hipSuccess; ++i) {
+            if (dir == 0 || dir == 2) e = issue(s1, 0);
+            if (e == hipSuccess && dir == 1) e = issue(s1, 1);
+            if (e == hipSuccess && dir == 2) e = issue(s2, 1);
+        }
+        if (e == hipSuccess) e = hipEventRecord(c, s2);
+        if (e == hipSuccess) e = hipStreamWaitEvent(s1, c, 0);
+        if (e == hipSuccess) e = hipEventRecord(b, s1);
+        if (e == hipSuccess) e = hipEventSynchronize(b);
+    }
+    float t = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, a, b);
+    (void)hipStreamDestroy(s1);
+    (void)hipStreamDestroy(s2);
+    (void)hipEventDestroy(a);
+    (void)hipEventDestroy(b);
+    (void)hipEventDestroy(c);
+    if (e != hipSuccess) return hip_fail(nullptr, e, "probe link", false);
+    *ms = t / iters;
+    return SS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,146 @@
+"""Side-by-side replay of a trace through the HIP library and the CPU oracle.
+
+Used by the GPU parity tests and by ``__graft_entry__.smoke``.  Each step
+compares, exactly: victims (eviction order), loads (demand then prefetch),
+counts, unit totals, the whole block table, the resident flags, the bytes
+written back to every victim's host copy, and the bytes of resident units in
+the device pool (all of them or a seeded sample)."""
+from __future__ import annotations
+
+import sys
+import time
+
+import numpy as np
+import torch
+
+import workloads as W
+from oracle import OraclePool
+from paper_2601_21473_amd import binding as B
+from paper_2601_21473_amd.memory import PoolMemory
+
+S = W.SENTINEL
+POISON = 0xA5
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def upload_trace(trace, device=0):
+    dev = torch.device("cuda", device)
+    dist = torch.from_numpy(np.ascontiguousarray(trace.dist).view(np.int32)).to(dev)
+    act = torch.from_numpy(np.ascontiguousarray(trace.active)).to(dev)
+    torch.cuda.synchronize()
+    return dist, act
+
+
+def fill_host(mem, content, spec, batch_bytes=256 << 20):
+    """Every agent's host copy := its content (agent, unit, plane order)."""
+    units = spec.agent_units.astype(np.int64)
+    N = len(units)
+    batch_units = max(1, batch_bytes // spec.unit_bytes)
+    a0 = 0
+    while a0 < N:
+        a1 = a0
+        tot = 0
+        while a1 < N and (tot == 0 or tot + units[a1] <= batch_units):
+            tot += units[a1]
+            a1 += 1
+        A = np.repeat(np.arange(a0, a1), units[a0:a1])
+        J = np.concatenate([np.arange(k) for k in units[a0:a1]])
+        data = content.units_bytes(A, J).reshape(-1)
+        off = int(mem.host_off[a0])
+        mem.host_np[off:off + len(data)] = data
+        a0 = a1
+
+
+def device_units(mem, spec, units):
+    """uint8 [K, unit_bytes] of the given physical units, read from the device."""
+    idx = torch.as_tensor(np.asarray(units, dtype=np.int64), device=mem.planes[0].device)
+    parts = []
+    for c, cb in enumerate(spec.chunk_bytes):
+        parts.append(mem.planes[c].view(spec.capacity_units, cb).index_select(0, idx))
+    return torch.cat(parts, dim=1).cpu().numpy()
+
+
+def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_bytes=True,
+               slot_units=8, ring_slots=2, sample_units=None, bt_every=1, seed=0, label=""):
+    spec = trace.pools[pool_index]
+    ub = spec.unit_bytes
+    staging_bytes = 2 * ring_slots * slot_units * ub
+    log(f"[parity] {label or trace.name} pool={spec.name} N={trace.n_agents} "
+        f"U={spec.capacity_units} unit={ub}B planes={spec.n_planes} theta={theta} "
+        f"budget={budget} slot_units={slot_units} ring={ring_slots}")
+    mem = PoolMemory(spec, staging_bytes, ring_slots)
+    content = W.Content(spec, seed=seed, pool_index=pool_index)
+    if check_bytes:
+        fill_host(mem, content, spec)
+    pool = mem.make_pool(timing=True)
+    opool = OraclePool(spec.capacity_units, spec.agent_units, ub)
+    dist, act = upload_trace(trace)
+    T = trace.n_steps if steps is None else steps
+    stream = torch.cuda.current_stream().cuda_stream
+    rng = np.random.default_rng(seed + 99)
+    units_i64 = spec.agent_units.astype(np.int64)
+    moved = 0
+    t0 = time.time()
+    for t in range(T):
+        g = pool.plan_step(dist[t].data_ptr(), act[t].data_ptr(), theta, budget, stream)
+        o = opool.plan_step(trace.dist[t], trace.active[t], theta, budget)
+        assert g["victims"].tolist() == o.victims.tolist(), (label, t, "victims")
+        assert g["loads"].tolist() == o.loads.tolist(), (label, t, "loads")
+        assert g["n_demand"] == o.n_demand, (label, t)
+        assert g["n_demand_victims"] == o.n_demand_victims, (label, t)
+        assert g["units_out"] == o.units_out and g["units_in"] == o.units_in, (label, t)
+        assert g["bytes_out"] == o.bytes_out and g["bytes_in"] == o.bytes_in, (label, t)
+        pool.evict_pack(stream)
+        pool.prefetch_unpack(stream)
+        torch.cuda.synchronize()
+        moved += o.units_in + o.units_out
+        if t % bt_every == 0 or t == T - 1:
+            bt = pool.block_table_host_all()
+            obt = np.concatenate(opool.bt)
+            assert np.array_equal(bt, obt.astype(np.int32)), (label, t, "block table")
+            assert np.array_equal(pool.resident_host().astype(bool), opool.resident), (label, t)
+        if check_bytes:
+            for v in o.victims:
+                v = int(v)
+                exp = content.units_bytes(np.full(units_i64[v], v), np.arange(units_i64[v]))
+                assert np.array_equal(mem.host_copy(v), exp.reshape(-1)), (label, t, "host", v)
+            res = np.flatnonzero(opool.resident)
+            if len(res):
+                A = np.repeat(res, units_i64[res])
+                J = np.concatenate([np.arange(units_i64[a]) for a in res])
+                U = np.concatenate([opool.bt[a] for a in res])
+                if sample_units is not None and len(U) > sample_units:
+                    pick = rng.choice(len(U), sample_units, replace=False)
+                    A, J, U = A[pick], J[pick], U[pick]
+                got = device_units(mem, spec, U)
+                exp = content.units_bytes(A, J)
+                bad = np.flatnonzero((got != exp).any(axis=1))
+                assert len(bad) == 0, (label, t, "device bytes", A[bad[:4]], J[bad[:4]])
+            for a in o.loads:             # a resident agent's host copy is stale by design
+                mem.host_copy(int(a))[:] = POISON
+    st = pool.stats()
+    pool.close()
+    log(f"[parity] {label or trace.name}: {T} steps ok, {moved} units moved, "
+        f"{time.time() - t0:.1f}s")
+    return st
+
+
+def synthetic_trace(n_agents, capacity_units, n_steps, k_active, seed, units=None,
+                    chunk_bytes=(32, 16), noisy=False):
+    """A uniform random activation trace for edge cases."""
+    rng = np.random.default_rng(seed)
+    active = np.zeros((n_steps, n_agents), dtype=np.uint8)
+    for t in range(n_steps):
+        k = int(k_active(t, rng)) if callable(k_active) else int(k_active)
+        if k:
+            active[t, rng.choice(n_agents, k, replace=False)] = 1
+    if units is None:
+        units = np.ones(n_agents, dtype=np.uint32)
+    pool = W.PoolSpec("syn", capacity_units, list(chunk_bytes), np.asarray(units, np.uint32))
+    dt = W.exact_distances(active)
+    dist = W.noisy_distances(dt, 2.0, rng) if noisy else dt.copy()
+    return W.Trace(f"syn{n_agents}", n_agents, n_steps, [pool], active, dist, dt, {})

@@ -1,0 +1,165 @@
+"""HIP path against the CPU oracle, bit for bit, through the C ABI.
+
+Every comparison is exact (tolerance 0): all of the path is integer indexing
+and byte movement.  Cases:
+  * the tiny workload at full size, seeds 0-4, thresholds 0 / 2 / none;
+  * all five workloads at their full agent counts and pool capacities, every
+    step, with the chunk sizes shrunk so that every agent's host copy fits
+    (the plan does not depend on chunk sizes; bytes are still checked for
+    every resident unit);
+  * the real unit layouts (64 x 32 KiB KV pages, 448-plane LoRA adapters,
+    512 KiB unified units) on agent subsets, with sampled byte checks;
+  * edge cases: one-unit ring slots, no prefetch, budgets, an agent count
+    that is not a multiple of the wave or block size, lists larger than the
+    plan kernel's LDS sort buffer, empty steps, overcommit and call order."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from gpu_harness import run_parity, synthetic_trace, upload_trace, log
+from paper_2601_21473_amd import binding as B
+from paper_2601_21473_amd.memory import PoolMemory
+
+pytestmark = pytest.mark.gpu
+S = W.SENTINEL
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    B.load()
+
+
+def small(trace, planes=(32, 48)):
+    return W.shrink_planes(trace, lambda p: list(planes))
+
+
+@pytest.mark.parametrize("seed", range(5))
+@pytest.mark.parametrize("theta", [0, 2, S])
+def test_tiny_full_size(seed, theta):
+    run_parity(W.make_trace("tiny", seed), theta=theta, slot_units=3, ring_slots=2,
+               label=f"tiny s{seed} t{theta}")
+
+
+def test_tiny_one_unit_slots():
+    st = run_parity(W.make_trace("tiny", 1), theta=S, slot_units=1, ring_slots=1,
+                    label="tiny one-unit ring")
+    assert st["pack_launches"] > 100 and st["unpack_launches"] > 100
+
+
+@pytest.mark.parametrize("name,pool_index", [("roundrobin", 0), ("bursty", 0), ("zipf_lora", 0),
+                                             ("zipf_lora", 1), ("diffusion", 0)])
+def test_workload_full_counts(name, pool_index):
+    tr = small(W.make_trace(name, 0))
+    sample = 20000 if name == "diffusion" else None
+    run_parity(tr, pool_index=pool_index, theta=S, slot_units=4096, ring_slots=2,
+               sample_units=sample, label=f"{name}[{pool_index}] full counts")
+
+
+@pytest.mark.parametrize("name,theta,budget", [("roundrobin", 0, None), ("bursty", 0, None),
+                                               ("bursty", S, 500), ("roundrobin", 4, 300),
+                                               ("diffusion", 3, None)])
+def test_workload_thresholds_and_budgets(name, theta, budget):
+    tr = small(W.make_trace(name, 1), planes=(16,))
+    steps = 150 if name == "diffusion" else None
+    run_parity(tr, theta=theta, budget=budget, steps=steps, slot_units=2048, ring_slots=3,
+               sample_units=5000, label=f"{name} t{theta} b{budget}")
+
+
+@pytest.mark.parametrize("name,n_agents,steps,pool_index", [
+    ("roundrobin", 40, 60, 0),     # 64 planes x 32 KiB
+    ("bursty", 150, 40, 0),        # same unit, lognormal sizes
+    ("zipf_lora", 40, 60, 1),      # 448 planes of 32-448 KiB, 80 MiB units
+    ("diffusion", 150, 40, 0),     # one 512 KiB plane
+])
+def test_real_layouts(name, n_agents, steps, pool_index):
+    tr = W.subsample_agents(W.make_trace(name, 0), n_agents)
+    spec = tr.pools[pool_index]
+    slot_units = max(1, (256 << 20) // spec.unit_bytes)
+    run_parity(tr, pool_index=pool_index, theta=S, steps=steps, slot_units=slot_units,
+               ring_slots=3, sample_units=48, label=f"{name} layout sub{n_agents}")
+
+
+def test_ragged_agent_count_and_sizes():
+    rng = np.random.default_rng(5)
+    units = rng.integers(1, 9, size=1037).astype(np.uint32)
+    tr = synthetic_trace(1037, 900, 60, lambda t, r: r.integers(0, 60), seed=5, units=units,
+                         noisy=True)
+    run_parity(tr, theta=S, slot_units=37, ring_slots=2, label="ragged 1037")
+    run_parity(tr, theta=5, budget=40, slot_units=37, ring_slots=2, label="ragged 1037 t5 b40")
+
+
+def test_lists_beyond_lds_sort_buffer():
+    # 40,000 unit-size agents, room for 20,000: the evictable list and the
+    # candidate prefix both exceed the 16,384 keys the plan kernel sorts in LDS
+    tr = synthetic_trace(40000, 20000, 25, 600, seed=11, chunk_bytes=(16,))
+    run_parity(tr, theta=S, slot_units=8192, ring_slots=2, sample_units=4000,
+               label="global sort path")
+
+
+def test_empty_steps_and_idle_pool():
+    tr = synthetic_trace(100, 40, 30, lambda t, r: 0 if t % 3 else r.integers(0, 30), seed=2)
+    run_parity(tr, theta=S, slot_units=5, ring_slots=2, label="empty steps")
+
+
+def test_sentinel_and_extreme_distances():
+    tr = synthetic_trace(300, 120, 40, 20, seed=3, chunk_bytes=(16,))
+    d = tr.dist.copy()
+    rng = np.random.default_rng(3)
+    d[rng.random(d.shape) < 0.2] = S
+    d[rng.random(d.shape) < 0.1] = S - 1
+    tr.dist[:] = d
+    for theta in (S, S - 1, 1):
+        run_parity(tr, theta=theta, slot_units=64, ring_slots=2, label=f"extreme t{theta}")
+
+
+def test_overcommit_and_call_order():
+    units = np.full(8, 3, dtype=np.uint32)
+    tr = synthetic_trace(8, 9, 3, 0, seed=0, units=units)
+    tr.active[0, [0, 1]] = 1
+    tr.active[1, [0, 1, 2, 3]] = 1        # 12 units > 9: overcommit
+    tr.active[2, [2]] = 1
+    spec = tr.pools[0]
+    mem = PoolMemory(spec, 2 * 2 * spec.unit_bytes * 3, 2)
+    pool = mem.make_pool()
+    dist, act = upload_trace(tr)
+    st = torch.cuda.current_stream().cuda_stream
+    with pytest.raises(B.ScaleSimError) as e:
+        pool.evict_pack(st)
+    assert e.value.status == B.SS_ERR_ORDER
+    p0 = pool.plan_step(dist[0].data_ptr(), act[0].data_ptr(), S, None, st)
+    assert p0["loads"].tolist() == [0, 1]
+    with pytest.raises(B.ScaleSimError) as e:
+        pool.plan_step(dist[0].data_ptr(), act[0].data_ptr(), S, None, st)
+    assert e.value.status == B.SS_ERR_ORDER
+    with pytest.raises(B.ScaleSimError) as e:
+        pool.prefetch_unpack(st)
+    assert e.value.status == B.SS_ERR_ORDER
+    pool.evict_pack(st)
+    pool.prefetch_unpack(st)
+    bt_before = pool.block_table_host_all().copy()
+    res_before = pool.resident_host().copy()
+    with pytest.raises(B.OvercommitError):
+        pool.plan_step(dist[1].data_ptr(), act[1].data_ptr(), S, None, st)
+    assert np.array_equal(pool.block_table_host_all(), bt_before)
+    assert np.array_equal(pool.resident_host(), res_before)
+    p2 = pool.plan_step(dist[2].data_ptr(), act[2].data_ptr(), S, None, st)
+    assert p2["n_demand"] == 1 and p2["loads"][0] == 2
+    pool.evict_pack(st)
+    pool.prefetch_unpack(st)
+    torch.cuda.synchronize()
+    pool.close()
+
+
+def test_host_pointer_for_distances_is_rejected():
+    tr = synthetic_trace(16, 8, 1, 2, seed=0)
+    spec = tr.pools[0]
+    mem = PoolMemory(spec, 4 * spec.unit_bytes, 1)
+    pool = mem.make_pool()
+    d = np.ascontiguousarray(tr.dist[0])
+    a = np.ascontiguousarray(tr.active[0])
+    with pytest.raises(B.ScaleSimError) as e:
+        pool.plan_step(d.ctypes.data, a.ctypes.data, S)
+    assert e.value.status == B.SS_ERR_ARG
+    pool.close()

@@ -275,6 +275,21 @@ def shrink_planes(trace: Trace, chunk_bytes_fn) -> Trace:
                  trace.active, trace.dist, trace.dist_true, dict(trace.meta))
 
 
+def subsample_agents(trace: Trace, n_agents: int) -> Trace:
+    """The first ``n_agents`` agents of a workload with every pool's capacity
+    scaled by the same fraction (kept at least as large as the most units the
+    kept agents ever need at once)."""
+    act = trace.active[:, :n_agents]
+    pools = []
+    for p in trace.pools:
+        units = p.agent_units[:n_agents]
+        need = int((act.astype(np.int64) * units.astype(np.int64)[None, :]).sum(1).max())
+        cap = max(need, int(round(p.capacity_units * n_agents / trace.n_agents)), 1)
+        pools.append(PoolSpec(p.name, cap, list(p.chunk_bytes), units))
+    return Trace(trace.name + "_sub%d" % n_agents, n_agents, trace.n_steps, pools, act,
+                 trace.dist[:, :n_agents], trace.dist_true[:, :n_agents], dict(trace.meta))
+
+
 def random_tiny_trace(rng: np.random.Generator, n_agents: int, n_steps: int,
                       max_active: int, capacity_agents: int, units=None):
     """A small random request trace for brute-force checks."""
@@ -342,6 +357,18 @@ class Content:
             lo, hi = self.plane_off[c] // 8, self.plane_off[c + 1] // 8
             out[:, lo:hi] = pat[None, :] ^ self.tag(a, j, c)[:, None]
         return out.reshape(-1).view(np.uint8)
+
+    def units_bytes(self, a: np.ndarray, j: np.ndarray) -> np.ndarray:
+        """Bytes of units (a[k], j[k]) for arrays of agents and logical units:
+        uint8 [K, unit_bytes], planes concatenated in order."""
+        a = np.asarray(a, dtype=np.uint64)
+        j = np.asarray(j, dtype=np.uint64)
+        W = self.pool.unit_bytes // 8
+        out = np.empty((len(a), W), dtype=np.uint64)
+        for c, pat in enumerate(self.patterns):
+            lo, hi = self.plane_off[c] // 8, self.plane_off[c + 1] // 8
+            out[:, lo:hi] = pat[None, :] ^ self.tag(a, j, c)[:, None]
+        return out.view(np.uint8)
 
     def unit_chunk_words0(self, a: np.ndarray, j: np.ndarray, c: int) -> np.ndarray:
         """First 64-bit word of chunk (a, j, c) for arrays of (a, j): a cheap
