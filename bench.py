@@ -37,9 +37,56 @@ WORKLOAD_TEXT = {
 }
 
 
+PMC_KERNELS = {"void ss::k_copy<true>(ss::CopyArgs)": "pack",
+               "void ss::k_copy<false>(ss::CopyArgs)": "unpack"}
+PROBE_KERNEL = "ss::k_probe_copy(char*, char const*, unsigned long long)"
+PROBE_BYTES = 2 << 30          # bytes read and written by the probe copy (see probes())
+COPY_ITEM_BYTES = 32768        # largest piece one wave copies (kItemBytes in the library)
+COPY_BLOCK = 512               # threads per copy block (kCopyThreads)
+
+
 def kernel_source_hash():
     p = os.path.join(ROOT, "paper_2601_21473_amd", "csrc", "ss_kernels.hip")
     return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def summarize_pmc(fetch_csv, write_csv, workload, out_json, commands):
+    """Per-dispatch HBM traffic of the copy kernels from two rocprofv3 --pmc
+    runs (FETCH_SIZE, WRITE_SIZE in KiB), each scaled by the ratio of known
+    bytes to the same counter on the probe's plain copy of PROBE_BYTES."""
+    import csv
+    import collections
+    import workloads as W
+    spec = W.make_trace(workload, 0).pools[0]
+    n_items = sum((c + COPY_ITEM_BYTES - 1) // COPY_ITEM_BYTES for c in spec.chunk_bytes)
+    groups = (n_items + COPY_BLOCK // 64 - 1) // (COPY_BLOCK // 64)
+    vals = {}
+    for path, counter in ((fetch_csv, "FETCH_SIZE"), (write_csv, "WRITE_SIZE")):
+        per = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == counter:
+                per[r["Kernel_Name"]].append((float(r["Counter_Value"]), int(r["Grid_Size"])))
+        vals[counter] = per
+    factor = {c: PROBE_BYTES / 1024 / np.mean([v for v, _ in vals[c][PROBE_KERNEL]])
+              for c in vals}
+    out = {"workload": workload, "kernel_source_sha256_16": kernel_source_hash(),
+           "commands": commands, "probe_scale_factor": factor, "kernels": {}}
+    for name, short in PMC_KERNELS.items():
+        f = vals["FETCH_SIZE"].get(name, [])
+        w = vals["WRITE_SIZE"].get(name, [])
+        if not f or not w:
+            continue
+        alg = [2 * (g // COPY_BLOCK // groups) * spec.unit_bytes for _, g in f]
+        fetch_b = np.mean([v for v, _ in f]) * 1024 * factor["FETCH_SIZE"]
+        write_b = np.mean([v for v, _ in w]) * 1024 * factor["WRITE_SIZE"]
+        out["kernels"][short] = {
+            "dispatches": len(f), "hbm_read_bytes_per_launch": fetch_b,
+            "hbm_write_bytes_per_launch": write_b,
+            "hbm_bytes_per_launch": fetch_b + write_b,
+            "algorithmic_bytes_per_launch": float(np.mean(alg)),
+            "traffic_over_algorithmic": (fetch_b + write_b) / float(np.mean(alg))}
+    json.dump(out, open(out_json, "w"), indent=1)
+    return out
 
 
 def parse():
@@ -51,8 +98,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--threshold", type=int, default=0xFFFFFFFF)
     ap.add_argument("--budget", type=int, default=None)
-    ap.add_argument("--staging-mib", type=int, default=4096)
-    ap.add_argument("--ring", type=int, default=8)
+    ap.add_argument("--staging-mib", type=int, default=8192)
+    ap.add_argument("--ring", type=int, default=4)
     ap.add_argument("--host-copies", type=int, default=128,
                     help="distinct host copies shared round-robin by agents; 0 = one per agent")
     ap.add_argument("--plan-steps", type=int, default=20)
@@ -60,6 +107,9 @@ def parse():
     ap.add_argument("--cpu-agents", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true")
+    ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "OUT_JSON"),
+                    help="write the copy kernels' HBM traffic from two rocprofv3 --pmc runs")
+    ap.add_argument("--pmc-commands", nargs="*", default=[])
     return ap.parse_args()
 
 
@@ -135,6 +185,10 @@ def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        print(json.dumps(summarize_pmc(*args.summarize_pmc[:2], args.workload,
+                                       args.summarize_pmc[2], args.pmc_commands), indent=1))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: this build has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
@@ -231,11 +285,11 @@ def main():
     }
     dom = "pack" if pack_ms >= unpack_ms else "unpack"
     traffic = None
-    pmc_path = os.path.join(ROOT, "profiles", f"{dom}_{args.workload}_pmc.json")
+    pmc_path = os.path.join(ROOT, "profiles", f"k_copy_{args.workload}_pmc.json")
     if os.path.exists(pmc_path):
         pmc = json.load(open(pmc_path))
         if pmc.get("kernel_source_sha256_16") == kernel_source_hash():
-            traffic = pmc.get("hbm_bytes_per_launch")
+            traffic = pmc["kernels"].get(dom, {}).get("hbm_bytes_per_launch")
     roofline = {"bound": "hbm", "kernel": f"k_copy<{dom}>", "achieved": kern[dom]["GBps"],
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": kern[dom]["GBps"] / HBM_PEAK_GBPS,
                 "traffic": traffic,
@@ -248,8 +302,11 @@ def main():
            "d2h_GBps": d2h_b / max(d2h_ms, 1e-9) / 1e6, "h2d_GBps": h2d_b / max(h2d_ms, 1e-9) / 1e6,
            "wall_GBps": moved / wall / 1e9}
     if probe:
+        # shortest time the measured link allows: each direction at its own
+        # one-way rate, and both together at the measured two-way rate
         duplex = probe["duplex_GBps"] > 1.2 * max(probe["h2d_GBps"], probe["d2h_GBps"])
-        ideal = (max(out_b / probe["d2h_GBps"], in_b / probe["h2d_GBps"]) if duplex
+        one_way = max(out_b / probe["d2h_GBps"], in_b / probe["h2d_GBps"])
+        ideal = (max(one_way, (out_b + in_b) / probe["duplex_GBps"]) if duplex
                  else out_b / probe["d2h_GBps"] + in_b / probe["h2d_GBps"]) / 1e9
         dma["ideal_s"] = ideal
         dma["frac_of_measured_link"] = ideal / wall

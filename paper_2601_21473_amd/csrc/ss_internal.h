@@ -94,7 +94,7 @@ struct CopyArgs {
     u64 count;                      // units in this launch
     const CopyItem* items;
     unsigned n_items;               // items per unit
-    unsigned pad;
+    unsigned item_groups;           // ceil(n_items / kCopyWavesPerBlock) blocks per unit
     const u64* plane_base;          // [P] device addresses
     const u64* chunk_bytes;         // [P]
     char* staging;                  // slot base
@@ -102,9 +102,9 @@ struct CopyArgs {
     u64 capacity;                   // U; unit ids outside [0, U) are skipped
 };
 
-constexpr int kCopyThreads = 256;                 // 4 waves, one item per wave
+constexpr int kCopyThreads = 512;                 // 8 waves, one item per wave
 constexpr int kCopyWavesPerBlock = kCopyThreads / 64;
-constexpr unsigned kItemBytes = 16384;            // max bytes per item
+constexpr unsigned kItemBytes = 32768;            // max bytes per item
 constexpr int kCoreThreads = 1024;
 constexpr int kLdsKeys = 16384;                   // 128 KiB of u64 keys in LDS
 

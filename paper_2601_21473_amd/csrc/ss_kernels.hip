@@ -15,7 +15,7 @@
 // Data movement:
 //   k_copy<pack>  gathers (pack) or scatters (unpack) whole units between the
 //                pool's planes and a contiguous staging slot, one wave per
-//                piece of at most 16 KiB, 16-byte non-temporal accesses.
+//                piece of at most 32 KiB, 16-byte non-temporal accesses.
 //
 // Nothing here is a dense contraction; all work is integer indexing and byte
 // movement, so there is no MFMA.
@@ -484,7 +484,8 @@ __global__ void __launch_bounds__(256) k_bt_loads(BtArgs B) {
 
 // One wave copies len bytes (multiple of 16, at most kItemBytes): lane l moves
 // the 16-byte words l, l+64, l+128, ...; eight words per lane are loaded
-// before any is stored so that each wave keeps 8 KiB in flight.
+// before any is stored so that each wave keeps 8 KiB in flight.  Loads and
+// stores are non-temporal: every byte is touched once.
 __device__ __forceinline__ void wave_copy(char* dst, const char* src, unsigned len) {
     const v4u* s = reinterpret_cast<const v4u*>(src);
     v4u* d = reinterpret_cast<v4u*>(dst);
@@ -500,19 +501,23 @@ __device__ __forceinline__ void wave_copy(char* dst, const char* src, unsigned l
     for (; i < n16; i += 64) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
 }
 
+// Block b copies items [g*8, g*8+8) of unit p = b / item_groups of the launch
+// (g = b % item_groups), one item per wave; consecutive blocks walk a unit's
+// bytes in order.  The item index is wave-uniform, so its descriptor and the
+// plane's base and stride are scalar loads.
 template <bool kPack>
 __global__ void __launch_bounds__(kCopyThreads) k_copy(CopyArgs A) {
-    const u64 w = (u64)blockIdx.x * kCopyWavesPerBlock + (threadIdx.x >> 6);
-    const u64 total = A.count * A.n_items;
-    if (w >= total) return;
-    const u64 p = w / A.n_items;
-    const unsigned r = (unsigned)(w - p * A.n_items);
+    const unsigned b = blockIdx.x;
+    const unsigned p = b / A.item_groups;
+    const unsigned g = b - p * A.item_groups;
+    const unsigned r = __builtin_amdgcn_readfirstlane(g * kCopyWavesPerBlock + (threadIdx.x >> 6));
+    if (r >= A.n_items) return;
     const u64 u = (u64)(unsigned)A.units_list[A.first + p];
     if (u >= A.capacity) return;
     const CopyItem it = A.items[r];
     char* chunk = reinterpret_cast<char*>(A.plane_base[it.plane]) + u * A.chunk_bytes[it.plane] +
                   it.chunk_off;
-    char* stage = A.staging + p * A.unit_bytes + it.unit_off;
+    char* stage = A.staging + (u64)p * A.unit_bytes + it.unit_off;
     if (kPack) wave_copy(stage, chunk, it.len);
     else wave_copy(chunk, stage, it.len);
 }
@@ -555,10 +560,9 @@ hipError_t launch_bt_update(const BtArgs& b, unsigned n_agents, hipStream_t st) 
 }
 
 static hipError_t launch_copy(const CopyArgs& a, hipStream_t st, bool pack) {
-    const u64 waves = a.count * a.n_items;
-    if (waves == 0) return hipSuccess;
-    const u64 blocks = (waves + kCopyWavesPerBlock - 1) / kCopyWavesPerBlock;
-    if (blocks > 0x7fffffffull) return hipErrorInvalidValue;
+    if (a.count == 0) return hipSuccess;
+    const u64 blocks = a.count * a.item_groups;
+    if (blocks > 0x7fffffffull || a.item_groups == 0) return hipErrorInvalidValue;
     if (pack) hipLaunchKernelGGL(k_copy<true>, dim3((unsigned)blocks), dim3(kCopyThreads), 0, st, a);
     else hipLaunchKernelGGL(k_copy<false>, dim3((unsigned)blocks), dim3(kCopyThreads), 0, st, a);
     return hipGetLastError();

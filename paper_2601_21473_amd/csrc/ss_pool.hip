@@ -1,18 +1,21 @@
 // Host side of libscalesim: the C ABI declared in include/scalesim.h.
 //
-// Streams (all created non-blocking at the default priority):
-//   plan    classify -> plan core -> block-table update
-//   pack    pack kernels, one per eviction ring slot
-//   d2h     hipMemcpyAsync of packed slots to the victims' host copies
-//   h2d     hipMemcpyAsync of the loads' host copies into load ring slots
-//   unpack  unpack kernels, one per load ring slot
-// Hazards ordered with events:
-//   * a pack slot is rewritten only after its previous D2H finished;
-//   * a load slot is refilled only after its previous unpack finished;
-//   * an unpack that writes units released by this step's victims waits for
-//     the pack that read them (loads take pre-step free units first, then the
-//     released units in eviction order, so this is one monotone dependency);
-//   * the next step's plan waits for all of this step's copies.
+// Two library streams (non-blocking, default priority):
+//   out   plan kernels, then per eviction ring slot: pack kernel ->
+//         hipMemcpyAsync of the slot to the victims' host copies
+//   in    per load ring slot: hipMemcpyAsync of the loads' host copies into
+//         the slot -> unpack kernel
+// Each stream is FIFO, so a ring slot is refilled only after the copy or
+// kernel that last used it finished, and the two copy directions proceed side
+// by side on the host link.  One cross-stream dependency remains: an unpack
+// that writes units released by this step's victims waits for the pack that
+// read them.  Loads take the pre-step free units first and then the released
+// units in eviction order, so slot k of the loads depends on a single pack
+// slot.  The next step's plan waits for both streams.
+//
+// Two streams (plus the caller's) fit in the four hardware queues the HIP
+// runtime gives a process by default, so the two directions never share a
+// queue with each other.
 #include "scalesim.h"
 #include "ss_internal.h"
 
@@ -95,18 +98,16 @@ struct ss_pool {
     unsigned* h_victims_dev = nullptr;
     unsigned* h_loads_dev = nullptr;
 
-    hipStream_t st_plan = nullptr, st_pack = nullptr, st_d2h = nullptr, st_h2d = nullptr,
-                st_unpack = nullptr;
+    hipStream_t st_out = nullptr, st_in = nullptr;
     hipEvent_t ev_planned = nullptr, ev_bt = nullptr, ev_caller = nullptr,
-               ev_d2h_done = nullptr, ev_unpack_done = nullptr;
+               ev_out_done = nullptr, ev_in_done = nullptr;
     std::vector<hipEvent_t> ev_packed;            // per eviction slot index in the step
-    std::vector<hipEvent_t> ev_out_free, ev_in_ready, ev_in_free;   // per ring slot
 
-    // timing (SS_FLAG_TIMING)
-    std::vector<TimedPair> t_pack, t_unpack;
-    size_t n_t_pack = 0, n_t_unpack = 0;
-    TimedPair t_d2h, t_h2d, t_plan;
-    bool t_d2h_used = false, t_h2d_used = false, t_plan_used = false;
+    // timing (SS_FLAG_TIMING): one pair per launch or per slot's copies
+    std::vector<TimedPair> t_pack, t_unpack, t_d2h, t_h2d;
+    size_t n_t_pack = 0, n_t_unpack = 0, n_t_d2h = 0, n_t_h2d = 0;
+    TimedPair t_plan;
+    bool t_plan_used = false;
     ss_stats stats{};
 
     // plan of the current step (host)
@@ -157,7 +158,7 @@ unsigned pow2ceil_u(unsigned n) {
 void free_pool(ss_pool* p) {
     if (!p) return;
     DeviceGuard g(p->device);
-    hipStream_t sts[] = {p->st_plan, p->st_pack, p->st_d2h, p->st_h2d, p->st_unpack};
+    hipStream_t sts[] = {p->st_out, p->st_in};
     for (hipStream_t s : sts)
         if (s) (void)hipStreamSynchronize(s);
     void* dptrs[] = {p->d_units, p->d_agent_off, p->d_bt, p->d_resident, p->d_occ, p->d_cnt,
@@ -172,14 +173,13 @@ void free_pool(ss_pool* p) {
         if (h) (void)hipHostFree(h);
     for (hipStream_t s : sts)
         if (s) (void)hipStreamDestroy(s);
-    hipEvent_t evs[] = {p->ev_planned, p->ev_bt, p->ev_caller, p->ev_d2h_done, p->ev_unpack_done,
-                        p->t_d2h.a, p->t_d2h.b, p->t_h2d.a, p->t_h2d.b, p->t_plan.a, p->t_plan.b};
+    hipEvent_t evs[] = {p->ev_planned, p->ev_bt, p->ev_caller, p->ev_out_done, p->ev_in_done,
+                        p->t_plan.a, p->t_plan.b};
     for (hipEvent_t e : evs)
         if (e) (void)hipEventDestroy(e);
-    for (auto* v : {&p->ev_packed, &p->ev_out_free, &p->ev_in_ready, &p->ev_in_free})
-        for (hipEvent_t e : *v)
-            if (e) (void)hipEventDestroy(e);
-    for (auto* v : {&p->t_pack, &p->t_unpack})
+    for (hipEvent_t e : p->ev_packed)
+        if (e) (void)hipEventDestroy(e);
+    for (auto* v : {&p->t_pack, &p->t_unpack, &p->t_d2h, &p->t_h2d})
         for (auto& tp : *v) {
             if (tp.a) (void)hipEventDestroy(tp.a);
             if (tp.b) (void)hipEventDestroy(tp.b);
@@ -208,31 +208,26 @@ hipError_t timed_pair(std::vector<TimedPair>& v, size_t idx, TimedPair** out) {
 // step's work is known to have finished.
 void collect_timing(ss_pool* p) {
     if (!(p->flags & SS_FLAG_TIMING)) return;
+    auto fold = [](std::vector<TimedPair>& v, size_t n, double* ms_acc, uint64_t* bytes_acc,
+                   uint64_t* count) {
+        float ms = 0.f;
+        for (size_t i = 0; i < n; ++i)
+            if (hipEventElapsedTime(&ms, v[i].a, v[i].b) == hipSuccess) {
+                *ms_acc += ms;
+                *bytes_acc += v[i].bytes;
+                if (count) (*count)++;
+            }
+    };
+    fold(p->t_pack, p->n_t_pack, &p->stats.pack_ms, &p->stats.pack_bytes, &p->stats.pack_launches);
+    fold(p->t_unpack, p->n_t_unpack, &p->stats.unpack_ms, &p->stats.unpack_bytes,
+         &p->stats.unpack_launches);
+    fold(p->t_d2h, p->n_t_d2h, &p->stats.d2h_ms, &p->stats.d2h_bytes, nullptr);
+    fold(p->t_h2d, p->n_t_h2d, &p->stats.h2d_ms, &p->stats.h2d_bytes, nullptr);
     float ms = 0.f;
-    for (size_t i = 0; i < p->n_t_pack; ++i)
-        if (hipEventElapsedTime(&ms, p->t_pack[i].a, p->t_pack[i].b) == hipSuccess) {
-            p->stats.pack_ms += ms;
-            p->stats.pack_bytes += p->t_pack[i].bytes;
-            p->stats.pack_launches++;
-        }
-    for (size_t i = 0; i < p->n_t_unpack; ++i)
-        if (hipEventElapsedTime(&ms, p->t_unpack[i].a, p->t_unpack[i].b) == hipSuccess) {
-            p->stats.unpack_ms += ms;
-            p->stats.unpack_bytes += p->t_unpack[i].bytes;
-            p->stats.unpack_launches++;
-        }
-    if (p->t_d2h_used && hipEventElapsedTime(&ms, p->t_d2h.a, p->t_d2h.b) == hipSuccess) {
-        p->stats.d2h_ms += ms;
-        p->stats.d2h_bytes += p->t_d2h.bytes;
-    }
-    if (p->t_h2d_used && hipEventElapsedTime(&ms, p->t_h2d.a, p->t_h2d.b) == hipSuccess) {
-        p->stats.h2d_ms += ms;
-        p->stats.h2d_bytes += p->t_h2d.bytes;
-    }
     if (p->t_plan_used && hipEventElapsedTime(&ms, p->t_plan.a, p->t_plan.b) == hipSuccess)
         p->stats.plan_gpu_ms += ms;
-    p->n_t_pack = p->n_t_unpack = 0;
-    p->t_d2h_used = p->t_h2d_used = p->t_plan_used = false;
+    p->n_t_pack = p->n_t_unpack = p->n_t_d2h = p->n_t_h2d = 0;
+    p->t_plan_used = false;
 }
 
 // True if [ptr, ptr + bytes) lies inside one allocation of device memory on
@@ -460,26 +455,19 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(hipMemcpy(p->d_chunk_bytes, p->chunk_bytes.data(), p->P * sizeof(u64),
                          hipMemcpyHostToDevice));
 
-    for (hipStream_t* s : {&p->st_plan, &p->st_pack, &p->st_d2h, &p->st_h2d, &p->st_unpack})
+    for (hipStream_t* s : {&p->st_out, &p->st_in})
         CREATE_TRY(hipStreamCreateWithFlags(s, hipStreamNonBlocking));
-    for (hipEvent_t* ev : {&p->ev_planned, &p->ev_bt, &p->ev_caller, &p->ev_d2h_done,
-                           &p->ev_unpack_done})
+    for (hipEvent_t* ev : {&p->ev_planned, &p->ev_bt, &p->ev_caller, &p->ev_out_done,
+                           &p->ev_in_done})
         CREATE_TRY(make_event(ev, false));
-    for (auto* v : {&p->ev_out_free, &p->ev_in_ready, &p->ev_in_free}) {
-        v->resize(p->ring, nullptr);
-        for (auto& ev : *v) {
-            CREATE_TRY(make_event(&ev, false));
-            CREATE_TRY(hipEventRecord(ev, p->st_plan));
-        }
+    if (p->flags & SS_FLAG_TIMING) {
+        CREATE_TRY(make_event(&p->t_plan.a, true));
+        CREATE_TRY(make_event(&p->t_plan.b, true));
     }
-    if (p->flags & SS_FLAG_TIMING)
-        for (TimedPair* tp : {&p->t_d2h, &p->t_h2d, &p->t_plan}) {
-            CREATE_TRY(make_event(&tp->a, true));
-            CREATE_TRY(make_event(&tp->b, true));
-        }
-    CREATE_TRY(hipEventRecord(p->ev_d2h_done, p->st_plan));
-    CREATE_TRY(hipEventRecord(p->ev_unpack_done, p->st_plan));
-    CREATE_TRY(hipStreamSynchronize(p->st_plan));
+    CREATE_TRY(hipEventRecord(p->ev_out_done, p->st_out));
+    CREATE_TRY(hipEventRecord(p->ev_in_done, p->st_in));
+    CREATE_TRY(hipStreamSynchronize(p->st_out));
+    CREATE_TRY(hipStreamSynchronize(p->st_in));
 #undef CREATE_TRY
     *out = p;
     return SS_OK;
@@ -504,9 +492,10 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     hipStream_t caller = static_cast<hipStream_t>(stream);
 
     TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_plan, p->ev_caller, 0), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_plan, p->ev_d2h_done, 0), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_plan, p->ev_unpack_done, 0), true);
+    // the out stream is FIFO behind the previous step's evictions; it also
+    // waits for the previous step's loads and for the caller's work
+    TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_caller, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_in_done, 0), true);
 
     PlanArgs A{};
     A.dist = distances;
@@ -539,11 +528,11 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     A.loads_host = p->h_loads_dev;
 
     const bool timing = p->flags & SS_FLAG_TIMING;
-    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.a, p->st_plan), true);
-    TRY_HIP(p, launch_classify(A, p->st_plan), true);
-    TRY_HIP(p, launch_plan_core(A, p->st_plan), true);
-    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.b, p->st_plan), true);
-    TRY_HIP(p, hipEventRecord(p->ev_planned, p->st_plan), true);
+    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.a, p->st_out), true);
+    TRY_HIP(p, launch_classify(A, p->st_out), true);
+    TRY_HIP(p, launch_plan_core(A, p->st_out), true);
+    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.b, p->st_out), true);
+    TRY_HIP(p, hipEventRecord(p->ev_planned, p->st_out), true);
 
     BtArgs B{};
     B.res = p->d_res;
@@ -559,8 +548,8 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     B.vunits = p->d_vunits;
     B.lunits = p->d_lunits;
     B.capacity = p->U;
-    TRY_HIP(p, launch_bt_update(B, p->N, p->st_plan), true);
-    TRY_HIP(p, hipEventRecord(p->ev_bt, p->st_plan), true);
+    TRY_HIP(p, launch_bt_update(B, p->N, p->st_out), true);
+    TRY_HIP(p, hipEventRecord(p->ev_bt, p->st_out), true);
 
     TRY_HIP(p, hipEventSynchronize(p->ev_planned), true);
     // the previous step finished before the plan kernels ran
@@ -605,9 +594,7 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
     hipStream_t caller = static_cast<hipStream_t>(stream);
     const bool timing = p->flags & SS_FLAG_TIMING;
     TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_pack, p->ev_caller, 0), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_pack, p->ev_bt, 0), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_d2h, p->ev_caller, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_caller, 0), true);
 
     const u64 total = p->res.units_out;
     const u64 ups = p->units_per_slot;
@@ -621,34 +608,31 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
     C.units_list = p->d_vunits;
     C.items = p->d_items;
     C.n_items = p->n_items;
+    C.item_groups = (p->n_items + kCopyWavesPerBlock - 1) / kCopyWavesPerBlock;
     C.plane_base = p->d_plane_base;
     C.chunk_bytes = p->d_chunk_bytes;
     C.unit_bytes = p->unit_bytes;
     C.capacity = p->U;
     size_t vi = 0;
     for (u64 k = 0; k < nslots; ++k) {
-        const unsigned r = (unsigned)(k % p->ring);
         const u64 p0 = k * ups, p1 = std::min(total, p0 + ups);
-        char* slot = p->stage_out + (u64)r * p->slot_bytes;
-        TRY_HIP(p, hipStreamWaitEvent(p->st_pack, p->ev_out_free[r], 0), true);
+        char* slot = p->stage_out + (k % p->ring) * p->slot_bytes;
         C.first = p0;
         C.count = p1 - p0;
         C.staging = slot;
         TimedPair* tp = nullptr;
         if (timing) {
-            TRY_HIP(p, timed_pair(p->t_pack, p->n_t_pack, &tp), true);
-            p->n_t_pack++;
+            TRY_HIP(p, timed_pair(p->t_pack, p->n_t_pack++, &tp), true);
             tp->bytes = (p1 - p0) * p->unit_bytes;
-            TRY_HIP(p, hipEventRecord(tp->a, p->st_pack), true);
+            TRY_HIP(p, hipEventRecord(tp->a, p->st_out), true);
         }
-        TRY_HIP(p, launch_pack(C, p->st_pack), true);
-        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_pack), true);
-        TRY_HIP(p, hipEventRecord(p->ev_packed[k], p->st_pack), true);
-        TRY_HIP(p, hipStreamWaitEvent(p->st_d2h, p->ev_packed[k], 0), true);
-        if (timing && k == 0) {
-            TRY_HIP(p, hipEventRecord(p->t_d2h.a, p->st_d2h), true);
-            p->t_d2h_used = true;
-            p->t_d2h.bytes = total * p->unit_bytes;
+        TRY_HIP(p, launch_pack(C, p->st_out), true);
+        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_out), true);
+        TRY_HIP(p, hipEventRecord(p->ev_packed[k], p->st_out), true);
+        if (timing) {
+            TRY_HIP(p, timed_pair(p->t_d2h, p->n_t_d2h++, &tp), true);
+            tp->bytes = (p1 - p0) * p->unit_bytes;
+            TRY_HIP(p, hipEventRecord(tp->a, p->st_out), true);
         }
         // each victim's bytes inside [p0, p1) go to its host copy
         while (vi < p->res.n_victims && p->voff[vi + 1] <= p0) vi++;
@@ -658,12 +642,11 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
             char* dst = p->host + p->host_off[v] + (lo - p->voff[i]) * p->unit_bytes;
             const char* src = slot + (lo - p0) * p->unit_bytes;
             TRY_HIP(p, hipMemcpyAsync(dst, src, (hi - lo) * p->unit_bytes, hipMemcpyDeviceToHost,
-                                      p->st_d2h), true);
+                                      p->st_out), true);
         }
-        TRY_HIP(p, hipEventRecord(p->ev_out_free[r], p->st_d2h), true);
+        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_out), true);
     }
-    if (timing && nslots > 0) TRY_HIP(p, hipEventRecord(p->t_d2h.b, p->st_d2h), true);
-    TRY_HIP(p, hipEventRecord(p->ev_d2h_done, p->st_d2h), true);
+    TRY_HIP(p, hipEventRecord(p->ev_out_done, p->st_out), true);
     p->state = kPacked;
     return SS_OK;
 }
@@ -677,9 +660,8 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
     hipStream_t caller = static_cast<hipStream_t>(stream);
     const bool timing = p->flags & SS_FLAG_TIMING;
     TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_h2d, p->ev_caller, 0), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_unpack, p->ev_caller, 0), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_unpack, p->ev_bt, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_caller, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_bt, 0), true);
 
     const u64 total = p->res.units_in;
     const u64 ups = p->units_per_slot;
@@ -689,20 +671,20 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
     C.units_list = p->d_lunits;
     C.items = p->d_items;
     C.n_items = p->n_items;
+    C.item_groups = (p->n_items + kCopyWavesPerBlock - 1) / kCopyWavesPerBlock;
     C.plane_base = p->d_plane_base;
     C.chunk_bytes = p->d_chunk_bytes;
     C.unit_bytes = p->unit_bytes;
     C.capacity = p->U;
     size_t li = 0;
     for (u64 k = 0; k < nslots; ++k) {
-        const unsigned r = (unsigned)(k % p->ring);
         const u64 q0 = k * ups, q1 = std::min(total, q0 + ups);
-        char* slot = p->stage_in + (u64)r * p->slot_bytes;
-        TRY_HIP(p, hipStreamWaitEvent(p->st_h2d, p->ev_in_free[r], 0), true);
-        if (timing && k == 0) {
-            TRY_HIP(p, hipEventRecord(p->t_h2d.a, p->st_h2d), true);
-            p->t_h2d_used = true;
-            p->t_h2d.bytes = total * p->unit_bytes;
+        char* slot = p->stage_in + (k % p->ring) * p->slot_bytes;
+        TimedPair* tp = nullptr;
+        if (timing) {
+            TRY_HIP(p, timed_pair(p->t_h2d, p->n_t_h2d++, &tp), true);
+            tp->bytes = (q1 - q0) * p->unit_bytes;
+            TRY_HIP(p, hipEventRecord(tp->a, p->st_in), true);
         }
         while (li < p->res.n_loads && p->loff[li + 1] <= q0) li++;
         for (size_t i = li; i < p->res.n_loads && p->loff[i] < q1; ++i) {
@@ -711,34 +693,29 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
             const char* src = p->host + p->host_off[a] + (lo - p->loff[i]) * p->unit_bytes;
             char* dst = slot + (lo - q0) * p->unit_bytes;
             TRY_HIP(p, hipMemcpyAsync(dst, src, (hi - lo) * p->unit_bytes, hipMemcpyHostToDevice,
-                                      p->st_h2d), true);
+                                      p->st_in), true);
         }
-        TRY_HIP(p, hipEventRecord(p->ev_in_ready[r], p->st_h2d), true);
-        TRY_HIP(p, hipStreamWaitEvent(p->st_unpack, p->ev_in_ready[r], 0), true);
+        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_in), true);
         // units released by victims are overwritten only after the pack read them
         const u64 last = q1 - 1;
         if (last >= nF) {
             const u64 kv = (last - nF) / ups;
-            TRY_HIP(p, hipStreamWaitEvent(p->st_unpack, p->ev_packed[kv], 0), true);
+            TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_packed[kv], 0), true);
         }
         C.first = q0;
         C.count = q1 - q0;
         C.staging = slot;
-        TimedPair* tp = nullptr;
         if (timing) {
-            TRY_HIP(p, timed_pair(p->t_unpack, p->n_t_unpack, &tp), true);
-            p->n_t_unpack++;
+            TRY_HIP(p, timed_pair(p->t_unpack, p->n_t_unpack++, &tp), true);
             tp->bytes = (q1 - q0) * p->unit_bytes;
-            TRY_HIP(p, hipEventRecord(tp->a, p->st_unpack), true);
+            TRY_HIP(p, hipEventRecord(tp->a, p->st_in), true);
         }
-        TRY_HIP(p, launch_unpack(C, p->st_unpack), true);
-        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_unpack), true);
-        TRY_HIP(p, hipEventRecord(p->ev_in_free[r], p->st_unpack), true);
+        TRY_HIP(p, launch_unpack(C, p->st_in), true);
+        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_in), true);
     }
-    if (timing && nslots > 0) TRY_HIP(p, hipEventRecord(p->t_h2d.b, p->st_h2d), true);
-    TRY_HIP(p, hipEventRecord(p->ev_unpack_done, p->st_unpack), true);
-    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_unpack_done, 0), true);
-    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_d2h_done, 0), true);
+    TRY_HIP(p, hipEventRecord(p->ev_in_done, p->st_in), true);
+    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_in_done, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_out_done, 0), true);
     p->state = kIdle;
     return SS_OK;
 }
@@ -760,7 +737,7 @@ ss_status ss_block_table_host(ss_pool* p, uint32_t agent, int32_t* out, uint32_t
     DeviceGuard g(p->device);
     u64 off = 0;
     for (uint32_t a = 0; a < agent; ++a) off += p->s[a];
-    TRY_HIP(p, hipStreamSynchronize(p->st_plan), false);
+    TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
     TRY_HIP(p, hipMemcpy(out, p->d_bt + off, s * sizeof(int32_t), hipMemcpyDeviceToHost), false);
     return SS_OK;
 }
@@ -775,7 +752,7 @@ ss_status ss_block_table_host_all(ss_pool* p, int32_t* out, uint64_t cap, uint64
     if (cap < total) return set_err(SS_ERR_ARG, "cap %llu < %llu entries", (unsigned long long)cap,
                                     (unsigned long long)total);
     DeviceGuard g(p->device);
-    TRY_HIP(p, hipStreamSynchronize(p->st_plan), false);
+    TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
     TRY_HIP(p, hipMemcpy(out, p->d_bt, total * sizeof(int32_t), hipMemcpyDeviceToHost), false);
     return SS_OK;
 }
@@ -785,7 +762,7 @@ ss_status ss_resident_host(ss_pool* p, uint8_t* out) {
     if (st) return st;
     if (!out) return set_err(SS_ERR_ARG, "NULL output");
     DeviceGuard g(p->device);
-    TRY_HIP(p, hipStreamSynchronize(p->st_plan), false);
+    TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
     TRY_HIP(p, hipMemcpy(out, p->d_resident, p->N, hipMemcpyDeviceToHost), false);
     return SS_OK;
 }
@@ -793,7 +770,7 @@ ss_status ss_resident_host(ss_pool* p, uint8_t* out) {
 ss_status ss_get_stats(ss_pool* p, ss_stats* out) {
     if (!p || !out) return set_err(SS_ERR_ARG, "NULL argument");
     DeviceGuard g(p->device);
-    for (hipStream_t s : {p->st_plan, p->st_pack, p->st_d2h, p->st_h2d, p->st_unpack})
+    for (hipStream_t s : {p->st_out, p->st_in})
         TRY_HIP(p, hipStreamSynchronize(s), false);
     collect_timing(p);
     *out = p->stats;
@@ -803,7 +780,7 @@ ss_status ss_get_stats(ss_pool* p, ss_stats* out) {
 ss_status ss_reset_stats(ss_pool* p) {
     if (!p) return set_err(SS_ERR_ARG, "NULL pool");
     DeviceGuard g(p->device);
-    for (hipStream_t s : {p->st_plan, p->st_pack, p->st_d2h, p->st_h2d, p->st_unpack})
+    for (hipStream_t s : {p->st_out, p->st_in})
         TRY_HIP(p, hipStreamSynchronize(s), false);
     collect_timing(p);
     p->stats = ss_stats{};
