@@ -113,23 +113,22 @@ def parse():
     return ap.parse_args()
 
 
-def probes(torch, binding):
-    dev = torch.device("cuda", 0)
+def probes(binding):
+    from paper_2601_21473_amd.memory import DeviceBuffer, HostBuffer
     out = {}
     n = 2 << 30
-    a = torch.empty(n, dtype=torch.uint8, device=dev)
-    b = torch.empty(n, dtype=torch.uint8, device=dev)
-    ms = binding.probe_copy(b.data_ptr(), a.data_ptr(), n, iters=10)
+    a, b = DeviceBuffer(n), DeviceBuffer(n)
+    ms = binding.probe_copy(b.ptr, a.ptr, n, iters=10)
     out["hbm_copy_GBps"] = 2 * n / ms / 1e6
-    del a, b
+    a.free()
+    b.free()
     m = 1 << 30
-    h = torch.empty(2 * m, dtype=torch.uint8, pin_memory=True)
-    d = torch.empty(2 * m, dtype=torch.uint8, device=dev)
-    out["h2d_GBps"] = m / binding.probe_link(h.data_ptr(), d.data_ptr(), m, 0, 5) / 1e6
-    out["d2h_GBps"] = m / binding.probe_link(h.data_ptr(), d.data_ptr(), m, 1, 5) / 1e6
-    out["duplex_GBps"] = 2 * m / binding.probe_link(h.data_ptr(), d.data_ptr(), m, 2, 5) / 1e6
-    del h, d
-    torch.cuda.empty_cache()
+    h, d = HostBuffer(2 * m), DeviceBuffer(2 * m)
+    out["h2d_GBps"] = m / binding.probe_link(h.ptr, d.ptr, m, 0, 5) / 1e6
+    out["d2h_GBps"] = m / binding.probe_link(h.ptr, d.ptr, m, 1, 5) / 1e6
+    out["duplex_GBps"] = 2 * m / binding.probe_link(h.ptr, d.ptr, m, 2, 5) / 1e6
+    h.free()
+    d.free()
     return out
 
 
@@ -193,13 +192,11 @@ def main():
         print(f"bench.py runs on one GPU: this build has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
         sys.exit(2)
-    import torch
     import workloads as W
     from paper_2601_21473_amd import binding
-    from paper_2601_21473_amd.memory import PoolMemory
+    from paper_2601_21473_amd.memory import DeviceBuffer, PoolMemory
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    binding.load()
+    assert binding.device_count() > 0, "bench.py needs a GPU"
     trace = W.make_trace(args.workload, args.seed)
     T_need = args.warmup + args.steps + args.plan_steps
     if T_need > trace.n_steps:
@@ -207,7 +204,7 @@ def main():
     budget = args.budget
     thr = args.threshold
 
-    probe = {} if args.no_probe else probes(torch, binding)
+    probe = {} if args.no_probe else probes(binding)
 
     mems, pools = [], []
     for spec in trace.pools:
@@ -215,14 +212,20 @@ def main():
         mem = PoolMemory(spec, args.staging_mib << 20, args.ring, host_slots=host_slots)
         mems.append(mem)
         pools.append(mem.make_pool(timing=True))
-    dev = torch.device("cuda", 0)
-    dist = torch.from_numpy(np.ascontiguousarray(trace.dist).view(np.int32)).to(dev)
-    act = torch.from_numpy(np.ascontiguousarray(trace.active)).to(dev)
-    torch.cuda.synchronize()
-    stream = torch.cuda.current_stream().cuda_stream
+    N = trace.n_agents
+    d_np = np.ascontiguousarray(trace.dist, dtype=np.uint32)
+    a_np = np.ascontiguousarray(trace.active, dtype=np.uint8)
+    dist, act = DeviceBuffer(d_np.nbytes), DeviceBuffer(a_np.nbytes)
+    dist.upload(d_np)
+    act.upload(a_np)
+    stream = 0
+
+    def sync():
+        for p in pools:
+            p.sync()
 
     def step(t):
-        plans = [p.plan_step(dist[t].data_ptr(), act[t].data_ptr(), thr, budget, stream)
+        plans = [p.plan_step(dist.ptr + 4 * N * t, act.ptr + N * t, thr, budget, stream)
                  for p in pools]
         for p in pools:
             p.evict_pack(stream)
@@ -232,12 +235,12 @@ def main():
 
     for t in range(args.warmup):
         step(t)
-    torch.cuda.synchronize()
+    sync()
     for p in pools:
         p.reset_stats()
     moved = out_b = in_b = 0
     step_wall = []
-    torch.cuda.synchronize()
+    sync()
     t0 = time.perf_counter()
     for k in range(args.steps):
         ts = time.perf_counter()
@@ -246,7 +249,7 @@ def main():
         for pl in plans:
             out_b += pl["bytes_out"]
             in_b += pl["bytes_in"]
-    torch.cuda.synchronize()
+    sync()
     wall = time.perf_counter() - t0
     moved = out_b + in_b
     stats = [p.stats() for p in pools]
@@ -254,20 +257,24 @@ def main():
     # plan latency: each plan issued with the device idle
     lat = []
     for k in range(args.plan_steps):
-        torch.cuda.synchronize()
+        sync()
+        t = args.warmup + args.steps + k
         ts = time.perf_counter()
         for p in pools:
-            p.plan_step(dist[args.warmup + args.steps + k].data_ptr(),
-                        act[args.warmup + args.steps + k].data_ptr(), thr, budget, stream)
+            p.plan_step(dist.ptr + 4 * N * t, act.ptr + N * t, thr, budget, stream)
         lat.append(time.perf_counter() - ts)
         for p in pools:
             p.evict_pack(stream)
         for p in pools:
             p.prefetch_unpack(stream)
-    torch.cuda.synchronize()
+    sync()
     plan_stats = [p.stats() for p in pools]
     for p in pools:
         p.close()
+    for m in mems:
+        m.free()
+    dist.free()
+    act.free()
 
     pack_ms = sum(s["pack_ms"] for s in stats)
     unpack_ms = sum(s["unpack_ms"] for s in stats)

@@ -200,6 +200,26 @@ ss_status ss_probe_copy(void* dst, const void* src, uint64_t bytes, int iters, f
 ss_status ss_probe_link(void* host, void* dev, uint64_t bytes, int dir, int iters,
                         float* ms_per_iter);
 
+/* Block until all work the pool has queued (plan, copies, kernels) is done. */
+ss_status ss_sync(ss_pool* pool);
+
+/* Plumbing for callers without a framework allocator: thin wrappers over the
+ * HIP runtime this library is linked with.  Memory must be allocated by the
+ * same runtime instance that runs the pool; a process that has loaded another
+ * copy of the HIP runtime (for example one bundled with a Python framework)
+ * must allocate through that one and must not mix the two.
+ *   ss_device_count   number of visible devices (0 when none; not an error)
+ *   ss_device_alloc   hipMalloc of `bytes` on `device`
+ *   ss_host_alloc     pinned host memory (hipHostMalloc), device-accessible
+ *   ss_device_free / ss_host_free   release them (NULL is ignored)
+ *   ss_copy           synchronous copy of `bytes` between any two of them */
+ss_status ss_device_count(int32_t* n);
+ss_status ss_device_alloc(int32_t device, uint64_t bytes, void** out);
+ss_status ss_host_alloc(uint64_t bytes, void** out);
+ss_status ss_device_free(void* ptr);
+ss_status ss_host_free(void* ptr);
+ss_status ss_copy(void* dst, const void* src, uint64_t bytes);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* ss_last_error(void);
 

@@ -27,7 +27,9 @@ SS_FLAG_TIMING = 1
 
 EXPORTS = ["ss_pool_create", "ss_pool_destroy", "ss_plan_step", "ss_evict_pack",
            "ss_prefetch_unpack", "ss_block_table", "ss_block_table_host", "ss_block_table_host_all", "ss_resident_host",
-           "ss_get_stats", "ss_reset_stats", "ss_probe_copy", "ss_probe_link", "ss_last_error"]
+           "ss_get_stats", "ss_reset_stats", "ss_probe_copy", "ss_probe_link", "ss_sync",
+           "ss_device_count", "ss_device_alloc", "ss_host_alloc", "ss_device_free", "ss_host_free",
+           "ss_copy", "ss_last_error"]
 
 
 class ss_pool_desc(C.Structure):
@@ -97,6 +99,13 @@ def load():
         "ss_reset_stats": ([P], C.c_int32),
         "ss_probe_copy": ([P, P, C.c_uint64, C.c_int, C.POINTER(C.c_float)], C.c_int32),
         "ss_probe_link": ([P, P, C.c_uint64, C.c_int, C.c_int, C.POINTER(C.c_float)], C.c_int32),
+        "ss_sync": ([P], C.c_int32),
+        "ss_device_count": ([C.POINTER(C.c_int32)], C.c_int32),
+        "ss_device_alloc": ([C.c_int32, C.c_uint64, C.POINTER(P)], C.c_int32),
+        "ss_host_alloc": ([C.c_uint64, C.POINTER(P)], C.c_int32),
+        "ss_device_free": ([P], C.c_int32),
+        "ss_host_free": ([P], C.c_int32),
+        "ss_copy": ([P, P, C.c_uint64], C.c_int32),
         "ss_last_error": ([], C.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -215,6 +224,10 @@ class Pool:
         _check(load().ss_resident_host(self._h, out.ctypes.data_as(C.POINTER(C.c_uint8))))
         return out
 
+    def sync(self):
+        """Wait for all of the pool's queued work."""
+        _check(load().ss_sync(self._h))
+
     def stats(self) -> dict:
         s = ss_stats()
         _check(load().ss_get_stats(self._h, C.byref(s)))
@@ -222,6 +235,36 @@ class Pool:
 
     def reset_stats(self):
         _check(load().ss_reset_stats(self._h))
+
+
+def device_count() -> int:
+    n = C.c_int32()
+    _check(load().ss_device_count(C.byref(n)))
+    return n.value
+
+
+def device_alloc(nbytes: int, device: int = 0) -> int:
+    p = C.c_void_p()
+    _check(load().ss_device_alloc(int(device), int(nbytes), C.byref(p)))
+    return p.value
+
+
+def host_alloc(nbytes: int) -> int:
+    p = C.c_void_p()
+    _check(load().ss_host_alloc(int(nbytes), C.byref(p)))
+    return p.value
+
+
+def device_free(ptr: int):
+    _check(load().ss_device_free(ptr))
+
+
+def host_free(ptr: int):
+    _check(load().ss_host_free(ptr))
+
+
+def copy(dst: int, src: int, nbytes: int):
+    _check(load().ss_copy(int(dst), int(src), int(nbytes)))
 
 
 def probe_copy(dst: int, src: int, nbytes: int, iters: int = 10) -> float:

@@ -787,6 +787,73 @@ ss_status ss_reset_stats(ss_pool* p) {
     return SS_OK;
 }
 
+ss_status ss_sync(ss_pool* p) {
+    if (!p) return set_err(SS_ERR_ARG, "NULL pool");
+    DeviceGuard g(p->device);
+    for (hipStream_t s : {p->st_out, p->st_in})
+        TRY_HIP(p, hipStreamSynchronize(s), true);
+    return SS_OK;
+}
+
+ss_status ss_device_count(int32_t* n) {
+    if (!n) return set_err(SS_ERR_ARG, "NULL output");
+    int c = 0;
+    if (hipGetDeviceCount(&c) != hipSuccess) {
+        (void)hipGetLastError();
+        c = 0;
+    }
+    *n = c;
+    return SS_OK;
+}
+
+ss_status ss_device_alloc(int32_t device, uint64_t bytes, void** out) {
+    if (!out || bytes == 0) return set_err(SS_ERR_ARG, "bad allocation arguments");
+    *out = nullptr;
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev) {
+        (void)hipGetLastError();
+        return set_err(SS_ERR_ARG, "device %d not present", (int)device);
+    }
+    DeviceGuard g(device);
+    hipError_t e = hipMalloc(out, bytes);
+    if (e != hipSuccess) {
+        *out = nullptr;
+        return set_err(e == hipErrorOutOfMemory ? SS_ERR_NOMEM : SS_ERR_HIP,
+                       "hipMalloc(%llu) failed: %s", (unsigned long long)bytes, hipGetErrorString(e));
+    }
+    return SS_OK;
+}
+
+ss_status ss_host_alloc(uint64_t bytes, void** out) {
+    if (!out || bytes == 0) return set_err(SS_ERR_ARG, "bad allocation arguments");
+    *out = nullptr;
+    hipError_t e = hipHostMalloc(out, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        *out = nullptr;
+        return set_err(e == hipErrorOutOfMemory ? SS_ERR_NOMEM : SS_ERR_HIP,
+                       "hipHostMalloc(%llu) failed: %s", (unsigned long long)bytes,
+                       hipGetErrorString(e));
+    }
+    return SS_OK;
+}
+
+ss_status ss_device_free(void* ptr) {
+    if (ptr) TRY_HIP(nullptr, hipFree(ptr), false);
+    return SS_OK;
+}
+
+ss_status ss_host_free(void* ptr) {
+    if (ptr) TRY_HIP(nullptr, hipHostFree(ptr), false);
+    return SS_OK;
+}
+
+ss_status ss_copy(void* dst, const void* src, uint64_t bytes) {
+    if (!dst || !src) return set_err(SS_ERR_ARG, "NULL pointer");
+    if (bytes == 0) return SS_OK;
+    TRY_HIP(nullptr, hipMemcpy(dst, src, bytes, hipMemcpyDefault), false);
+    return SS_OK;
+}
+
 ss_status ss_probe_copy(void* dst, const void* src, uint64_t bytes, int iters, float* ms) {
     if (!dst || !src || !ms || iters < 1 || bytes == 0 || bytes % 16)
         return set_err(SS_ERR_ARG, "bad probe arguments");

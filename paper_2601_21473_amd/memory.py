@@ -1,14 +1,66 @@
-"""Device and pinned-host buffers for a pool, allocated with PyTorch.
+"""Device and pinned-host buffers of a pool, allocated through libscalesim.
 
-PyTorch is used here only as an allocator (HBM tensors, pinned host tensors)
-and for stream handles; the library never sees a torch type, only addresses.
+The library's own allocation calls (thin wrappers over the HIP runtime it is
+linked with) keep every buffer and every copy on one HIP runtime instance.
+On that runtime both directions of ``hipMemcpyAsync`` run on the copy
+engines, leaving the compute units to the pack and unpack kernels.
 """
 from __future__ import annotations
 
+import ctypes as C
+
 import numpy as np
-import torch
 
 from . import binding
+
+
+class DeviceBuffer:
+    def __init__(self, nbytes: int, device: int = 0):
+        self.nbytes = int(nbytes)
+        self.ptr = binding.device_alloc(self.nbytes, device)
+
+    def upload(self, arr: np.ndarray, offset: int = 0):
+        a = np.ascontiguousarray(arr)
+        assert offset + a.nbytes <= self.nbytes
+        binding.copy(self.ptr + offset, a.ctypes.data, a.nbytes)
+
+    def download(self, offset: int, nbytes: int) -> np.ndarray:
+        assert offset + nbytes <= self.nbytes
+        out = np.empty(nbytes, dtype=np.uint8)
+        binding.copy(out.ctypes.data, self.ptr + offset, nbytes)
+        return out
+
+    def free(self):
+        if self.ptr:
+            binding.device_free(self.ptr)
+            self.ptr = 0
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+class HostBuffer:
+    """Pinned host memory with a numpy uint8 view."""
+
+    def __init__(self, nbytes: int):
+        self.nbytes = int(nbytes)
+        self.ptr = binding.host_alloc(self.nbytes)
+        self.np = np.ctypeslib.as_array((C.c_uint8 * self.nbytes).from_address(self.ptr))
+
+    def free(self):
+        if self.ptr:
+            self.np = None
+            binding.host_free(self.ptr)
+            self.ptr = 0
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
 
 
 class PoolMemory:
@@ -22,11 +74,9 @@ class PoolMemory:
 
     def __init__(self, spec, staging_bytes: int, ring_slots: int, host_slots=None,
                  device: int = 0):
-        dev = torch.device("cuda", device)
         self.spec = spec
-        self.planes = [torch.empty(spec.capacity_units * cb, dtype=torch.uint8, device=dev)
-                       for cb in spec.chunk_bytes]
-        self.staging = torch.empty(staging_bytes, dtype=torch.uint8, device=dev)
+        self.planes = [DeviceBuffer(spec.capacity_units * cb, device) for cb in spec.chunk_bytes]
+        self.staging = DeviceBuffer(staging_bytes, device)
         ub = spec.unit_bytes
         units = np.asarray(spec.agent_units, dtype=np.uint64)
         if host_slots is None:
@@ -37,8 +87,8 @@ class PoolMemory:
             self.host_off = (np.arange(len(units), dtype=np.uint64) % np.uint64(host_slots)) * \
                 np.uint64(slot)
             host_bytes = int(host_slots) * slot
-        self.host = torch.empty(host_bytes, dtype=torch.uint8, pin_memory=True)
-        self.host_np = self.host.numpy()
+        self.host = HostBuffer(host_bytes)
+        self.host_np = self.host.np
         self.ring_slots = ring_slots
         self.device = device
 
@@ -46,10 +96,10 @@ class PoolMemory:
         s = self.spec
         return binding.Pool(capacity_units=s.capacity_units, chunk_bytes=s.chunk_bytes,
                             agent_units=s.agent_units,
-                            plane_base=[p.data_ptr() for p in self.planes],
-                            host_backing=self.host.data_ptr(), host_bytes=self.host.numel(),
-                            host_off=self.host_off, dev_staging=self.staging.data_ptr(),
-                            staging_bytes=self.staging.numel(), ring_slots=self.ring_slots,
+                            plane_base=[p.ptr for p in self.planes],
+                            host_backing=self.host.ptr, host_bytes=self.host.nbytes,
+                            host_off=self.host_off, dev_staging=self.staging.ptr,
+                            staging_bytes=self.staging.nbytes, ring_slots=self.ring_slots,
                             device=self.device, timing=timing)
 
     def host_copy(self, agent: int) -> np.ndarray:
@@ -58,6 +108,23 @@ class PoolMemory:
         n = int(self.spec.agent_units[agent]) * self.spec.unit_bytes
         return self.host_np[off:off + n]
 
-    def unit_chunk(self, unit: int, plane: int) -> torch.Tensor:
-        cb = self.spec.chunk_bytes[plane]
-        return self.planes[plane][unit * cb:(unit + 1) * cb]
+    def units_bytes(self, units) -> np.ndarray:
+        """uint8 [K, unit_bytes] of the given physical units, read from the device
+        (whole planes when they are small, else chunk by chunk)."""
+        s = self.spec
+        units = np.asarray(units, dtype=np.int64)
+        out = np.empty((len(units), s.unit_bytes), dtype=np.uint8)
+        off = 0
+        for c, cb in enumerate(s.chunk_bytes):
+            if s.capacity_units * cb <= (256 << 20):
+                plane = self.planes[c].download(0, s.capacity_units * cb).reshape(-1, cb)
+                out[:, off:off + cb] = plane[units]
+            else:
+                for k, u in enumerate(units):
+                    out[k, off:off + cb] = self.planes[c].download(int(u) * cb, cb)
+            off += cb
+        return out
+
+    def free(self):
+        for b in self.planes + [self.staging, self.host]:
+            b.free()

@@ -11,12 +11,11 @@ import sys
 import time
 
 import numpy as np
-import torch
 
 import workloads as W
 from oracle import OraclePool
 from paper_2601_21473_amd import binding as B
-from paper_2601_21473_amd.memory import PoolMemory
+from paper_2601_21473_amd.memory import DeviceBuffer, PoolMemory
 
 S = W.SENTINEL
 POISON = 0xA5
@@ -27,12 +26,32 @@ def log(msg):
     sys.stdout.flush()
 
 
+class DeviceTrace:
+    """A trace's distances and masks resident in device memory; ``dist(t)``
+    and ``active(t)`` are the device addresses of step t's arrays."""
+
+    def __init__(self, trace, device=0):
+        self.N = trace.n_agents
+        d = np.ascontiguousarray(trace.dist, dtype=np.uint32)
+        a = np.ascontiguousarray(trace.active, dtype=np.uint8)
+        self.d = DeviceBuffer(d.nbytes, device)
+        self.a = DeviceBuffer(a.nbytes, device)
+        self.d.upload(d)
+        self.a.upload(a)
+
+    def dist(self, t):
+        return self.d.ptr + 4 * self.N * t
+
+    def active(self, t):
+        return self.a.ptr + self.N * t
+
+    def free(self):
+        self.d.free()
+        self.a.free()
+
+
 def upload_trace(trace, device=0):
-    dev = torch.device("cuda", device)
-    dist = torch.from_numpy(np.ascontiguousarray(trace.dist).view(np.int32)).to(dev)
-    act = torch.from_numpy(np.ascontiguousarray(trace.active)).to(dev)
-    torch.cuda.synchronize()
-    return dist, act
+    return DeviceTrace(trace, device)
 
 
 def fill_host(mem, content, spec, batch_bytes=256 << 20):
@@ -55,15 +74,6 @@ def fill_host(mem, content, spec, batch_bytes=256 << 20):
         a0 = a1
 
 
-def device_units(mem, spec, units):
-    """uint8 [K, unit_bytes] of the given physical units, read from the device."""
-    idx = torch.as_tensor(np.asarray(units, dtype=np.int64), device=mem.planes[0].device)
-    parts = []
-    for c, cb in enumerate(spec.chunk_bytes):
-        parts.append(mem.planes[c].view(spec.capacity_units, cb).index_select(0, idx))
-    return torch.cat(parts, dim=1).cpu().numpy()
-
-
 def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_bytes=True,
                slot_units=8, ring_slots=2, sample_units=None, bt_every=1, seed=0, label=""):
     spec = trace.pools[pool_index]
@@ -78,15 +88,15 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
         fill_host(mem, content, spec)
     pool = mem.make_pool(timing=True)
     opool = OraclePool(spec.capacity_units, spec.agent_units, ub)
-    dist, act = upload_trace(trace)
+    dev = upload_trace(trace)
     T = trace.n_steps if steps is None else steps
-    stream = torch.cuda.current_stream().cuda_stream
+    stream = 0
     rng = np.random.default_rng(seed + 99)
     units_i64 = spec.agent_units.astype(np.int64)
     moved = 0
     t0 = time.time()
     for t in range(T):
-        g = pool.plan_step(dist[t].data_ptr(), act[t].data_ptr(), theta, budget, stream)
+        g = pool.plan_step(dev.dist(t), dev.active(t), theta, budget, stream)
         o = opool.plan_step(trace.dist[t], trace.active[t], theta, budget)
         assert g["victims"].tolist() == o.victims.tolist(), (label, t, "victims")
         assert g["loads"].tolist() == o.loads.tolist(), (label, t, "loads")
@@ -96,7 +106,7 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
         assert g["bytes_out"] == o.bytes_out and g["bytes_in"] == o.bytes_in, (label, t)
         pool.evict_pack(stream)
         pool.prefetch_unpack(stream)
-        torch.cuda.synchronize()
+        pool.sync()
         moved += o.units_in + o.units_out
         if t % bt_every == 0 or t == T - 1:
             bt = pool.block_table_host_all()
@@ -116,7 +126,7 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
                 if sample_units is not None and len(U) > sample_units:
                     pick = rng.choice(len(U), sample_units, replace=False)
                     A, J, U = A[pick], J[pick], U[pick]
-                got = device_units(mem, spec, U)
+                got = mem.units_bytes(U)
                 exp = content.units_bytes(A, J)
                 bad = np.flatnonzero((got != exp).any(axis=1))
                 assert len(bad) == 0, (label, t, "device bytes", A[bad[:4]], J[bad[:4]])
@@ -124,6 +134,8 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
                 mem.host_copy(int(a))[:] = POISON
     st = pool.stats()
     pool.close()
+    dev.free()
+    mem.free()
     log(f"[parity] {label or trace.name}: {T} steps ok, {moved} units moved, "
         f"{time.time() - t0:.1f}s")
     return st

@@ -131,6 +131,19 @@ def test_null_arguments():
     L.ss_pool_destroy(None)
 
 
+def test_plumbing_argument_checks():
+    L = B.load()
+    p = C.c_void_p()
+    assert L.ss_device_alloc(0, 0, C.byref(p)) == B.SS_ERR_ARG
+    assert L.ss_host_alloc(0, C.byref(p)) == B.SS_ERR_ARG
+    assert L.ss_copy(None, None, 16) == B.SS_ERR_ARG
+    assert L.ss_device_free(None) == B.SS_OK
+    assert L.ss_host_free(None) == B.SS_OK
+    assert L.ss_sync(None) == B.SS_ERR_ARG
+    n = C.c_int32(-1)
+    assert L.ss_device_count(C.byref(n)) == B.SS_OK and n.value >= 0
+
+
 def test_probe_argument_checks():
     L = B.load()
     ms = C.c_float()
@@ -140,8 +153,7 @@ def test_probe_argument_checks():
 
 
 def test_no_device_is_an_argument_error_not_a_crash():
-    import torch
-    if torch.cuda.is_available():
+    if B.device_count() > 0:
         pytest.skip("a GPU is present")
     L = B.load()
     d, keep = _desc()
