@@ -124,6 +124,9 @@ typedef struct {                    /* cumulative since create or ss_reset_stats
     uint64_t d2h_bytes, h2d_bytes;
     double   d2h_ms, h2d_ms;               /* per step: first to last copy on its stream */
     double   plan_gpu_ms;                  /* event time of the plan kernels             */
+    double   plan_phase_us[7];             /* plan-core phases (classify, demand and
+                                              evictable sorts, candidate select, candidate
+                                              sort, acceptance, lists, free units)          */
 } ss_stats;
 
 /* Create a pool (Appendix A: register a memory module).  Validates every
@@ -142,8 +145,10 @@ void ss_pool_destroy(ss_pool* pool);
  * turns distances and the activation mask into victims and loads and updates
  * the block table.  `distances` [N] uint32 and `active` [N] uint8 (0/1) are
  * DEVICE pointers read during the call's kernels.  The call returns after the
- * plan is known on the host (one device-to-host readback); the block-table
- * update continues on the device and is ordered before the copy kernels.
+ * plan is known on the host (one device-to-host readback).  The block-table
+ * update that the plan implies is queued on the device by the next call that
+ * needs it (ss_evict_pack, ss_block_table*, ss_resident_host, ss_sync) and is
+ * ordered before the copy kernels.
  * Previous step's data movement is waited for on the device first.
  * SS_ERR_OVERCOMMIT if the active agents need more than capacity_units
  * (pool unchanged).  SS_ERR_ORDER if the previous step was not completed with
@@ -168,8 +173,9 @@ ss_status ss_prefetch_unpack(ss_pool* pool, void* stream);
 
 /* The device block table in CSR form: agent a's logical unit j is physical
  * unit (*d_units)[(*d_agent_off)[a] + j], or -1 when a is not resident.
- * Pool-owned device memory, valid until ss_pool_destroy; current after the
- * work of ss_plan_step has run on the device. */
+ * Pool-owned device memory, valid until ss_pool_destroy.  The call queues any
+ * pending block-table update; the table is current once that work has run
+ * (for instance after ss_sync). */
 ss_status ss_block_table(ss_pool* pool, const int32_t** d_units, const uint64_t** d_agent_off);
 
 /* Copy agent's block-table row to host (synchronous).  *n = agent's units;

@@ -58,7 +58,8 @@ class ss_stats(C.Structure):
                 ("unpack_launches", C.c_uint64), ("pack_bytes", C.c_uint64),
                 ("unpack_bytes", C.c_uint64), ("pack_ms", C.c_double), ("unpack_ms", C.c_double),
                 ("d2h_bytes", C.c_uint64), ("h2d_bytes", C.c_uint64), ("d2h_ms", C.c_double),
-                ("h2d_ms", C.c_double), ("plan_gpu_ms", C.c_double)]
+                ("h2d_ms", C.c_double), ("plan_gpu_ms", C.c_double),
+                ("plan_phase_us", C.c_double * 7)]
 
 
 class ScaleSimError(RuntimeError):
@@ -231,7 +232,9 @@ class Pool:
     def stats(self) -> dict:
         s = ss_stats()
         _check(load().ss_get_stats(self._h, C.byref(s)))
-        return {k: getattr(s, k) for k, _ in ss_stats._fields_}
+        out = {k: getattr(s, k) for k, _ in ss_stats._fields_}
+        out["plan_phase_us"] = list(out["plan_phase_us"])
+        return out
 
     def reset_stats(self):
         _check(load().ss_reset_stats(self._h))

@@ -70,7 +70,22 @@ struct PlanArgs {
     PlanResult* res_host;           // mapped pinned host
     unsigned* victims_host;         // mapped pinned host [N]
     unsigned* loads_host;           // mapped pinned host [N]
+    unsigned fused;                 // 1: the plan core classifies the agents itself
+    unsigned pad2;
+    u64* phase;                     // [kPlanPhases] wall-clock stamps of the plan core, or null
+    u64* hist_w;                    // [kDistBuckets] candidate units per distance bucket
 };
+
+// Candidate distance histogram: bucket(d) = d below 1024, then 32 buckets per
+// power of two (monotone in d).
+constexpr unsigned kDistBuckets = 2048;
+__host__ __device__ inline unsigned dist_bucket(unsigned d) {
+    if (d < 1024u) return d;
+    const unsigned p = 31u - (unsigned)__builtin_clz(d);
+    return 1024u + 32u * (p - 10u) + ((d >> (p - 5u)) & 31u);
+}
+
+constexpr int kPlanPhases = 10;
 
 struct BtArgs {
     const PlanResult* res;
@@ -111,6 +126,7 @@ constexpr int kLdsKeys = 16384;                   // 128 KiB of u64 keys in LDS
 hipError_t launch_classify(const PlanArgs& a, hipStream_t st);
 hipError_t launch_plan_core(const PlanArgs& a, hipStream_t st);
 hipError_t launch_bt_update(const BtArgs& a, unsigned n_agents, hipStream_t st);
+constexpr unsigned kFuseAgents = 16384;           // plan core classifies up to this many
 hipError_t launch_pack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_unpack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_zero_u32(unsigned* p, u64 n, hipStream_t st);

@@ -64,8 +64,10 @@ __device__ __forceinline__ void wave_append(bool pred, u64 key, u64* list, unsig
     if (pred) list[base + mbcnt(mask)] = key;
 }
 
-__global__ void __launch_bounds__(256) k_classify(PlanArgs A) {
-    const unsigned a = blockIdx.x * 256u + threadIdx.x;
+// Classify agent a (a >= n: no agent) and add it to the lists and sums kept
+// in `cnt` (global memory for the multi-block kernel, LDS in the fused plan
+// core).  Every lane of the wave must call it.
+__device__ __forceinline__ void classify_agent(const PlanArgs& A, unsigned a, PlanCounters* cnt) {
     const bool valid = a < A.n;
     unsigned D = 0;
     bool act = false, res = false;
@@ -81,21 +83,88 @@ __global__ void __launch_bounds__(256) k_classify(PlanArgs A) {
     const bool isE = valid && res && !act;            // evictable resident
     const bool isL = valid && act && !res;            // demand load
     const bool isC = valid && !res && !act && D < A.threshold;   // prefetch candidate
-    wave_append(isE, key, A.listE, &A.cnt->n_E);
-    wave_append(isL, key, A.listL, &A.cnt->n_L);
-    wave_append(isC, key, A.listC, &A.cnt->n_C);
+    if (isC) atomicAdd(&A.hist_w[dist_bucket(D)], s);
+    wave_append(isE, key, A.listE, &cnt->n_E);
+    wave_append(isL, key, A.listL, &cnt->n_L);
+    wave_append(isC, key, A.listC, &cnt->n_C);
     const u64 s_act = wave_sum(act ? s : 0);
     const u64 s_res = wave_sum(res ? s : 0);
     const u64 s_dem = wave_sum(isL ? s : 0);
     const u64 s_evi = wave_sum(isE ? s : 0);
     const u64 s_can = wave_sum(isC ? s : 0);
     if (lane_id() == 0) {
-        if (s_act) atomicAdd(&A.cnt->sum_active, s_act);
-        if (s_res) atomicAdd(&A.cnt->sum_resident, s_res);
-        if (s_dem) atomicAdd(&A.cnt->sum_demand, s_dem);
-        if (s_evi) atomicAdd(&A.cnt->sum_evictable, s_evi);
-        if (s_can) atomicAdd(&A.cnt->sum_cand, s_can);
+        if (s_act) atomicAdd(&cnt->sum_active, s_act);
+        if (s_res) atomicAdd(&cnt->sum_resident, s_res);
+        if (s_dem) atomicAdd(&cnt->sum_demand, s_dem);
+        if (s_evi) atomicAdd(&cnt->sum_evictable, s_evi);
+        if (s_can) atomicAdd(&cnt->sum_cand, s_can);
     }
+}
+
+// Block-local slot of this lane in a list (one LDS atomic per wave).
+__device__ __forceinline__ unsigned wave_reserve(bool pred, unsigned* counter) {
+    const u64 mask = __ballot(pred);
+    if (mask == 0) return 0;                         // wave-uniform
+    unsigned base = 0;
+    if (lane_id() == 0) base = atomicAdd(counter, (unsigned)__popcll(mask));
+    return __shfl(base, 0) + mbcnt(mask);
+}
+
+// Multi-block classification: counts and sums are gathered per block in LDS
+// and reach the global counters with one atomic per block and counter.
+__global__ void __launch_bounds__(256) k_classify(PlanArgs A) {
+    __shared__ PlanCounters lc;
+    __shared__ unsigned gbase[3];
+    const unsigned a = blockIdx.x * 256u + threadIdx.x;
+    if (threadIdx.x == 0) lc = PlanCounters{};
+    __syncthreads();
+    const bool valid = a < A.n;
+    unsigned D = 0;
+    bool act = false, res = false;
+    u64 s = 0;
+    if (valid) {
+        D = A.dist[a];
+        act = A.active[a] != 0;
+        res = A.resident[a] != 0;
+        s = A.units[a];
+    }
+    const u64 d = act ? 0ull : (u64)D;
+    const u64 key = (d << A.idbits) | a;
+    const bool isE = valid && res && !act;
+    const bool isL = valid && act && !res;
+    const bool isC = valid && !res && !act && D < A.threshold;
+    if (isC) atomicAdd(&A.hist_w[dist_bucket(D)], s);
+    const unsigned oE = wave_reserve(isE, &lc.n_E);
+    const unsigned oL = wave_reserve(isL, &lc.n_L);
+    const unsigned oC = wave_reserve(isC, &lc.n_C);
+    const u64 s_act = wave_sum(act ? s : 0);
+    const u64 s_res = wave_sum(res ? s : 0);
+    const u64 s_dem = wave_sum(isL ? s : 0);
+    const u64 s_evi = wave_sum(isE ? s : 0);
+    const u64 s_can = wave_sum(isC ? s : 0);
+    if (lane_id() == 0) {
+        atomicAdd(&lc.sum_active, s_act);
+        atomicAdd(&lc.sum_resident, s_res);
+        atomicAdd(&lc.sum_demand, s_dem);
+        atomicAdd(&lc.sum_evictable, s_evi);
+        atomicAdd(&lc.sum_cand, s_can);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        PlanCounters* g = A.cnt;
+        gbase[0] = lc.n_E ? atomicAdd(&g->n_E, lc.n_E) : 0;
+        gbase[1] = lc.n_L ? atomicAdd(&g->n_L, lc.n_L) : 0;
+        gbase[2] = lc.n_C ? atomicAdd(&g->n_C, lc.n_C) : 0;
+        if (lc.sum_active) atomicAdd(&g->sum_active, lc.sum_active);
+        if (lc.sum_resident) atomicAdd(&g->sum_resident, lc.sum_resident);
+        if (lc.sum_demand) atomicAdd(&g->sum_demand, lc.sum_demand);
+        if (lc.sum_evictable) atomicAdd(&g->sum_evictable, lc.sum_evictable);
+        if (lc.sum_cand) atomicAdd(&g->sum_cand, lc.sum_cand);
+    }
+    __syncthreads();
+    if (isE) A.listE[gbase[0] + oE] = key;
+    if (isL) A.listL[gbase[1] + oL] = key;
+    if (isC) A.listC[gbase[2] + oC] = key;
 }
 
 // ---------------------------------------------------------------------------
@@ -103,6 +172,7 @@ __global__ void __launch_bounds__(256) k_classify(PlanArgs A) {
 // ---------------------------------------------------------------------------
 
 struct CoreShared {
+    PlanCounters cnt;               // fused classification
     u64 wsum[kCoreThreads / 64 + 1];
     u64 hist[256];
     unsigned hcnt[256];
@@ -173,6 +243,81 @@ __device__ void bitonic_asc(u64* buf, unsigned npad) {
     }
 }
 
+__device__ __forceinline__ void cmp_keep(u64& x, u64 p, bool keep_min) {
+    x = keep_min ? (p < x ? p : x) : (p > x ? p : x);
+}
+
+// Compare-exchange of the pairs (r, r | JR) a thread holds in registers
+// (element index i = t + 1024 r; partner i ^ (JR << 10)).
+constexpr unsigned kRegKeys = 8;                  // keys per thread in the register sort
+
+template <unsigned JR>
+__device__ __forceinline__ void reg_stage(u64 (&x)[kRegKeys], unsigned E, unsigned t, unsigned k) {
+#pragma unroll
+    for (unsigned r = 0; r < kRegKeys; ++r) {
+        if ((r & JR) == 0 && (r | JR) < E) {
+            const bool asc = ((t + (r << 10)) & k) == 0;
+            const u64 a = x[r], b = x[r | JR];
+            if ((a > b) == asc) {
+                x[r] = b;
+                x[r | JR] = a;
+            }
+        }
+    }
+}
+
+// Ascending bitonic sort of lds[0..npad), npad a power of two <= 1024 *
+// kRegKeys, by a 1024-thread block.  Thread t keeps elements t + 1024 r in registers:
+// stages with stride >= 1024 stay inside the thread, strides 64..512 go
+// through LDS (two barriers each), strides < 64 are wave shuffles.
+__device__ void bitonic_lds_fast(u64* lds, unsigned npad) {
+    const unsigned t = threadIdx.x;
+    const unsigned E = npad > 1024 ? npad >> 10 : 1;
+    u64 x[kRegKeys];
+#pragma unroll
+    for (unsigned r = 0; r < kRegKeys; ++r) {
+        const unsigned i = t + (r << 10);
+        x[r] = (r < E && i < npad) ? lds[i] : ~0ull;
+    }
+    for (unsigned k = 2; k <= npad; k <<= 1) {
+        for (unsigned j = k >> 1; j > 0; j >>= 1) {
+            if (j >= 1024) {
+                if (j == 1024) reg_stage<1>(x, E, t, k);
+                else if (j == 2048) reg_stage<2>(x, E, t, k);
+                else reg_stage<4>(x, E, t, k);
+            } else if (j >= 64) {
+#pragma unroll
+                for (unsigned r = 0; r < kRegKeys; ++r) {
+                    const unsigned i = t + (r << 10);
+                    if (r < E && i < npad) lds[i] = x[r];
+                }
+                __syncthreads();
+#pragma unroll
+                for (unsigned r = 0; r < kRegKeys; ++r) {
+                    const unsigned i = t + (r << 10);
+                    if (r < E && i < npad) cmp_keep(x[r], lds[i ^ j], ((i & j) == 0) == ((i & k) == 0));
+                }
+                __syncthreads();
+            } else {
+#pragma unroll
+                for (unsigned r = 0; r < kRegKeys; ++r) {
+                    if (r < E) {
+                        const unsigned i = t + (r << 10);
+                        const u64 p = __shfl_xor(x[r], (int)j);
+                        cmp_keep(x[r], p, ((i & j) == 0) == ((i & k) == 0));
+                    }
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (unsigned r = 0; r < kRegKeys; ++r) {
+        const unsigned i = t + (r << 10);
+        if (r < E && i < npad) lds[i] = x[r];
+    }
+    __syncthreads();
+}
+
 // Sort the keys src[i] < kstar (there are exactly m of them) ascending into
 // dst[0..m).  dst has room for pow2ceil(N) keys and doubles as the sort buffer
 // when m exceeds the LDS budget.
@@ -196,10 +341,35 @@ __device__ void select_sort(const u64* src, unsigned n_src, u64 kstar, unsigned 
     }
     for (unsigned i = m + threadIdx.x; i < npad; i += blockDim.x) buf[i] = ~0ull;
     __syncthreads();
-    bitonic_asc(buf, npad);
+    if (npad <= 1024 * kRegKeys) bitonic_lds_fast(lds, npad);
+    else bitonic_asc(buf, npad);
     if (buf == lds) {
         for (unsigned i = threadIdx.x; i < m; i += blockDim.x) dst[i] = lds[i];
         __syncthreads();
+    }
+}
+
+// Add (bin, w) of every lane with `valid` to the LDS histogram.  Lanes that
+// share a bin are summed first (a few rounds of leader election), so heavily
+// concentrated digits cost one atomic per bin and wave; whatever is left after
+// four rounds (spread digits) goes through plain atomics.
+__device__ __forceinline__ void hist_add(CoreShared& S, bool valid, unsigned bin, u64 w) {
+    const unsigned l = lane_id();
+    u64 active = __ballot(valid);
+    for (int round = 0; round < 4 && active; ++round) {
+        const unsigned leader = (unsigned)__ffsll((long long)active) - 1;
+        const unsigned lb = __shfl(bin, leader);
+        const u64 same = __ballot(valid && bin == lb) & active;
+        const u64 sum = wave_sum(((same >> l) & 1) ? w : 0);
+        if (l == leader) {
+            atomicAdd(&S.hist[lb], sum);
+            atomicAdd(&S.hcnt[lb], (unsigned)__popcll(same));
+        }
+        active &= ~same;
+    }
+    if ((active >> l) & 1) {
+        atomicAdd(&S.hist[bin], w);
+        atomicAdd(&S.hcnt[bin], 1u);
     }
 }
 
@@ -230,13 +400,11 @@ __device__ u64 weighted_select(const u64* keys, unsigned n, const unsigned* unit
             S.hcnt[b] = 0;
         }
         __syncthreads();
-        for (unsigned i = threadIdx.x; i < n; i += blockDim.x) {
-            const u64 k = keys[i];
-            if ((k & pmask) == prefix) {
-                const unsigned b = (unsigned)(k >> shift) & 255u;
-                atomicAdd(&S.hist[b], (u64)units[k & idmask]);
-                atomicAdd(&S.hcnt[b], 1u);
-            }
+        for (unsigned base = 0; base < n; base += blockDim.x) {
+            const unsigned i = base + threadIdx.x;
+            const u64 k = i < n ? keys[i] : 0;
+            const bool in = i < n && (k & pmask) == prefix;
+            hist_add(S, in, (unsigned)(k >> shift) & 255u, in ? (u64)units[k & idmask] : 0);
         }
         __syncthreads();
         if (threadIdx.x < 64) {
@@ -290,18 +458,30 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
     __shared__ u64 lds[kLdsKeys];
     __shared__ CoreShared S;
     const unsigned tid = threadIdx.x;
-    const PlanCounters c = *A.cnt;
+    auto stamp = [&](int k) {
+        if (A.phase && tid == 0) A.phase[k] = wall_clock64();
+    };
+    stamp(0);
     const u64 idmask = (1ull << A.idbits) - 1;
     const unsigned* units = A.units;
+    if (A.fused) {
+        if (tid == 0) S.cnt = PlanCounters{};
+        __syncthreads();
+        for (unsigned base = 0; base < A.n; base += blockDim.x) classify_agent(A, base + tid, &S.cnt);
+        __syncthreads();
+    }
+    const PlanCounters c = A.fused ? S.cnt : *A.cnt;
     __syncthreads();
+    stamp(1);
 
     if (c.sum_active > A.capacity) {                 // overcommit: change nothing
+        for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
         if (tid == 0) {
             PlanResult r = {};
             r.status = 1;
             *A.res = r;
             *A.res_host = r;
-            *A.cnt = PlanCounters{};
+            if (!A.fused) *A.cnt = PlanCounters{};
         }
         return;
     }
@@ -316,6 +496,7 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
     block_prefix(nE, [&](unsigned i) { return (u64)units[sortE[nE - 1 - i] & idmask]; },
                  A.prefE, S);
     block_prefix(nL, [&](unsigned i) { return (u64)units[A.sortL[i] & idmask]; }, A.loff, S);
+    stamp(2);
 
     // demand victims: shortest prefix of the eviction order covering `need`
     if (tid == 0) {
@@ -337,17 +518,86 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
     const u64 avail = free1 + (A.prefE[nE] - A.prefE[n_d]);
     const u64 cap = A.budget < avail ? A.budget : avail;
 
-    // candidates whose cumulative units can stay within cap, sorted by key
+    // candidates whose cumulative units can stay within cap, sorted by key:
+    // the distance histogram gives the bucket where the cumulative units pass
+    // cap; the candidates up to that bucket are sorted and the prefix that
+    // fits is kept (radix select when that set is larger than the LDS buffer)
     unsigned m = nC;
     u64 kstar = ~0ull;
-    if (c.sum_cand > cap) kstar = weighted_select(A.listC, nC, units, idmask, cap, S, &m);
-    select_sort(A.listC, nC, kstar, m, A.sortC, lds, S);
+    bool sorted = false;
+    if (c.sum_cand > cap) {
+        u64 carry_w = 0;
+        if (tid == 0) S.uscal[5] = kDistBuckets;
+        __syncthreads();
+        for (unsigned b0 = 0; b0 < kDistBuckets; b0 += blockDim.x) {
+            const unsigned b = b0 + tid;
+            const u64 w = b < kDistBuckets ? A.hist_w[b] : 0;
+            u64 tw;
+            const u64 ew = block_excl_scan(w, S, &tw);
+            if (b < kDistBuckets && carry_w + ew <= cap && carry_w + ew + w > cap)
+                S.uscal[5] = b;                       // crossing bucket (unique)
+            carry_w += tw;
+        }
+        __syncthreads();
+        const unsigned bstar = S.uscal[5];
+        // candidates up to the crossing bucket into LDS (count them on the way)
+        if (tid == 0) S.uscal[7] = 0;
+        __syncthreads();
+        for (unsigned i = tid; i < nC; i += blockDim.x) {
+            const u64 k = A.listC[i];
+            if (dist_bucket((unsigned)(k >> A.idbits)) <= bstar) {
+                const unsigned pos = atomicAdd(&S.uscal[7], 1u);
+                if (pos < (unsigned)kLdsKeys) lds[pos] = k;
+            }
+        }
+        __syncthreads();
+        const unsigned mprime = S.uscal[7];
+        if (bstar < kDistBuckets && mprime > 0 && mprime <= (unsigned)kLdsKeys) {
+            const unsigned npad = pow2ceil(mprime);
+            for (unsigned i = mprime + tid; i < npad; i += blockDim.x) lds[i] = ~0ull;
+            __syncthreads();
+            if (npad <= 1024 * kRegKeys) bitonic_lds_fast(lds, npad);
+            else bitonic_asc(lds, npad);
+            // inclusive prefix of units over the sorted keys; m = count <= cap
+            u64 carry = 0;
+            if (tid == 0) S.uscal[4] = mprime;
+            __syncthreads();
+            for (unsigned b0 = 0; b0 < mprime; b0 += blockDim.x) {
+                const unsigned i = b0 + tid;
+                const u64 w = i < mprime ? (u64)units[lds[i] & idmask] : 0;
+                u64 tot;
+                const u64 ex = block_excl_scan(w, S, &tot);
+                if (i < mprime && carry + ex <= cap && carry + ex + w > cap) S.uscal[4] = i;
+                carry += tot;
+            }
+            __syncthreads();
+            m = S.uscal[4];
+            for (unsigned i = tid; i < m; i += blockDim.x) A.sortC[i] = lds[i];
+            __syncthreads();
+            sorted = true;
+        } else {
+            kstar = weighted_select(A.listC, nC, units, idmask, cap, S, &m);
+        }
+        // the histogram starts the next step at zero
+        for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
+    } else {
+        for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
+    }
+    stamp(3);
+    if (!sorted) select_sort(A.listC, nC, kstar, m, A.sortC, lds, S);
     const u64* sortC = A.sortC;
     block_prefix(m, [&](unsigned i) { return (u64)units[sortC[i] & idmask]; }, A.prefC, S);
+    stamp(4);
 
     // acceptance: S_i <= budget and S_i <= free1 + (units of the remaining
     // evictable residents with distance strictly larger than d_i)
     if (tid == 0) S.uscal[3] = m;
+    // the evictable keys in LDS for the searches below (the sort buffer is free)
+    const u64* keysE = sortE;
+    if (nE <= (unsigned)kLdsKeys) {
+        for (unsigned i = tid; i < nE; i += blockDim.x) lds[i] = sortE[i];
+        keysE = lds;
+    }
     __syncthreads();
     for (unsigned i = tid; i < m; i += blockDim.x) {
         const u64 di = sortC[i] >> A.idbits;
@@ -355,13 +605,14 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
         unsigned lo = 0, hi = nE;                    // first eviction index with d <= di
         while (lo < hi) {
             const unsigned mid = (lo + hi) >> 1;
-            if ((sortE[nE - 1 - mid] >> A.idbits) > di) lo = mid + 1; else hi = mid;
+            if ((keysE[nE - 1 - mid] >> A.idbits) > di) lo = mid + 1; else hi = mid;
         }
         const u64 G = lo > n_d ? A.prefE[lo] - A.prefE[n_d] : 0;
         const bool ok = Si <= A.budget && Si <= free1 + G;
         if (!ok) atomicMin(&S.uscal[3], i);
     }
     __syncthreads();
+    stamp(5);
     const unsigned n_p = S.uscal[3];
     if (tid == 0) {
         unsigned n_v = n_d;
@@ -389,6 +640,7 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
         A.victims_host[i] = v;
         A.resident[v] = 0;
     }
+
     for (unsigned i = tid; i < n_l; i += blockDim.x) {
         const unsigned a = (unsigned)((i < nL ? A.sortL[i] : sortC[i - nL]) & idmask);
         A.loads[i] = a;
@@ -397,6 +649,7 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
         if (i >= nL) A.loff[i + 1] = c.sum_demand + A.prefC[i - nL + 1];
     }
 
+    stamp(6);
     // pre-step free units in ascending order, as many as the loads can use
     const u64 n_free_used = units_in < free_before ? units_in : free_before;
     if (n_free_used > 0) {
@@ -419,6 +672,7 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
     }
 
     __syncthreads();
+    stamp(7);
     if (tid == 0) {
         PlanResult r = {};
         r.status = 0;
@@ -432,7 +686,7 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
         r.n_free_used = n_free_used;
         *A.res = r;
         *A.res_host = r;
-        *A.cnt = PlanCounters{};
+        if (!A.fused) *A.cnt = PlanCounters{};
     }
 }
 
@@ -440,6 +694,9 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
 // block table
 // ---------------------------------------------------------------------------
 
+// Release the victims' units (one block per victim): record them in eviction
+// order for the pack and the loads, clear the block-table entries and the
+// occupancy bits.
 __global__ void __launch_bounds__(256) k_bt_victims(BtArgs B) {
     if (B.res->status != 0) return;
     const unsigned nv = B.res->n_victims;
@@ -458,6 +715,8 @@ __global__ void __launch_bounds__(256) k_bt_victims(BtArgs B) {
     }
 }
 
+// Hand units to the loads (one block per load): the pre-step free units
+// first, then the victims' units in eviction order.
 __global__ void __launch_bounds__(256) k_bt_loads(BtArgs B) {
     if (B.res->status != 0) return;
     const unsigned nl = B.res->n_loads;

@@ -85,6 +85,10 @@ struct ss_pool {
     unsigned *d_victims = nullptr, *d_loads = nullptr;
     int *d_vunits = nullptr, *d_lunits = nullptr, *d_free_old = nullptr;
     PlanResult* d_res = nullptr;
+    u64* d_phase = nullptr;
+    u64* d_hist_w = nullptr;
+    bool phase_pending = false;
+    double us_per_tick = 0.01;     // device wall clock
     CopyItem* d_items = nullptr;
     unsigned n_items = 0;
     u64* d_plane_base = nullptr;
@@ -117,6 +121,7 @@ struct ss_pool {
 
     State state = kIdle;
     bool poisoned = false;
+    bool bt_pending = false;     // block-table update of the last plan not yet queued
 };
 
 namespace {
@@ -164,7 +169,8 @@ void free_pool(ss_pool* p) {
     void* dptrs[] = {p->d_units, p->d_agent_off, p->d_bt, p->d_resident, p->d_occ, p->d_cnt,
                      p->d_listE, p->d_listC, p->d_listL, p->d_sortE, p->d_sortC, p->d_sortL,
                      p->d_prefE, p->d_prefC, p->d_loff, p->d_victims, p->d_loads, p->d_vunits,
-                     p->d_lunits, p->d_free_old, p->d_res, p->d_items, p->d_plane_base,
+                     p->d_lunits, p->d_free_old, p->d_res, p->d_phase, p->d_hist_w,
+                     p->d_items, p->d_plane_base,
                      p->d_chunk_bytes};
     for (void* d : dptrs)
         if (d) (void)hipFree(d);
@@ -272,6 +278,47 @@ bool pinned_range_ok(const void* ptr, u64 bytes) {
 ss_status check_usable(ss_pool* p) {
     if (!p) return set_err(SS_ERR_ARG, "pool is NULL");
     if (p->poisoned) return set_err(SS_ERR_POISONED, "pool is poisoned by an earlier HIP failure");
+    return SS_OK;
+}
+
+// Fold the finished previous step's copy events and this plan's event time
+// and phase stamps into the stats (timing mode).  The previous step's work
+// completed before this plan's kernels ran, and the plan kernels completed
+// before ss_plan_step returned.
+ss_status collect_plan_timing(ss_pool* p) {
+    if (!(p->flags & SS_FLAG_TIMING)) return SS_OK;
+    collect_timing(p);
+    if (p->phase_pending) {
+        p->phase_pending = false;
+        u64 ph[kPlanPhases];
+        TRY_HIP(p, hipMemcpy(ph, p->d_phase, sizeof ph, hipMemcpyDeviceToHost), true);
+        for (int k = 1; k < 8; ++k)
+            if (ph[k] >= ph[k - 1])
+                p->stats.plan_phase_us[k - 1] += (double)(ph[k] - ph[k - 1]) * p->us_per_tick;
+    }
+    return SS_OK;
+}
+
+// Queue the block-table update of the last plan on the out stream (once).
+ss_status flush_bt(ss_pool* p) {
+    if (!p->bt_pending) return SS_OK;
+    BtArgs B{};
+    B.res = p->d_res;
+    B.victims = p->d_victims;
+    B.loads = p->d_loads;
+    B.units = p->d_units;
+    B.agent_off = p->d_agent_off;
+    B.bt = p->d_bt;
+    B.occ = p->d_occ;
+    B.voff = p->d_prefE;
+    B.loff = p->d_loff;
+    B.free_old = p->d_free_old;
+    B.vunits = p->d_vunits;
+    B.lunits = p->d_lunits;
+    B.capacity = p->U;
+    p->bt_pending = false;
+    TRY_HIP(p, launch_bt_update(B, p->N, p->st_out), true);
+    TRY_HIP(p, hipEventRecord(p->ev_bt, p->st_out), true);
     return SS_OK;
 }
 
@@ -404,6 +451,14 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(dalloc(&p->d_lunits, U));
     CREATE_TRY(dalloc(&p->d_free_old, U));
     CREATE_TRY(dalloc(&p->d_res, 1));
+    CREATE_TRY(dalloc(&p->d_phase, kPlanPhases));
+    CREATE_TRY(dalloc(&p->d_hist_w, kDistBuckets));
+    {
+        int khz = 0;
+        if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, p->device) == hipSuccess &&
+            khz > 0)
+            p->us_per_tick = 1000.0 / khz;
+    }
     CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_res), sizeof(PlanResult),
                              hipHostMallocMapped));
     CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_victims), N * sizeof(unsigned),
@@ -449,6 +504,10 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(hipMemcpy(p->d_occ, occ.data(), occ.size() * sizeof(unsigned), hipMemcpyHostToDevice));
     CREATE_TRY(hipMemcpy(p->d_resident, zeros_n.data(), N, hipMemcpyHostToDevice));
     CREATE_TRY(hipMemcpy(p->d_cnt, &zc, sizeof zc, hipMemcpyHostToDevice));
+    {
+        std::vector<u64> zw(kDistBuckets, 0);
+        CREATE_TRY(hipMemcpy(p->d_hist_w, zw.data(), kDistBuckets * sizeof(u64), hipMemcpyHostToDevice));
+    }
     CREATE_TRY(hipMemcpy(p->d_items, items.data(), items.size() * sizeof(CopyItem),
                          hipMemcpyHostToDevice));
     CREATE_TRY(hipMemcpy(p->d_plane_base, bases.data(), p->P * sizeof(u64), hipMemcpyHostToDevice));
@@ -526,35 +585,24 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     A.res_host = p->h_res_dev;
     A.victims_host = p->h_victims_dev;
     A.loads_host = p->h_loads_dev;
+    A.fused = p->N <= kFuseAgents ? 1u : 0u;
+    A.phase = (p->flags & SS_FLAG_TIMING) ? p->d_phase : nullptr;
+    A.hist_w = p->d_hist_w;
 
     const bool timing = p->flags & SS_FLAG_TIMING;
     if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.a, p->st_out), true);
-    TRY_HIP(p, launch_classify(A, p->st_out), true);
+    if (!A.fused) TRY_HIP(p, launch_classify(A, p->st_out), true);
     TRY_HIP(p, launch_plan_core(A, p->st_out), true);
     if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.b, p->st_out), true);
     TRY_HIP(p, hipEventRecord(p->ev_planned, p->st_out), true);
 
-    BtArgs B{};
-    B.res = p->d_res;
-    B.victims = p->d_victims;
-    B.loads = p->d_loads;
-    B.units = p->d_units;
-    B.agent_off = p->d_agent_off;
-    B.bt = p->d_bt;
-    B.occ = p->d_occ;
-    B.voff = p->d_prefE;
-    B.loff = p->d_loff;
-    B.free_old = p->d_free_old;
-    B.vunits = p->d_vunits;
-    B.lunits = p->d_lunits;
-    B.capacity = p->U;
-    TRY_HIP(p, launch_bt_update(B, p->N, p->st_out), true);
-    TRY_HIP(p, hipEventRecord(p->ev_bt, p->st_out), true);
-
     TRY_HIP(p, hipEventSynchronize(p->ev_planned), true);
-    // the previous step finished before the plan kernels ran
-    collect_timing(p);
-    if (timing) p->t_plan_used = true;
+    // event times of the previous step and of this plan are folded into the
+    // stats by ss_evict_pack, off the path that returns the plan
+    if (timing) {
+        p->t_plan_used = true;
+        p->phase_pending = true;
+    }
 
     const PlanResult r = *p->h_res;
     if (r.status == 1) {
@@ -562,6 +610,7 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
                        (unsigned long long)p->U);
     }
     p->res = r;
+    p->bt_pending = true;
     p->voff.resize(r.n_victims + 1);
     p->loff.resize(r.n_loads + 1);
     p->voff[0] = 0;
@@ -591,6 +640,10 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
     if (st) return st;
     if (p->state != kPlanned) return set_err(SS_ERR_ORDER, "ss_evict_pack must follow ss_plan_step");
     DeviceGuard g(p->device);
+    st = flush_bt(p);
+    if (st) return st;
+    st = collect_plan_timing(p);
+    if (st) return st;
     hipStream_t caller = static_cast<hipStream_t>(stream);
     const bool timing = p->flags & SS_FLAG_TIMING;
     TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
@@ -722,6 +775,11 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
 
 ss_status ss_block_table(ss_pool* p, const int32_t** d_units, const uint64_t** d_agent_off) {
     if (!p || !d_units || !d_agent_off) return set_err(SS_ERR_ARG, "NULL argument");
+    if (!p->poisoned) {
+        DeviceGuard g(p->device);
+        ss_status st = flush_bt(p);
+        if (st) return st;
+    }
     *d_units = p->d_bt;
     *d_agent_off = reinterpret_cast<const uint64_t*>(p->d_agent_off);
     return SS_OK;
@@ -735,6 +793,8 @@ ss_status ss_block_table_host(ss_pool* p, uint32_t agent, int32_t* out, uint32_t
     *n = s;
     if (cap < s) return set_err(SS_ERR_ARG, "cap %u < %u units", cap, s);
     DeviceGuard g(p->device);
+    st = flush_bt(p);
+    if (st) return st;
     u64 off = 0;
     for (uint32_t a = 0; a < agent; ++a) off += p->s[a];
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
@@ -752,6 +812,8 @@ ss_status ss_block_table_host_all(ss_pool* p, int32_t* out, uint64_t cap, uint64
     if (cap < total) return set_err(SS_ERR_ARG, "cap %llu < %llu entries", (unsigned long long)cap,
                                     (unsigned long long)total);
     DeviceGuard g(p->device);
+    st = flush_bt(p);
+    if (st) return st;
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
     TRY_HIP(p, hipMemcpy(out, p->d_bt, total * sizeof(int32_t), hipMemcpyDeviceToHost), false);
     return SS_OK;
@@ -762,6 +824,8 @@ ss_status ss_resident_host(ss_pool* p, uint8_t* out) {
     if (st) return st;
     if (!out) return set_err(SS_ERR_ARG, "NULL output");
     DeviceGuard g(p->device);
+    st = flush_bt(p);
+    if (st) return st;
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
     TRY_HIP(p, hipMemcpy(out, p->d_resident, p->N, hipMemcpyDeviceToHost), false);
     return SS_OK;
@@ -772,7 +836,8 @@ ss_status ss_get_stats(ss_pool* p, ss_stats* out) {
     DeviceGuard g(p->device);
     for (hipStream_t s : {p->st_out, p->st_in})
         TRY_HIP(p, hipStreamSynchronize(s), false);
-    collect_timing(p);
+    ss_status st = collect_plan_timing(p);
+    if (st) return st;
     *out = p->stats;
     return SS_OK;
 }
@@ -782,14 +847,18 @@ ss_status ss_reset_stats(ss_pool* p) {
     DeviceGuard g(p->device);
     for (hipStream_t s : {p->st_out, p->st_in})
         TRY_HIP(p, hipStreamSynchronize(s), false);
-    collect_timing(p);
+    ss_status st = collect_plan_timing(p);
+    if (st) return st;
     p->stats = ss_stats{};
     return SS_OK;
 }
 
 ss_status ss_sync(ss_pool* p) {
-    if (!p) return set_err(SS_ERR_ARG, "NULL pool");
+    ss_status st = check_usable(p);
+    if (st) return st;
     DeviceGuard g(p->device);
+    st = flush_bt(p);
+    if (st) return st;
     for (hipStream_t s : {p->st_out, p->st_in})
         TRY_HIP(p, hipStreamSynchronize(s), true);
     return SS_OK;
