@@ -127,6 +127,8 @@ typedef struct {                    /* cumulative since create or ss_reset_stats
     double   plan_phase_us[7];             /* plan-core phases (classify, demand and
                                               evictable sorts, candidate select, candidate
                                               sort, acceptance, lists, free units)          */
+    double   plan_host_us[3];              /* ss_plan_step on the host: queueing the plan,
+                                              waiting for it, reading it back              */
 } ss_stats;
 
 /* Create a pool (Appendix A: register a memory module).  Validates every

@@ -59,7 +59,7 @@ class ss_stats(C.Structure):
                 ("unpack_bytes", C.c_uint64), ("pack_ms", C.c_double), ("unpack_ms", C.c_double),
                 ("d2h_bytes", C.c_uint64), ("h2d_bytes", C.c_uint64), ("d2h_ms", C.c_double),
                 ("h2d_ms", C.c_double), ("plan_gpu_ms", C.c_double),
-                ("plan_phase_us", C.c_double * 7)]
+                ("plan_phase_us", C.c_double * 7), ("plan_host_us", C.c_double * 3)]
 
 
 class ScaleSimError(RuntimeError):
@@ -234,6 +234,7 @@ class Pool:
         _check(load().ss_get_stats(self._h, C.byref(s)))
         out = {k: getattr(s, k) for k, _ in ss_stats._fields_}
         out["plan_phase_us"] = list(out["plan_phase_us"])
+        out["plan_host_us"] = list(out["plan_host_us"])
         return out
 
     def reset_stats(self):

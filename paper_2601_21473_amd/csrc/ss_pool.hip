@@ -13,16 +13,21 @@
 // units in eviction order, so slot k of the loads depends on a single pack
 // slot.  The next step's plan waits for both streams.
 //
-// Two streams (plus the caller's) fit in the four hardware queues the HIP
-// runtime gives a process by default, so the two directions never share a
-// queue with each other.
+// The two streams are shared by all pools of a device, so any number of pools
+// (plus the caller's stream) fits in the four hardware queues the HIP runtime
+// gives a process by default and the two directions never share a queue.
+// Every cross-stream wait refers to an event recorded earlier in host order,
+// so sharing cannot form a cycle.
 #include "scalesim.h"
 #include "ss_internal.h"
 
 #include <algorithm>
+#include <chrono>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -126,6 +131,44 @@ struct ss_pool {
 
 namespace {
 
+// Per-device out/in stream pair, shared by the device's pools.
+struct SharedStreams {
+    hipStream_t out = nullptr, in = nullptr;
+    int refs = 0;
+};
+std::mutex g_streams_mu;
+std::map<int, SharedStreams> g_streams;
+
+hipError_t acquire_streams(int device, hipStream_t* out, hipStream_t* in) {
+    std::lock_guard<std::mutex> lk(g_streams_mu);
+    SharedStreams& ss = g_streams[device];
+    if (ss.refs == 0) {
+        hipError_t e = hipStreamCreateWithFlags(&ss.out, hipStreamNonBlocking);
+        if (e != hipSuccess) return e;
+        e = hipStreamCreateWithFlags(&ss.in, hipStreamNonBlocking);
+        if (e != hipSuccess) {
+            (void)hipStreamDestroy(ss.out);
+            ss.out = nullptr;
+            return e;
+        }
+    }
+    ss.refs++;
+    *out = ss.out;
+    *in = ss.in;
+    return hipSuccess;
+}
+
+void release_streams(int device) {
+    std::lock_guard<std::mutex> lk(g_streams_mu);
+    auto it = g_streams.find(device);
+    if (it == g_streams.end() || it->second.refs == 0) return;
+    if (--it->second.refs == 0) {
+        (void)hipStreamDestroy(it->second.out);
+        (void)hipStreamDestroy(it->second.in);
+        g_streams.erase(it);
+    }
+}
+
 struct DeviceGuard {
     int prev = -1;
     explicit DeviceGuard(int dev) {
@@ -177,8 +220,7 @@ void free_pool(ss_pool* p) {
     void* hptrs[] = {p->h_res, p->h_victims, p->h_loads};
     for (void* h : hptrs)
         if (h) (void)hipHostFree(h);
-    for (hipStream_t s : sts)
-        if (s) (void)hipStreamDestroy(s);
+    if (p->st_out) release_streams(p->device);
     hipEvent_t evs[] = {p->ev_planned, p->ev_bt, p->ev_caller, p->ev_out_done, p->ev_in_done,
                         p->t_plan.a, p->t_plan.b};
     for (hipEvent_t e : evs)
@@ -514,8 +556,7 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(hipMemcpy(p->d_chunk_bytes, p->chunk_bytes.data(), p->P * sizeof(u64),
                          hipMemcpyHostToDevice));
 
-    for (hipStream_t* s : {&p->st_out, &p->st_in})
-        CREATE_TRY(hipStreamCreateWithFlags(s, hipStreamNonBlocking));
+    CREATE_TRY(acquire_streams(p->device, &p->st_out, &p->st_in));
     for (hipEvent_t* ev : {&p->ev_planned, &p->ev_bt, &p->ev_caller, &p->ev_out_done,
                            &p->ev_in_done})
         CREATE_TRY(make_event(ev, false));
@@ -544,6 +585,7 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
         return set_err(SS_ERR_ORDER, "previous step not finished: call ss_evict_pack and "
                                      "ss_prefetch_unpack before the next ss_plan_step");
     DeviceGuard g(p->device);
+    const auto h0 = std::chrono::steady_clock::now();
     if (!device_range_ok(distances, (u64)p->N * 4, p->device) ||
         !device_range_ok(active, (u64)p->N, p->device))
         return set_err(SS_ERR_ARG, "distances [N] and active [N] must be device memory of "
@@ -596,7 +638,9 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.b, p->st_out), true);
     TRY_HIP(p, hipEventRecord(p->ev_planned, p->st_out), true);
 
+    const auto h1 = std::chrono::steady_clock::now();
     TRY_HIP(p, hipEventSynchronize(p->ev_planned), true);
+    const auto h2 = std::chrono::steady_clock::now();
     // event times of the previous step and of this plan are folded into the
     // stats by ss_evict_pack, off the path that returns the plan
     if (timing) {
@@ -632,6 +676,15 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     *out = pl;
     p->state = kPlanned;
     p->stats.steps++;
+    if (timing) {
+        const auto h3 = std::chrono::steady_clock::now();
+        auto us = [](std::chrono::steady_clock::duration d) {
+            return std::chrono::duration<double, std::micro>(d).count();
+        };
+        p->stats.plan_host_us[0] += us(h1 - h0);
+        p->stats.plan_host_us[1] += us(h2 - h1);
+        p->stats.plan_host_us[2] += us(h3 - h2);
+    }
     return SS_OK;
 }
 

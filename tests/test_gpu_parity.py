@@ -79,6 +79,51 @@ def test_real_layouts(name, n_agents, steps, pool_index):
                ring_slots=3, sample_units=48, label=f"{name} layout sub{n_agents}")
 
 
+def test_two_pools_share_streams():
+    """The KV and LoRA pools of one workload stepped together (they share the
+    device's streams), each against its own oracle, bytes included."""
+    from oracle import OraclePool
+    tr = W.shrink_planes(W.make_trace("zipf_lora", 1), lambda p: [32, 16, 48][:2 + p.n_planes % 2])
+    dev = upload_trace(tr)
+    mems, pools, opools, contents = [], [], [], []
+    for k, spec in enumerate(tr.pools):
+        mem = PoolMemory(spec, 2 * 2 * 64 * spec.unit_bytes, 2)
+        c = W.Content(spec, seed=0, pool_index=k)
+        from gpu_harness import fill_host
+        fill_host(mem, c, spec)
+        mems.append(mem)
+        contents.append(c)
+        pools.append(mem.make_pool())
+        opools.append(OraclePool(spec.capacity_units, spec.agent_units, spec.unit_bytes))
+    for t in range(tr.n_steps):
+        plans = [p.plan_step(dev.dist(t), dev.active(t), S) for p in pools]
+        for p in pools:
+            p.evict_pack(0)
+        for p in pools:
+            p.prefetch_unpack(0)
+        for k, (p, op) in enumerate(zip(pools, opools)):
+            o = op.plan_step(tr.dist[t], tr.active[t], S)
+            assert plans[k]["victims"].tolist() == o.victims.tolist(), (k, t)
+            assert plans[k]["loads"].tolist() == o.loads.tolist(), (k, t)
+        for p in pools:
+            p.sync()
+        for k, (p, op, mem, c) in enumerate(zip(pools, opools, mems, contents)):
+            assert np.array_equal(p.block_table_host_all(), np.concatenate(op.bt).astype(np.int32))
+            res = np.flatnonzero(op.resident)
+            s = tr.pools[k].agent_units.astype(np.int64)
+            A = np.repeat(res, s[res])
+            J = np.concatenate([np.arange(s[a]) for a in res])
+            U = np.concatenate([op.bt[a] for a in res])
+            assert np.array_equal(mem.units_bytes(U), c.units_bytes(A, J)), (k, t)
+            for a in plans[k]["loads"]:
+                mem.host_copy(int(a))[:] = 0xA5
+    for p in pools:
+        p.close()
+    for m in mems:
+        m.free()
+    dev.free()
+
+
 def test_ragged_agent_count_and_sizes():
     rng = np.random.default_rng(5)
     units = rng.integers(1, 9, size=1037).astype(np.uint32)
