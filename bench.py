@@ -112,6 +112,9 @@ def parse():
     ap.add_argument("--cpu-agents", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true")
+    ap.add_argument("--clean-evict", action="store_true",
+                    help="mark every agent's memory unchanged: evictions release units "
+                         "without writing back (write-back elision)")
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "OUT_JSON"),
                     help="write the copy kernels' HBM traffic from two rocprofv3 --pmc runs")
     ap.add_argument("--pmc-commands", nargs="*", default=[])
@@ -228,14 +231,18 @@ def main():
     dist.upload(d_np)
     act.upload(a_np)
     stream = 0
+    clean = DeviceBuffer(N) if args.clean_evict else None
+    if clean is not None:
+        clean.upload(np.zeros(N, dtype=np.uint8))
+    dirty_ptr = clean.ptr if clean is not None else 0
 
     def sync():
         for p in pools:
             p.sync()
 
     def step(t):
-        plans = [p.plan_step(dist.ptr + 4 * N * t, act.ptr + N * t, thr, budget, stream)
-                 for p in pools]
+        plans = [p.plan_step(dist.ptr + 4 * N * t, act.ptr + N * t, thr, budget, stream,
+                             dirty_ptr) for p in pools]
         for p in pools:
             p.evict_pack(stream)
         for p in pools:
@@ -270,7 +277,7 @@ def main():
         t = args.warmup + args.steps + k
         ts = time.perf_counter()
         for p in pools:
-            p.plan_step(dist.ptr + 4 * N * t, act.ptr + N * t, thr, budget, stream)
+            p.plan_step(dist.ptr + 4 * N * t, act.ptr + N * t, thr, budget, stream, dirty_ptr)
         lat.append(time.perf_counter() - ts)
         for p in pools:
             p.evict_pack(stream)
@@ -284,6 +291,8 @@ def main():
         m.free()
     dist.free()
     act.free()
+    if clean is not None:
+        clean.free()
 
     pack_ms = sum(s["pack_ms"] for s in stats)
     unpack_ms = sum(s["unpack_ms"] for s in stats)
@@ -349,6 +358,7 @@ def main():
         "config": {"workload": f"{args.workload}: {WORKLOAD_TEXT[args.workload]}",
                    "seed": args.seed, "threshold": thr, "budget_units": budget,
                    "staging_bytes": args.staging_mib << 20, "ring_slots": args.ring,
+                   "write_back": "none (clean evictions)" if args.clean_evict else "every eviction",
                    "host_copies": ("one per agent" if args.host_copies == 0 else
                                    f"{args.host_copies} shared round-robin"),
                    "bytes_out": out_b, "bytes_in": in_b},

@@ -102,6 +102,12 @@ typedef struct {
 typedef struct {
     uint32_t threshold;             /* prefetch agents with distance < threshold (0 = off) */
     uint64_t budget_units;          /* max prefetched units per step; SS_NO_BUDGET = none  */
+    const uint8_t* dirty;           /* [N] DEVICE, optional: 1 = the agent's memory changed
+                                       since it was loaded, so an eviction writes it back;
+                                       0 = its host copy is current and its units are
+                                       released without a copy.  NULL = every eviction
+                                       writes back (Section 3.3: evicted memory is restored
+                                       from its host copy).                               */
 } ss_plan_params;
 
 typedef struct {
@@ -112,8 +118,10 @@ typedef struct {
     const uint32_t* victims;        /* [n_victims] host, eviction order; pool-owned,
                                        valid until the next ss_plan_step               */
     const uint32_t* loads;          /* [n_loads] host: demand loads by id, then prefetches */
-    uint64_t        units_out, units_in;
-    uint64_t        bytes_out, bytes_in;
+    uint64_t        units_out, units_in;   /* units released by victims / loaded    */
+    uint64_t        bytes_out, bytes_in;   /* bytes written back / loaded           */
+    uint64_t        units_written;         /* victims' units written back (<= units_out) */
+    const uint8_t*  victim_written;        /* [n_victims] host: 1 = written back     */
 } ss_plan;
 
 typedef struct {                    /* cumulative since create or ss_reset_stats          */
@@ -159,9 +167,10 @@ ss_status ss_plan_step(ss_pool* pool, const uint32_t* distances, const uint8_t* 
                        const ss_plan_params* params, ss_plan* out, void* stream);
 
 /* Evict (Section 3.3: eviction writes the victims' memory back to host):
- * packs the victims' units (victim, then logical unit, then plane) into the
- * eviction staging ring with the pack kernel and copies each victim's bytes
- * to its host copy with hipMemcpyAsync, ring slot by ring slot.  Returns once
+ * packs the written-back victims' units (victim, then logical unit, then
+ * plane) into the eviction staging ring with the pack kernel and copies each
+ * such victim's bytes to its host copy with hipMemcpyAsync, ring slot by ring
+ * slot.  Clean victims (dirty mask) are not copied.  Returns once
  * queued.  SS_ERR_ORDER unless called right after ss_plan_step. */
 ss_status ss_evict_pack(ss_pool* pool, void* stream);
 

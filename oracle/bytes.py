@@ -9,6 +9,9 @@ Section 4.1, "Baselines", on host-backed prefix nodes).  Content never
 changes while it sits on the GPU, so a write-back returns the same bytes
 (R9: every eviction writes back).
 
+Only the victims in ``plan.written`` are written back (all victims unless a
+dirty mask marked some clean; a clean victim's host copy is already current).
+
 Byte order, for both directions: agents in plan order, then the agent's
 logical units j = 0.., then the unit's planes c = 0..; an agent's host copy
 holds its units in that order, so an agent's bytes are one contiguous range
@@ -53,13 +56,13 @@ def apply_step_bytes(bpool: BytePool, plan, agent_units, host_read, host_write,
                      staging_out=None, staging_in=None):
     """Move one step's bytes.
 
-    ``host_write(agent, bytes)`` receives each victim's evicted bytes;
+    ``host_write(agent, bytes)`` receives each written-back victim's bytes;
     ``host_read(agent)`` returns a loaded agent's host copy.  Returns the two
     staging streams (evicted, loaded) for comparison; ``staging_out`` and
     ``staging_in`` are optional preallocated byte buffers for them."""
-    staging_out = bpool.gather(plan.victim_units, out=staging_out)
+    staging_out = bpool.gather(plan.written_units, out=staging_out)
     pos = 0
-    for v in plan.victims:
+    for v in plan.written:
         k = int(agent_units[v]) * bpool.unit_bytes
         host_write(int(v), staging_out[pos:pos + k])
         pos += k

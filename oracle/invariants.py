@@ -64,6 +64,8 @@ def check_step(pool, plan, D, active, threshold, budget, resident_before):
             avail += int(s[v])
             e += 1
     assert e == len(plan.victims), "I6: victims beyond what the loads need"
+    assert set(int(v) for v in plan.written) <= V, "written-back agent is not a victim"
+    assert plan.units_written == int(s[plan.written].sum())
 
 
 def check_i7(pool, D, active, threshold):

@@ -42,7 +42,11 @@ fixed rule that the HIP path must reproduce):
       released by this step's victims in eviction order, are handed to the
       loads in load order (demand loads first, then prefetches), logical
       unit j in order;
-* R11 whole-agent granularity per pool.
+* R11 whole-agent granularity per pool;
+* R13 write-back elision (optional ``dirty`` mask): an evicted agent whose
+      memory did not change since it was loaded still has a current host
+      copy, so its units are released without being written back; without a
+      mask every eviction writes back (R9).
 """
 from __future__ import annotations
 
@@ -63,15 +67,18 @@ class Plan:
     loads: np.ndarray          # agent ids, demand loads (id order) then prefetches (key ascending)
     n_demand: int              # leading entries of `loads` that are demand loads
     n_demand_victims: int      # leading entries of `victims` evicted for demand
-    victim_units: np.ndarray   # physical units read by the eviction, victim then j order
+    victim_units: np.ndarray   # physical units released by the eviction, victim then j order
     load_units: np.ndarray     # physical units written by the loads, load then j order
-    units_out: int
+    units_out: int             # units released by the victims
     units_in: int
     unit_bytes: int
+    written: np.ndarray = None       # victims whose bytes are written back, eviction order
+    written_units: np.ndarray = None  # their units, victim then j order
+    units_written: int = 0
 
     @property
     def bytes_out(self) -> int:
-        return self.units_out * self.unit_bytes
+        return self.units_written * self.unit_bytes
 
     @property
     def bytes_in(self) -> int:
@@ -93,7 +100,7 @@ class OraclePool:
         self.owner = np.full(self.U, -1, dtype=np.int64)   # agent owning each unit, -1 = free
 
     # ------------------------------------------------------------------
-    def plan_step(self, D, active, threshold: int, budget=None) -> Plan:
+    def plan_step(self, D, active, threshold: int, budget=None, dirty=None) -> Plan:
         D = np.asarray(D, dtype=np.uint64)
         act = np.asarray(active).astype(bool)
         s, res, N = self.s, self.resident, self.N
@@ -164,6 +171,12 @@ class OraclePool:
             self.resident[v] = False
         victim_units = (np.concatenate(released) if released
                         else np.zeros(0, dtype=np.int64))
+        # R13: only victims whose memory changed are written back
+        wmask = (np.ones(len(V), dtype=bool) if dirty is None
+                 else np.asarray(dirty)[V].astype(bool))
+        written = V[wmask]
+        written_units = (np.concatenate([r for r, w in zip(released, wmask) if w])
+                         if wmask.any() else np.zeros(0, dtype=np.int64))
 
         # 10. hand out units (R10): old free units ascending, then released ones
         F = np.concatenate([free_before, victim_units]).astype(np.int64)
@@ -184,7 +197,9 @@ class OraclePool:
         return Plan(victims=V.astype(np.int64), loads=loads, n_demand=len(L),
                     n_demand_victims=n_d, victim_units=victim_units,
                     load_units=load_units, units_out=int(s[V].sum()),
-                    units_in=int(s[loads].sum()), unit_bytes=self.unit_bytes)
+                    units_in=int(s[loads].sum()), unit_bytes=self.unit_bytes,
+                    written=written.astype(np.int64), written_units=written_units,
+                    units_written=int(s[written].sum()))
 
     # ------------------------------------------------------------------
     def block_table_csr(self):
@@ -195,7 +210,7 @@ class OraclePool:
 
 
 def run_trace(trace, threshold: int, budget=None, pool_index: int = 0, steps=None,
-              use_true_distance: bool = False, on_step=None):
+              use_true_distance: bool = False, on_step=None, dirty=None):
     """Replay a trace through one pool; returns the list of plans."""
     p = trace.pools[pool_index]
     pool = OraclePool(p.capacity_units, p.agent_units, p.unit_bytes)
@@ -203,7 +218,8 @@ def run_trace(trace, threshold: int, budget=None, pool_index: int = 0, steps=Non
     T = trace.n_steps if steps is None else steps
     plans = []
     for t in range(T):
-        plan = pool.plan_step(dist[t], trace.active[t], threshold, budget)
+        plan = pool.plan_step(dist[t], trace.active[t], threshold, budget,
+                              None if dirty is None else dirty[t])
         plans.append(plan)
         if on_step is not None:
             on_step(t, pool, plan)

@@ -43,14 +43,15 @@ class ss_pool_desc(C.Structure):
 
 
 class ss_plan_params(C.Structure):
-    _fields_ = [("threshold", C.c_uint32), ("budget_units", C.c_uint64)]
+    _fields_ = [("threshold", C.c_uint32), ("budget_units", C.c_uint64), ("dirty", C.c_void_p)]
 
 
 class ss_plan(C.Structure):
     _fields_ = [("n_victims", C.c_uint32), ("n_loads", C.c_uint32), ("n_demand", C.c_uint32),
                 ("n_demand_victims", C.c_uint32), ("victims", C.POINTER(C.c_uint32)),
                 ("loads", C.POINTER(C.c_uint32)), ("units_out", C.c_uint64),
-                ("units_in", C.c_uint64), ("bytes_out", C.c_uint64), ("bytes_in", C.c_uint64)]
+                ("units_in", C.c_uint64), ("bytes_out", C.c_uint64), ("bytes_in", C.c_uint64),
+                ("units_written", C.c_uint64), ("victim_written", C.POINTER(C.c_uint8))]
 
 
 class ss_stats(C.Structure):
@@ -175,9 +176,11 @@ class Pool:
             pass
 
     def plan_step(self, distances_ptr: int, active_ptr: int, threshold: int, budget=None,
-                  stream: int = 0):
-        """``ss_plan_step``; returns a dict with numpy copies of the plan."""
-        prm = ss_plan_params(int(threshold), SS_NO_BUDGET if budget is None else int(budget))
+                  stream: int = 0, dirty_ptr: int = 0):
+        """``ss_plan_step``; returns a dict with numpy copies of the plan.
+        ``dirty_ptr``: device address of the [N] write-back mask, 0 = none."""
+        prm = ss_plan_params(int(threshold), SS_NO_BUDGET if budget is None else int(budget),
+                             int(dirty_ptr) or None)
         out = ss_plan()
         _check(load().ss_plan_step(self._h, int(distances_ptr), int(active_ptr), C.byref(prm),
                                    C.byref(out), int(stream) or None))
@@ -186,9 +189,12 @@ class Pool:
                    else np.zeros(0, np.uint32))
         loads = (np.ctypeslib.as_array(out.loads, shape=(nl,)).copy() if nl
                  else np.zeros(0, np.uint32))
+        written = (np.ctypeslib.as_array(out.victim_written, shape=(nv,)).copy() if nv
+                   else np.zeros(0, np.uint8))
         return {"victims": victims, "loads": loads, "n_demand": out.n_demand,
                 "n_demand_victims": out.n_demand_victims, "units_out": out.units_out,
-                "units_in": out.units_in, "bytes_out": out.bytes_out, "bytes_in": out.bytes_in}
+                "units_in": out.units_in, "bytes_out": out.bytes_out, "bytes_in": out.bytes_in,
+                "units_written": out.units_written, "victim_written": written}
 
     def evict_pack(self, stream: int = 0):
         _check(load().ss_evict_pack(self._h, int(stream) or None))

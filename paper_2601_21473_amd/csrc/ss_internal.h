@@ -27,6 +27,7 @@ struct PlanResult {
     u64 units_out, units_in;
     u64 free_before;            // free units before the step
     u64 n_free_used;            // loads' units taken from the pre-step free units
+    u64 units_written;          // victims' units written back
 };
 
 // One wave-sized piece of a unit: `len` bytes of plane `plane`, starting at
@@ -74,6 +75,10 @@ struct PlanArgs {
     unsigned pad2;
     u64* phase;                     // [kPlanPhases] wall-clock stamps of the plan core, or null
     u64* hist_w;                    // [kDistBuckets] candidate units per distance bucket
+    const unsigned char* dirty;     // [N] optional write-back mask (device)
+    unsigned char* vwritten;        // [N] per victim: written back (device)
+    unsigned char* vwritten_host;   // mapped pinned host [N]
+    u64* woff;                      // [N+1] prefix units over written-back victims
 };
 
 // Candidate distance histogram: bucket(d) = d below 1024, then 32 buckets per
@@ -101,6 +106,9 @@ struct BtArgs {
     int* vunits;                    // [U] victims' old units, victim then j order
     int* lunits;                    // [U] loads' new units, load then j order
     u64 capacity;                   // U
+    const unsigned char* vwritten;  // [N] per victim: written back
+    const u64* woff;                // [N+1] prefix units over written-back victims
+    int* wunits;                    // [U] written-back victims' units (pack source)
 };
 
 struct CopyArgs {

@@ -636,10 +636,18 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
     // plan lists, load offsets, residency
     for (unsigned i = tid; i < n_v; i += blockDim.x) {
         const unsigned v = (unsigned)(sortE[nE - 1 - i] & idmask);
+        const unsigned char w = (!A.dirty || A.dirty[v]) ? 1 : 0;
         A.victims[i] = v;
         A.victims_host[i] = v;
+        A.vwritten[i] = w;
+        A.vwritten_host[i] = w;
         A.resident[v] = 0;
     }
+    // offsets of the written-back victims' units (all of them without a mask)
+    block_prefix(n_v, [&](unsigned i) {
+        const unsigned v = (unsigned)(sortE[nE - 1 - i] & idmask);
+        return (!A.dirty || A.dirty[v]) ? (u64)units[v] : 0ull;
+    }, A.woff, S);
 
     for (unsigned i = tid; i < n_l; i += blockDim.x) {
         const unsigned a = (unsigned)((i < nL ? A.sortL[i] : sortC[i - nL]) & idmask);
@@ -684,6 +692,7 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
         r.units_in = units_in;
         r.free_before = free_before;
         r.n_free_used = n_free_used;
+        r.units_written = A.woff[n_v];
         *A.res = r;
         *A.res_host = r;
         if (!A.fused) *A.cnt = PlanCounters{};
@@ -695,8 +704,8 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
 // ---------------------------------------------------------------------------
 
 // Release the victims' units (one block per victim): record them in eviction
-// order for the pack and the loads, clear the block-table entries and the
-// occupancy bits.
+// order for the loads (and, for victims that are written back, for the pack),
+// clear the block-table entries and the occupancy bits.
 __global__ void __launch_bounds__(256) k_bt_victims(BtArgs B) {
     if (B.res->status != 0) return;
     const unsigned nv = B.res->n_victims;
@@ -705,9 +714,12 @@ __global__ void __launch_bounds__(256) k_bt_victims(BtArgs B) {
         const u64 base = B.agent_off[v];
         const unsigned s = B.units[v];
         const u64 o = B.voff[i];
+        const bool written = B.vwritten[i] != 0;
+        const u64 ow = B.woff[i];
         for (unsigned j = threadIdx.x; j < s; j += blockDim.x) {
             const int u = B.bt[base + j];
             B.vunits[o + j] = u;
+            if (written) B.wunits[ow + j] = u;
             B.bt[base + j] = -1;
             if ((u64)(unsigned)u < B.capacity)
                 atomicAnd(&B.occ[(unsigned)u >> 5], ~(1u << ((unsigned)u & 31u)));

@@ -88,7 +88,9 @@ struct ss_pool {
     u64 *d_sortE = nullptr, *d_sortC = nullptr, *d_sortL = nullptr;
     u64 *d_prefE = nullptr, *d_prefC = nullptr, *d_loff = nullptr;
     unsigned *d_victims = nullptr, *d_loads = nullptr;
-    int *d_vunits = nullptr, *d_lunits = nullptr, *d_free_old = nullptr;
+    int *d_vunits = nullptr, *d_lunits = nullptr, *d_free_old = nullptr, *d_wunits = nullptr;
+    unsigned char* d_vwritten = nullptr;
+    u64* d_woff = nullptr;
     PlanResult* d_res = nullptr;
     u64* d_phase = nullptr;
     u64* d_hist_w = nullptr;
@@ -103,9 +105,11 @@ struct ss_pool {
     PlanResult* h_res = nullptr;
     unsigned* h_victims = nullptr;
     unsigned* h_loads = nullptr;
+    unsigned char* h_vwritten = nullptr;
     PlanResult* h_res_dev = nullptr;
     unsigned* h_victims_dev = nullptr;
     unsigned* h_loads_dev = nullptr;
+    unsigned char* h_vwritten_dev = nullptr;
 
     hipStream_t st_out = nullptr, st_in = nullptr;
     hipEvent_t ev_planned = nullptr, ev_bt = nullptr, ev_caller = nullptr,
@@ -122,7 +126,8 @@ struct ss_pool {
     // plan of the current step (host)
     ss_plan plan{};
     PlanResult res{};
-    std::vector<u64> voff, loff;
+    std::vector<u64> voff, loff, woff;
+    std::vector<long long> last_written;   // per victim: last written-back victim <= i, or -1
 
     State state = kIdle;
     bool poisoned = false;
@@ -213,11 +218,11 @@ void free_pool(ss_pool* p) {
                      p->d_listE, p->d_listC, p->d_listL, p->d_sortE, p->d_sortC, p->d_sortL,
                      p->d_prefE, p->d_prefC, p->d_loff, p->d_victims, p->d_loads, p->d_vunits,
                      p->d_lunits, p->d_free_old, p->d_res, p->d_phase, p->d_hist_w,
-                     p->d_items, p->d_plane_base,
+                     p->d_wunits, p->d_vwritten, p->d_woff, p->d_items, p->d_plane_base,
                      p->d_chunk_bytes};
     for (void* d : dptrs)
         if (d) (void)hipFree(d);
-    void* hptrs[] = {p->h_res, p->h_victims, p->h_loads};
+    void* hptrs[] = {p->h_res, p->h_victims, p->h_loads, p->h_vwritten};
     for (void* h : hptrs)
         if (h) (void)hipHostFree(h);
     if (p->st_out) release_streams(p->device);
@@ -358,6 +363,9 @@ ss_status flush_bt(ss_pool* p) {
     B.vunits = p->d_vunits;
     B.lunits = p->d_lunits;
     B.capacity = p->U;
+    B.vwritten = p->d_vwritten;
+    B.woff = p->d_woff;
+    B.wunits = p->d_wunits;
     p->bt_pending = false;
     TRY_HIP(p, launch_bt_update(B, p->N, p->st_out), true);
     TRY_HIP(p, hipEventRecord(p->ev_bt, p->st_out), true);
@@ -492,6 +500,9 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(dalloc(&p->d_vunits, U));
     CREATE_TRY(dalloc(&p->d_lunits, U));
     CREATE_TRY(dalloc(&p->d_free_old, U));
+    CREATE_TRY(dalloc(&p->d_wunits, U));
+    CREATE_TRY(dalloc(&p->d_vwritten, N));
+    CREATE_TRY(dalloc(&p->d_woff, N + 1));
     CREATE_TRY(dalloc(&p->d_res, 1));
     CREATE_TRY(dalloc(&p->d_phase, kPlanPhases));
     CREATE_TRY(dalloc(&p->d_hist_w, kDistBuckets));
@@ -510,6 +521,8 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_res_dev), p->h_res, 0));
     CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_victims_dev), p->h_victims, 0));
     CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_loads_dev), p->h_loads, 0));
+    CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_vwritten), N, hipHostMallocMapped));
+    CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_vwritten_dev), p->h_vwritten, 0));
 
     // copy items: pieces of at most kItemBytes, plane by plane
     std::vector<CopyItem> items;
@@ -590,6 +603,8 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
         !device_range_ok(active, (u64)p->N, p->device))
         return set_err(SS_ERR_ARG, "distances [N] and active [N] must be device memory of "
                                    "device %d", p->device);
+    if (params->dirty && !device_range_ok(params->dirty, (u64)p->N, p->device))
+        return set_err(SS_ERR_ARG, "dirty [N] must be device memory of device %d", p->device);
     hipStream_t caller = static_cast<hipStream_t>(stream);
 
     TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
@@ -630,6 +645,10 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     A.fused = p->N <= kFuseAgents ? 1u : 0u;
     A.phase = (p->flags & SS_FLAG_TIMING) ? p->d_phase : nullptr;
     A.hist_w = p->d_hist_w;
+    A.dirty = params->dirty;
+    A.vwritten = p->d_vwritten;
+    A.vwritten_host = p->h_vwritten_dev;
+    A.woff = p->d_woff;
 
     const bool timing = p->flags & SS_FLAG_TIMING;
     if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.a, p->st_out), true);
@@ -661,6 +680,14 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     for (unsigned i = 0; i < r.n_victims; ++i) p->voff[i + 1] = p->voff[i] + p->s[p->h_victims[i]];
     p->loff[0] = 0;
     for (unsigned i = 0; i < r.n_loads; ++i) p->loff[i + 1] = p->loff[i] + p->s[p->h_loads[i]];
+    p->woff.resize(r.n_victims + 1);
+    p->last_written.resize(r.n_victims);
+    p->woff[0] = 0;
+    for (unsigned i = 0; i < r.n_victims; ++i) {
+        const bool w = p->h_vwritten[i] != 0;
+        p->woff[i + 1] = p->woff[i] + (w ? p->s[p->h_victims[i]] : 0);
+        p->last_written[i] = w ? (long long)i : (i ? p->last_written[i - 1] : -1);
+    }
 
     ss_plan& pl = p->plan;
     pl.n_victims = r.n_victims;
@@ -671,8 +698,10 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     pl.loads = p->h_loads;
     pl.units_out = r.units_out;
     pl.units_in = r.units_in;
-    pl.bytes_out = r.units_out * p->unit_bytes;
+    pl.bytes_out = r.units_written * p->unit_bytes;
     pl.bytes_in = r.units_in * p->unit_bytes;
+    pl.units_written = r.units_written;
+    pl.victim_written = p->h_vwritten;
     *out = pl;
     p->state = kPlanned;
     p->stats.steps++;
@@ -702,7 +731,7 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
     TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
     TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_caller, 0), true);
 
-    const u64 total = p->res.units_out;
+    const u64 total = p->res.units_written;
     const u64 ups = p->units_per_slot;
     const u64 nslots = (total + ups - 1) / ups;
     while (p->ev_packed.size() < nslots) {
@@ -711,7 +740,7 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
         p->ev_packed.push_back(ev);
     }
     CopyArgs C{};
-    C.units_list = p->d_vunits;
+    C.units_list = p->d_wunits;
     C.items = p->d_items;
     C.n_items = p->n_items;
     C.item_groups = (p->n_items + kCopyWavesPerBlock - 1) / kCopyWavesPerBlock;
@@ -740,12 +769,13 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
             tp->bytes = (p1 - p0) * p->unit_bytes;
             TRY_HIP(p, hipEventRecord(tp->a, p->st_out), true);
         }
-        // each victim's bytes inside [p0, p1) go to its host copy
-        while (vi < p->res.n_victims && p->voff[vi + 1] <= p0) vi++;
-        for (size_t i = vi; i < p->res.n_victims && p->voff[i] < p1; ++i) {
-            const u64 lo = std::max(p0, p->voff[i]), hi = std::min(p1, p->voff[i + 1]);
+        // each written-back victim's bytes inside [p0, p1) go to its host copy
+        while (vi < p->res.n_victims && p->woff[vi + 1] <= p0) vi++;
+        for (size_t i = vi; i < p->res.n_victims && p->woff[i] < p1; ++i) {
+            if (p->woff[i + 1] == p->woff[i]) continue;              // clean victim
+            const u64 lo = std::max(p0, p->woff[i]), hi = std::min(p1, p->woff[i + 1]);
             const unsigned v = p->h_victims[i];
-            char* dst = p->host + p->host_off[v] + (lo - p->voff[i]) * p->unit_bytes;
+            char* dst = p->host + p->host_off[v] + (lo - p->woff[i]) * p->unit_bytes;
             const char* src = slot + (lo - p0) * p->unit_bytes;
             TRY_HIP(p, hipMemcpyAsync(dst, src, (hi - lo) * p->unit_bytes, hipMemcpyDeviceToHost,
                                       p->st_out), true);
@@ -782,7 +812,7 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
     C.chunk_bytes = p->d_chunk_bytes;
     C.unit_bytes = p->unit_bytes;
     C.capacity = p->U;
-    size_t li = 0;
+    size_t li = 0, ri = 0;
     for (u64 k = 0; k < nslots; ++k) {
         const u64 q0 = k * ups, q1 = std::min(total, q0 + ups);
         char* slot = p->stage_in + (k % p->ring) * p->slot_bytes;
@@ -802,11 +832,17 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
                                       p->st_in), true);
         }
         if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_in), true);
-        // units released by victims are overwritten only after the pack read them
-        const u64 last = q1 - 1;
-        if (last >= nF) {
-            const u64 kv = (last - nF) / ups;
-            TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_packed[kv], 0), true);
+        // units released by victims are overwritten only after the pack read
+        // them: released positions [r0, r1) of this slot; the last written-back
+        // victim overlapping them gives the last pack slot to wait for
+        if (q1 > nF) {
+            const u64 r0 = q0 > nF ? q0 - nF : 0, r1 = q1 - nF;
+            while (ri + 1 < p->res.n_victims && p->voff[ri + 1] < r1) ri++;
+            const long long j = p->res.n_victims ? p->last_written[ri] : -1;
+            if (j >= 0 && p->voff[j + 1] > r0) {
+                const u64 maxpos = p->woff[j] + std::min(r1, p->voff[j + 1]) - p->voff[j] - 1;
+                TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_packed[maxpos / ups], 0), true);
+            }
         }
         C.first = q0;
         C.count = q1 - q0;

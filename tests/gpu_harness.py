@@ -75,7 +75,8 @@ def fill_host(mem, content, spec, batch_bytes=256 << 20):
 
 
 def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_bytes=True,
-               slot_units=8, ring_slots=2, sample_units=None, bt_every=1, seed=0, label=""):
+               slot_units=8, ring_slots=2, sample_units=None, bt_every=1, seed=0, label="",
+               dirty=None):
     spec = trace.pools[pool_index]
     ub = spec.unit_bytes
     staging_bytes = 2 * ring_slots * slot_units * ub
@@ -89,6 +90,11 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
     pool = mem.make_pool(timing=True)
     opool = OraclePool(spec.capacity_units, spec.agent_units, ub)
     dev = upload_trace(trace)
+    d_dirty = None
+    if dirty is not None:
+        dm = np.ascontiguousarray(dirty, dtype=np.uint8)
+        d_dirty = DeviceBuffer(dm.nbytes)
+        d_dirty.upload(dm)
     T = trace.n_steps if steps is None else steps
     stream = 0
     rng = np.random.default_rng(seed + 99)
@@ -96,8 +102,17 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
     moved = 0
     t0 = time.time()
     for t in range(T):
-        g = pool.plan_step(dev.dist(t), dev.active(t), theta, budget, stream)
-        o = opool.plan_step(trace.dist[t], trace.active[t], theta, budget)
+        g = pool.plan_step(dev.dist(t), dev.active(t), theta, budget, stream,
+                           0 if d_dirty is None else d_dirty.ptr + trace.n_agents * t)
+        o = opool.plan_step(trace.dist[t], trace.active[t], theta, budget,
+                            None if dirty is None else dirty[t])
+        assert g["units_written"] == o.units_written, (label, t)
+        assert g["victim_written"].astype(bool).tolist() == \
+            [int(v) in set(o.written.tolist()) for v in o.victims], (label, t)
+        if check_bytes and dirty is not None:
+            # a written-back victim's host copy must be rewritten by this step
+            for v in o.written:
+                mem.host_copy(int(v))[:] = POISON
         assert g["victims"].tolist() == o.victims.tolist(), (label, t, "victims")
         assert g["loads"].tolist() == o.loads.tolist(), (label, t, "loads")
         assert g["n_demand"] == o.n_demand, (label, t)
@@ -114,7 +129,7 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
             assert np.array_equal(bt, obt.astype(np.int32)), (label, t, "block table")
             assert np.array_equal(pool.resident_host().astype(bool), opool.resident), (label, t)
         if check_bytes:
-            for v in o.victims:
+            for v in o.victims:           # written back, or clean and still current
                 v = int(v)
                 exp = content.units_bytes(np.full(units_i64[v], v), np.arange(units_i64[v]))
                 assert np.array_equal(mem.host_copy(v), exp.reshape(-1)), (label, t, "host", v)
@@ -130,12 +145,15 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
                 exp = content.units_bytes(A, J)
                 bad = np.flatnonzero((got != exp).any(axis=1))
                 assert len(bad) == 0, (label, t, "device bytes", A[bad[:4]], J[bad[:4]])
-            for a in o.loads:             # a resident agent's host copy is stale by design
-                mem.host_copy(int(a))[:] = POISON
+            if dirty is None:
+                for a in o.loads:         # a resident agent's host copy is stale by design
+                    mem.host_copy(int(a))[:] = POISON
     st = pool.stats()
     pool.close()
     dev.free()
     mem.free()
+    if d_dirty is not None:
+        d_dirty.free()
     log(f"[parity] {label or trace.name}: {T} steps ok, {moved} units moved, "
         f"{time.time() - t0:.1f}s")
     return st

@@ -79,6 +79,21 @@ def test_real_layouts(name, n_agents, steps, pool_index):
                ring_slots=3, sample_units=48, label=f"{name} layout sub{n_agents}")
 
 
+@pytest.mark.parametrize("mode", ["clean", "mixed"])
+def test_write_back_elision(mode):
+    tr = W.make_trace("tiny", 4)
+    rng = np.random.default_rng(11)
+    dirty = (np.zeros(tr.active.shape, np.uint8) if mode == "clean"
+             else (rng.random(tr.active.shape) < 0.4).astype(np.uint8))
+    st = run_parity(tr, theta=S, slot_units=2, ring_slots=2, dirty=dirty, label=f"elision {mode}")
+    if mode == "clean":
+        assert st["pack_launches"] == 0 and st["d2h_bytes"] == 0
+    trb = W.shrink_planes(W.make_trace("bursty", 2), lambda p: [32, 16])
+    dirty = (rng.random(trb.active.shape) < (0.0 if mode == "clean" else 0.5)).astype(np.uint8)
+    run_parity(trb, theta=S, slot_units=512, ring_slots=3, dirty=dirty, steps=120,
+               label=f"bursty elision {mode}")
+
+
 def test_two_pools_share_streams():
     """The KV and LoRA pools of one workload stepped together (they share the
     device's streams), each against its own oracle, bytes included."""
