@@ -154,12 +154,13 @@ void ss_pool_destroy(ss_pool* pool);
 /* Plan one step (Section 3.3 and Appendix A, Evict + DispatchLoadTasks):
  * turns distances and the activation mask into victims and loads and updates
  * the block table.  `distances` [N] uint32 and `active` [N] uint8 (0/1) are
- * DEVICE pointers read during the call's kernels.  The call returns after the
- * plan is known on the host (one device-to-host readback).  The block-table
+ * DEVICE pointers read during the call's kernels, which run on `stream`
+ * after the work queued there before the call and after the previous step's
+ * loads.  The call returns after the plan is known on the host (one
+ * device-to-host readback).  The block-table
  * update that the plan implies is queued on the device by the next call that
  * needs it (ss_evict_pack, ss_block_table*, ss_resident_host, ss_sync) and is
  * ordered before the copy kernels.
- * Previous step's data movement is waited for on the device first.
  * SS_ERR_OVERCOMMIT if the active agents need more than capacity_units
  * (pool unchanged).  SS_ERR_ORDER if the previous step was not completed with
  * ss_evict_pack and ss_prefetch_unpack. */

@@ -328,12 +328,13 @@ ss_status check_usable(ss_pool* p) {
     return SS_OK;
 }
 
-// Fold the finished previous step's copy events and this plan's event time
-// and phase stamps into the stats (timing mode).  The previous step's work
-// completed before this plan's kernels ran, and the plan kernels completed
-// before ss_plan_step returned.
+// Fold the previous step's copy events and this plan's event time and phase
+// stamps into the stats (timing mode).  The previous step's loads completed
+// before this plan's kernels ran and the plan kernels before ss_plan_step
+// returned; its evictions are waited for here.
 ss_status collect_plan_timing(ss_pool* p) {
     if (!(p->flags & SS_FLAG_TIMING)) return SS_OK;
+    TRY_HIP(p, hipEventSynchronize(p->ev_out_done), true);
     collect_timing(p);
     if (p->phase_pending) {
         p->phase_pending = false;
@@ -367,6 +368,7 @@ ss_status flush_bt(ss_pool* p) {
     B.woff = p->d_woff;
     B.wunits = p->d_wunits;
     p->bt_pending = false;
+    TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_planned, 0), true);
     TRY_HIP(p, launch_bt_update(B, p->N, p->st_out), true);
     TRY_HIP(p, hipEventRecord(p->ev_bt, p->st_out), true);
     return SS_OK;
@@ -607,11 +609,12 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
         return set_err(SS_ERR_ARG, "dirty [N] must be device memory of device %d", p->device);
     hipStream_t caller = static_cast<hipStream_t>(stream);
 
-    TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
-    // the out stream is FIFO behind the previous step's evictions; it also
-    // waits for the previous step's loads and for the caller's work
-    TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_caller, 0), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_in_done, 0), true);
+    // The plan kernels run on the caller's stream, after the caller's earlier
+    // work (which may produce the distances) and after the previous step's
+    // loads (which read the plan buffers this plan rewrites; that step's
+    // block-table update precedes them).  The block-table update of this plan
+    // is queued on the out stream behind ev_planned (flush_bt).
+    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_in_done, 0), true);
 
     PlanArgs A{};
     A.dist = distances;
@@ -651,11 +654,11 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     A.woff = p->d_woff;
 
     const bool timing = p->flags & SS_FLAG_TIMING;
-    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.a, p->st_out), true);
-    if (!A.fused) TRY_HIP(p, launch_classify(A, p->st_out), true);
-    TRY_HIP(p, launch_plan_core(A, p->st_out), true);
-    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.b, p->st_out), true);
-    TRY_HIP(p, hipEventRecord(p->ev_planned, p->st_out), true);
+    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.a, caller), true);
+    if (!A.fused) TRY_HIP(p, launch_classify(A, caller), true);
+    TRY_HIP(p, launch_plan_core(A, caller), true);
+    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.b, caller), true);
+    TRY_HIP(p, hipEventRecord(p->ev_planned, caller), true);
 
     const auto h1 = std::chrono::steady_clock::now();
     TRY_HIP(p, hipEventSynchronize(p->ev_planned), true);
