@@ -290,6 +290,28 @@ def subsample_agents(trace: Trace, n_agents: int) -> Trace:
                  trace.dist[:, :n_agents], trace.dist_true[:, :n_agents], dict(trace.meta))
 
 
+def prefix_tree_objects(n_agents: int, branching: int, depth: int, seed: int,
+                        node_pages=(1, 8)):
+    """Memory objects of a shared prefix tree: a root shared by every agent,
+    internal nodes shared by the agents below them, and one private leaf per
+    agent; agents are spread uniformly over the tree's paths.  Returns the
+    CSR map object -> referencing agents (``obj_off`` [M+1], ``obj_agents``)
+    and each object's size in pages."""
+    rng = np.random.default_rng(seed)
+    paths = rng.integers(0, branching, size=(n_agents, depth))
+    members = {}
+    for a in range(n_agents):
+        for lvl in range(depth + 1):
+            members.setdefault(tuple(paths[a, :lvl]), []).append(a)
+    nodes = sorted(members, key=lambda k: (len(k), k))
+    lists = [members[k] for k in nodes] + [[a] for a in range(n_agents)]     # + leaves
+    obj_off = np.zeros(len(lists) + 1, dtype=np.uint64)
+    obj_off[1:] = np.cumsum([len(x) for x in lists])
+    obj_agents = np.concatenate([np.asarray(x, dtype=np.uint32) for x in lists])
+    sizes = rng.integers(node_pages[0], node_pages[1] + 1, size=len(lists)).astype(np.uint32)
+    return obj_off, obj_agents, sizes
+
+
 def random_tiny_trace(rng: np.random.Generator, n_agents: int, n_steps: int,
                       max_active: int, capacity_agents: int, units=None):
     """A small random request trace for brute-force checks."""
