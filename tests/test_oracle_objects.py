@@ -11,7 +11,7 @@ S = W.SENTINEL
 
 
 def test_paper_example_min_of_sharers():
-    fx = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "shared_object_min.json")))
+    fx = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "objects", "shared_object_min.json")))
     d, a = object_distances(fx["obj_off"], np.array(fx["obj_agents"]), np.array(fx["dist"]),
                             np.array(fx["active"]))
     assert d.tolist() == fx["expect_dist"] and a.tolist() == fx["expect_active"]
