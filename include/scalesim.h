@@ -218,6 +218,39 @@ ss_status ss_probe_copy(void* dst, const void* src, uint64_t bytes, int iters, f
 ss_status ss_probe_link(void* host, void* dev, uint64_t bytes, int dir, int iters,
                         float* ms_per_iter);
 
+/* ---- Distance estimation (inputs of ss_plan_step) ------------------------
+ *
+ * Shared memory objects (Appendix A, "Fine-grained distance assignment"): an
+ * object referenced by several agents, such as a node of a shared prefix
+ * tree, gets the smallest distance of the agents that reference it, and is
+ * needed now when any of them is active.  Planning a pool whose "agents" are
+ * objects then uses obj_distances / obj_active as its distances and mask.
+ *
+ *   obj_off      [n_objects + 1] nondecreasing, obj_off[0] = 0,
+ *                obj_off[n_objects] = n_refs: object o is referenced by
+ *                obj_agents[obj_off[o] .. obj_off[o+1]).
+ *   obj_agents   [n_refs] agent ids; ids >= n_agents are ignored.
+ *   distances    [n_agents] agent distances, active [n_agents] 0/1.
+ *   obj_distances [n_objects] out: min over the referencing agents of
+ *                (0 if active else distance); 0xFFFFFFFF when no agent
+ *                references the object.
+ *   obj_active   [n_objects] out: 1 if any referencing agent is active.
+ *   workspace    device memory of at least
+ *                ss_object_distances_workspace(n_objects, n_refs) bytes,
+ *                owned by the caller; its contents need no initialisation.
+ * Every array is device memory of the current device, owned by the caller.
+ * The work is queued on `stream` (a hipStream_t, NULL = the null stream) and
+ * the call returns without waiting.  n_objects and n_refs must be below 2^31.
+ * Offsets that break the rules above give unspecified output values but no
+ * access outside the arrays.  SS_ERR_ARG for NULL, too small or non-device
+ * arguments (nothing queued), SS_ERR_HIP if a launch fails. */
+uint64_t ss_object_distances_workspace(uint32_t n_objects, uint32_t n_refs);
+ss_status ss_object_distances(const uint32_t* obj_off, const uint32_t* obj_agents,
+                              uint32_t n_objects, uint32_t n_refs, const uint32_t* distances,
+                              const uint8_t* active, uint32_t n_agents, uint32_t* obj_distances,
+                              uint8_t* obj_active, void* workspace, uint64_t workspace_bytes,
+                              void* stream);
+
 /* Block until all work the pool has queued (plan, copies, kernels) is done. */
 ss_status ss_sync(ss_pool* pool);
 

@@ -7,7 +7,8 @@ several agents (for example a node of a shared prefix tree) gets the minimum
 invocation distance of the agents that currently reference it.  Reading R14:
 the object is needed now if any referencing agent is active, and an active
 object's distance is 0 (the activation mask is authoritative, R5); an object
-that no agent references has no future use (distance 0xFFFFFFFF).
+that no agent references has no future use (distance 0xFFFFFFFF).  A
+reference to an id outside the agent arrays names no agent and is skipped.
 """
 from __future__ import annotations
 
@@ -22,7 +23,7 @@ def object_distances(obj_off, obj_agents, D, active):
     dist = np.full(M, SENTINEL, dtype=np.uint32)
     act = np.zeros(M, dtype=np.uint8)
     for o in range(M):
-        refs = obj_agents[obj_off[o]:obj_off[o + 1]]
+        refs = [int(a) for a in obj_agents[obj_off[o]:obj_off[o + 1]] if int(a) < len(D)]
         if len(refs) == 0:
             continue
         if any(active[a] for a in refs):

@@ -1,8 +1,11 @@
-// Declarations shared by the device kernels (ss_kernels.hip) and the host
-// library (ss_pool.hip).  Internal to libscalesim.
+// Declarations shared by the device kernels (ss_kernels.hip), the host
+// library (ss_pool.hip) and the distance kernels (ss_distance.hip).  Internal
+// to libscalesim.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include "scalesim.h"
 
 namespace ss {
 
@@ -139,5 +142,9 @@ hipError_t launch_pack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_unpack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_zero_u32(unsigned* p, u64 n, hipStream_t st);
 hipError_t launch_probe_copy(void* dst, const void* src, u64 bytes, hipStream_t st);
+
+// Host helpers defined in ss_pool.hip.
+ss_status set_err(ss_status st, const char* fmt, ...);       // sets ss_last_error
+bool device_range_ok(const void* ptr, u64 bytes, int device); // one device allocation
 
 }  // namespace ss

@@ -35,9 +35,10 @@
 using namespace ss;
 
 namespace {
-
 thread_local std::string g_err;
+}  // namespace
 
+namespace ss {
 ss_status set_err(ss_status st, const char* fmt, ...) {
     char buf[512];
     va_list ap;
@@ -47,6 +48,9 @@ ss_status set_err(ss_status st, const char* fmt, ...) {
     g_err = buf;
     return st;
 }
+}  // namespace ss
+
+namespace {
 
 enum State { kIdle = 0, kPlanned = 1, kPacked = 2 };
 
@@ -283,6 +287,9 @@ void collect_timing(ss_pool* p) {
     p->t_plan_used = false;
 }
 
+}  // namespace
+
+namespace ss {
 // True if [ptr, ptr + bytes) lies inside one allocation of device memory on
 // `device` (or managed memory).
 bool device_range_ok(const void* ptr, u64 bytes, int device) {
@@ -302,6 +309,10 @@ bool device_range_ok(const void* ptr, u64 bytes, int device) {
     const u64 off = reinterpret_cast<uintptr_t>(ptr) - reinterpret_cast<uintptr_t>(base);
     return off <= size && bytes <= size - off;
 }
+
+}  // namespace ss
+
+namespace {
 
 // True if host_ptr is pinned (page-locked) host memory; when the runtime
 // reports the allocation's extent, [host_ptr, host_ptr + bytes) must fit in it.

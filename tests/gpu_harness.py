@@ -76,7 +76,9 @@ def fill_host(mem, content, spec, batch_bytes=256 << 20):
 
 def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_bytes=True,
                slot_units=8, ring_slots=2, sample_units=None, bt_every=1, seed=0, label="",
-               dirty=None):
+               dirty=None, device_inputs=None):
+    """``device_inputs(t) -> (distances_ptr, active_ptr)`` replaces the uploaded
+    trace on the HIP side (the oracle side always reads ``trace``)."""
     spec = trace.pools[pool_index]
     ub = spec.unit_bytes
     staging_bytes = 2 * ring_slots * slot_units * ub
@@ -89,7 +91,7 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
         fill_host(mem, content, spec)
     pool = mem.make_pool(timing=True)
     opool = OraclePool(spec.capacity_units, spec.agent_units, ub)
-    dev = upload_trace(trace)
+    dev = upload_trace(trace) if device_inputs is None else None
     d_dirty = None
     if dirty is not None:
         dm = np.ascontiguousarray(dirty, dtype=np.uint8)
@@ -102,7 +104,8 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
     moved = 0
     t0 = time.time()
     for t in range(T):
-        g = pool.plan_step(dev.dist(t), dev.active(t), theta, budget, stream,
+        d_ptr, a_ptr = (dev.dist(t), dev.active(t)) if dev is not None else device_inputs(t)
+        g = pool.plan_step(d_ptr, a_ptr, theta, budget, stream,
                            0 if d_dirty is None else d_dirty.ptr + trace.n_agents * t)
         o = opool.plan_step(trace.dist[t], trace.active[t], theta, budget,
                             None if dirty is None else dirty[t])
@@ -150,7 +153,8 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
                     mem.host_copy(int(a))[:] = POISON
     st = pool.stats()
     pool.close()
-    dev.free()
+    if dev is not None:
+        dev.free()
     mem.free()
     if d_dirty is not None:
         d_dirty.free()

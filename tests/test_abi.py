@@ -152,6 +152,30 @@ def test_probe_argument_checks():
     assert L.ss_probe_link(C.c_void_p(16), C.c_void_p(32), 16, 3, 1, C.byref(ms)) == B.SS_ERR_ARG
 
 
+def test_object_distances_argument_checks():
+    L = B.load()
+    V = C.c_void_p
+    # one carry record of 16 bytes per 2048 merge items (objects + references)
+    assert L.ss_object_distances_workspace(1, 0) == 16
+    assert L.ss_object_distances_workspace(2048, 0) == 16
+    assert L.ss_object_distances_workspace(2048, 1) == 32
+    assert L.ss_object_distances_workspace(5000, 100000) == 16 * ((105000 + 2047) // 2048)
+    args = lambda **kw: [kw.get(k, d) for k, d in (
+        ("off", V(256)), ("agents", V(512)), ("M", 4), ("R", 8), ("dist", V(1024)),
+        ("act", V(2048)), ("N", 3), ("od", V(4096)), ("oa", V(8192)), ("ws", V(16384)),
+        ("wsb", 1 << 20), ("st", None))]
+    assert L.ss_object_distances(*args(M=0)) == B.SS_OK            # nothing to do
+    assert L.ss_object_distances(*args(M=1 << 31)) == B.SS_ERR_ARG
+    assert L.ss_object_distances(*args(R=1 << 31)) == B.SS_ERR_ARG
+    assert L.ss_object_distances(*args(off=None)) == B.SS_ERR_ARG
+    assert L.ss_object_distances(*args(agents=None)) == B.SS_ERR_ARG
+    assert L.ss_object_distances(*args(ws=None)) == B.SS_ERR_ARG
+    assert L.ss_object_distances(*args(wsb=15)) == B.SS_ERR_ARG
+    assert "workspace_bytes" in L.ss_last_error().decode()
+    # host addresses are never taken for device memory
+    assert L.ss_object_distances(*args()) == B.SS_ERR_ARG
+
+
 def test_no_device_is_an_argument_error_not_a_crash():
     if B.device_count() > 0:
         pytest.skip("a GPU is present")

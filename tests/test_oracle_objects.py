@@ -45,3 +45,9 @@ def test_unreferenced_object_has_no_future_use():
     d, a = object_distances([0, 0, 1], np.array([0], np.uint32), np.array([5], np.uint32),
                             np.array([0], np.uint8))
     assert d.tolist() == [S, 5] and a.tolist() == [0, 0]
+
+
+def test_unknown_agent_ids_are_skipped():
+    d, a = object_distances([0, 2, 3], np.array([7, 1, 9], np.uint32), np.array([3, 4], np.uint32),
+                            np.array([0, 0], np.uint8))
+    assert d.tolist() == [4, S] and a.tolist() == [0, 0]

@@ -299,16 +299,23 @@ def prefix_tree_objects(n_agents: int, branching: int, depth: int, seed: int,
     and each object's size in pages."""
     rng = np.random.default_rng(seed)
     paths = rng.integers(0, branching, size=(n_agents, depth))
-    members = {}
-    for a in range(n_agents):
-        for lvl in range(depth + 1):
-            members.setdefault(tuple(paths[a, :lvl]), []).append(a)
-    nodes = sorted(members, key=lambda k: (len(k), k))
-    lists = [members[k] for k in nodes] + [[a] for a in range(n_agents)]     # + leaves
-    obj_off = np.zeros(len(lists) + 1, dtype=np.uint64)
-    obj_off[1:] = np.cumsum([len(x) for x in lists])
-    obj_agents = np.concatenate([np.asarray(x, dtype=np.uint32) for x in lists])
-    sizes = rng.integers(node_pages[0], node_pages[1] + 1, size=len(lists)).astype(np.uint32)
+    offs, lists = [np.zeros(1, np.int64)], []
+    code = np.zeros(n_agents, dtype=np.int64)       # path prefix as a base-`branching` number
+    total = 0
+    for lvl in range(depth + 1):                    # nodes by depth, then by path
+        if lvl:
+            code = code * branching + paths[:, lvl - 1]
+        order = np.argsort(code, kind="stable")     # members of a node in agent order
+        _, counts = np.unique(code[order], return_counts=True)
+        lists.append(order.astype(np.uint32))
+        offs.append(total + np.cumsum(counts))
+        total += n_agents
+    lists.append(np.arange(n_agents, dtype=np.uint32))                # private leaves
+    offs.append(total + np.arange(1, n_agents + 1))
+    obj_off = np.concatenate(offs).astype(np.uint64)
+    obj_agents = np.concatenate(lists)
+    n_obj = len(obj_off) - 1
+    sizes = rng.integers(node_pages[0], node_pages[1] + 1, size=n_obj).astype(np.uint32)
     return obj_off, obj_agents, sizes
 
 
