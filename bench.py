@@ -115,6 +115,13 @@ def parse():
     ap.add_argument("--clean-evict", action="store_true",
                     help="mark every agent's memory unchanged: evictions release units "
                          "without writing back (write-back elision)")
+    ap.add_argument("--no-objects", action="store_true",
+                    help="skip the shared-object distance kernel measurement")
+    ap.add_argument("--objects-only", action="store_true",
+                    help="only the shared-object distance measurement (for profiling)")
+    ap.add_argument("--objects-trees", type=int, default=160)
+    ap.add_argument("--objects-agents", type=int, default=50_000)
+    ap.add_argument("--objects-depth", type=int, default=5)
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "OUT_JSON"),
                     help="write the copy kernels' HBM traffic from two rocprofv3 --pmc runs")
     ap.add_argument("--pmc-commands", nargs="*", default=[])
@@ -141,6 +148,64 @@ def probes(binding):
     out["duplex_GBps"] = 2 * m / best(2) / 1e6
     h.free()
     d.free()
+    return out
+
+
+OBJ_BRANCH = 8                   # prefix trees of the shared-object measurement
+
+
+def object_bench(args, binding, W, DeviceBuffer):
+    """Shared-object distances (Appendix A, fine-grained distance assignment)
+    on a prefix forest: ``objects-trees`` simulations of ``objects-agents``
+    agents (default 160 x 50,000, the diffusion workload's agent count), each
+    sharing a branching-8 prefix tree of ``objects-depth`` levels with one
+    private leaf per agent, agents spread uniformly over the tree; 1% of agents
+    active, distances uniform in [1, 2^20).  Also the latency at 16,384 agents
+    and the oracle's rate on that small map."""
+    def measure(off, agents, n, iters, rng):
+        M, R = len(off) - 1, int(off[-1])
+        D = rng.integers(1, 1 << 20, size=n).astype(np.uint32)
+        act = (rng.random(n) < 0.01).astype(np.uint8)
+        bufs = [DeviceBuffer(4 * (M + 1)), DeviceBuffer(4 * R), DeviceBuffer(4 * n),
+                DeviceBuffer(n), DeviceBuffer(4 * M), DeviceBuffer(M)]
+        wsb = binding.object_distances_workspace(M, R, n)
+        ws = DeviceBuffer(wsb)
+        for b, a in zip(bufs, [off.astype(np.uint32), agents, D, act]):
+            b.upload(a)
+        ms = binding.probe_object_distances(bufs[0].ptr, bufs[1].ptr, M, R, bufs[2].ptr,
+                                            bufs[3].ptr, n, bufs[4].ptr, bufs[5].ptr, ws.ptr,
+                                            wsb, iters)
+        for b in bufs + [ws]:
+            b.free()
+        alg = 4 * (M + 1) + 4 * R + 5 * n + 5 * M
+        return M, R, ms, alg, (D, act)
+
+    rng = np.random.default_rng(args.seed + 17)
+    off, agents, _ = W.prefix_forest(args.objects_trees, args.objects_agents, OBJ_BRANCH,
+                                     args.objects_depth, seed=args.seed)
+    n = args.objects_trees * args.objects_agents
+    M, R, ms, alg, _ = measure(off, agents, n, 20, rng)
+    del off, agents
+    small_off, small_agents, _ = W.prefix_tree_objects(16384, 4, 6, seed=args.seed)
+    m2, r2, ms2, alg2, (D2, act2) = measure(small_off, small_agents, 16384, 200, rng)
+    out = {"workload": f"{args.objects_trees} prefix trees x {args.objects_agents} agents, "
+                       f"branching {OBJ_BRANCH}, depth {args.objects_depth}, private leaves; "
+                       "1% active, distances uniform in [1, 2^20)",
+           "objects": M, "refs": R, "agents": n,
+           "kernels": "k_obj_prep + k_obj_min + k_obj_fix (event time of the three)",
+           "us_per_call": 1e3 * ms, "algorithmic_bytes": alg,
+           "roofline": {"bound": "hbm", "achieved": alg / ms / 1e6, "peak": HBM_PEAK_GBPS,
+                        "unit": "GB/s", "frac": alg / ms / 1e6 / HBM_PEAK_GBPS, "traffic": None},
+           "small": {"agents": 16384, "objects": m2, "refs": r2, "us_per_call": 1e3 * ms2,
+                     "GBps": alg2 / ms2 / 1e6}}
+    if not args.no_cpu_baseline:
+        from oracle.objects import object_distances
+        t0 = time.perf_counter()
+        object_distances(small_off, small_agents, D2, act2)
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": m2 / dt, "unit": "objects/s", "cores": 1,
+                               "kind": "oracle", "sample": f"the 16,384-agent map ({m2} objects)",
+                               "gpu_objects_per_s": M / (ms * 1e-3)}
     return out
 
 
@@ -209,6 +274,10 @@ def main():
     from paper_2601_21473_amd.memory import DeviceBuffer, PoolMemory
 
     assert binding.device_count() > 0, "bench.py needs a GPU"
+    if args.objects_only:
+        print(json.dumps({"object_distances": object_bench(args, binding, W, DeviceBuffer)}),
+              flush=True)
+        return
     trace = W.make_trace(args.workload, args.seed)
     T_need = args.warmup + args.steps + args.plan_steps
     if T_need > trace.n_steps:
@@ -346,6 +415,8 @@ def main():
             "host_enqueue_us": host[0] / nps, "host_wait_us": host[1] / nps,
             "host_readback_us": host[2] / nps}
 
+    objects = None if args.no_objects else object_bench(args, binding, W, DeviceBuffer)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(trace, args.warmup, args.cpu_steps, args.cpu_agents, thr, budget)
@@ -367,6 +438,7 @@ def main():
         "dma": dma,
         "plan_latency_us": plan,
         "kernels": kern,
+        "object_distances": objects,
         "probe": probe,
         "step_wall_ms": {"median": 1e3 * float(np.median(step_wall)),
                          "max": 1e3 * float(np.max(step_wall))},

@@ -236,20 +236,32 @@ ss_status ss_probe_link(void* host, void* dev, uint64_t bytes, int dir, int iter
  *                references the object.
  *   obj_active   [n_objects] out: 1 if any referencing agent is active.
  *   workspace    device memory of at least
- *                ss_object_distances_workspace(n_objects, n_refs) bytes,
- *                owned by the caller; its contents need no initialisation.
+ *                ss_object_distances_workspace(n_objects, n_refs, n_agents)
+ *                bytes, 16-byte aligned, owned by the caller; its contents
+ *                need no initialisation.
  * Every array is device memory of the current device, owned by the caller.
  * The work is queued on `stream` (a hipStream_t, NULL = the null stream) and
  * the call returns without waiting.  n_objects and n_refs must be below 2^31.
  * Offsets that break the rules above give unspecified output values but no
  * access outside the arrays.  SS_ERR_ARG for NULL, too small or non-device
  * arguments (nothing queued), SS_ERR_HIP if a launch fails. */
-uint64_t ss_object_distances_workspace(uint32_t n_objects, uint32_t n_refs);
+uint64_t ss_object_distances_workspace(uint32_t n_objects, uint32_t n_refs, uint32_t n_agents);
 ss_status ss_object_distances(const uint32_t* obj_off, const uint32_t* obj_agents,
                               uint32_t n_objects, uint32_t n_refs, const uint32_t* distances,
                               const uint8_t* active, uint32_t n_agents, uint32_t* obj_distances,
                               uint8_t* obj_active, void* workspace, uint64_t workspace_bytes,
                               void* stream);
+
+/* Measurement probe (not part of a step): runs ss_object_distances `iters`
+ * times back to back on a private stream after one warm-up run and returns the
+ * event time per run.  Same arguments and errors as ss_object_distances;
+ * n_objects must be >= 1.  Synchronous. */
+ss_status ss_probe_object_distances(const uint32_t* obj_off, const uint32_t* obj_agents,
+                                    uint32_t n_objects, uint32_t n_refs,
+                                    const uint32_t* distances, const uint8_t* active,
+                                    uint32_t n_agents, uint32_t* obj_distances,
+                                    uint8_t* obj_active, void* workspace,
+                                    uint64_t workspace_bytes, int iters, float* ms_per_iter);
 
 /* Block until all work the pool has queued (plan, copies, kernels) is done. */
 ss_status ss_sync(ss_pool* pool);

@@ -29,7 +29,8 @@ EXPORTS = ["ss_pool_create", "ss_pool_destroy", "ss_plan_step", "ss_evict_pack",
            "ss_prefetch_unpack", "ss_block_table", "ss_block_table_host", "ss_block_table_host_all", "ss_resident_host",
            "ss_get_stats", "ss_reset_stats", "ss_probe_copy", "ss_probe_link", "ss_sync",
            "ss_device_count", "ss_device_alloc", "ss_host_alloc", "ss_device_free", "ss_host_free",
-           "ss_copy", "ss_last_error", "ss_object_distances_workspace", "ss_object_distances"]
+           "ss_copy", "ss_last_error", "ss_object_distances_workspace", "ss_object_distances",
+           "ss_probe_object_distances"]
 
 
 class ss_pool_desc(C.Structure):
@@ -109,9 +110,11 @@ def load():
         "ss_host_free": ([P], C.c_int32),
         "ss_copy": ([P, P, C.c_uint64], C.c_int32),
         "ss_last_error": ([], C.c_char_p),
-        "ss_object_distances_workspace": ([C.c_uint32, C.c_uint32], C.c_uint64),
+        "ss_object_distances_workspace": ([C.c_uint32, C.c_uint32, C.c_uint32], C.c_uint64),
         "ss_object_distances": ([P, P, C.c_uint32, C.c_uint32, P, P, C.c_uint32, P, P, P,
                                  C.c_uint64, P], C.c_int32),
+        "ss_probe_object_distances": ([P, P, C.c_uint32, C.c_uint32, P, P, C.c_uint32, P, P, P,
+                                       C.c_uint64, C.c_int, C.POINTER(C.c_float)], C.c_int32),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -293,8 +296,8 @@ def probe_link(host: int, dev: int, nbytes: int, direction: int, iters: int = 5)
     return ms.value
 
 
-def object_distances_workspace(n_objects: int, n_refs: int) -> int:
-    return int(load().ss_object_distances_workspace(int(n_objects), int(n_refs)))
+def object_distances_workspace(n_objects: int, n_refs: int, n_agents: int) -> int:
+    return int(load().ss_object_distances_workspace(int(n_objects), int(n_refs), int(n_agents)))
 
 
 def object_distances(obj_off: int, obj_agents: int, n_objects: int, n_refs: int,
@@ -305,3 +308,17 @@ def object_distances(obj_off: int, obj_agents: int, n_objects: int, n_refs: int,
                                       int(distances), int(active), int(n_agents),
                                       int(obj_distances), int(obj_active), int(workspace),
                                       int(workspace_bytes), int(stream)))
+
+
+def probe_object_distances(obj_off: int, obj_agents: int, n_objects: int, n_refs: int,
+                           distances: int, active: int, n_agents: int, obj_distances: int,
+                           obj_active: int, workspace: int, workspace_bytes: int,
+                           iters: int = 20) -> float:
+    """Event time (ms) per ``ss_object_distances`` run, back to back."""
+    ms = C.c_float()
+    _check(load().ss_probe_object_distances(int(obj_off), int(obj_agents), int(n_objects),
+                                            int(n_refs), int(distances), int(active),
+                                            int(n_agents), int(obj_distances), int(obj_active),
+                                            int(workspace), int(workspace_bytes), int(iters),
+                                            C.byref(ms)))
+    return ms.value

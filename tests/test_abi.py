@@ -155,11 +155,14 @@ def test_probe_argument_checks():
 def test_object_distances_argument_checks():
     L = B.load()
     V = C.c_void_p
-    # one carry record of 16 bytes per 2048 merge items (objects + references)
-    assert L.ss_object_distances_workspace(1, 0) == 16
-    assert L.ss_object_distances_workspace(2048, 0) == 16
-    assert L.ss_object_distances_workspace(2048, 1) == 32
-    assert L.ss_object_distances_workspace(5000, 100000) == 16 * ((105000 + 2047) // 2048)
+    # per 2048 merge items (objects + references) a 16-byte carry record, a
+    # 4-byte merge-path coordinate per workgroup boundary (padded to 16 bytes)
+    # and an 8-byte word per agent
+    ws = lambda blocks, n: 16 * blocks + 4 * ((blocks + 1 + 3) // 4 * 4) + 8 * n
+    assert L.ss_object_distances_workspace(1, 0, 0) == ws(1, 0)
+    assert L.ss_object_distances_workspace(2048, 0, 5) == ws(1, 5)
+    assert L.ss_object_distances_workspace(2048, 1, 7) == ws(2, 7)
+    assert L.ss_object_distances_workspace(5000, 100000, 3) == ws((105000 + 2047) // 2048, 3)
     args = lambda **kw: [kw.get(k, d) for k, d in (
         ("off", V(256)), ("agents", V(512)), ("M", 4), ("R", 8), ("dist", V(1024)),
         ("act", V(2048)), ("N", 3), ("od", V(4096)), ("oa", V(8192)), ("ws", V(16384)),

@@ -32,7 +32,7 @@ class GpuObjects:
         self.act = DeviceBuffer(max(1, n_agents))
         self.od = DeviceBuffer(max(4, 4 * self.M))
         self.oa = DeviceBuffer(max(1, self.M))
-        self.wsb = B.object_distances_workspace(self.M, self.R)
+        self.wsb = B.object_distances_workspace(self.M, self.R, n_agents)
         self.ws = DeviceBuffer(max(16, self.wsb))
         self.bufs += [self.dist, self.act, self.od, self.oa, self.ws]
 
@@ -191,3 +191,34 @@ def test_object_pool_plans_from_object_distances():
         g.free()
         dD.free()
         dA.free()
+
+
+def test_bench_forest_sampled():
+    """The forest the benchmark times (8 trees x 1M agents, branching 8,
+    depth 6), on a seeded sample of objects including every tree's root."""
+    trees, n1 = 8, 1_000_000
+    off, agents, _ = W.prefix_forest(trees, n1, 8, 6, seed=0)
+    rng = np.random.default_rng(17)
+    n = trees * n1
+    D = rng.integers(1, 1 << 20, size=n).astype(np.uint32)
+    act = (rng.random(n) < 0.01).astype(np.uint8)
+    g = GpuObjects(off, agents, n)
+    try:
+        log(f"[objects] forest: M={g.M} R={g.R} N={n}")
+        d, a = g.run(D, act)
+    finally:
+        g.free()
+    M = len(off) - 1
+    per_tree = M // trees
+    idx = np.unique(np.concatenate([np.arange(trees) * per_tree, [M - 1],
+                                    rng.choice(M, 4000, replace=False)]))
+    sub_off = np.concatenate([[0], np.cumsum(off[idx + 1] - off[idx])]).astype(np.int64)
+    sub_agents = np.concatenate([agents[off[i]:off[i + 1]] for i in idx])
+    ed, ea = object_distances(sub_off, sub_agents, D, act)
+    assert np.array_equal(d[idx], ed) and np.array_equal(a[idx], ea)
+    # properties at every object: an active object is at 0; every tree's root
+    # holds the minimum of its tree
+    assert (d[a == 1] == 0).all()
+    for k in range(trees):
+        Dk = np.where(act[k * n1:(k + 1) * n1] == 1, 0, D[k * n1:(k + 1) * n1])
+        assert d[k * per_tree] == Dk.min()

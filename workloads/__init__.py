@@ -7,4 +7,4 @@ arithmetic does.
 from .traces import (SENTINEL, PoolSpec, Trace, Content, CONFIGS, make_trace,
                      exact_distances, noisy_distances, random_tiny_trace,
                      shrink_planes, subsample_agents, splitmix64, lora_chunk_bytes,
-                     prefix_tree_objects)
+                     prefix_tree_objects, prefix_forest)

@@ -319,6 +319,18 @@ def prefix_tree_objects(n_agents: int, branching: int, depth: int, seed: int,
     return obj_off, obj_agents, sizes
 
 
+def prefix_forest(n_trees: int, n_agents: int, branching: int, depth: int, seed: int):
+    """``n_trees`` independent simulations of ``n_agents`` agents, each with a
+    shared prefix tree (``prefix_tree_objects``): the trees' objects one after
+    another, agent ids of tree k offset by k * n_agents."""
+    off, agents, sizes = prefix_tree_objects(n_agents, branching, depth, seed)
+    R = np.uint64(off[-1])
+    offs = [off[:1]] + [off[1:] + np.uint64(k) * R for k in range(n_trees)]
+    ags = [agents + np.uint32(k * n_agents) for k in range(n_trees)]
+    return (np.concatenate(offs).astype(np.uint64), np.concatenate(ags),
+            np.tile(sizes, n_trees))
+
+
 def random_tiny_trace(rng: np.random.Generator, n_agents: int, n_steps: int,
                       max_active: int, capacity_agents: int, units=None):
     """A small random request trace for brute-force checks."""
