@@ -244,7 +244,7 @@ def _diffusion(seed: int) -> Trace:
     dt = exact_distances(active)
     nrng = np.random.default_rng([seed, 1])
     return Trace("diffusion", N, T, [pool], active, noisy_distances(dt, 2.0, nrng), dt,
-                 {"seed": seed, "lora_rank": ranks})
+                 {"seed": seed, "lora_rank": ranks, "out_neighbors": out})
 
 
 CONFIGS = {
