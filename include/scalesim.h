@@ -263,6 +263,56 @@ ss_status ss_probe_object_distances(const uint32_t* obj_off, const uint32_t* obj
                                     uint8_t* obj_active, void* workspace,
                                     uint64_t workspace_bytes, int iters, float* ms_per_iter);
 
+/* Hop counts (Section 3.2, "predefined activation paths": an agent's
+ * distance is its hop count from the origin of the propagation).  A
+ * breadth-first search along the directed edges of a CSR graph from the
+ * sources (the agents holding the information now, hop 0):
+ *   row_off  [n_vertices + 1] nondecreasing, row_off[n_vertices] = n_edges;
+ *   col      [n_edges]: col[row_off[u] .. row_off[u+1]) are u's out-neighbours;
+ *   sources  [n_sources] vertex ids (ids >= n_vertices are skipped,
+ *            repeated ids count once);
+ *   hops     [n_vertices] out: edges on a shortest path from the nearest
+ *            source, or 0xFFFFFFFF if no source reaches the vertex within
+ *            max_hops edges (0xFFFFFFFF = no horizon);
+ *   workspace  ss_hop_distances_workspace(n_vertices) bytes of device memory,
+ *            256-byte aligned, owned by the caller, no initialisation needed.
+ * Every array is device memory of the current device, owned by the caller.
+ * The search runs as one cooperative launch queued on `stream`; the call
+ * returns without waiting.  The 32-bit word at workspace offset 20 is 1 after
+ * the search if a grid barrier wait ever exceeded its bound (the hop counts
+ * are then incomplete); it stays 0 otherwise.  n_vertices and n_edges must be
+ * below 2^31; offsets that break the rules above give unspecified hop counts
+ * but no access outside the arrays.  SS_ERR_ARG for NULL, too small or
+ * non-device arguments, SS_ERR_HIP if the device has no cooperative launch or
+ * a launch fails. */
+uint64_t ss_hop_distances_workspace(uint32_t n_vertices);
+ss_status ss_hop_distances(const uint32_t* row_off, const uint32_t* col, uint32_t n_vertices,
+                           uint32_t n_edges, const uint32_t* sources, uint32_t n_sources,
+                           uint32_t max_hops, uint32_t* hops, void* workspace,
+                           uint64_t workspace_bytes, void* stream);
+
+/* Interaction distances (Section 3.2, interaction-involved simulations:
+ * D = min(D_action, D_interaction), D_interaction = physical distance /
+ * velocity).  Per agent i:
+ *   out[i] = min(d_action[i], floor(max(0, isqrt(d2_i) - radius) / velocity))
+ * with d2_i the squared Euclidean distance to the nearest other agent, or
+ * out[i] = d_action[i] when there is no other agent.
+ *   pos_xy   [n_agents][2] int32 tile coordinates (x, y), each in [0, 32768);
+ *            other values give unspecified results but no fault;
+ *   d_action [n_agents] remaining steps of each agent's current action;
+ *   velocity closing speed in tiles per step (>= 1); radius in tiles;
+ *   out      [n_agents] out (may alias d_action);
+ *   workspace  ss_interaction_distances_workspace(n_agents) bytes of device
+ *            memory, owned by the caller, no initialisation needed.
+ * Device memory of the current device, owned by the caller; queued on
+ * `stream`, returns without waiting.  SS_ERR_ARG for NULL, too small or
+ * non-device arguments or velocity 0, SS_ERR_HIP if a launch fails. */
+uint64_t ss_interaction_distances_workspace(uint32_t n_agents);
+ss_status ss_interaction_distances(const int32_t* pos_xy, const uint32_t* d_action,
+                                   uint32_t n_agents, uint32_t velocity, uint32_t radius,
+                                   uint32_t* out, void* workspace, uint64_t workspace_bytes,
+                                   void* stream);
+
 /* Block until all work the pool has queued (plan, copies, kernels) is done. */
 ss_status ss_sync(ss_pool* pool);
 

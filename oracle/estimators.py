@@ -61,24 +61,27 @@ def hop_distances(row_off, col, sources, max_hops=None):
     return hops
 
 
+def interaction_distance_one(pos, i, d_action_i, velocity, radius=0):
+    """D of agent i: min(D_action, D_interaction) over all other agents."""
+    assert velocity >= 1 and radius >= 0
+    best = None
+    xi, yi = int(pos[i][0]), int(pos[i][1])
+    for j in range(len(pos)):
+        if j == i:
+            continue
+        dx = xi - int(pos[j][0])
+        dy = yi - int(pos[j][1])
+        d2 = dx * dx + dy * dy
+        if best is None or d2 < best:
+            best = d2
+    if best is None:
+        return int(d_action_i)
+    return min(int(d_action_i), max(0, math.isqrt(best) - radius) // velocity)
+
+
 def interaction_distances(pos, d_action, velocity, radius=0):
     """D = min(D_action, D_interaction) per agent; ``pos`` is int [N, 2]."""
-    pos = np.asarray(pos, dtype=np.int64)
-    N = len(pos)
-    assert velocity >= 1 and radius >= 0
-    out = np.asarray(d_action, dtype=np.uint32).copy()
-    for i in range(N):
-        best = None
-        for j in range(N):
-            if j == i:
-                continue
-            dx = int(pos[i, 0]) - int(pos[j, 0])
-            dy = int(pos[i, 1]) - int(pos[j, 1])
-            d2 = dx * dx + dy * dy
-            if best is None or d2 < best:
-                best = d2
-        if best is None:
-            continue
-        d_int = max(0, math.isqrt(best) - radius) // velocity
-        out[i] = min(int(out[i]), d_int)
-    return out
+    pos = np.asarray(pos, dtype=np.int64).tolist()
+    d_action = np.asarray(d_action, dtype=np.uint32)
+    return np.array([interaction_distance_one(pos, i, d_action[i], velocity, radius)
+                     for i in range(len(pos))], dtype=np.uint32)

@@ -30,7 +30,8 @@ EXPORTS = ["ss_pool_create", "ss_pool_destroy", "ss_plan_step", "ss_evict_pack",
            "ss_get_stats", "ss_reset_stats", "ss_probe_copy", "ss_probe_link", "ss_sync",
            "ss_device_count", "ss_device_alloc", "ss_host_alloc", "ss_device_free", "ss_host_free",
            "ss_copy", "ss_last_error", "ss_object_distances_workspace", "ss_object_distances",
-           "ss_probe_object_distances"]
+           "ss_probe_object_distances", "ss_hop_distances_workspace", "ss_hop_distances",
+           "ss_interaction_distances_workspace", "ss_interaction_distances"]
 
 
 class ss_pool_desc(C.Structure):
@@ -115,6 +116,12 @@ def load():
                                  C.c_uint64, P], C.c_int32),
         "ss_probe_object_distances": ([P, P, C.c_uint32, C.c_uint32, P, P, C.c_uint32, P, P, P,
                                        C.c_uint64, C.c_int, C.POINTER(C.c_float)], C.c_int32),
+        "ss_hop_distances_workspace": ([C.c_uint32], C.c_uint64),
+        "ss_hop_distances": ([P, P, C.c_uint32, C.c_uint32, P, C.c_uint32, C.c_uint32, P, P,
+                              C.c_uint64, P], C.c_int32),
+        "ss_interaction_distances_workspace": ([C.c_uint32], C.c_uint64),
+        "ss_interaction_distances": ([P, P, C.c_uint32, C.c_uint32, C.c_uint32, P, P, C.c_uint64,
+                                      P], C.c_int32),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -322,3 +329,29 @@ def probe_object_distances(obj_off: int, obj_agents: int, n_objects: int, n_refs
                                             int(workspace), int(workspace_bytes), int(iters),
                                             C.byref(ms)))
     return ms.value
+
+
+def hop_distances_workspace(n_vertices: int) -> int:
+    return int(load().ss_hop_distances_workspace(int(n_vertices)))
+
+
+def hop_distances(row_off: int, col: int, n_vertices: int, n_edges: int, sources: int,
+                  n_sources: int, max_hops: int, hops: int, workspace: int,
+                  workspace_bytes: int, stream: int = 0):
+    """Queue ``ss_hop_distances`` (device addresses)."""
+    _check(load().ss_hop_distances(int(row_off), int(col), int(n_vertices), int(n_edges),
+                                   int(sources), int(n_sources), int(max_hops), int(hops),
+                                   int(workspace), int(workspace_bytes), int(stream)))
+
+
+def interaction_distances_workspace(n_agents: int) -> int:
+    return int(load().ss_interaction_distances_workspace(int(n_agents)))
+
+
+def interaction_distances(pos_xy: int, d_action: int, n_agents: int, velocity: int,
+                          radius: int, out: int, workspace: int, workspace_bytes: int,
+                          stream: int = 0):
+    """Queue ``ss_interaction_distances`` (device addresses)."""
+    _check(load().ss_interaction_distances(int(pos_xy), int(d_action), int(n_agents),
+                                           int(velocity), int(radius), int(out), int(workspace),
+                                           int(workspace_bytes), int(stream)))

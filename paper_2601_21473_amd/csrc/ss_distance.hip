@@ -1,4 +1,5 @@
-// Distance kernels for gfx950: invocation distances of shared memory objects.
+// Distance kernels for gfx950: invocation distances of shared memory objects
+// and the on-device distance estimators of Section 3.2.
 //
 // ss_object_distances (Appendix A, fine-grained distance assignment): an
 // object referenced by several agents takes the smallest distance among them,
@@ -24,7 +25,29 @@
 //               carry record for the row that continues past it.
 //   k_obj_fix   applies the carry records with global atomic min / stores,
 //               after every k_obj_min block has written its rows.
-// No dense contraction here; the kernel is bound by HBM bytes.
+// No dense contraction here; the kernel is bound by HBM bytes and by the rate
+// of random gathers.
+//
+// ss_hop_distances (predefined activation paths): multi-source breadth-first
+// hop counts over a CSR graph in one cooperative launch.
+//   k_bfs       level-synchronous, frontier queues in device memory; every
+//               thread takes one frontier vertex and claims its unvisited
+//               out-neighbours eight edges at a time with atomic
+//               compare-and-swap, appending winners to the next queue with one
+//               counter atomic per wave; a grid barrier (atomic arrival
+//               counter and generation word, bounded spin) separates levels,
+//               so the whole search is one launch and needs no host round
+//               trip per level.
+//
+// ss_interaction_distances (interaction-involved simulations): D =
+// min(D_action, floor(max(0, isqrt(d2) - radius) / velocity)) with d2 the
+// squared distance to the nearest other agent on an integer tile grid.
+//   k_pair_min  all pairs, 256 agents per workgroup against a slice of the
+//               others staged through LDS; 24-bit integer multiply-adds, one
+//               atomic min per agent and slice.
+//   k_pair_fin  integer square root, radius, velocity and the min with
+//               D_action.
+// Both are plain integer ALU work (no contraction), so no MFMA.
 #include "scalesim.h"
 #include "ss_internal.h"
 
@@ -265,6 +288,231 @@ __global__ void __launch_bounds__(256) k_obj_fix(const ObjCarry* __restrict__ ca
     if (c.act) out_act[c.row] = 1;
 }
 
+// ---------------------------------------------------------------------------
+// Hop counts
+// ---------------------------------------------------------------------------
+
+constexpr int kBfsThreads = 256;
+constexpr int kBfsEdges = 8;                 // edges claimed per thread per round
+constexpr unsigned kBfsSpin = 1u << 24;      // barrier spin bound (about 0.5 s)
+
+struct BfsArgs {
+    const unsigned* row_off;                 // [V + 1]
+    const unsigned* col;                     // [E]
+    const unsigned* src;                     // [n_src]
+    unsigned V, E, n_src, max_hops;
+    unsigned* hops;                          // [V]
+    unsigned* q0;                            // [V] frontier queues
+    unsigned* q1;
+    unsigned* ctl;                           // [8] see kCtl*
+};
+constexpr int kCtlCnt = 0;                   // [0..2] queue lengths, rotating
+constexpr int kCtlBarCount = 3;              // grid barrier arrivals
+constexpr int kCtlBarGen = 4;                // grid barrier generation
+constexpr int kCtlError = 5;                 // 1 if a barrier wait hit its bound
+constexpr int kCtlLevels = 6;                // levels expanded
+
+// Grid-wide barrier for a cooperative launch (all workgroups resident).
+// Returns false for every thread of a workgroup whose wait exceeded the
+// bound; the caller then leaves the kernel, so every wave exits.
+__device__ bool grid_barrier(unsigned* ctl) {
+    __shared__ int s_ok;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int ok = 1;
+        const unsigned gen = __hip_atomic_load(&ctl[kCtlBarGen], __ATOMIC_ACQUIRE,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+        const unsigned arrived = __hip_atomic_fetch_add(&ctl[kCtlBarCount], 1u, __ATOMIC_ACQ_REL,
+                                                        __HIP_MEMORY_SCOPE_AGENT) + 1;
+        if (arrived == gridDim.x) {
+            __hip_atomic_store(&ctl[kCtlBarCount], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_add(&ctl[kCtlBarGen], 1u, __ATOMIC_RELEASE,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            unsigned spin = 0;
+            while (__hip_atomic_load(&ctl[kCtlBarGen], __ATOMIC_ACQUIRE,
+                                     __HIP_MEMORY_SCOPE_AGENT) == gen) {
+                if (++spin > kBfsSpin) {
+                    ok = 0;
+                    __hip_atomic_store(&ctl[kCtlError], 1u, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(2);
+            }
+        }
+        s_ok = ok;
+    }
+    __syncthreads();
+    return s_ok != 0;
+}
+
+// Append the lanes' claimed vertices (claim[k] for k < n) to queue q with one
+// counter atomic per wave.  Called by every lane of the wave.
+template <int n>
+__device__ __forceinline__ void wave_append(const bool (&claim)[n], const unsigned (&v)[n],
+                                            unsigned* q, unsigned* cnt) {
+    u64 m[n];
+    unsigned total = 0;
+#pragma unroll
+    for (int k = 0; k < n; ++k) {
+        m[k] = __ballot(claim[k]);
+        total += __popcll(m[k]);
+    }
+    if (total == 0) return;
+    unsigned base = 0;
+    if (__lane_id() == 0)
+        base = __hip_atomic_fetch_add(cnt, total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    base = __shfl(base, 0);
+#pragma unroll
+    for (int k = 0; k < n; ++k) {
+        const unsigned below = __builtin_amdgcn_mbcnt_hi((unsigned)(m[k] >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((unsigned)m[k], 0u));
+        if (claim[k]) q[base + below] = v[k];
+        base += __popcll(m[k]);
+    }
+}
+
+__global__ void __launch_bounds__(kBfsThreads) k_bfs_init(unsigned* ctl) {
+    if (threadIdx.x < 8) ctl[threadIdx.x] = 0;
+}
+
+__global__ void __launch_bounds__(kBfsThreads) k_bfs(BfsArgs A) {
+    const unsigned lane = __lane_id();
+    const unsigned gsz = gridDim.x * kBfsThreads;
+    const unsigned wbase = blockIdx.x * kBfsThreads + (threadIdx.x & ~63u);   // wave's first thread
+    for (unsigned v = blockIdx.x * kBfsThreads + threadIdx.x; v < A.V; v += gsz)
+        A.hops[v] = kNone;
+    if (!grid_barrier(A.ctl)) return;
+
+    // sources: hop 0, each vertex once
+    for (unsigned b0 = wbase; b0 < A.n_src; b0 += gsz) {
+        const unsigned i = b0 + lane;
+        bool claim[1] = {false};
+        unsigned v[1] = {kNone};
+        if (i < A.n_src) {
+            v[0] = A.src[i];
+            if (v[0] < A.V) claim[0] = atomicCAS(&A.hops[v[0]], kNone, 0u) == kNone;
+        }
+        wave_append(claim, v, A.q0, &A.ctl[kCtlCnt + 0]);
+    }
+    if (!grid_barrier(A.ctl)) return;
+
+    for (unsigned level = 0;; ++level) {
+        const unsigned n = __hip_atomic_load(&A.ctl[kCtlCnt + level % 3], __ATOMIC_ACQUIRE,
+                                             __HIP_MEMORY_SCOPE_AGENT);
+        if (n == 0 || level >= A.max_hops) break;
+        if (blockIdx.x == 0 && threadIdx.x == 0) {
+            __hip_atomic_store(&A.ctl[kCtlCnt + (level + 2) % 3], 0u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&A.ctl[kCtlLevels], level + 1, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+        const unsigned* cur = (level & 1) ? A.q1 : A.q0;
+        unsigned* nxt = (level & 1) ? A.q0 : A.q1;
+        unsigned* cnt = &A.ctl[kCtlCnt + (level + 1) % 3];
+        for (unsigned b0 = wbase; b0 < n; b0 += gsz) {
+            const unsigned i = b0 + lane;
+            const unsigned u = i < n ? cur[i] : kNone;
+            unsigned e = 0, e1 = 0;
+            if (u < A.V) {
+                e = min(A.row_off[u], A.E);
+                e1 = min(A.row_off[u + 1], A.E);
+            }
+            while (__ballot(e < e1)) {
+                unsigned v[kBfsEdges];
+                bool claim[kBfsEdges];
+#pragma unroll
+                for (int k = 0; k < kBfsEdges; ++k) v[k] = e + k < e1 ? A.col[e + k] : kNone;
+#pragma unroll
+                for (int k = 0; k < kBfsEdges; ++k) claim[k] = v[k] < A.V && A.hops[v[k]] == kNone;
+#pragma unroll
+                for (int k = 0; k < kBfsEdges; ++k)
+                    if (claim[k]) claim[k] = atomicCAS(&A.hops[v[k]], kNone, level + 1) == kNone;
+                wave_append(claim, v, nxt, cnt);
+                e += kBfsEdges;
+            }
+        }
+        if (!grid_barrier(A.ctl)) return;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Interaction distances
+// ---------------------------------------------------------------------------
+
+constexpr int kPairThreads = 256;            // agents i per workgroup
+constexpr int kPairTile = 256;               // agents j staged per LDS round
+
+// Partial minimum of the squared distance from each agent i of the workgroup
+// to the agents j of slice [j_lo, j_hi), excluding j = i, into d2min[i].
+__global__ void __launch_bounds__(kPairThreads) k_pair_min(const int* __restrict__ pos,
+                                                           unsigned n, unsigned slice,
+                                                           unsigned* __restrict__ d2min) {
+    __shared__ int2 s_p[kPairTile];
+    const unsigned i = blockIdx.x * kPairThreads + threadIdx.x;
+    const unsigned j_lo = blockIdx.y * slice, j_hi = min(j_lo + slice, n);
+    int xi = 0, yi = 0;
+    if (i < n) {
+        xi = pos[2 * i];
+        yi = pos[2 * i + 1];
+    }
+    unsigned best = kNone;
+    for (unsigned j0 = j_lo; j0 < j_hi; j0 += kPairTile) {
+        const unsigned j = j0 + threadIdx.x;
+        if (j < j_hi) s_p[threadIdx.x] = make_int2(pos[2 * j], pos[2 * j + 1]);
+        __syncthreads();
+        const unsigned cnt = min((unsigned)kPairTile, j_hi - j0);
+        if (i - j0 < cnt) {                  // this tile holds i itself: skip the self pair
+            for (unsigned k = 0; k < cnt; ++k) {
+                const int dx = xi - s_p[k].x, dy = yi - s_p[k].y;
+                const unsigned d2 = (unsigned)(__mul24(dx, dx) + __mul24(dy, dy));
+                if (j0 + k != i) best = min(best, d2);
+            }
+        } else if (cnt == kPairTile) {
+#pragma unroll 16
+            for (unsigned k = 0; k < kPairTile; ++k) {
+                const int dx = xi - s_p[k].x, dy = yi - s_p[k].y;
+                best = min(best, (unsigned)(__mul24(dx, dx) + __mul24(dy, dy)));
+            }
+        } else {
+            for (unsigned k = 0; k < cnt; ++k) {
+                const int dx = xi - s_p[k].x, dy = yi - s_p[k].y;
+                best = min(best, (unsigned)(__mul24(dx, dx) + __mul24(dy, dy)));
+            }
+        }
+        __syncthreads();
+    }
+    if (i < n && best != kNone) atomicMin(&d2min[i], best);
+}
+
+__global__ void __launch_bounds__(256) k_pair_init(unsigned* d2min, unsigned n) {
+    const unsigned i = blockIdx.x * 256u + threadIdx.x;
+    if (i < n) d2min[i] = kNone;
+}
+
+__device__ __forceinline__ unsigned isqrt_u32(unsigned x) {
+    unsigned r = (unsigned)sqrt((double)x);
+    while ((u64)r * r > x) --r;
+    while ((u64)(r + 1) * (r + 1) <= x) ++r;
+    return r;
+}
+
+__global__ void __launch_bounds__(256) k_pair_fin(const unsigned* __restrict__ d2min,
+                                                  const unsigned* __restrict__ d_action,
+                                                  unsigned n, unsigned velocity, unsigned radius,
+                                                  unsigned* __restrict__ out) {
+    const unsigned i = blockIdx.x * 256u + threadIdx.x;
+    if (i >= n) return;
+    unsigned d = d_action[i];
+    const unsigned m = d2min[i];
+    if (m != kNone) {
+        const unsigned dist = isqrt_u32(m);
+        d = min(d, (dist > radius ? dist - radius : 0u) / velocity);
+    }
+    out[i] = d;
+}
+
 inline unsigned obj_blocks(unsigned M, unsigned R) {
     return (unsigned)(((u64)M + R + kObjTile - 1) / kObjTile);
 }
@@ -401,6 +649,126 @@ ss_status ss_probe_object_distances(const uint32_t* obj_off, const uint32_t* obj
     if (b) (void)hipEventDestroy(b);
     if (e != hipSuccess) return set_err(SS_ERR_HIP, "object distance probe: %s", hipGetErrorString(e));
     *ms_per_iter = t / iters;
+    return SS_OK;
+}
+
+uint64_t ss_hop_distances_workspace(uint32_t n_vertices) {
+    return 64 + 2 * (((uint64_t)n_vertices * 4 + 255) & ~255ull);
+}
+
+ss_status ss_hop_distances(const uint32_t* row_off, const uint32_t* col, uint32_t n_vertices,
+                           uint32_t n_edges, const uint32_t* sources, uint32_t n_sources,
+                           uint32_t max_hops, uint32_t* hops, void* workspace,
+                           uint64_t workspace_bytes, void* stream) {
+    if (n_vertices >= (1u << 31) || n_edges >= (1u << 31))
+        return set_err(SS_ERR_ARG, "n_vertices and n_edges must be below 2^31");
+    if (n_vertices == 0) return SS_OK;
+    if (!row_off || !hops || !workspace || (n_edges && !col) || (n_sources && !sources))
+        return set_err(SS_ERR_ARG, "NULL argument");
+    const u64 need = ss_hop_distances_workspace(n_vertices);
+    if (workspace_bytes < need)
+        return set_err(SS_ERR_ARG, "workspace_bytes %llu < %llu", (unsigned long long)workspace_bytes,
+                       (unsigned long long)need);
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return set_err(SS_ERR_ARG, "no current device");
+    }
+    if (!device_range_ok(row_off, ((u64)n_vertices + 1) * 4, dev) ||
+        (n_edges && !device_range_ok(col, (u64)n_edges * 4, dev)) ||
+        (n_sources && !device_range_ok(sources, (u64)n_sources * 4, dev)) ||
+        !device_range_ok(hops, (u64)n_vertices * 4, dev) || !device_range_ok(workspace, need, dev))
+        return set_err(SS_ERR_ARG, "every array must be device memory of the current device (%d)",
+                       dev);
+    int coop = 0, cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess ||
+        !coop || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(k_bfs),
+                                                     kBfsThreads, 0) != hipSuccess || per_cu < 1) {
+        (void)hipGetLastError();
+        return set_err(SS_ERR_HIP, "cooperative launch is not available on device %d", dev);
+    }
+    BfsArgs A;
+    A.row_off = row_off;
+    A.col = col;
+    A.src = sources;
+    A.V = n_vertices;
+    A.E = n_edges;
+    A.n_src = n_sources;
+    A.max_hops = max_hops;
+    A.hops = hops;
+    char* ws = static_cast<char*>(workspace);
+    A.ctl = reinterpret_cast<unsigned*>(ws);
+    const u64 qbytes = ((u64)n_vertices * 4 + 255) & ~255ull;
+    A.q0 = reinterpret_cast<unsigned*>(ws + 64);
+    A.q1 = reinterpret_cast<unsigned*>(ws + 64 + qbytes);
+    // one workgroup per CU at most (fewer for small graphs): the frontier of
+    // a level rarely exceeds 256 x 256 vertices, and fewer workgroups make
+    // the grid barrier cheaper
+    const u64 want = ((u64)std::max(n_vertices, n_sources) + kBfsThreads - 1) / kBfsThreads;
+    const unsigned grid = (unsigned)std::max<u64>(1, std::min<u64>(want, (u64)cus));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipLaunchKernelGGL(k_bfs_init, dim3(1), dim3(kBfsThreads), 0, st, A.ctl);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) {
+        void* args[] = {&A};
+        e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(k_bfs), dim3(grid),
+                                       dim3(kBfsThreads), args, 0, st);
+    }
+    if (e != hipSuccess) return set_err(SS_ERR_HIP, "hop distance kernels: %s", hipGetErrorString(e));
+    return SS_OK;
+}
+
+uint64_t ss_interaction_distances_workspace(uint32_t n_agents) { return (uint64_t)n_agents * 4; }
+
+ss_status ss_interaction_distances(const int32_t* pos_xy, const uint32_t* d_action,
+                                   uint32_t n_agents, uint32_t velocity, uint32_t radius,
+                                   uint32_t* out, void* workspace, uint64_t workspace_bytes,
+                                   void* stream) {
+    if (n_agents >= (1u << 31)) return set_err(SS_ERR_ARG, "n_agents must be below 2^31");
+    if (velocity == 0) return set_err(SS_ERR_ARG, "velocity must be >= 1");
+    if (n_agents == 0) return SS_OK;
+    if (!pos_xy || !d_action || !out || !workspace) return set_err(SS_ERR_ARG, "NULL argument");
+    const u64 need = ss_interaction_distances_workspace(n_agents);
+    if (workspace_bytes < need)
+        return set_err(SS_ERR_ARG, "workspace_bytes %llu < %llu", (unsigned long long)workspace_bytes,
+                       (unsigned long long)need);
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return set_err(SS_ERR_ARG, "no current device");
+    }
+    if (!device_range_ok(pos_xy, (u64)n_agents * 8, dev) ||
+        !device_range_ok(d_action, (u64)n_agents * 4, dev) ||
+        !device_range_ok(out, (u64)n_agents * 4, dev) || !device_range_ok(workspace, need, dev))
+        return set_err(SS_ERR_ARG, "every array must be device memory of the current device (%d)",
+                       dev);
+    int cus = 256;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 256;
+    unsigned* d2min = static_cast<unsigned*>(workspace);
+    const unsigned iblocks = (n_agents + kPairThreads - 1) / kPairThreads;
+    // split the other agents into slices so that about 8 workgroups run per CU
+    const unsigned want = (unsigned)std::max<u64>(1, (u64)cus * 8 / iblocks);
+    const unsigned tiles = (n_agents + kPairTile - 1) / kPairTile;
+    const unsigned slices = std::min(want, tiles);
+    const unsigned slice = (tiles + slices - 1) / slices * kPairTile;
+    const unsigned nslice = (n_agents + slice - 1) / slice;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const unsigned b256 = (n_agents + 255) / 256;
+    hipLaunchKernelGGL(k_pair_init, dim3(b256), dim3(256), 0, st, d2min, n_agents);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(k_pair_min, dim3(iblocks, nslice), dim3(kPairThreads), 0, st, pos_xy,
+                           n_agents, slice, d2min);
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess) {
+        hipLaunchKernelGGL(k_pair_fin, dim3(b256), dim3(256), 0, st, d2min, d_action, n_agents,
+                           velocity, radius, out);
+        e = hipGetLastError();
+    }
+    if (e != hipSuccess)
+        return set_err(SS_ERR_HIP, "interaction distance kernels: %s", hipGetErrorString(e));
     return SS_OK;
 }
 

@@ -179,6 +179,31 @@ def test_object_distances_argument_checks():
     assert L.ss_object_distances(*args()) == B.SS_ERR_ARG
 
 
+def test_estimator_argument_checks():
+    L = B.load()
+    V = C.c_void_p
+    assert L.ss_hop_distances_workspace(1) == 64 + 2 * 256
+    assert L.ss_hop_distances_workspace(1000) == 64 + 2 * 4096
+    assert L.ss_interaction_distances_workspace(7) == 28
+    hop = lambda **kw: [kw.get(k, d) for k, d in (
+        ("off", V(256)), ("col", V(512)), ("V", 4), ("E", 8), ("src", V(1024)), ("ns", 1),
+        ("mh", 0xFFFFFFFF), ("hops", V(2048)), ("ws", V(4096)), ("wsb", 1 << 20), ("st", None))]
+    assert L.ss_hop_distances(*hop(V=0)) == B.SS_OK
+    assert L.ss_hop_distances(*hop(V=1 << 31)) == B.SS_ERR_ARG
+    assert L.ss_hop_distances(*hop(off=None)) == B.SS_ERR_ARG
+    assert L.ss_hop_distances(*hop(src=None)) == B.SS_ERR_ARG
+    assert L.ss_hop_distances(*hop(wsb=64)) == B.SS_ERR_ARG
+    assert L.ss_hop_distances(*hop()) == B.SS_ERR_ARG          # host addresses
+    it = lambda **kw: [kw.get(k, d) for k, d in (
+        ("pos", V(256)), ("da", V(512)), ("n", 4), ("v", 1), ("r", 0), ("out", V(1024)),
+        ("ws", V(2048)), ("wsb", 16), ("st", None))]
+    assert L.ss_interaction_distances(*it(n=0)) == B.SS_OK
+    assert L.ss_interaction_distances(*it(v=0)) == B.SS_ERR_ARG
+    assert L.ss_interaction_distances(*it(pos=None)) == B.SS_ERR_ARG
+    assert L.ss_interaction_distances(*it(wsb=15)) == B.SS_ERR_ARG
+    assert L.ss_interaction_distances(*it()) == B.SS_ERR_ARG
+
+
 def test_no_device_is_an_argument_error_not_a_crash():
     if B.device_count() > 0:
         pytest.skip("a GPU is present")
