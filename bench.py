@@ -119,6 +119,10 @@ def parse():
                     help="skip the shared-object distance kernel measurement")
     ap.add_argument("--objects-only", action="store_true",
                     help="only the shared-object distance measurement (for profiling)")
+    ap.add_argument("--no-estimators", action="store_true",
+                    help="skip the distance estimator measurements")
+    ap.add_argument("--estimators-only", action="store_true",
+                    help="only the distance estimator measurements (for profiling)")
     ap.add_argument("--objects-trees", type=int, default=160)
     ap.add_argument("--objects-agents", type=int, default=50_000)
     ap.add_argument("--objects-depth", type=int, default=5)
@@ -209,6 +213,90 @@ def object_bench(args, binding, W, DeviceBuffer):
     return out
 
 
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12   # 32-bit VALU lane-instructions/s, MI355X
+PAIR_VALU = 2.5                # packed subtract + dot2 + half a min3 per pair (k_pair_min)
+
+
+def estimator_bench(args, binding, W, DeviceBuffer):
+    """Distance estimators of Section 3.2: hop counts on the diffusion
+    workload's graph (50,000 agents, out-degree 8, sources = the agents
+    active at step 10) and on a 4M-vertex out-degree-8 random graph from 1%
+    sources; interaction distances of 10,000 and 50,000 agents on a
+    2048 x 2048 tile grid."""
+    rng = np.random.default_rng(args.seed + 23)
+    out = {}
+
+    def timed(fn, iters):
+        t = binding.EventTimer()
+        try:
+            fn(t.handle)                       # warm-up
+            with t:
+                for _ in range(iters):
+                    fn(t.handle)
+            return t.ms / iters
+        finally:
+            t.close()
+
+    def hops_case(off, col, src, label, iters):
+        V, E = len(off) - 1, len(col)
+        b = [DeviceBuffer(4 * (V + 1)), DeviceBuffer(max(4, 4 * E)), DeviceBuffer(max(4, 4 * len(src))),
+             DeviceBuffer(4 * V)]
+        wsb = binding.hop_distances_workspace(V)
+        ws = DeviceBuffer(wsb)
+        b[0].upload(np.asarray(off, np.uint32))
+        b[1].upload(np.asarray(col, np.uint32))
+        b[2].upload(np.asarray(src, np.uint32))
+        ms = timed(lambda st: binding.hop_distances(b[0].ptr, b[1].ptr, V, E, b[2].ptr, len(src),
+                                                    0xFFFFFFFF, b[3].ptr, ws.ptr, wsb, st), iters)
+        h = b[3].download(0, 4 * V).view(np.uint32)
+        reached = h != 0xFFFFFFFF
+        deg = np.diff(np.asarray(off, np.int64))
+        traversed = int(deg[reached].sum())
+        levels = int(h[reached].max()) if reached.any() else 0
+        for x in b + [ws]:
+            x.free()
+        alg = 4 * (V + 1) + 4 * E + 20 * V
+        return {"graph": label, "vertices": V, "edges": E, "sources": len(src), "levels": levels,
+                "us_per_call": 1e3 * ms, "edges_traversed": traversed,
+                "GTEPS": traversed / ms / 1e6, "algorithmic_bytes": alg,
+                "GBps": alg / ms / 1e6, "hbm_frac": alg / ms / 1e6 / HBM_PEAK_GBPS}
+
+    tr = W.make_trace("diffusion", args.seed)
+    nb = tr.meta["out_neighbors"]
+    V = nb.shape[0]
+    out["hops_diffusion"] = hops_case(np.arange(0, 8 * V + 1, 8), nb.reshape(-1),
+                                      np.flatnonzero(tr.active[10]),
+                                      "diffusion workload graph (50,000 x out-degree 8)", 50)
+    V2 = 4_000_000
+    col = rng.integers(0, V2, size=8 * V2).astype(np.uint32)
+    out["hops_large"] = hops_case(np.arange(0, 8 * V2 + 1, 8), col,
+                                  rng.choice(V2, V2 // 100, replace=False),
+                                  "random 4,000,000 x out-degree 8", 10)
+    del col
+
+    for n in (10_000, 50_000):
+        pos = rng.integers(0, 2048, size=(n, 2)).astype(np.int32)
+        d_act = rng.integers(0, 100, size=n).astype(np.uint32)
+        b = [DeviceBuffer(8 * n), DeviceBuffer(4 * n), DeviceBuffer(4 * n)]
+        wsb = binding.interaction_distances_workspace(n)
+        ws = DeviceBuffer(wsb)
+        b[0].upload(pos.reshape(-1))
+        b[1].upload(d_act)
+        ms = timed(lambda st: binding.interaction_distances(b[0].ptr, b[1].ptr, n, 3, 2, b[2].ptr,
+                                                            ws.ptr, wsb, st), 20)
+        for x in b + [ws]:
+            x.free()
+        pairs = n * (n - 1)
+        ach = pairs * PAIR_VALU / ms / 1e9
+        out[f"interaction_{n}"] = {
+            "agents": n, "grid": "2048 x 2048 tiles", "velocity": 3, "radius": 2,
+            "us_per_call": 1e3 * ms, "Gpairs_per_s": pairs / ms / 1e6,
+            "roofline": {"bound": "alu", "achieved": ach, "peak": VALU_PEAK_TOPS,
+                         "unit": "T VALU lane-instructions/s", "frac": ach / VALU_PEAK_TOPS,
+                         "per_pair": PAIR_VALU}}
+    return out
+
+
 def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
     """The CPU oracle on a bounded sample: the oracle plan for every agent on
     steps [warmup, warmup + n_steps) (after replaying the earlier steps'
@@ -276,6 +364,10 @@ def main():
     assert binding.device_count() > 0, "bench.py needs a GPU"
     if args.objects_only:
         print(json.dumps({"object_distances": object_bench(args, binding, W, DeviceBuffer)}),
+              flush=True)
+        return
+    if args.estimators_only:
+        print(json.dumps({"estimators": estimator_bench(args, binding, W, DeviceBuffer)}),
               flush=True)
         return
     trace = W.make_trace(args.workload, args.seed)
@@ -416,6 +508,7 @@ def main():
             "host_readback_us": host[2] / nps}
 
     objects = None if args.no_objects else object_bench(args, binding, W, DeviceBuffer)
+    estimators = None if args.no_estimators else estimator_bench(args, binding, W, DeviceBuffer)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -439,6 +532,7 @@ def main():
         "plan_latency_us": plan,
         "kernels": kern,
         "object_distances": objects,
+        "estimators": estimators,
         "probe": probe,
         "step_wall_ms": {"median": 1e3 * float(np.median(step_wall)),
                          "max": 1e3 * float(np.max(step_wall))},

@@ -275,10 +275,10 @@ ss_status ss_probe_object_distances(const uint32_t* obj_off, const uint32_t* obj
  *            source, or 0xFFFFFFFF if no source reaches the vertex within
  *            max_hops edges (0xFFFFFFFF = no horizon);
  *   workspace  ss_hop_distances_workspace(n_vertices) bytes of device memory,
- *            256-byte aligned, owned by the caller, no initialisation needed.
+ *            8-byte aligned, owned by the caller, no initialisation needed.
  * Every array is device memory of the current device, owned by the caller.
- * The search runs as one cooperative launch queued on `stream`; the call
- * returns without waiting.  The 32-bit word at workspace offset 20 is 1 after
+ * The search is queued on `stream` (two ordinary launches, then one
+ * cooperative launch for the levels); the call returns without waiting.  The 32-bit word at workspace offset 20 is 1 after
  * the search if a grid barrier wait ever exceeded its bound (the hop counts
  * are then incomplete); it stays 0 otherwise.  n_vertices and n_edges must be
  * below 2^31; offsets that break the rules above give unspecified hop counts
@@ -332,6 +332,20 @@ ss_status ss_host_alloc(uint64_t bytes, void** out);
 ss_status ss_device_free(void* ptr);
 ss_status ss_host_free(void* ptr);
 ss_status ss_copy(void* dst, const void* src, uint64_t bytes);
+
+/* Streams and events of the same runtime, for callers that time or order
+ * the calls above without a framework:
+ *   ss_stream_create   non-blocking stream at the default priority on the
+ *                      current device; ss_stream_destroy / ss_stream_sync
+ *   ss_event_create    timing event; ss_event_record on a stream;
+ *   ss_event_elapsed   waits for `end`, then milliseconds from start to end */
+ss_status ss_stream_create(void** stream);
+ss_status ss_stream_destroy(void* stream);
+ss_status ss_stream_sync(void* stream);
+ss_status ss_event_create(void** event);
+ss_status ss_event_destroy(void* event);
+ss_status ss_event_record(void* event, void* stream);
+ss_status ss_event_elapsed(void* start, void* end, float* ms);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char* ss_last_error(void);

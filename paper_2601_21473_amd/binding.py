@@ -31,7 +31,9 @@ EXPORTS = ["ss_pool_create", "ss_pool_destroy", "ss_plan_step", "ss_evict_pack",
            "ss_device_count", "ss_device_alloc", "ss_host_alloc", "ss_device_free", "ss_host_free",
            "ss_copy", "ss_last_error", "ss_object_distances_workspace", "ss_object_distances",
            "ss_probe_object_distances", "ss_hop_distances_workspace", "ss_hop_distances",
-           "ss_interaction_distances_workspace", "ss_interaction_distances"]
+           "ss_interaction_distances_workspace", "ss_interaction_distances",
+           "ss_stream_create", "ss_stream_destroy", "ss_stream_sync", "ss_event_create",
+           "ss_event_destroy", "ss_event_record", "ss_event_elapsed"]
 
 
 class ss_pool_desc(C.Structure):
@@ -116,6 +118,13 @@ def load():
                                  C.c_uint64, P], C.c_int32),
         "ss_probe_object_distances": ([P, P, C.c_uint32, C.c_uint32, P, P, C.c_uint32, P, P, P,
                                        C.c_uint64, C.c_int, C.POINTER(C.c_float)], C.c_int32),
+        "ss_stream_create": ([C.POINTER(P)], C.c_int32),
+        "ss_stream_destroy": ([P], C.c_int32),
+        "ss_stream_sync": ([P], C.c_int32),
+        "ss_event_create": ([C.POINTER(P)], C.c_int32),
+        "ss_event_destroy": ([P], C.c_int32),
+        "ss_event_record": ([P, P], C.c_int32),
+        "ss_event_elapsed": ([P, P, C.POINTER(C.c_float)], C.c_int32),
         "ss_hop_distances_workspace": ([C.c_uint32], C.c_uint64),
         "ss_hop_distances": ([P, P, C.c_uint32, C.c_uint32, P, C.c_uint32, C.c_uint32, P, P,
                               C.c_uint64, P], C.c_int32),
@@ -355,3 +364,41 @@ def interaction_distances(pos_xy: int, d_action: int, n_agents: int, velocity: i
     _check(load().ss_interaction_distances(int(pos_xy), int(d_action), int(n_agents),
                                            int(velocity), int(radius), int(out), int(workspace),
                                            int(workspace_bytes), int(stream)))
+
+
+class EventTimer:
+    """Event time of work queued on one library stream:
+    ``with EventTimer() as t: f(t.stream)`` then ``t.ms``."""
+
+    def __init__(self):
+        L = load()
+        self.stream, self._a, self._b = C.c_void_p(), C.c_void_p(), C.c_void_p()
+        _check(L.ss_stream_create(C.byref(self.stream)))
+        _check(L.ss_event_create(C.byref(self._a)))
+        _check(L.ss_event_create(C.byref(self._b)))
+        self.ms = None
+
+    def __enter__(self):
+        _check(load().ss_event_record(self._a, self.stream))
+        return self
+
+    def __exit__(self, *exc):
+        L = load()
+        if exc[0] is None:
+            _check(L.ss_event_record(self._b, self.stream))
+            ms = C.c_float()
+            _check(L.ss_event_elapsed(self._a, self._b, C.byref(ms)))
+            self.ms = ms.value
+        else:
+            L.ss_stream_sync(self.stream)
+        return False
+
+    @property
+    def handle(self) -> int:
+        return self.stream.value or 0
+
+    def close(self):
+        L = load()
+        L.ss_event_destroy(self._a)
+        L.ss_event_destroy(self._b)
+        L.ss_stream_destroy(self.stream)

@@ -43,8 +43,9 @@
 // min(D_action, floor(max(0, isqrt(d2) - radius) / velocity)) with d2 the
 // squared distance to the nearest other agent on an integer tile grid.
 //   k_pair_min  all pairs, 256 agents per workgroup against a slice of the
-//               others staged through LDS; 24-bit integer multiply-adds, one
-//               atomic min per agent and slice.
+//               others staged through LDS as packed 16-bit (x, y); per pair a
+//               packed 16-bit subtract and a 16-bit dot product give dx^2 +
+//               dy^2 exactly; one atomic min per agent and slice.
 //   k_pair_fin  integer square root, radius, velocity and the min with
 //               D_action.
 // Both are plain integer ALU work (no contraction), so no MFMA.
@@ -293,7 +294,8 @@ __global__ void __launch_bounds__(256) k_obj_fix(const ObjCarry* __restrict__ ca
 // ---------------------------------------------------------------------------
 
 constexpr int kBfsThreads = 256;
-constexpr int kBfsEdges = 8;                 // edges claimed per thread per round
+constexpr int kBfsEdges = 8;                 // edges claimed per vertex per round
+constexpr int kBfsVerts = 2;                 // frontier vertices per thread per round
 constexpr unsigned kBfsSpin = 1u << 24;      // barrier spin bound (about 0.5 s)
 
 struct BfsArgs {
@@ -302,8 +304,8 @@ struct BfsArgs {
     const unsigned* src;                     // [n_src]
     unsigned V, E, n_src, max_hops;
     unsigned* hops;                          // [V]
-    unsigned* q0;                            // [V] frontier queues
-    unsigned* q1;
+    uint2* q0;                               // [V] frontier queues: edge ranges
+    uint2* q1;
     unsigned* ctl;                           // [8] see kCtl*
 };
 constexpr int kCtlCnt = 0;                   // [0..2] queue lengths, rotating
@@ -313,24 +315,30 @@ constexpr int kCtlError = 5;                 // 1 if a barrier wait hit its boun
 constexpr int kCtlLevels = 6;                // levels expanded
 
 // Grid-wide barrier for a cooperative launch (all workgroups resident).
-// Returns false for every thread of a workgroup whose wait exceeded the
-// bound; the caller then leaves the kernel, so every wave exits.
+// Thread 0 of each workgroup publishes the workgroup's writes with one
+// agent-scope release fence and arrives on a counter; the last arrival bumps
+// the generation word.  Waiters poll the generation with relaxed loads (an
+// acquire per poll would invalidate the XCD's L2 each time) and take one
+// acquire fence when it changes.  Returns false for every thread of a
+// workgroup whose wait exceeded the bound; the caller then leaves the kernel,
+// so every wave exits.
 __device__ bool grid_barrier(unsigned* ctl) {
     __shared__ int s_ok;
     __syncthreads();
     if (threadIdx.x == 0) {
         int ok = 1;
-        const unsigned gen = __hip_atomic_load(&ctl[kCtlBarGen], __ATOMIC_ACQUIRE,
+        const unsigned gen = __hip_atomic_load(&ctl[kCtlBarGen], __ATOMIC_RELAXED,
                                                __HIP_MEMORY_SCOPE_AGENT);
-        const unsigned arrived = __hip_atomic_fetch_add(&ctl[kCtlBarCount], 1u, __ATOMIC_ACQ_REL,
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        const unsigned arrived = __hip_atomic_fetch_add(&ctl[kCtlBarCount], 1u, __ATOMIC_RELAXED,
                                                         __HIP_MEMORY_SCOPE_AGENT) + 1;
         if (arrived == gridDim.x) {
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
             __hip_atomic_store(&ctl[kCtlBarCount], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_fetch_add(&ctl[kCtlBarGen], 1u, __ATOMIC_RELEASE,
-                                   __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_add(&ctl[kCtlBarGen], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         } else {
             unsigned spin = 0;
-            while (__hip_atomic_load(&ctl[kCtlBarGen], __ATOMIC_ACQUIRE,
+            while (__hip_atomic_load(&ctl[kCtlBarGen], __ATOMIC_RELAXED,
                                      __HIP_MEMORY_SCOPE_AGENT) == gen) {
                 if (++spin > kBfsSpin) {
                     ok = 0;
@@ -340,6 +348,7 @@ __device__ bool grid_barrier(unsigned* ctl) {
                 }
                 __builtin_amdgcn_s_sleep(2);
             }
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         }
         s_ok = ok;
     }
@@ -347,11 +356,14 @@ __device__ bool grid_barrier(unsigned* ctl) {
     return s_ok != 0;
 }
 
-// Append the lanes' claimed vertices (claim[k] for k < n) to queue q with one
-// counter atomic per wave.  Called by every lane of the wave.
+// Append the lanes' claimed vertices (claim[k] for k < n) to queue q as their
+// edge ranges [row_off[v], row_off[v + 1]), with one counter atomic per wave;
+// the range loads and the counter atomic are in flight together.  Entries at
+// or beyond `cap` are dropped (a vertex is claimed once, so a queue never
+// holds more than the vertex count).  Called by every lane of the wave.
 template <int n>
 __device__ __forceinline__ void wave_append(const bool (&claim)[n], const unsigned (&v)[n],
-                                            unsigned* q, unsigned* cnt) {
+                                            const BfsArgs& A, uint2* q, unsigned* cnt) {
     u64 m[n];
     unsigned total = 0;
 #pragma unroll
@@ -360,6 +372,12 @@ __device__ __forceinline__ void wave_append(const bool (&claim)[n], const unsign
         total += __popcll(m[k]);
     }
     if (total == 0) return;
+    uint2 r[n];
+#pragma unroll
+    for (int k = 0; k < n; ++k) {
+        r[k] = make_uint2(0u, 0u);
+        if (claim[k]) r[k] = make_uint2(min(A.row_off[v[k]], A.E), min(A.row_off[v[k] + 1], A.E));
+    }
     unsigned base = 0;
     if (__lane_id() == 0)
         base = __hip_atomic_fetch_add(cnt, total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -368,39 +386,40 @@ __device__ __forceinline__ void wave_append(const bool (&claim)[n], const unsign
     for (int k = 0; k < n; ++k) {
         const unsigned below = __builtin_amdgcn_mbcnt_hi((unsigned)(m[k] >> 32),
                                                          __builtin_amdgcn_mbcnt_lo((unsigned)m[k], 0u));
-        if (claim[k]) q[base + below] = v[k];
+        if (claim[k] && base + below < A.V) q[base + below] = r[k];
         base += __popcll(m[k]);
     }
 }
 
-__global__ void __launch_bounds__(kBfsThreads) k_bfs_init(unsigned* ctl) {
-    if (threadIdx.x < 8) ctl[threadIdx.x] = 0;
+// Every vertex unvisited, counters and barrier words zero.
+__global__ void __launch_bounds__(kBfsThreads) k_bfs_init(BfsArgs A) {
+    const unsigned v = blockIdx.x * kBfsThreads + threadIdx.x;
+    if (v < A.V) A.hops[v] = kNone;
+    if (blockIdx.x == 0 && threadIdx.x < 8) A.ctl[threadIdx.x] = 0;
 }
 
+// Sources: hop 0, each vertex once, into the first queue.
+__global__ void __launch_bounds__(kBfsThreads) k_bfs_src(BfsArgs A) {
+    const unsigned i = blockIdx.x * kBfsThreads + threadIdx.x;
+    bool claim[1] = {false};
+    unsigned v[1] = {kNone};
+    if (i < A.n_src) {
+        v[0] = A.src[i];
+        if (v[0] < A.V) claim[0] = atomicCAS(&A.hops[v[0]], kNone, 0u) == kNone;
+    }
+    wave_append(claim, v, A, A.q0, &A.ctl[kCtlCnt + 0]);
+}
+
+// The levels, in one cooperative launch.
 __global__ void __launch_bounds__(kBfsThreads) k_bfs(BfsArgs A) {
     const unsigned lane = __lane_id();
     const unsigned gsz = gridDim.x * kBfsThreads;
     const unsigned wbase = blockIdx.x * kBfsThreads + (threadIdx.x & ~63u);   // wave's first thread
-    for (unsigned v = blockIdx.x * kBfsThreads + threadIdx.x; v < A.V; v += gsz)
-        A.hops[v] = kNone;
-    if (!grid_barrier(A.ctl)) return;
-
-    // sources: hop 0, each vertex once
-    for (unsigned b0 = wbase; b0 < A.n_src; b0 += gsz) {
-        const unsigned i = b0 + lane;
-        bool claim[1] = {false};
-        unsigned v[1] = {kNone};
-        if (i < A.n_src) {
-            v[0] = A.src[i];
-            if (v[0] < A.V) claim[0] = atomicCAS(&A.hops[v[0]], kNone, 0u) == kNone;
-        }
-        wave_append(claim, v, A.q0, &A.ctl[kCtlCnt + 0]);
-    }
-    if (!grid_barrier(A.ctl)) return;
-
     for (unsigned level = 0;; ++level) {
-        const unsigned n = __hip_atomic_load(&A.ctl[kCtlCnt + level % 3], __ATOMIC_ACQUIRE,
-                                             __HIP_MEMORY_SCOPE_AGENT);
+        // ordered by the kernel start or the barrier's acquire fence; capped
+        // at the queue length
+        const unsigned n = min(__hip_atomic_load(&A.ctl[kCtlCnt + level % 3], __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT), A.V);
         if (n == 0 || level >= A.max_hops) break;
         if (blockIdx.x == 0 && threadIdx.x == 0) {
             __hip_atomic_store(&A.ctl[kCtlCnt + (level + 2) % 3], 0u, __ATOMIC_RELAXED,
@@ -408,29 +427,48 @@ __global__ void __launch_bounds__(kBfsThreads) k_bfs(BfsArgs A) {
             __hip_atomic_store(&A.ctl[kCtlLevels], level + 1, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
         }
-        const unsigned* cur = (level & 1) ? A.q1 : A.q0;
-        unsigned* nxt = (level & 1) ? A.q0 : A.q1;
+        const uint2* cur = (level & 1) ? A.q1 : A.q0;
+        uint2* nxt = (level & 1) ? A.q0 : A.q1;
         unsigned* cnt = &A.ctl[kCtlCnt + (level + 1) % 3];
-        for (unsigned b0 = wbase; b0 < n; b0 += gsz) {
-            const unsigned i = b0 + lane;
-            const unsigned u = i < n ? cur[i] : kNone;
-            unsigned e = 0, e1 = 0;
-            if (u < A.V) {
-                e = min(A.row_off[u], A.E);
-                e1 = min(A.row_off[u + 1], A.E);
+        // Large frontiers first read a vertex's state and try to claim it only
+        // while unvisited (fewer atomics); small ones go straight to the
+        // compare-and-swap (one dependent access less per level).
+        const bool precheck = n > 32768u;
+        // each lane expands kBfsVerts frontier vertices per round, eight of
+        // their edges at a time, so that many independent loads are in flight
+        for (unsigned b0 = wbase * kBfsVerts; b0 < n; b0 += gsz * kBfsVerts) {
+            unsigned e[kBfsVerts], e1[kBfsVerts];
+#pragma unroll
+            for (int f = 0; f < kBfsVerts; ++f) {
+                const unsigned i = b0 + f * 64u + lane;
+                const uint2 r = i < n ? cur[i] : make_uint2(0u, 0u);
+                e[f] = r.x;
+                e1[f] = min(r.y, A.E);
             }
-            while (__ballot(e < e1)) {
-                unsigned v[kBfsEdges];
-                bool claim[kBfsEdges];
+            bool more = false;
 #pragma unroll
-                for (int k = 0; k < kBfsEdges; ++k) v[k] = e + k < e1 ? A.col[e + k] : kNone;
+            for (int f = 0; f < kBfsVerts; ++f) more |= e[f] < e1[f];
+            while (__ballot(more)) {
+                unsigned v[kBfsVerts * kBfsEdges];
+                bool claim[kBfsVerts * kBfsEdges];
 #pragma unroll
-                for (int k = 0; k < kBfsEdges; ++k) claim[k] = v[k] < A.V && A.hops[v[k]] == kNone;
+                for (int f = 0; f < kBfsVerts; ++f)
 #pragma unroll
-                for (int k = 0; k < kBfsEdges; ++k)
+                    for (int k = 0; k < kBfsEdges; ++k)
+                        v[f * kBfsEdges + k] = e[f] + k < e1[f] ? A.col[e[f] + k] : kNone;
+#pragma unroll
+                for (int k = 0; k < kBfsVerts * kBfsEdges; ++k)
+                    claim[k] = v[k] < A.V && (!precheck || A.hops[v[k]] == kNone);
+#pragma unroll
+                for (int k = 0; k < kBfsVerts * kBfsEdges; ++k)
                     if (claim[k]) claim[k] = atomicCAS(&A.hops[v[k]], kNone, level + 1) == kNone;
-                wave_append(claim, v, nxt, cnt);
-                e += kBfsEdges;
+                wave_append(claim, v, A, nxt, cnt);
+                more = false;
+#pragma unroll
+                for (int f = 0; f < kBfsVerts; ++f) {
+                    e[f] += kBfsEdges;
+                    more |= e[f] < e1[f];
+                }
             }
         }
         if (!grid_barrier(A.ctl)) return;
@@ -444,42 +482,44 @@ __global__ void __launch_bounds__(kBfsThreads) k_bfs(BfsArgs A) {
 constexpr int kPairThreads = 256;            // agents i per workgroup
 constexpr int kPairTile = 256;               // agents j staged per LDS round
 
+typedef short short2_t __attribute__((ext_vector_type(2)));
+
+// Squared distance of two grid points held as packed 16-bit (x, y): one packed
+// subtract and one 16-bit dot product (coordinates below 2^15, so neither the
+// differences nor the sum of squares overflow).  The dot product is written
+// in its three-operand form with a zero addend; the compiler's two-operand
+// form would need a register cleared before every pair.
+__device__ __forceinline__ unsigned dist2(short2_t a, short2_t b) {
+    const short2_t d = a - b;
+    int r;
+    asm("v_dot2_i32_i16 %0, %1, %1, 0" : "=v"(r) : "v"(d));
+    return (unsigned)r;
+}
+
 // Partial minimum of the squared distance from each agent i of the workgroup
 // to the agents j of slice [j_lo, j_hi), excluding j = i, into d2min[i].
 __global__ void __launch_bounds__(kPairThreads) k_pair_min(const int* __restrict__ pos,
                                                            unsigned n, unsigned slice,
                                                            unsigned* __restrict__ d2min) {
-    __shared__ int2 s_p[kPairTile];
+    __shared__ short2_t s_p[kPairTile];
     const unsigned i = blockIdx.x * kPairThreads + threadIdx.x;
     const unsigned j_lo = blockIdx.y * slice, j_hi = min(j_lo + slice, n);
-    int xi = 0, yi = 0;
-    if (i < n) {
-        xi = pos[2 * i];
-        yi = pos[2 * i + 1];
-    }
+    short2_t pi = {0, 0};
+    if (i < n) pi = short2_t{(short)pos[2 * i], (short)pos[2 * i + 1]};
     unsigned best = kNone;
     for (unsigned j0 = j_lo; j0 < j_hi; j0 += kPairTile) {
         const unsigned j = j0 + threadIdx.x;
-        if (j < j_hi) s_p[threadIdx.x] = make_int2(pos[2 * j], pos[2 * j + 1]);
+        if (j < j_hi) s_p[threadIdx.x] = short2_t{(short)pos[2 * j], (short)pos[2 * j + 1]};
         __syncthreads();
         const unsigned cnt = min((unsigned)kPairTile, j_hi - j0);
         if (i - j0 < cnt) {                  // this tile holds i itself: skip the self pair
-            for (unsigned k = 0; k < cnt; ++k) {
-                const int dx = xi - s_p[k].x, dy = yi - s_p[k].y;
-                const unsigned d2 = (unsigned)(__mul24(dx, dx) + __mul24(dy, dy));
-                if (j0 + k != i) best = min(best, d2);
-            }
+            for (unsigned k = 0; k < cnt; ++k)
+                if (j0 + k != i) best = min(best, dist2(pi, s_p[k]));
         } else if (cnt == kPairTile) {
-#pragma unroll 16
-            for (unsigned k = 0; k < kPairTile; ++k) {
-                const int dx = xi - s_p[k].x, dy = yi - s_p[k].y;
-                best = min(best, (unsigned)(__mul24(dx, dx) + __mul24(dy, dy)));
-            }
+#pragma unroll 32
+            for (unsigned k = 0; k < kPairTile; ++k) best = min(best, dist2(pi, s_p[k]));
         } else {
-            for (unsigned k = 0; k < cnt; ++k) {
-                const int dx = xi - s_p[k].x, dy = yi - s_p[k].y;
-                best = min(best, (unsigned)(__mul24(dx, dx) + __mul24(dy, dy)));
-            }
+            for (unsigned k = 0; k < cnt; ++k) best = min(best, dist2(pi, s_p[k]));
         }
         __syncthreads();
     }
@@ -653,7 +693,7 @@ ss_status ss_probe_object_distances(const uint32_t* obj_off, const uint32_t* obj
 }
 
 uint64_t ss_hop_distances_workspace(uint32_t n_vertices) {
-    return 64 + 2 * (((uint64_t)n_vertices * 4 + 255) & ~255ull);
+    return 64 + 2 * (((uint64_t)n_vertices * 8 + 255) & ~255ull);
 }
 
 ss_status ss_hop_distances(const uint32_t* row_off, const uint32_t* col, uint32_t n_vertices,
@@ -699,17 +739,23 @@ ss_status ss_hop_distances(const uint32_t* row_off, const uint32_t* col, uint32_
     A.hops = hops;
     char* ws = static_cast<char*>(workspace);
     A.ctl = reinterpret_cast<unsigned*>(ws);
-    const u64 qbytes = ((u64)n_vertices * 4 + 255) & ~255ull;
-    A.q0 = reinterpret_cast<unsigned*>(ws + 64);
-    A.q1 = reinterpret_cast<unsigned*>(ws + 64 + qbytes);
-    // one workgroup per CU at most (fewer for small graphs): the frontier of
-    // a level rarely exceeds 256 x 256 vertices, and fewer workgroups make
-    // the grid barrier cheaper
-    const u64 want = ((u64)std::max(n_vertices, n_sources) + kBfsThreads - 1) / kBfsThreads;
+    const u64 qbytes = ((u64)n_vertices * 8 + 255) & ~255ull;
+    A.q0 = reinterpret_cast<uint2*>(ws + 64);
+    A.q1 = reinterpret_cast<uint2*>(ws + 64 + qbytes);
+    // one workgroup per 512 vertices, at most one per CU: every workgroup
+    // pays an L2 write-back and invalidate at each grid barrier, so fewer,
+    // wider workgroups (two vertices per thread per round) are cheaper
+    const u64 want = ((u64)n_vertices + kBfsThreads * kBfsVerts - 1) / (kBfsThreads * kBfsVerts);
     const unsigned grid = (unsigned)std::max<u64>(1, std::min<u64>(want, (u64)cus));
     hipStream_t st = static_cast<hipStream_t>(stream);
-    hipLaunchKernelGGL(k_bfs_init, dim3(1), dim3(kBfsThreads), 0, st, A.ctl);
+    hipLaunchKernelGGL(k_bfs_init, dim3((n_vertices + kBfsThreads - 1) / kBfsThreads),
+                       dim3(kBfsThreads), 0, st, A);
     hipError_t e = hipGetLastError();
+    if (e == hipSuccess && n_sources) {
+        hipLaunchKernelGGL(k_bfs_src, dim3((n_sources + kBfsThreads - 1) / kBfsThreads),
+                           dim3(kBfsThreads), 0, st, A);
+        e = hipGetLastError();
+    }
     if (e == hipSuccess) {
         void* args[] = {&A};
         e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(k_bfs), dim3(grid),

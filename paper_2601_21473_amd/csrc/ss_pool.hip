@@ -1026,6 +1026,52 @@ ss_status ss_copy(void* dst, const void* src, uint64_t bytes) {
     return SS_OK;
 }
 
+ss_status ss_stream_create(void** stream) {
+    if (!stream) return set_err(SS_ERR_ARG, "NULL output");
+    hipStream_t s = nullptr;
+    TRY_HIP(nullptr, hipStreamCreateWithFlags(&s, hipStreamNonBlocking), false);
+    *stream = s;
+    return SS_OK;
+}
+
+ss_status ss_stream_destroy(void* stream) {
+    if (stream) TRY_HIP(nullptr, hipStreamDestroy(static_cast<hipStream_t>(stream)), false);
+    return SS_OK;
+}
+
+ss_status ss_stream_sync(void* stream) {
+    TRY_HIP(nullptr, hipStreamSynchronize(static_cast<hipStream_t>(stream)), false);
+    return SS_OK;
+}
+
+ss_status ss_event_create(void** event) {
+    if (!event) return set_err(SS_ERR_ARG, "NULL output");
+    hipEvent_t e = nullptr;
+    TRY_HIP(nullptr, hipEventCreate(&e), false);
+    *event = e;
+    return SS_OK;
+}
+
+ss_status ss_event_destroy(void* event) {
+    if (event) TRY_HIP(nullptr, hipEventDestroy(static_cast<hipEvent_t>(event)), false);
+    return SS_OK;
+}
+
+ss_status ss_event_record(void* event, void* stream) {
+    if (!event) return set_err(SS_ERR_ARG, "NULL event");
+    TRY_HIP(nullptr, hipEventRecord(static_cast<hipEvent_t>(event), static_cast<hipStream_t>(stream)),
+            false);
+    return SS_OK;
+}
+
+ss_status ss_event_elapsed(void* start, void* end, float* ms) {
+    if (!start || !end || !ms) return set_err(SS_ERR_ARG, "NULL argument");
+    TRY_HIP(nullptr, hipEventSynchronize(static_cast<hipEvent_t>(end)), false);
+    TRY_HIP(nullptr, hipEventElapsedTime(ms, static_cast<hipEvent_t>(start),
+                                         static_cast<hipEvent_t>(end)), false);
+    return SS_OK;
+}
+
 ss_status ss_probe_copy(void* dst, const void* src, uint64_t bytes, int iters, float* ms) {
     if (!dst || !src || !ms || iters < 1 || bytes == 0 || bytes % 16)
         return set_err(SS_ERR_ARG, "bad probe arguments");

@@ -183,7 +183,7 @@ def test_estimator_argument_checks():
     L = B.load()
     V = C.c_void_p
     assert L.ss_hop_distances_workspace(1) == 64 + 2 * 256
-    assert L.ss_hop_distances_workspace(1000) == 64 + 2 * 4096
+    assert L.ss_hop_distances_workspace(1000) == 64 + 2 * 8192
     assert L.ss_interaction_distances_workspace(7) == 28
     hop = lambda **kw: [kw.get(k, d) for k, d in (
         ("off", V(256)), ("col", V(512)), ("V", 4), ("E", 8), ("src", V(1024)), ("ns", 1),
@@ -202,6 +202,16 @@ def test_estimator_argument_checks():
     assert L.ss_interaction_distances(*it(pos=None)) == B.SS_ERR_ARG
     assert L.ss_interaction_distances(*it(wsb=15)) == B.SS_ERR_ARG
     assert L.ss_interaction_distances(*it()) == B.SS_ERR_ARG
+
+
+def test_stream_event_argument_checks():
+    L = B.load()
+    assert L.ss_stream_create(None) == B.SS_ERR_ARG
+    assert L.ss_event_create(None) == B.SS_ERR_ARG
+    assert L.ss_event_record(None, None) == B.SS_ERR_ARG
+    ms = C.c_float()
+    assert L.ss_event_elapsed(None, None, C.byref(ms)) == B.SS_ERR_ARG
+    assert L.ss_stream_destroy(None) == B.SS_OK and L.ss_event_destroy(None) == B.SS_OK
 
 
 def test_no_device_is_an_argument_error_not_a_crash():
