@@ -313,6 +313,84 @@ ss_status ss_interaction_distances(const int32_t* pos_xy, const uint32_t* d_acti
                                    uint32_t* out, void* workspace, uint64_t workspace_bytes,
                                    void* stream);
 
+/* ---- Load-task scheduler (Appendix A, "Load task scheduler" and
+ * "Preemption support") ------------------------------------------------------
+ *
+ * One centralized scheduler for every CPU-to-GPU load of its memory modules
+ * (each described by an ss_pool_desc, the same data model as a pool: planes,
+ * agent sizes, pinned host copies, a staging buffer cut into ring_slots
+ * slots; the loader uses all of the staging buffer for loads).  Tasks are
+ * ordered by (distance, agent, module), smallest first.  A task loads one
+ * agent's memory of one module into the destination units it names and runs
+ * as chunks of whole units (as many as fit in one staging slot): a copy of
+ * the chunk from the agent's host copy into a slot, then a scatter into the
+ * destination units on the device.  Before every chunk the scheduler checks
+ * the preemption signal: if a queued task's distance is strictly smaller than
+ * the running task's, the running task returns to the queue with its
+ * progress (it later resumes at its next chunk) and the urgent task runs.
+ * At most min(ring_slots) chunks are in flight, and each decision is taken
+ * after the chunk that many places earlier has finished, so an urgent task
+ * waits for at most that many chunks. */
+typedef struct ss_loader ss_loader;
+
+#define SS_LOADER_NO_PREEMPT 2u     /* tasks start in key order but always finish   */
+
+#define SS_LOAD_START        1u     /* log flag: the task starts or resumes         */
+#define SS_LOAD_PREEMPT      2u     /* log flag: it interrupted the running task    */
+#define SS_LOAD_DONE         4u     /* log flag: the task's last chunk              */
+
+typedef struct {
+    uint32_t       module;          /* index into the loader's modules               */
+    uint32_t       agent;           /* agent id within the module                    */
+    uint32_t       distance;        /* invocation distance (0 = needed now)          */
+    uint32_t       pad;
+    const int32_t* units;           /* device: destination unit of each of the agent's
+                                       agent_units[agent] logical units (caller-owned,
+                                       valid until the task's last chunk has run);
+                                       unit ids outside [0, capacity) are skipped  */
+} ss_load_task;
+
+typedef struct {
+    uint32_t module, agent;
+    uint32_t first;                 /* first logical unit of the chunk               */
+    uint32_t count;                 /* units in the chunk                            */
+    uint32_t flags;                 /* SS_LOAD_*                                     */
+    uint32_t pad;
+} ss_load_log;
+
+typedef struct {
+    uint64_t submitted, completed;  /* tasks                                         */
+    uint64_t chunks, bytes;         /* chunks issued and their bytes                 */
+    uint64_t preemptions;
+} ss_loader_stats;
+
+/* Create a scheduler over n_modules modules, all on one device (flags:
+ * SS_LOADER_NO_PREEMPT or 0).  Every staging slot must hold at least one
+ * unit.  SS_ERR_ARG for an invalid descriptor (message in ss_last_error). */
+ss_status ss_loader_create(const ss_pool_desc* modules, uint32_t n_modules, uint32_t flags,
+                           ss_loader** out);
+/* Waits for issued chunks, then frees the scheduler (NULL is ignored). */
+void ss_loader_destroy(ss_loader* loader);
+/* DispatchLoadTasks: queue tasks.  A task whose (module, agent) is already
+ * queued or running only takes the new distance (its units are kept); one
+ * submitted after the agent's previous task completed is a new task.  All
+ * tasks are checked before any is queued (SS_ERR_ARG: module or agent out of
+ * range, units not device memory of the right size).  Thread-safe with
+ * ss_loader_pump. */
+ss_status ss_loader_submit(ss_loader* loader, const ss_load_task* tasks, uint32_t n);
+/* Issue up to max_chunks chunks in priority order, checking the preemption
+ * signal before each; blocks while the in-flight window is full.  Writes one
+ * entry per issued chunk to log (up to log_cap; log may be NULL when log_cap
+ * is 0) and the number issued to *n_issued.  Returns when max_chunks are
+ * issued or no task is left.  One thread at a time. */
+ss_status ss_loader_pump(ss_loader* loader, uint32_t max_chunks, ss_load_log* log,
+                         uint32_t log_cap, uint32_t* n_issued);
+/* Tasks waiting in the queue and whether one is running. */
+ss_status ss_loader_pending(ss_loader* loader, uint32_t* queued, uint32_t* running);
+/* Block until every issued chunk has landed in its destination units. */
+ss_status ss_loader_sync(ss_loader* loader);
+ss_status ss_loader_get_stats(ss_loader* loader, ss_loader_stats* out);
+
 /* Block until all work the pool has queued (plan, copies, kernels) is done. */
 ss_status ss_sync(ss_pool* pool);
 

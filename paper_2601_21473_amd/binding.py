@@ -33,7 +33,24 @@ EXPORTS = ["ss_pool_create", "ss_pool_destroy", "ss_plan_step", "ss_evict_pack",
            "ss_probe_object_distances", "ss_hop_distances_workspace", "ss_hop_distances",
            "ss_interaction_distances_workspace", "ss_interaction_distances",
            "ss_stream_create", "ss_stream_destroy", "ss_stream_sync", "ss_event_create",
-           "ss_event_destroy", "ss_event_record", "ss_event_elapsed"]
+           "ss_event_destroy", "ss_event_record", "ss_event_elapsed", "ss_loader_create",
+           "ss_loader_destroy", "ss_loader_submit", "ss_loader_pump", "ss_loader_pending",
+           "ss_loader_sync", "ss_loader_get_stats"]
+
+
+class ss_load_task(C.Structure):
+    _fields_ = [("module", C.c_uint32), ("agent", C.c_uint32), ("distance", C.c_uint32),
+                ("pad", C.c_uint32), ("units", C.c_void_p)]
+
+
+class ss_load_log(C.Structure):
+    _fields_ = [("module", C.c_uint32), ("agent", C.c_uint32), ("first", C.c_uint32),
+                ("count", C.c_uint32), ("flags", C.c_uint32), ("pad", C.c_uint32)]
+
+
+class ss_loader_stats(C.Structure):
+    _fields_ = [("submitted", C.c_uint64), ("completed", C.c_uint64), ("chunks", C.c_uint64),
+                ("bytes", C.c_uint64), ("preemptions", C.c_uint64)]
 
 
 class ss_pool_desc(C.Structure):
@@ -125,6 +142,15 @@ def load():
         "ss_event_destroy": ([P], C.c_int32),
         "ss_event_record": ([P, P], C.c_int32),
         "ss_event_elapsed": ([P, P, C.POINTER(C.c_float)], C.c_int32),
+        "ss_loader_create": ([C.POINTER(ss_pool_desc), C.c_uint32, C.c_uint32, C.POINTER(P)],
+                             C.c_int32),
+        "ss_loader_destroy": ([P], None),
+        "ss_loader_submit": ([P, C.POINTER(ss_load_task), C.c_uint32], C.c_int32),
+        "ss_loader_pump": ([P, C.c_uint32, C.POINTER(ss_load_log), C.c_uint32,
+                            C.POINTER(C.c_uint32)], C.c_int32),
+        "ss_loader_pending": ([P, C.POINTER(C.c_uint32), C.POINTER(C.c_uint32)], C.c_int32),
+        "ss_loader_sync": ([P], C.c_int32),
+        "ss_loader_get_stats": ([P, C.POINTER(ss_loader_stats)], C.c_int32),
         "ss_hop_distances_workspace": ([C.c_uint32], C.c_uint64),
         "ss_hop_distances": ([P, P, C.c_uint32, C.c_uint32, P, C.c_uint32, C.c_uint32, P, P,
                               C.c_uint64, P], C.c_int32),
@@ -152,6 +178,31 @@ def _u64(a):
     return np.ascontiguousarray(a, dtype=np.uint64)
 
 
+def make_desc(*, capacity_units, chunk_bytes, agent_units, plane_base, host_backing, host_bytes,
+              dev_staging, staging_bytes, ring_slots, host_off=None, device=0, flags=0):
+    """An ``ss_pool_desc`` and the arrays it points to (keep them alive)."""
+    chunk = _u64(chunk_bytes)
+    units = np.ascontiguousarray(agent_units, dtype=np.uint32)
+    bases = (C.c_void_p * len(plane_base))(*[int(b) for b in plane_base])
+    hoff = None if host_off is None else _u64(host_off)
+    d = ss_pool_desc()
+    d.n_agents = len(units)
+    d.capacity_units = int(capacity_units)
+    d.n_planes = len(chunk)
+    d.plane_base = bases
+    d.chunk_bytes = chunk.ctypes.data_as(C.POINTER(C.c_uint64))
+    d.agent_units = units.ctypes.data_as(C.POINTER(C.c_uint32))
+    d.host_backing = int(host_backing)
+    d.host_off = None if hoff is None else hoff.ctypes.data_as(C.POINTER(C.c_uint64))
+    d.host_bytes = int(host_bytes)
+    d.dev_staging = int(dev_staging)
+    d.staging_bytes = int(staging_bytes)
+    d.ring_slots = int(ring_slots)
+    d.device = int(device)
+    d.flags = int(flags)
+    return d, (chunk, units, bases, hoff)
+
+
 class Pool:
     """One memory module's pool (``ss_pool``).  Pointers are plain integers
     (device addresses, pinned host addresses, hipStream_t handles)."""
@@ -160,27 +211,15 @@ class Pool:
                  host_bytes, dev_staging, staging_bytes, ring_slots, host_off=None, device=0,
                  timing=False):
         L = load()
-        self._chunk = _u64(chunk_bytes)
-        self._units = np.ascontiguousarray(agent_units, dtype=np.uint32)
-        self._bases = (C.c_void_p * len(plane_base))(*[int(b) for b in plane_base])
-        self._host_off = None if host_off is None else _u64(host_off)
+        d, self._keep = make_desc(capacity_units=capacity_units, chunk_bytes=chunk_bytes,
+                                  agent_units=agent_units, plane_base=plane_base,
+                                  host_backing=host_backing, host_bytes=host_bytes,
+                                  dev_staging=dev_staging, staging_bytes=staging_bytes,
+                                  ring_slots=ring_slots, host_off=host_off, device=device,
+                                  flags=SS_FLAG_TIMING if timing else 0)
+        self._chunk = self._keep[0]
+        self._units = self._keep[1]
         self.n_agents = len(self._units)
-        d = ss_pool_desc()
-        d.n_agents = self.n_agents
-        d.capacity_units = int(capacity_units)
-        d.n_planes = len(self._chunk)
-        d.plane_base = self._bases
-        d.chunk_bytes = self._chunk.ctypes.data_as(C.POINTER(C.c_uint64))
-        d.agent_units = self._units.ctypes.data_as(C.POINTER(C.c_uint32))
-        d.host_backing = int(host_backing)
-        d.host_off = (None if self._host_off is None
-                      else self._host_off.ctypes.data_as(C.POINTER(C.c_uint64)))
-        d.host_bytes = int(host_bytes)
-        d.dev_staging = int(dev_staging)
-        d.staging_bytes = int(staging_bytes)
-        d.ring_slots = int(ring_slots)
-        d.device = int(device)
-        d.flags = SS_FLAG_TIMING if timing else 0
         h = C.c_void_p()
         _check(L.ss_pool_create(C.byref(d), C.byref(h)))
         self._h = h
@@ -402,3 +441,66 @@ class EventTimer:
         L.ss_event_destroy(self._a)
         L.ss_event_destroy(self._b)
         L.ss_stream_destroy(self.stream)
+
+
+SS_LOADER_NO_PREEMPT = 2
+SS_LOAD_START, SS_LOAD_PREEMPT, SS_LOAD_DONE = 1, 2, 4
+
+
+class Loader:
+    """The load-task scheduler (``ss_loader``) over one or more modules, each
+    given as the keyword arguments of ``make_desc``."""
+
+    def __init__(self, modules, preempt=True):
+        L = load()
+        descs, self._keep = [], []
+        for m in modules:
+            d, keep = make_desc(**m)
+            descs.append(d)
+            self._keep.append(keep)
+        arr = (ss_pool_desc * len(descs))(*descs)
+        h = C.c_void_p()
+        _check(L.ss_loader_create(arr, len(descs), 0 if preempt else SS_LOADER_NO_PREEMPT,
+                                  C.byref(h)))
+        self._h = h
+
+    def submit(self, tasks):
+        """``tasks``: iterable of (module, agent, distance, units device pointer)."""
+        tasks = list(tasks)
+        arr = (ss_load_task * max(1, len(tasks)))()
+        for i, (m, a, d, u) in enumerate(tasks):
+            arr[i] = ss_load_task(int(m), int(a), int(d), 0, int(u))
+        _check(load().ss_loader_submit(self._h, arr, len(tasks)))
+
+    def pump(self, max_chunks):
+        """Issue up to ``max_chunks`` chunks; returns their log as tuples
+        (module, agent, first, count, flags)."""
+        cap = int(max_chunks)
+        log = (ss_load_log * max(1, min(cap, 1 << 20)))()
+        n = C.c_uint32()
+        _check(load().ss_loader_pump(self._h, cap, log, min(cap, 1 << 20), C.byref(n)))
+        return [(e.module, e.agent, e.first, e.count, e.flags) for e in log[:min(n.value, cap)]]
+
+    def pending(self):
+        q, r = C.c_uint32(), C.c_uint32()
+        _check(load().ss_loader_pending(self._h, C.byref(q), C.byref(r)))
+        return q.value, r.value
+
+    def sync(self):
+        _check(load().ss_loader_sync(self._h))
+
+    def stats(self) -> dict:
+        st = ss_loader_stats()
+        _check(load().ss_loader_get_stats(self._h, C.byref(st)))
+        return {k: getattr(st, k) for k, _ in st._fields_}
+
+    def close(self):
+        if getattr(self, "_h", None):
+            load().ss_loader_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

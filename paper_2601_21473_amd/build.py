@@ -9,7 +9,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["ss_kernels.hip", "ss_pool.hip", "ss_distance.hip"]
+SOURCES = ["ss_kernels.hip", "ss_pool.hip", "ss_distance.hip", "ss_loader.hip"]
 LIB = os.path.join(HERE, "libscalesim.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

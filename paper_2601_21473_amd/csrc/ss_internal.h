@@ -146,5 +146,6 @@ hipError_t launch_probe_copy(void* dst, const void* src, u64 bytes, hipStream_t 
 // Host helpers defined in ss_pool.hip.
 ss_status set_err(ss_status st, const char* fmt, ...);       // sets ss_last_error
 bool device_range_ok(const void* ptr, u64 bytes, int device); // one device allocation
+bool pinned_range_ok(const void* ptr, u64 bytes);             // pinned host memory
 
 }  // namespace ss

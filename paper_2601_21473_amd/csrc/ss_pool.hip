@@ -310,9 +310,6 @@ bool device_range_ok(const void* ptr, u64 bytes, int device) {
     return off <= size && bytes <= size - off;
 }
 
-}  // namespace ss
-
-namespace {
 
 // True if host_ptr is pinned (page-locked) host memory; when the runtime
 // reports the allocation's extent, [host_ptr, host_ptr + bytes) must fit in it.
@@ -332,6 +329,9 @@ bool pinned_range_ok(const void* ptr, u64 bytes) {
     const u64 off = reinterpret_cast<uintptr_t>(ptr) - reinterpret_cast<uintptr_t>(base);
     return off <= size && bytes <= size - off;
 }
+}  // namespace ss
+
+namespace {
 
 ss_status check_usable(ss_pool* p) {
     if (!p) return set_err(SS_ERR_ARG, "pool is NULL");

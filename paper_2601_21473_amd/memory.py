@@ -92,6 +92,16 @@ class PoolMemory:
         self.ring_slots = ring_slots
         self.device = device
 
+    def desc_args(self) -> dict:
+        """Keyword arguments of ``binding.make_desc`` for these buffers."""
+        s = self.spec
+        return dict(capacity_units=s.capacity_units, chunk_bytes=s.chunk_bytes,
+                    agent_units=s.agent_units, plane_base=[p.ptr for p in self.planes],
+                    host_backing=self.host.ptr, host_bytes=self.host.nbytes,
+                    host_off=self.host_off, dev_staging=self.staging.ptr,
+                    staging_bytes=self.staging.nbytes, ring_slots=self.ring_slots,
+                    device=self.device)
+
     def make_pool(self, timing: bool = False) -> binding.Pool:
         s = self.spec
         return binding.Pool(capacity_units=s.capacity_units, chunk_bytes=s.chunk_bytes,

@@ -32,7 +32,8 @@ def test_header_functions_exported():
 
 def test_struct_layouts_match_header(tmp_path):
     structs = {"ss_pool_desc": B.ss_pool_desc, "ss_plan_params": B.ss_plan_params,
-               "ss_plan": B.ss_plan, "ss_stats": B.ss_stats}
+               "ss_plan": B.ss_plan, "ss_stats": B.ss_stats, "ss_load_task": B.ss_load_task,
+               "ss_load_log": B.ss_load_log, "ss_loader_stats": B.ss_loader_stats}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "scalesim.h"', "int main(void){"]
     for sname, cls in structs.items():
         lines.append(f'printf("{sname} size %zu\\n", sizeof({sname}));')
@@ -57,6 +58,9 @@ def test_constants_match_header():
     for name in ["SS_OK", "SS_ERR_ARG", "SS_ERR_OVERCOMMIT", "SS_ERR_ORDER", "SS_ERR_HIP",
                  "SS_ERR_NOMEM", "SS_ERR_POISONED"]:
         m = re.search(rf"#define {name}\s+\(?(-?\d+)\)?", text)
+        assert int(m.group(1)) == getattr(B, name), name
+    for name in ["SS_LOADER_NO_PREEMPT", "SS_LOAD_START", "SS_LOAD_PREEMPT", "SS_LOAD_DONE"]:
+        m = re.search(rf"#define {name}\s+(\d+)u", text)
         assert int(m.group(1)) == getattr(B, name), name
 
 
@@ -212,6 +216,25 @@ def test_stream_event_argument_checks():
     ms = C.c_float()
     assert L.ss_event_elapsed(None, None, C.byref(ms)) == B.SS_ERR_ARG
     assert L.ss_stream_destroy(None) == B.SS_OK and L.ss_event_destroy(None) == B.SS_OK
+
+
+def test_loader_argument_checks():
+    L = B.load()
+    h = C.c_void_p()
+    assert L.ss_loader_create(None, 1, 0, C.byref(h)) == B.SS_ERR_ARG
+    d, keep = _desc()
+    arr = (B.ss_pool_desc * 1)(d)
+    assert L.ss_loader_create(arr, 0, 0, C.byref(h)) == B.SS_ERR_ARG
+    assert L.ss_loader_create(arr, 1, 1, C.byref(h)) == B.SS_ERR_ARG       # unknown flag
+    bad, keep2 = _desc(ring_slots=0)
+    arr2 = (B.ss_pool_desc * 1)(bad)
+    assert L.ss_loader_create(arr2, 1, 0, C.byref(h)) == B.SS_ERR_ARG
+    assert L.ss_loader_submit(None, None, 0) == B.SS_ERR_ARG
+    n = C.c_uint32()
+    assert L.ss_loader_pump(None, 1, None, 0, C.byref(n)) == B.SS_ERR_ARG
+    assert L.ss_loader_pending(None, None, None) == B.SS_ERR_ARG
+    assert L.ss_loader_sync(None) == B.SS_ERR_ARG
+    L.ss_loader_destroy(None)
 
 
 def test_no_device_is_an_argument_error_not_a_crash():
