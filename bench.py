@@ -322,11 +322,12 @@ def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
         t0 = time.perf_counter()
         plan = opool.plan_step(trace.dist[t], trace.active[t], threshold, budget)
         t_plan += time.perf_counter() - t0
-        V = plan.victims[:n_agents_moved]
+        V = plan.written[:n_agents_moved]
         Ld = plan.loads[:n_agents_moved]
         nvu = int(s[V].sum())
         nlu = int(s[Ld].sum())
-        sub = SimpleNamespace(victims=V, loads=Ld, victim_units=plan.victim_units[:nvu],
+        sub = SimpleNamespace(victims=V, written=V, loads=Ld, victim_units=plan.written_units[:nvu],
+                              written_units=plan.written_units[:nvu],
                               load_units=plan.load_units[:nlu])
         slot = {int(a): i for i, a in enumerate(list(V) + list(Ld))}
         for u in np.concatenate([sub.victim_units, sub.load_units]):   # warm the pages
