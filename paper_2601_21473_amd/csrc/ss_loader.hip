@@ -15,9 +15,11 @@
 // host keeps at most `window` chunks in flight (the smallest ring of the
 // modules) and takes each decision only after the chunk `window` places
 // earlier has finished, so an urgent task submitted from another thread
-// waits for at most `window` chunks.  Chunks run in issue order on one
-// stream (non-blocking, default priority), so a staging slot is refilled only
-// after its previous unpack.
+// waits for at most `window` chunks.  Copies run in issue order on a copy
+// stream and unpacks in issue order on a compute stream (both non-blocking,
+// default priority): each unpack waits for its chunk's copy, and a copy into
+// a staging slot waits for the unpack that last read the slot, so the copy
+// engine moves the next chunk while the previous one is unpacked.
 #include "scalesim.h"
 #include "ss_internal.h"
 
@@ -44,6 +46,8 @@ struct Module {
     u64 slot_bytes = 0;
     unsigned slots = 0, next_slot = 0;
     unsigned chunk_units = 0;
+    std::vector<hipEvent_t> slot_free;  // recorded after the unpack that read each slot
+    std::vector<bool> slot_used;
     CopyItem* d_items = nullptr;
     unsigned n_items = 0;
     u64* d_plane_base = nullptr;
@@ -65,8 +69,10 @@ struct ss_loader {
     std::vector<Module> mods;
     int device = 0;
     bool preempt = true;
-    hipStream_t st = nullptr;
-    std::vector<hipEvent_t> window;   // one per chunk in flight
+    hipStream_t st = nullptr;         // unpacks
+    hipStream_t cp = nullptr;         // host-to-device copies
+    hipEvent_t copied = nullptr;      // recorded after each copy, waited on by its unpack
+    std::vector<hipEvent_t> window;   // one per chunk in flight (after its unpack)
     u64 issued_total = 0;
     std::map<Id, Task> tasks;
     std::set<Key> queue;              // tasks not running
@@ -104,15 +110,20 @@ struct DeviceScope {
 
 void free_loader(ss_loader* L) {
     if (!L) return;
+    if (L->cp) (void)hipStreamSynchronize(L->cp);
     if (L->st) (void)hipStreamSynchronize(L->st);
     for (Module& m : L->mods) {
+        for (hipEvent_t e : m.slot_free)
+            if (e) (void)hipEventDestroy(e);
         if (m.d_items) (void)hipFree(m.d_items);
         if (m.d_plane_base) (void)hipFree(m.d_plane_base);
         if (m.d_chunk_bytes) (void)hipFree(m.d_chunk_bytes);
     }
     for (hipEvent_t e : L->window)
         if (e) (void)hipEventDestroy(e);
+    if (L->copied) (void)hipEventDestroy(L->copied);
     if (L->st) (void)hipStreamDestroy(L->st);
+    if (L->cp) (void)hipStreamDestroy(L->cp);
     delete L;
 }
 
@@ -242,8 +253,13 @@ ss_status ss_loader_create(const ss_pool_desc* modules, uint32_t n_modules, uint
         C_TRY(hipMemcpy(m.d_plane_base, bases.data(), m.P * sizeof(u64), hipMemcpyHostToDevice));
         C_TRY(hipMemcpy(m.d_chunk_bytes, cb.data(), m.P * sizeof(u64), hipMemcpyHostToDevice));
         window = std::min(window, m.slots);
+        m.slot_free.assign(m.slots, nullptr);
+        m.slot_used.assign(m.slots, false);
+        for (auto& e : m.slot_free) C_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     }
     C_TRY(hipStreamCreateWithFlags(&L->st, hipStreamNonBlocking));
+    C_TRY(hipStreamCreateWithFlags(&L->cp, hipStreamNonBlocking));
+    C_TRY(hipEventCreateWithFlags(&L->copied, hipEventDisableTiming));
     L->window.assign(window, nullptr);
     for (auto& e : L->window) C_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
 #undef C_TRY
@@ -348,8 +364,12 @@ ss_status ss_loader_pump(ss_loader* L, uint32_t max_chunks, ss_load_log* log, ui
         const unsigned slot = m.next_slot;
         m.next_slot = (slot + 1) % m.slots;
         char* stage = m.staging + (u64)slot * m.slot_bytes;
+        // the copy refills the slot only after the unpack that last read it
+        if (m.slot_used[slot]) L_TRY(L, hipStreamWaitEvent(L->cp, m.slot_free[slot], 0));
         L_TRY(L, hipMemcpyAsync(stage, m.host + m.host_off[a] + (u64)T.cursor * m.unit_bytes,
-                                (u64)cnt * m.unit_bytes, hipMemcpyHostToDevice, L->st));
+                                (u64)cnt * m.unit_bytes, hipMemcpyHostToDevice, L->cp));
+        L_TRY(L, hipEventRecord(L->copied, L->cp));
+        L_TRY(L, hipStreamWaitEvent(L->st, L->copied, 0));
         CopyArgs C{};
         C.units_list = T.units;
         C.first = T.cursor;
@@ -363,6 +383,8 @@ ss_status ss_loader_pump(ss_loader* L, uint32_t max_chunks, ss_load_log* log, ui
         C.unit_bytes = m.unit_bytes;
         C.capacity = m.U;
         L_TRY(L, launch_unpack(C, L->st));
+        L_TRY(L, hipEventRecord(m.slot_free[slot], L->st));
+        m.slot_used[slot] = true;
         L_TRY(L, hipEventRecord(L->window[L->issued_total % L->window.size()], L->st));
         L->issued_total++;
         const uint32_t first = T.cursor;
@@ -393,6 +415,7 @@ ss_status ss_loader_pending(ss_loader* L, uint32_t* queued, uint32_t* running) {
 ss_status ss_loader_sync(ss_loader* L) {
     if (!L) return set_err(SS_ERR_ARG, "loader is NULL");
     DeviceScope g(L->device);
+    L_TRY(L, hipStreamSynchronize(L->cp));
     L_TRY(L, hipStreamSynchronize(L->st));
     return SS_OK;
 }
