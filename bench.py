@@ -56,15 +56,19 @@ def kernel_source_hash():
 
 
 def summarize_pmc(fetch_csv, write_csv, workload, out_json, commands):
-    """Per-dispatch HBM traffic of the copy kernels from two rocprofv3 --pmc
-    runs (FETCH_SIZE, WRITE_SIZE in KiB), each scaled by the ratio of known
-    bytes to the same counter on the probe's plain copy of PROBE_BYTES."""
+    """HBM traffic of the copy kernels from two rocprofv3 --pmc runs
+    (FETCH_SIZE, WRITE_SIZE in KiB per dispatch), each scaled by the ratio of
+    known bytes to the same counter on the probe's plain copy of PROBE_BYTES.
+    Counted over the launches that cover a whole staging slot (largest grid),
+    whose unit count follows from the grid: pack launches item_groups blocks
+    per unit, unpack n_items blocks per 8 units."""
     import csv
     import collections
     import workloads as W
     spec = W.make_trace(workload, 0).pools[0]
     n_items = sum((c + COPY_ITEM_BYTES - 1) // COPY_ITEM_BYTES for c in spec.chunk_bytes)
-    groups = (n_items + COPY_BLOCK // 64 - 1) // (COPY_BLOCK // 64)
+    waves = COPY_BLOCK // 64
+    groups = (n_items + waves - 1) // waves
     vals = {}
     for path, counter in ((fetch_csv, "FETCH_SIZE"), (write_csv, "WRITE_SIZE")):
         per = collections.defaultdict(list)
@@ -81,17 +85,62 @@ def summarize_pmc(fetch_csv, write_csv, workload, out_json, commands):
         w = vals["WRITE_SIZE"].get(name, [])
         if not f or not w:
             continue
-        alg = [2 * (g // COPY_BLOCK // groups) * spec.unit_bytes for _, g in f]
-        fetch_b = np.mean([v for v, _ in f]) * 1024 * factor["FETCH_SIZE"]
-        write_b = np.mean([v for v, _ in w]) * 1024 * factor["WRITE_SIZE"]
+        grid = max(g for _, g in f)
+        f = [v for v, g in f if g == grid]
+        w = [v for v, g in w if g == grid]
+        blocks = grid // COPY_BLOCK
+        units = blocks // groups if short == "pack" else blocks // n_items * waves
+        alg = 2 * units * spec.unit_bytes
+        fetch_b = np.mean(f) * 1024 * factor["FETCH_SIZE"]
+        write_b = np.mean(w) * 1024 * factor["WRITE_SIZE"]
         out["kernels"][short] = {
-            "dispatches": len(f), "hbm_read_bytes_per_launch": fetch_b,
-            "hbm_write_bytes_per_launch": write_b,
+            "dispatches": len(f), "grid_threads": grid, "units_per_launch": units,
+            "hbm_read_bytes_per_launch": fetch_b, "hbm_write_bytes_per_launch": write_b,
             "hbm_bytes_per_launch": fetch_b + write_b,
-            "algorithmic_bytes_per_launch": float(np.mean(alg)),
-            "traffic_over_algorithmic": (fetch_b + write_b) / float(np.mean(alg))}
+            "algorithmic_bytes_per_launch": float(alg),
+            "traffic_over_algorithmic": (fetch_b + write_b) / float(alg)}
     json.dump(out, open(out_json, "w"), indent=1)
     return out
+
+
+def summarize_trace(trace_csv, out_md, title, command, note=""):
+    """Markdown table of per-kernel launch counts and durations from a
+    rocprofv3 --kernel-trace CSV (every kernel, plus the copy kernels split
+    into full-slot launches and the rest)."""
+    import csv
+    import collections
+    rows = list(csv.DictReader(open(trace_csv)))
+    per = collections.defaultdict(list)
+    full = collections.defaultdict(list)
+    top = collections.Counter()
+    for r in rows:
+        n = r["Kernel_Name"]
+        us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        per[n].append(us)
+        if n in PMC_KERNELS:
+            top[(n, int(r["Grid_Size_X"]))] += 1
+    grid_full = {n: max((g for (k, g) in top if k == n), default=0) for n in PMC_KERNELS}
+    for r in rows:
+        n = r["Kernel_Name"]
+        if n in PMC_KERNELS and int(r["Grid_Size_X"]) == grid_full[n]:
+            full[n].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    lines = [f"# {title}", "", "Command (repository root = `$REPO`, on one MI355X):", "",
+             f"    {command}", "", f"Summary of `{os.path.basename(trace_csv)}` written by "
+             f"`python bench.py --summarize-trace`.", "",
+             "| Kernel | Calls | Total ms | Avg us | Min us | Max us |", "|---|---|---|---|---|---|"]
+    for n, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
+        short = n.replace("(anonymous namespace)::", "").split("(")[0].replace("void ", "")
+        lines.append(f"| `{short}` | {len(v)} | {sum(v) / 1e3:.2f} | {np.mean(v):.1f} | "
+                     f"{min(v):.1f} | {max(v):.1f} |")
+    lines += ["", "Copy kernels, launches over a whole staging slot (largest grid):", "",
+              "| Kernel | Grid (threads) | Calls | Avg us | Median us | Min us |", "|---|---|---|---|---|---|"]
+    for n, v in full.items():
+        lines.append(f"| `{PMC_KERNELS[n]}` | {grid_full[n]:,} | {len(v)} | {np.mean(v):.1f} | "
+                     f"{np.median(v):.1f} | {min(v):.1f} |")
+    if note:
+        lines += ["", note]
+    open(out_md, "w").write("\n".join(lines) + "\n")
+    return "\n".join(lines)
 
 
 def parse():
@@ -123,12 +172,18 @@ def parse():
                     help="skip the distance estimator measurements")
     ap.add_argument("--estimators-only", action="store_true",
                     help="only the distance estimator measurements (for profiling)")
+    ap.add_argument("--no-loader", action="store_true",
+                    help="skip the load-task scheduler measurement")
+    ap.add_argument("--loader-only", action="store_true",
+                    help="only the load-task scheduler measurement")
     ap.add_argument("--objects-trees", type=int, default=160)
     ap.add_argument("--objects-agents", type=int, default=50_000)
     ap.add_argument("--objects-depth", type=int, default=5)
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "OUT_JSON"),
                     help="write the copy kernels' HBM traffic from two rocprofv3 --pmc runs")
     ap.add_argument("--pmc-commands", nargs="*", default=[])
+    ap.add_argument("--summarize-trace", nargs=4, metavar=("TRACE_CSV", "OUT_MD", "TITLE", "COMMAND"),
+                    help="write a markdown summary of a rocprofv3 --kernel-trace CSV")
     return ap.parse_args()
 
 
@@ -297,6 +352,93 @@ def estimator_bench(args, binding, W, DeviceBuffer):
     return out
 
 
+LOADER_AGENTS = 128             # background load tasks of the scheduler measurement
+LOADER_URGENT = 8               # urgent (distance 0) arrivals timed per configuration
+
+
+def loader_bench(args, binding, W, spec0, PoolMemory, DeviceBuffer, probe):
+    """Load-task scheduler (Appendix A, load task scheduler and preemption
+    support) on the round-robin workload's module layout (2 MiB units of
+    64 x 32 KiB, agents of 32-128 units): for chunks of 4, 16 and 64 units
+    (8, 32 and 128 MiB; ring of 4 staging slots, so 4 chunks in flight)
+
+    * load rate: 128 queued tasks drained in distance order, bytes per second
+      of wall time against the measured one-way host-to-device rate;
+    * preemption latency: with the window full of a running task's chunks, a
+      distance-0 task arrives; time from its submission until all its units
+      have landed, with preemption and with preemption off (the running
+      task finishes first), median over 8 arrivals, next to the time its
+      own bytes need on the link.
+
+    ``spec0`` is the round-robin workload's pool; the module holds its first
+    136 agents.  Destination units are a seeded permutation of the module's
+    units (each task's units scattered over the pool)."""
+    n_agents = LOADER_AGENTS + LOADER_URGENT
+    units = np.asarray(spec0.agent_units[:n_agents], dtype=np.uint32)
+    cap = int(units.sum())
+    spec = W.PoolSpec("loader", cap, list(spec0.chunk_bytes), units)
+    ub = spec.unit_bytes
+    rng = np.random.default_rng(args.seed)
+    perm = rng.permutation(cap).astype(np.int32)
+    off = np.concatenate([[0], np.cumsum(units)]).astype(np.int64)
+    dist_bg = rng.permutation(np.arange(2, 2 + LOADER_AGENTS)).astype(np.uint32)
+    h2d = probe.get("h2d_GBps") if probe else None
+    out = {"module": "round-robin layout: 2 MiB units of 64 x 32 KiB, agents of 32-128 units",
+           "tasks": LOADER_AGENTS, "task_bytes": int(units[:LOADER_AGENTS].sum()) * ub,
+           "window_chunks": 4, "configs": []}
+    for chunk_units in (4, 16, 64):
+        mem = PoolMemory(spec, 4 * chunk_units * ub, 4, host_slots=16)
+        mem.host_np[:] = 1                    # host pages resident before timing
+        dl = DeviceBuffer(perm.nbytes)
+        dl.upload(perm)
+        ptr = lambda a: dl.ptr + 4 * int(off[a])
+        rec = {"chunk_units": chunk_units, "chunk_bytes": chunk_units * ub}
+        try:
+            for preempt in (True, False):
+                L = binding.Loader([mem.desc_args()], preempt=preempt)
+                try:
+                    if preempt:
+                        # load rate: drain every background task
+                        L.submit([(0, a, int(dist_bg[a]), ptr(a)) for a in range(LOADER_AGENTS)])
+                        t0 = time.perf_counter()
+                        L.pump(1 << 16)
+                        L.sync()
+                        wall = time.perf_counter() - t0
+                        rec["load_GBps"] = out["task_bytes"] / wall / 1e9
+                        if h2d:
+                            rec["frac_of_measured_h2d"] = rec["load_GBps"] / h2d
+                    L.submit([(0, a, int(dist_bg[a]), ptr(a)) for a in range(LOADER_AGENTS)])
+                    L.pump(4)                 # window full
+                    lat, own = [], []
+                    for k in range(LOADER_URGENT):
+                        ua = LOADER_AGENTS + k
+                        L.pump(4)
+                        t0 = time.perf_counter()
+                        L.submit([(0, ua, 0, ptr(ua))])
+                        done = False
+                        while not done:
+                            got = L.pump(1)
+                            assert got, "urgent task was not scheduled"
+                            done = any(a == ua and f & binding.SS_LOAD_DONE
+                                       for (_, a, _, _, f) in got)
+                        L.sync()
+                        lat.append(time.perf_counter() - t0)
+                        own.append(int(units[ua]) * ub)
+                    key = "preempt" if preempt else "no_preempt"
+                    rec[f"urgent_latency_ms_{key}"] = 1e3 * float(np.median(lat))
+                    if preempt:
+                        rec["preemptions"] = L.stats()["preemptions"]
+                        if h2d:
+                            rec["urgent_own_bytes_ms"] = 1e3 * float(np.median(own)) / h2d / 1e9
+                finally:
+                    L.close()
+        finally:
+            dl.free()
+            mem.free()
+        out["configs"].append(rec)
+    return out
+
+
 def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
     """The CPU oracle on a bounded sample: the oracle plan for every agent on
     steps [warmup, warmup + n_steps) (after replaying the earlier steps'
@@ -350,6 +492,9 @@ def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
 
 def main():
     args = parse()
+    if args.summarize_trace:
+        print(summarize_trace(*args.summarize_trace))
+        return
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc[:2], args.workload,
                                        args.summarize_pmc[2], args.pmc_commands), indent=1))
@@ -370,6 +515,12 @@ def main():
     if args.estimators_only:
         print(json.dumps({"estimators": estimator_bench(args, binding, W, DeviceBuffer)}),
               flush=True)
+        return
+    if args.loader_only:
+        rr = W.make_trace("roundrobin", 0).pools[0]
+        pr = {} if args.no_probe else probes(binding)
+        print(json.dumps({"loader": loader_bench(args, binding, W, rr, PoolMemory, DeviceBuffer,
+                                                 pr), "probe": pr}), flush=True)
         return
     trace = W.make_trace(args.workload, args.seed)
     T_need = args.warmup + args.steps + args.plan_steps
@@ -475,8 +626,11 @@ def main():
     pmc_path = os.path.join(ROOT, "profiles", f"k_copy_{args.workload}_pmc.json")
     if os.path.exists(pmc_path):
         pmc = json.load(open(pmc_path))
-        if pmc.get("kernel_source_sha256_16") == kernel_source_hash():
-            traffic = pmc["kernels"].get(dom, {}).get("hbm_bytes_per_launch")
+        ratio = pmc["kernels"].get(dom, {}).get("traffic_over_algorithmic")
+        if pmc.get("kernel_source_sha256_16") == kernel_source_hash() and ratio:
+            # HBM bytes per whole-slot launch over its algorithmic bytes, applied
+            # to the timed launches' average size
+            traffic = ratio * kern[dom]["bytes_per_launch"]
     roofline = {"bound": "hbm", "kernel": f"k_copy<{dom}>", "achieved": kern[dom]["GBps"],
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": kern[dom]["GBps"] / HBM_PEAK_GBPS,
                 "traffic": traffic,
@@ -508,6 +662,9 @@ def main():
             "host_enqueue_us": host[0] / nps, "host_wait_us": host[1] / nps,
             "host_readback_us": host[2] / nps}
 
+    rr = trace.pools[0] if args.workload == "roundrobin" else W.make_trace("roundrobin", 0).pools[0]
+    loader = (None if args.no_loader else
+              loader_bench(args, binding, W, rr, PoolMemory, DeviceBuffer, probe))
     objects = None if args.no_objects else object_bench(args, binding, W, DeviceBuffer)
     estimators = None if args.no_estimators else estimator_bench(args, binding, W, DeviceBuffer)
 
@@ -532,6 +689,7 @@ def main():
         "dma": dma,
         "plan_latency_us": plan,
         "kernels": kern,
+        "loader": loader,
         "object_distances": objects,
         "estimators": estimators,
         "probe": probe,

@@ -131,6 +131,7 @@ struct CopyArgs {
 constexpr int kCopyThreads = 512;                 // 8 waves, one item per wave
 constexpr int kCopyWavesPerBlock = kCopyThreads / 64;
 constexpr unsigned kItemBytes = 32768;            // max bytes per item
+static_assert(kItemBytes % 1024 == 0, "a wave moves 1 KiB per word round");
 constexpr int kCoreThreads = 1024;
 constexpr int kLdsKeys = 16384;                   // 128 KiB of u64 keys in LDS
 
