@@ -187,7 +187,12 @@ def parse():
     return ap.parse_args()
 
 
-def probes(binding):
+def probes(binding, host=None):
+    """Plain-copy HBM probe and pinned host-link probes (1 GiB copies: H2D,
+    D2H and both at once).  ``host`` is pinned memory of at least 2 GiB to
+    probe against (the pool's own host copies, so that the link is measured
+    to the memory the workload moves); without it a fresh pinned buffer is
+    used, whose NUMA placement may differ from the pool's."""
     from paper_2601_21473_amd.memory import DeviceBuffer, HostBuffer
     out = {}
     n = 2 << 30
@@ -197,15 +202,20 @@ def probes(binding):
     a.free()
     b.free()
     m = 1 << 30
-    h, d = HostBuffer(2 * m), DeviceBuffer(2 * m)
-    h.np[:] = 1                                  # host pages resident before timing
+    own = host is None or host.nbytes < 2 * m
+    h = HostBuffer(2 * m) if own else host
+    d = DeviceBuffer(2 * m)
+    if own:
+        h.np[:] = 1                              # host pages resident before timing
     # best of three trials of five copies each, per direction
     best = lambda direction: min(binding.probe_link(h.ptr, d.ptr, m, direction, 5)
                                  for _ in range(3))
     out["h2d_GBps"] = m / best(0) / 1e6
     out["d2h_GBps"] = m / best(1) / 1e6
     out["duplex_GBps"] = 2 * m / best(2) / 1e6
-    h.free()
+    out["host_memory"] = "fresh pinned buffer" if own else "the pool's pinned host copies"
+    if own:
+        h.free()
     d.free()
     return out
 
@@ -529,14 +539,13 @@ def main():
     budget = args.budget
     thr = args.threshold
 
-    probe = {} if args.no_probe else probes(binding)
-
     mems, pools = [], []
     for spec in trace.pools:
         host_slots = None if args.host_copies == 0 else args.host_copies
         mem = PoolMemory(spec, args.staging_mib << 20, args.ring, host_slots=host_slots)
         mems.append(mem)
         pools.append(mem.make_pool(timing=True))
+    probe = {} if args.no_probe else probes(binding, mems[0].host)
     N = trace.n_agents
     d_np = np.ascontiguousarray(trace.dist, dtype=np.uint32)
     a_np = np.ascontiguousarray(trace.active, dtype=np.uint8)
@@ -598,6 +607,11 @@ def main():
             p.prefetch_unpack(stream)
     sync()
     plan_stats = [p.stats() for p in pools]
+    if probe:
+        # a second probe after the timed steps: each direction keeps its better
+        # reading
+        again = probes(binding, mems[0].host)
+        probe = {k: (max(v, again[k]) if isinstance(v, float) else v) for k, v in probe.items()}
     for p in pools:
         p.close()
     for m in mems:

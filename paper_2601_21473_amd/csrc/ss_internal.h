@@ -121,6 +121,8 @@ struct CopyArgs {
     const CopyItem* items;
     unsigned n_items;               // items per unit
     unsigned item_groups;           // ceil(n_items / kCopyWavesPerBlock) blocks per unit
+    unsigned run_order;             // unpack: one block per (item, 8 consecutive units)
+    unsigned pad1;
     const u64* plane_base;          // [P] device addresses
     const u64* chunk_bytes;         // [P]
     char* staging;                  // slot base

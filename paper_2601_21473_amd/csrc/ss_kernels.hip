@@ -804,12 +804,15 @@ __device__ __forceinline__ void wave_copy_burst(char* dst, const char* src, unsi
 // Pack: block b copies items [g*8, g*8+8) of logical unit p = b / item_groups
 // (g = b % item_groups), so consecutive blocks walk a unit's bytes in order and
 // a block's stores fill 8 consecutive pieces of the staging slot.
-// Unpack: block b copies item r = b % n_items of the 8 logical units
-// [t*8, t*8+8), t = b / n_items, one unit per wave.  The loads' units mostly
-// come in runs of consecutive physical units (allocation hands out free units
-// in index order), so a block's stores fill one run of a plane: on the
-// round-robin workload's unit lists this ran at 5.7-5.8 TB/s against 5.6 for
-// the pack order (and 5.2 against 5.4 on random lists).
+// Unpack with run_order (set when every plane's chunk is a single item):
+// block b copies item r = b % n_items of the 8 logical units [t*8, t*8+8),
+// t = b / n_items, one unit per wave.  The loads' units mostly come in runs of
+// consecutive physical units (allocation hands out free units in index
+// order), and consecutive units of a plane are adjacent, so a block's stores
+// fill one run of a plane: on the round-robin workload's unit lists this ran
+// at 5.7-5.8 TB/s against 5.6 for the pack order (and 5.2 against 5.4 on
+// random lists).  Without run_order (chunks of several items, which already
+// give each block a contiguous range) the unpack takes the pack order.
 // The item index is wave-uniform, so its descriptor and the plane's base and
 // stride are scalar loads.
 template <bool kPack>
@@ -817,7 +820,7 @@ __global__ void __launch_bounds__(kCopyThreads) k_copy(CopyArgs A) {
     const unsigned b = blockIdx.x;
     const unsigned wid = threadIdx.x >> 6;
     unsigned p, r;
-    if (kPack) {
+    if (kPack || !A.run_order) {
         p = b / A.item_groups;
         r = __builtin_amdgcn_readfirstlane((b - p * A.item_groups) * kCopyWavesPerBlock + wid);
         if (r >= A.n_items) return;
@@ -877,8 +880,9 @@ hipError_t launch_bt_update(const BtArgs& b, unsigned n_agents, hipStream_t st) 
 static hipError_t launch_copy(const CopyArgs& a, hipStream_t st, bool pack) {
     if (a.count == 0) return hipSuccess;
     if (a.item_groups == 0 || a.n_items == 0) return hipErrorInvalidValue;
-    const u64 blocks = pack ? a.count * a.item_groups
-                            : (a.count + kCopyWavesPerBlock - 1) / kCopyWavesPerBlock * a.n_items;
+    const u64 blocks = (pack || !a.run_order)
+                           ? a.count * a.item_groups
+                           : (a.count + kCopyWavesPerBlock - 1) / kCopyWavesPerBlock * a.n_items;
     if (blocks > 0x7fffffffull) return hipErrorInvalidValue;
     if (pack) hipLaunchKernelGGL(k_copy<true>, dim3((unsigned)blocks), dim3(kCopyThreads), 0, st, a);
     else hipLaunchKernelGGL(k_copy<false>, dim3((unsigned)blocks), dim3(kCopyThreads), 0, st, a);

@@ -377,6 +377,7 @@ ss_status ss_loader_pump(ss_loader* L, uint32_t max_chunks, ss_load_log* log, ui
         C.items = m.d_items;
         C.n_items = m.n_items;
         C.item_groups = (m.n_items + kCopyWavesPerBlock - 1) / kCopyWavesPerBlock;
+        C.run_order = m.n_items == m.P;
         C.plane_base = m.d_plane_base;
         C.chunk_bytes = m.d_chunk_bytes;
         C.staging = stage;

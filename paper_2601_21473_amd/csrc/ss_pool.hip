@@ -758,6 +758,7 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
     C.items = p->d_items;
     C.n_items = p->n_items;
     C.item_groups = (p->n_items + kCopyWavesPerBlock - 1) / kCopyWavesPerBlock;
+    C.run_order = p->n_items == p->P;
     C.plane_base = p->d_plane_base;
     C.chunk_bytes = p->d_chunk_bytes;
     C.unit_bytes = p->unit_bytes;
@@ -822,6 +823,7 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
     C.items = p->d_items;
     C.n_items = p->n_items;
     C.item_groups = (p->n_items + kCopyWavesPerBlock - 1) / kCopyWavesPerBlock;
+    C.run_order = p->n_items == p->P;
     C.plane_base = p->d_plane_base;
     C.chunk_bytes = p->d_chunk_bytes;
     C.unit_bytes = p->unit_bytes;
