@@ -82,6 +82,7 @@ struct PlanArgs {
     unsigned char* vwritten;        // [N] per victim: written back (device)
     unsigned char* vwritten_host;   // mapped pinned host [N]
     u64* woff;                      // [N+1] prefix units over written-back victims
+    unsigned* done;                 // workgroups of k_classify_core finished (0 between steps)
 };
 
 // Candidate distance histogram: bucket(d) = d below 1024, then 32 buckets per
@@ -137,8 +138,9 @@ static_assert(kItemBytes % 1024 == 0, "a wave moves 1 KiB per word round");
 constexpr int kCoreThreads = 1024;
 constexpr int kLdsKeys = 16384;                   // 128 KiB of u64 keys in LDS
 
-hipError_t launch_classify(const PlanArgs& a, hipStream_t st);
-hipError_t launch_plan_core(const PlanArgs& a, hipStream_t st);
+// The plan kernels: the plan core alone (fused: it classifies the agents
+// itself), or classification over many workgroups whose last one runs the core.
+hipError_t launch_plan(const PlanArgs& a, hipStream_t st);
 hipError_t launch_bt_update(const BtArgs& a, unsigned n_agents, hipStream_t st);
 constexpr unsigned kFuseAgents = 16384;           // plan core classifies up to this many
 hipError_t launch_pack(const CopyArgs& a, hipStream_t st);

@@ -1,21 +1,25 @@
 // Device kernels of the invocation-distance memory manager for gfx950.
 //
 // Plan (per step, Section 3.3 of the paper and its Appendix A interface):
-//   k_classify   one pass over the agents: distance of active agents forced
-//                to 0, 64-bit priority keys (d, id), classification into
-//                evictable residents / demand loads / prefetch candidates,
-//                wave64 ballot + mbcnt stream compaction of each class, and
-//                the unit sums the plan needs.
-//   k_plan_core  one workgroup of 1024 threads: LDS bitonic sorts, weighted
+//   classification  one pass over the agents: distance of active agents
+//                forced to 0, 64-bit priority keys (d, id), classification
+//                into evictable residents / demand loads / prefetch
+//                candidates, wave64 ballot + mbcnt stream compaction of each
+//                class, and the unit sums the plan needs;
+//   plan core    one workgroup of 1024 threads: LDS bitonic sorts, weighted
 //                radix select of the candidate prefix that can possibly fit,
 //                prefix sums, the prefetch acceptance rule in closed form,
 //                the victim count, the free-unit list, and the plan written
 //                to a mapped host mirror.
+//   k_plan_core      the plan core, classifying the agents itself (N <= 16,384);
+//   k_classify_core  classification over N / 1024 workgroups, the last of
+//                    which runs the plan core (larger N), in one launch.
 //   k_bt_victims / k_bt_loads   block-table release and allocation.
 // Data movement:
 //   k_copy<pack>  gathers (pack) or scatters (unpack) whole units between the
 //                pool's planes and a contiguous staging slot, one wave per
-//                piece of at most 32 KiB, 16-byte non-temporal accesses.
+//                piece of at most 32 KiB moved as one burst of 16-byte
+//                non-temporal accesses.
 //
 // Nothing here is a dense contraction; all work is integer indexing and byte
 // movement, so there is no MFMA.
@@ -49,7 +53,7 @@ __device__ __forceinline__ u64 wave_incl_scan(u64 v) {
 }
 
 // ---------------------------------------------------------------------------
-// k_classify
+// classification
 // ---------------------------------------------------------------------------
 
 // Append `key` of every lane with `pred` to list[*counter ...]; one atomic per
@@ -108,63 +112,6 @@ __device__ __forceinline__ unsigned wave_reserve(bool pred, unsigned* counter) {
     unsigned base = 0;
     if (lane_id() == 0) base = atomicAdd(counter, (unsigned)__popcll(mask));
     return __shfl(base, 0) + mbcnt(mask);
-}
-
-// Multi-block classification: counts and sums are gathered per block in LDS
-// and reach the global counters with one atomic per block and counter.
-__global__ void __launch_bounds__(256) k_classify(PlanArgs A) {
-    __shared__ PlanCounters lc;
-    __shared__ unsigned gbase[3];
-    const unsigned a = blockIdx.x * 256u + threadIdx.x;
-    if (threadIdx.x == 0) lc = PlanCounters{};
-    __syncthreads();
-    const bool valid = a < A.n;
-    unsigned D = 0;
-    bool act = false, res = false;
-    u64 s = 0;
-    if (valid) {
-        D = A.dist[a];
-        act = A.active[a] != 0;
-        res = A.resident[a] != 0;
-        s = A.units[a];
-    }
-    const u64 d = act ? 0ull : (u64)D;
-    const u64 key = (d << A.idbits) | a;
-    const bool isE = valid && res && !act;
-    const bool isL = valid && act && !res;
-    const bool isC = valid && !res && !act && D < A.threshold;
-    if (isC) atomicAdd(&A.hist_w[dist_bucket(D)], s);
-    const unsigned oE = wave_reserve(isE, &lc.n_E);
-    const unsigned oL = wave_reserve(isL, &lc.n_L);
-    const unsigned oC = wave_reserve(isC, &lc.n_C);
-    const u64 s_act = wave_sum(act ? s : 0);
-    const u64 s_res = wave_sum(res ? s : 0);
-    const u64 s_dem = wave_sum(isL ? s : 0);
-    const u64 s_evi = wave_sum(isE ? s : 0);
-    const u64 s_can = wave_sum(isC ? s : 0);
-    if (lane_id() == 0) {
-        atomicAdd(&lc.sum_active, s_act);
-        atomicAdd(&lc.sum_resident, s_res);
-        atomicAdd(&lc.sum_demand, s_dem);
-        atomicAdd(&lc.sum_evictable, s_evi);
-        atomicAdd(&lc.sum_cand, s_can);
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        PlanCounters* g = A.cnt;
-        gbase[0] = lc.n_E ? atomicAdd(&g->n_E, lc.n_E) : 0;
-        gbase[1] = lc.n_L ? atomicAdd(&g->n_L, lc.n_L) : 0;
-        gbase[2] = lc.n_C ? atomicAdd(&g->n_C, lc.n_C) : 0;
-        if (lc.sum_active) atomicAdd(&g->sum_active, lc.sum_active);
-        if (lc.sum_resident) atomicAdd(&g->sum_resident, lc.sum_resident);
-        if (lc.sum_demand) atomicAdd(&g->sum_demand, lc.sum_demand);
-        if (lc.sum_evictable) atomicAdd(&g->sum_evictable, lc.sum_evictable);
-        if (lc.sum_cand) atomicAdd(&g->sum_cand, lc.sum_cand);
-    }
-    __syncthreads();
-    if (isE) A.listE[gbase[0] + oE] = key;
-    if (isL) A.listL[gbase[1] + oL] = key;
-    if (isC) A.listC[gbase[2] + oC] = key;
 }
 
 // ---------------------------------------------------------------------------
@@ -454,9 +401,10 @@ __device__ u64 weighted_select(const u64* keys, unsigned n, const unsigned* unit
 // k_plan_core
 // ---------------------------------------------------------------------------
 
-__global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
-    __shared__ u64 lds[kLdsKeys];
-    __shared__ CoreShared S;
+// The plan core: one workgroup of kCoreThreads threads; `lds` holds kLdsKeys
+// keys.  Inlined into both kernels below so that its LDS accesses stay LDS
+// instructions.
+__device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShared& S) {
     const unsigned tid = threadIdx.x;
     auto stamp = [&](int k) {
         if (A.phase && tid == 0) A.phase[k] = wall_clock64();
@@ -699,6 +647,85 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
     }
 }
 
+__global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
+    __shared__ u64 lds[kLdsKeys];
+    __shared__ CoreShared S;
+    plan_core(A, lds, S);
+}
+
+// Classification over many workgroups, then the plan core in the workgroup
+// that finishes last (N > kFuseAgents).  Each workgroup classifies 1024
+// agents, gathers its counts and sums in LDS and reaches the global counters
+// with one atomic per counter; its list entries go to the ranges those
+// atomics reserve.  Every workgroup then publishes its writes (agent-scope
+// fence) and counts itself done; the one that counts last acquires them all
+// and runs the plan core, so no workgroup ever waits for another and the core
+// starts without a second launch.  It resets the count for the next step.
+__global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
+    __shared__ u64 lds[kLdsKeys];
+    __shared__ CoreShared S;
+    const unsigned a = blockIdx.x * kCoreThreads + threadIdx.x;
+    if (threadIdx.x == 0) S.cnt = PlanCounters{};
+    __syncthreads();
+    const bool valid = a < A.n;
+    unsigned D = 0;
+    bool act = false, res = false;
+    u64 s = 0;
+    if (valid) {
+        D = A.dist[a];
+        act = A.active[a] != 0;
+        res = A.resident[a] != 0;
+        s = A.units[a];
+    }
+    const u64 d = act ? 0ull : (u64)D;               // active agents: distance 0
+    const u64 key = (d << A.idbits) | a;
+    const bool isE = valid && res && !act;            // evictable resident
+    const bool isL = valid && act && !res;            // demand load
+    const bool isC = valid && !res && !act && D < A.threshold;   // prefetch candidate
+    if (isC) atomicAdd(&A.hist_w[dist_bucket(D)], s);
+    const unsigned oE = wave_reserve(isE, &S.cnt.n_E);
+    const unsigned oL = wave_reserve(isL, &S.cnt.n_L);
+    const unsigned oC = wave_reserve(isC, &S.cnt.n_C);
+    const u64 s_act = wave_sum(act ? s : 0);
+    const u64 s_res = wave_sum(res ? s : 0);
+    const u64 s_dem = wave_sum(isL ? s : 0);
+    const u64 s_evi = wave_sum(isE ? s : 0);
+    const u64 s_can = wave_sum(isC ? s : 0);
+    if (lane_id() == 0) {
+        atomicAdd(&S.cnt.sum_active, s_act);
+        atomicAdd(&S.cnt.sum_resident, s_res);
+        atomicAdd(&S.cnt.sum_demand, s_dem);
+        atomicAdd(&S.cnt.sum_evictable, s_evi);
+        atomicAdd(&S.cnt.sum_cand, s_can);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        PlanCounters* g = A.cnt;
+        const PlanCounters& lc = S.cnt;
+        S.uscal[0] = lc.n_E ? atomicAdd(&g->n_E, lc.n_E) : 0;
+        S.uscal[1] = lc.n_L ? atomicAdd(&g->n_L, lc.n_L) : 0;
+        S.uscal[2] = lc.n_C ? atomicAdd(&g->n_C, lc.n_C) : 0;
+        if (lc.sum_active) atomicAdd(&g->sum_active, lc.sum_active);
+        if (lc.sum_resident) atomicAdd(&g->sum_resident, lc.sum_resident);
+        if (lc.sum_demand) atomicAdd(&g->sum_demand, lc.sum_demand);
+        if (lc.sum_evictable) atomicAdd(&g->sum_evictable, lc.sum_evictable);
+        if (lc.sum_cand) atomicAdd(&g->sum_cand, lc.sum_cand);
+    }
+    __syncthreads();
+    if (isE) A.listE[S.uscal[0] + oE] = key;
+    if (isL) A.listL[S.uscal[1] + oL] = key;
+    if (isC) A.listC[S.uscal[2] + oC] = key;
+    __threadfence();                                 // release this workgroup's writes
+    __syncthreads();
+    if (threadIdx.x == 0) S.uscal[3] = atomicAdd(A.done, 1u) == gridDim.x - 1;
+    __syncthreads();
+    if (!S.uscal[3]) return;                         // workgroup-uniform
+    __threadfence();                                 // acquire every workgroup's writes
+    if (threadIdx.x == 0) *A.done = 0;
+    __syncthreads();
+    plan_core(A, lds, S);
+}
+
 // ---------------------------------------------------------------------------
 // block table
 // ---------------------------------------------------------------------------
@@ -857,14 +884,13 @@ __global__ void k_zero_u32(unsigned* p, u64 n) {
 // launchers
 // ---------------------------------------------------------------------------
 
-hipError_t launch_classify(const PlanArgs& a, hipStream_t st) {
-    const unsigned blocks = (a.n + 255) / 256;
-    hipLaunchKernelGGL(k_classify, dim3(blocks), dim3(256), 0, st, a);
-    return hipGetLastError();
-}
-
-hipError_t launch_plan_core(const PlanArgs& a, hipStream_t st) {
-    hipLaunchKernelGGL(k_plan_core, dim3(1), dim3(kCoreThreads), 0, st, a);
+hipError_t launch_plan(const PlanArgs& a, hipStream_t st) {
+    if (a.fused) {
+        hipLaunchKernelGGL(k_plan_core, dim3(1), dim3(kCoreThreads), 0, st, a);
+    } else {
+        const unsigned blocks = (a.n + kCoreThreads - 1) / kCoreThreads;
+        hipLaunchKernelGGL(k_classify_core, dim3(blocks), dim3(kCoreThreads), 0, st, a);
+    }
     return hipGetLastError();
 }
 

@@ -88,6 +88,7 @@ struct ss_pool {
     unsigned* d_occ = nullptr;
     unsigned occ_words = 0;
     PlanCounters* d_cnt = nullptr;
+    unsigned* d_done = nullptr;
     u64 *d_listE = nullptr, *d_listC = nullptr, *d_listL = nullptr;
     u64 *d_sortE = nullptr, *d_sortC = nullptr, *d_sortL = nullptr;
     u64 *d_prefE = nullptr, *d_prefC = nullptr, *d_loff = nullptr;
@@ -223,7 +224,7 @@ void free_pool(ss_pool* p) {
                      p->d_prefE, p->d_prefC, p->d_loff, p->d_victims, p->d_loads, p->d_vunits,
                      p->d_lunits, p->d_free_old, p->d_res, p->d_phase, p->d_hist_w,
                      p->d_wunits, p->d_vwritten, p->d_woff, p->d_items, p->d_plane_base,
-                     p->d_chunk_bytes};
+                     p->d_chunk_bytes, p->d_done};
     for (void* d : dptrs)
         if (d) (void)hipFree(d);
     void* hptrs[] = {p->h_res, p->h_victims, p->h_loads, p->h_vwritten};
@@ -499,6 +500,7 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(dalloc(&p->d_resident, N));
     CREATE_TRY(dalloc(&p->d_occ, p->occ_words));
     CREATE_TRY(dalloc(&p->d_cnt, 1));
+    CREATE_TRY(dalloc(&p->d_done, 1));
     CREATE_TRY(dalloc(&p->d_listE, N));
     CREATE_TRY(dalloc(&p->d_listC, N));
     CREATE_TRY(dalloc(&p->d_listL, N));
@@ -572,6 +574,10 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(hipMemcpy(p->d_occ, occ.data(), occ.size() * sizeof(unsigned), hipMemcpyHostToDevice));
     CREATE_TRY(hipMemcpy(p->d_resident, zeros_n.data(), N, hipMemcpyHostToDevice));
     CREATE_TRY(hipMemcpy(p->d_cnt, &zc, sizeof zc, hipMemcpyHostToDevice));
+    {
+        const unsigned zero = 0;
+        CREATE_TRY(hipMemcpy(p->d_done, &zero, sizeof zero, hipMemcpyHostToDevice));
+    }
     {
         std::vector<u64> zw(kDistBuckets, 0);
         CREATE_TRY(hipMemcpy(p->d_hist_w, zw.data(), kDistBuckets * sizeof(u64), hipMemcpyHostToDevice));
@@ -663,11 +669,11 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     A.vwritten = p->d_vwritten;
     A.vwritten_host = p->h_vwritten_dev;
     A.woff = p->d_woff;
+    A.done = p->d_done;
 
     const bool timing = p->flags & SS_FLAG_TIMING;
     if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.a, caller), true);
-    if (!A.fused) TRY_HIP(p, launch_classify(A, caller), true);
-    TRY_HIP(p, launch_plan_core(A, caller), true);
+    TRY_HIP(p, launch_plan(A, caller), true);
     if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.b, caller), true);
     TRY_HIP(p, hipEventRecord(p->ev_planned, caller), true);
 
