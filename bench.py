@@ -157,6 +157,9 @@ def parse():
     ap.add_argument("--host-copies", type=int, default=128,
                     help="distinct host copies shared round-robin by agents; 0 = one per agent")
     ap.add_argument("--plan-steps", type=int, default=20)
+    ap.add_argument("--direct-mib", type=float, default=4,
+                    help="directions of a step that move at most this many MiB go by kernel "
+                         "straight between units and host copies (0 = always staged)")
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--cpu-agents", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -544,7 +547,7 @@ def main():
         host_slots = None if args.host_copies == 0 else args.host_copies
         mem = PoolMemory(spec, args.staging_mib << 20, args.ring, host_slots=host_slots)
         mems.append(mem)
-        pools.append(mem.make_pool(timing=True))
+        pools.append(mem.make_pool(timing=True, direct_bytes=int(args.direct_mib * (1 << 20))))
     probe = {} if args.no_probe else probes(binding, mems[0].host)
     N = trace.n_agents
     d_np = np.ascontiguousarray(trace.dist, dtype=np.uint32)
@@ -635,20 +638,39 @@ def main():
                    "avg_us": 1e3 * unpack_ms / max(unpack_n, 1),
                    "GBps": 2 * unpack_b / max(unpack_ms, 1e-9) / 1e6},
     }
+    direct = {k: sum(s[k] for s in stats) for k in
+              ("direct_out_launches", "direct_in_launches", "direct_out_bytes", "direct_in_bytes",
+               "direct_out_ms", "direct_in_ms")}
+    for d in ("out", "in"):
+        direct[f"direct_{d}_GBps"] = (direct[f"direct_{d}_bytes"] /
+                                      max(direct[f"direct_{d}_ms"], 1e-9) / 1e6)
     dom = "pack" if pack_ms >= unpack_ms else "unpack"
-    traffic = None
-    pmc_path = os.path.join(ROOT, "profiles", f"k_copy_{args.workload}_pmc.json")
-    if os.path.exists(pmc_path):
-        pmc = json.load(open(pmc_path))
-        ratio = pmc["kernels"].get(dom, {}).get("traffic_over_algorithmic")
-        if pmc.get("kernel_source_sha256_16") == kernel_source_hash() and ratio:
-            # HBM bytes per whole-slot launch over its algorithmic bytes, applied
-            # to the timed launches' average size
-            traffic = ratio * kern[dom]["bytes_per_launch"]
-    roofline = {"bound": "hbm", "kernel": f"k_copy<{dom}>", "achieved": kern[dom]["GBps"],
-                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": kern[dom]["GBps"] / HBM_PEAK_GBPS,
-                "traffic": traffic,
-                "algorithmic_bytes_per_launch": kern[dom]["bytes_per_launch"]}
+    if pack_ms + unpack_ms >= direct["direct_out_ms"] + direct["direct_in_ms"]:
+        traffic = None
+        pmc_path = os.path.join(ROOT, "profiles", f"k_copy_{args.workload}_pmc.json")
+        if os.path.exists(pmc_path):
+            pmc = json.load(open(pmc_path))
+            ratio = pmc["kernels"].get(dom, {}).get("traffic_over_algorithmic")
+            if pmc.get("kernel_source_sha256_16") == kernel_source_hash() and ratio:
+                # HBM bytes per whole-slot launch over its algorithmic bytes,
+                # applied to the timed launches' average size
+                traffic = ratio * kern[dom]["bytes_per_launch"]
+        roofline = {"bound": "hbm", "kernel": f"k_copy<{dom}>", "achieved": kern[dom]["GBps"],
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                    "frac": kern[dom]["GBps"] / HBM_PEAK_GBPS, "traffic": traffic,
+                    "algorithmic_bytes_per_launch": kern[dom]["bytes_per_launch"]}
+    else:
+        # steps small enough to move by kernel straight over the host link:
+        # the dominant launches are host-link bound (peak: the measured one-way
+        # copy-engine rate of the same direction)
+        d = "out" if direct["direct_out_ms"] >= direct["direct_in_ms"] else "in"
+        n = max(direct[f"direct_{d}_launches"], 1)
+        peak = (probe.get("d2h_GBps" if d == "out" else "h2d_GBps") if probe else None)
+        ach = direct[f"direct_{d}_GBps"]
+        roofline = {"bound": "host-link", "kernel": f"k_copy<{'pack' if d == 'out' else 'unpack'}>"
+                    " direct", "achieved": ach, "peak": peak, "unit": "GB/s",
+                    "frac": ach / peak if peak else None, "traffic": None,
+                    "algorithmic_bytes_per_launch": direct[f"direct_{d}_bytes"] / n}
     d2h_b = sum(s["d2h_bytes"] for s in stats)
     h2d_b = sum(s["h2d_bytes"] for s in stats)
     d2h_ms = sum(s["d2h_ms"] for s in stats)
@@ -695,6 +717,7 @@ def main():
                    "seed": args.seed, "threshold": thr, "budget_units": budget,
                    "staging_bytes": args.staging_mib << 20, "ring_slots": args.ring,
                    "write_back": "none (clean evictions)" if args.clean_evict else "every eviction",
+                   "direct_limit_bytes": int(args.direct_mib * (1 << 20)),
                    "host_copies": ("one per agent" if args.host_copies == 0 else
                                    f"{args.host_copies} shared round-robin"),
                    "bytes_out": out_b, "bytes_in": in_b},
@@ -703,6 +726,7 @@ def main():
         "dma": dma,
         "plan_latency_us": plan,
         "kernels": kern,
+        "direct": direct if args.direct_mib else None,
         "loader": loader,
         "object_distances": objects,
         "estimators": estimators,

@@ -97,6 +97,14 @@ typedef struct {
     uint32_t        ring_slots;     /* >= 1 slots per direction                            */
     int32_t         device;         /* HIP device ordinal                                  */
     uint32_t        flags;          /* SS_FLAG_*                                           */
+    uint64_t        direct_bytes;   /* a direction of a step that moves at most this many
+                                       bytes runs as one kernel straight between the pool's
+                                       units and the pinned host copies (no staging, no
+                                       copy commands), which suits small steps where the
+                                       latency of each copy dominates; larger steps use the
+                                       staged pipeline.  0 = always staged.  host_backing
+                                       must then be device-accessible pinned memory.
+                                       (The load scheduler ignores it.)                    */
 } ss_pool_desc;
 
 typedef struct {
@@ -137,6 +145,10 @@ typedef struct {                    /* cumulative since create or ss_reset_stats
                                               sort, acceptance, lists, free units)          */
     double   plan_host_us[3];              /* ss_plan_step on the host: queueing the plan,
                                               waiting for it, reading it back              */
+    uint64_t direct_out_launches, direct_in_launches;  /* directions moved by direct_bytes */
+    uint64_t direct_out_bytes, direct_in_bytes;        /* (not counted in pack/unpack or
+                                                          d2h/h2d above)                  */
+    double   direct_out_ms, direct_in_ms;              /* event time of those launches    */
 } ss_stats;
 
 /* Create a pool (Appendix A: register a memory module).  Validates every

@@ -60,7 +60,7 @@ class ss_pool_desc(C.Structure):
                 ("host_backing", C.c_void_p), ("host_off", C.POINTER(C.c_uint64)),
                 ("host_bytes", C.c_uint64), ("dev_staging", C.c_void_p),
                 ("staging_bytes", C.c_uint64), ("ring_slots", C.c_uint32),
-                ("device", C.c_int32), ("flags", C.c_uint32)]
+                ("device", C.c_int32), ("flags", C.c_uint32), ("direct_bytes", C.c_uint64)]
 
 
 class ss_plan_params(C.Structure):
@@ -81,7 +81,10 @@ class ss_stats(C.Structure):
                 ("unpack_bytes", C.c_uint64), ("pack_ms", C.c_double), ("unpack_ms", C.c_double),
                 ("d2h_bytes", C.c_uint64), ("h2d_bytes", C.c_uint64), ("d2h_ms", C.c_double),
                 ("h2d_ms", C.c_double), ("plan_gpu_ms", C.c_double),
-                ("plan_phase_us", C.c_double * 7), ("plan_host_us", C.c_double * 3)]
+                ("plan_phase_us", C.c_double * 7), ("plan_host_us", C.c_double * 3),
+                ("direct_out_launches", C.c_uint64), ("direct_in_launches", C.c_uint64),
+                ("direct_out_bytes", C.c_uint64), ("direct_in_bytes", C.c_uint64),
+                ("direct_out_ms", C.c_double), ("direct_in_ms", C.c_double)]
 
 
 class ScaleSimError(RuntimeError):
@@ -179,7 +182,8 @@ def _u64(a):
 
 
 def make_desc(*, capacity_units, chunk_bytes, agent_units, plane_base, host_backing, host_bytes,
-              dev_staging, staging_bytes, ring_slots, host_off=None, device=0, flags=0):
+              dev_staging, staging_bytes, ring_slots, host_off=None, device=0, flags=0,
+              direct_bytes=0):
     """An ``ss_pool_desc`` and the arrays it points to (keep them alive)."""
     chunk = _u64(chunk_bytes)
     units = np.ascontiguousarray(agent_units, dtype=np.uint32)
@@ -200,6 +204,7 @@ def make_desc(*, capacity_units, chunk_bytes, agent_units, plane_base, host_back
     d.ring_slots = int(ring_slots)
     d.device = int(device)
     d.flags = int(flags)
+    d.direct_bytes = int(direct_bytes)
     return d, (chunk, units, bases, hoff)
 
 
@@ -209,14 +214,15 @@ class Pool:
 
     def __init__(self, *, capacity_units, chunk_bytes, agent_units, plane_base, host_backing,
                  host_bytes, dev_staging, staging_bytes, ring_slots, host_off=None, device=0,
-                 timing=False):
+                 timing=False, direct_bytes=0):
         L = load()
         d, self._keep = make_desc(capacity_units=capacity_units, chunk_bytes=chunk_bytes,
                                   agent_units=agent_units, plane_base=plane_base,
                                   host_backing=host_backing, host_bytes=host_bytes,
                                   dev_staging=dev_staging, staging_bytes=staging_bytes,
                                   ring_slots=ring_slots, host_off=host_off, device=device,
-                                  flags=SS_FLAG_TIMING if timing else 0)
+                                  flags=SS_FLAG_TIMING if timing else 0,
+                                  direct_bytes=direct_bytes)
         self._chunk = self._keep[0]
         self._units = self._keep[1]
         self.n_agents = len(self._units)

@@ -113,6 +113,10 @@ struct BtArgs {
     const unsigned char* vwritten;  // [N] per victim: written back
     const u64* woff;                // [N+1] prefix units over written-back victims
     int* wunits;                    // [U] written-back victims' units (pack source)
+    const u64* host_off;            // [N] host-copy byte offset per agent (direct mode, else null)
+    u64 unit_bytes;
+    u64* whost;                     // [U] host byte offset of each written-back unit (or null)
+    u64* lhost;                     // [U] host byte offset of each loaded unit (or null)
 };
 
 struct CopyArgs {
@@ -126,7 +130,9 @@ struct CopyArgs {
     unsigned pad1;
     const u64* plane_base;          // [P] device addresses
     const u64* chunk_bytes;         // [P]
-    char* staging;                  // slot base
+    char* staging;                  // slot base (direct: device address of the host copies)
+    const u64* stage_off;           // direct: [first + p] byte offset of logical unit p from
+                                    // staging; null: unit p at staging + p * unit_bytes
     u64 unit_bytes;
     u64 capacity;                   // U; unit ids outside [0, U) are skipped
 };

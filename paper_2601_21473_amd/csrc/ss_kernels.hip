@@ -746,7 +746,10 @@ __global__ void __launch_bounds__(256) k_bt_victims(BtArgs B) {
         for (unsigned j = threadIdx.x; j < s; j += blockDim.x) {
             const int u = B.bt[base + j];
             B.vunits[o + j] = u;
-            if (written) B.wunits[ow + j] = u;
+            if (written) {
+                B.wunits[ow + j] = u;
+                if (B.whost) B.whost[ow + j] = B.host_off[v] + (u64)j * B.unit_bytes;
+            }
             B.bt[base + j] = -1;
             if ((u64)(unsigned)u < B.capacity)
                 atomicAnd(&B.occ[(unsigned)u >> 5], ~(1u << ((unsigned)u & 31u)));
@@ -770,6 +773,7 @@ __global__ void __launch_bounds__(256) k_bt_loads(BtArgs B) {
             const int u = q < nF ? B.free_old[q] : B.vunits[q - nF];
             B.bt[base + j] = u;
             B.lunits[q] = u;
+            if (B.lhost) B.lhost[q] = B.host_off[a] + (u64)j * B.unit_bytes;
             if ((u64)(unsigned)u < B.capacity)
                 atomicOr(&B.occ[(unsigned)u >> 5], 1u << ((unsigned)u & 31u));
         }
@@ -840,6 +844,9 @@ __device__ __forceinline__ void wave_copy_burst(char* dst, const char* src, unsi
 // at 5.7-5.8 TB/s against 5.6 for the pack order (and 5.2 against 5.4 on
 // random lists).  Without run_order (chunks of several items, which already
 // give each block a contiguous range) the unpack takes the pack order.
+// Direct mode (stage_off set): the "staging" side is each unit's place in its
+// agent's pinned host copy, so the same kernel moves the bytes over the host
+// link itself.
 // The item index is wave-uniform, so its descriptor and the plane's base and
 // stride are scalar loads.
 template <bool kPack>
@@ -862,7 +869,8 @@ __global__ void __launch_bounds__(kCopyThreads) k_copy(CopyArgs A) {
     const CopyItem it = A.items[r];
     char* chunk = reinterpret_cast<char*>(A.plane_base[it.plane]) + u * A.chunk_bytes[it.plane] +
                   it.chunk_off;
-    char* stage = A.staging + (u64)p * A.unit_bytes + it.unit_off;
+    char* stage = A.staging + (A.stage_off ? A.stage_off[A.first + p] : (u64)p * A.unit_bytes) +
+                  it.unit_off;
     if (kPack) wave_copy_burst(stage, chunk, it.len);
     else wave_copy_burst(chunk, stage, it.len);
 }

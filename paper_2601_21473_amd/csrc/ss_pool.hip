@@ -13,6 +13,14 @@
 // units in eviction order, so slot k of the loads depends on a single pack
 // slot.  The next step's plan waits for both streams.
 //
+// Direct transfers (direct_bytes): a direction whose bytes in the step are at
+// most the pool's limit skips the staging ring and the copy commands; one
+// pack (or unpack) launch reads (or writes) each unit's place in its agent's
+// pinned host copy over the host link, at the addresses the block-table
+// kernels record per moved unit.  Small steps are latency-bound, and one
+// launch costs less than the copy commands of every agent.  A direct unpack
+// that overwrites released units waits for the step's last pack.
+//
 // The two streams are shared by all pools of a device, so any number of pools
 // (plus the caller's stream) fits in the four hardware queues the HIP runtime
 // gives a process by default and the two directions never share a queue.
@@ -79,6 +87,8 @@ struct ss_pool {
     uint32_t ring = 1;
     u64 units_per_slot = 0;
     u64 slot_bytes = 0;
+    u64 direct_bytes = 0;          // directions of at most this many bytes go direct
+    char* host_dev = nullptr;      // device address of the host copies (direct mode)
 
     // device metadata
     unsigned* d_units = nullptr;
@@ -96,6 +106,8 @@ struct ss_pool {
     int *d_vunits = nullptr, *d_lunits = nullptr, *d_free_old = nullptr, *d_wunits = nullptr;
     unsigned char* d_vwritten = nullptr;
     u64* d_woff = nullptr;
+    u64* d_host_off = nullptr;     // direct mode: [N] host-copy offsets
+    u64 *d_whost = nullptr, *d_lhost = nullptr;   // direct mode: [U] per moved unit
     PlanResult* d_res = nullptr;
     u64* d_phase = nullptr;
     u64* d_hist_w = nullptr;
@@ -120,10 +132,12 @@ struct ss_pool {
     hipEvent_t ev_planned = nullptr, ev_bt = nullptr, ev_caller = nullptr,
                ev_out_done = nullptr, ev_in_done = nullptr;
     std::vector<hipEvent_t> ev_packed;            // per eviction slot index in the step
+    unsigned n_pack_step = 0;                     // pack launches of the current step
+    bool direct_out = false;                      // this step's eviction went direct
 
     // timing (SS_FLAG_TIMING): one pair per launch or per slot's copies
-    std::vector<TimedPair> t_pack, t_unpack, t_d2h, t_h2d;
-    size_t n_t_pack = 0, n_t_unpack = 0, n_t_d2h = 0, n_t_h2d = 0;
+    std::vector<TimedPair> t_pack, t_unpack, t_d2h, t_h2d, t_dout, t_din;
+    size_t n_t_pack = 0, n_t_unpack = 0, n_t_d2h = 0, n_t_h2d = 0, n_t_dout = 0, n_t_din = 0;
     TimedPair t_plan;
     bool t_plan_used = false;
     ss_stats stats{};
@@ -224,7 +238,7 @@ void free_pool(ss_pool* p) {
                      p->d_prefE, p->d_prefC, p->d_loff, p->d_victims, p->d_loads, p->d_vunits,
                      p->d_lunits, p->d_free_old, p->d_res, p->d_phase, p->d_hist_w,
                      p->d_wunits, p->d_vwritten, p->d_woff, p->d_items, p->d_plane_base,
-                     p->d_chunk_bytes, p->d_done};
+                     p->d_chunk_bytes, p->d_done, p->d_host_off, p->d_whost, p->d_lhost};
     for (void* d : dptrs)
         if (d) (void)hipFree(d);
     void* hptrs[] = {p->h_res, p->h_victims, p->h_loads, p->h_vwritten};
@@ -237,7 +251,7 @@ void free_pool(ss_pool* p) {
         if (e) (void)hipEventDestroy(e);
     for (hipEvent_t e : p->ev_packed)
         if (e) (void)hipEventDestroy(e);
-    for (auto* v : {&p->t_pack, &p->t_unpack, &p->t_d2h, &p->t_h2d})
+    for (auto* v : {&p->t_pack, &p->t_unpack, &p->t_d2h, &p->t_h2d, &p->t_dout, &p->t_din})
         for (auto& tp : *v) {
             if (tp.a) (void)hipEventDestroy(tp.a);
             if (tp.b) (void)hipEventDestroy(tp.b);
@@ -281,10 +295,14 @@ void collect_timing(ss_pool* p) {
          &p->stats.unpack_launches);
     fold(p->t_d2h, p->n_t_d2h, &p->stats.d2h_ms, &p->stats.d2h_bytes, nullptr);
     fold(p->t_h2d, p->n_t_h2d, &p->stats.h2d_ms, &p->stats.h2d_bytes, nullptr);
+    fold(p->t_dout, p->n_t_dout, &p->stats.direct_out_ms, &p->stats.direct_out_bytes,
+         &p->stats.direct_out_launches);
+    fold(p->t_din, p->n_t_din, &p->stats.direct_in_ms, &p->stats.direct_in_bytes,
+         &p->stats.direct_in_launches);
     float ms = 0.f;
     if (p->t_plan_used && hipEventElapsedTime(&ms, p->t_plan.a, p->t_plan.b) == hipSuccess)
         p->stats.plan_gpu_ms += ms;
-    p->n_t_pack = p->n_t_unpack = p->n_t_d2h = p->n_t_h2d = 0;
+    p->n_t_pack = p->n_t_unpack = p->n_t_d2h = p->n_t_h2d = p->n_t_dout = p->n_t_din = 0;
     p->t_plan_used = false;
 }
 
@@ -379,6 +397,10 @@ ss_status flush_bt(ss_pool* p) {
     B.vwritten = p->d_vwritten;
     B.woff = p->d_woff;
     B.wunits = p->d_wunits;
+    B.host_off = p->d_host_off;
+    B.unit_bytes = p->unit_bytes;
+    B.whost = p->d_whost;
+    B.lhost = p->d_lhost;
     p->bt_pending = false;
     TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_planned, 0), true);
     TRY_HIP(p, launch_bt_update(B, p->N, p->st_out), true);
@@ -472,6 +494,7 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     p->host_off = std::move(host_off);
     p->host = static_cast<char*>(d->host_backing);
     p->host_bytes = d->host_bytes;
+    p->direct_bytes = d->direct_bytes;
     p->ring = d->ring_slots;
     p->units_per_slot = ups;
     p->slot_bytes = ups * unit_bytes;
@@ -516,6 +539,20 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(dalloc(&p->d_lunits, U));
     CREATE_TRY(dalloc(&p->d_free_old, U));
     CREATE_TRY(dalloc(&p->d_wunits, U));
+    if (p->direct_bytes) {
+        if (hipHostGetDevicePointer(reinterpret_cast<void**>(&p->host_dev), p->host, 0) !=
+            hipSuccess) {
+            (void)hipGetLastError();
+            free_pool(p);
+            return set_err(SS_ERR_ARG, "direct_bytes > 0 needs host_backing that the device can "
+                                       "access (pinned, mapped)");
+        }
+        CREATE_TRY(dalloc(&p->d_host_off, N));
+        CREATE_TRY(dalloc(&p->d_whost, U));
+        CREATE_TRY(dalloc(&p->d_lhost, U));
+        CREATE_TRY(hipMemcpy(p->d_host_off, p->host_off.data(), N * sizeof(u64),
+                             hipMemcpyHostToDevice));
+    }
     CREATE_TRY(dalloc(&p->d_vwritten, N));
     CREATE_TRY(dalloc(&p->d_woff, N + 1));
     CREATE_TRY(dalloc(&p->d_res, 1));
@@ -753,12 +790,15 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
 
     const u64 total = p->res.units_written;
     const u64 ups = p->units_per_slot;
-    const u64 nslots = (total + ups - 1) / ups;
+    const bool direct = p->direct_bytes && total && total * p->unit_bytes <= p->direct_bytes;
+    const u64 nslots = direct ? 1 : (total + ups - 1) / ups;
     while (p->ev_packed.size() < nslots) {
         hipEvent_t ev;
         TRY_HIP(p, make_event(&ev, false), true);
         p->ev_packed.push_back(ev);
     }
+    p->n_pack_step = (unsigned)nslots;
+    p->direct_out = direct;
     CopyArgs C{};
     C.units_list = p->d_wunits;
     C.items = p->d_items;
@@ -769,8 +809,24 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
     C.chunk_bytes = p->d_chunk_bytes;
     C.unit_bytes = p->unit_bytes;
     C.capacity = p->U;
+    if (direct) {
+        // one launch gathers every written-back unit straight into its host copy
+        C.first = 0;
+        C.count = total;
+        C.staging = p->host_dev;
+        C.stage_off = p->d_whost;
+        TimedPair* tp = nullptr;
+        if (timing) {
+            TRY_HIP(p, timed_pair(p->t_dout, p->n_t_dout++, &tp), true);
+            tp->bytes = total * p->unit_bytes;
+            TRY_HIP(p, hipEventRecord(tp->a, p->st_out), true);
+        }
+        TRY_HIP(p, launch_pack(C, p->st_out), true);
+        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_out), true);
+        TRY_HIP(p, hipEventRecord(p->ev_packed[0], p->st_out), true);
+    }
     size_t vi = 0;
-    for (u64 k = 0; k < nslots; ++k) {
+    for (u64 k = 0; !direct && k < nslots; ++k) {
         const u64 p0 = k * ups, p1 = std::min(total, p0 + ups);
         char* slot = p->stage_out + (k % p->ring) * p->slot_bytes;
         C.first = p0;
@@ -822,7 +878,8 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
 
     const u64 total = p->res.units_in;
     const u64 ups = p->units_per_slot;
-    const u64 nslots = (total + ups - 1) / ups;
+    const bool direct = p->direct_bytes && total && total * p->unit_bytes <= p->direct_bytes;
+    const u64 nslots = direct ? 0 : (total + ups - 1) / ups;
     const u64 nF = p->res.n_free_used;
     CopyArgs C{};
     C.units_list = p->d_lunits;
@@ -834,6 +891,24 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
     C.chunk_bytes = p->d_chunk_bytes;
     C.unit_bytes = p->unit_bytes;
     C.capacity = p->U;
+    if (direct) {
+        // one launch scatters every load straight from its host copy; units
+        // released this step are overwritten only after the packs read them
+        if (total > nF && p->n_pack_step)
+            TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_packed[p->n_pack_step - 1], 0), true);
+        C.first = 0;
+        C.count = total;
+        C.staging = p->host_dev;
+        C.stage_off = p->d_lhost;
+        TimedPair* tp = nullptr;
+        if (timing) {
+            TRY_HIP(p, timed_pair(p->t_din, p->n_t_din++, &tp), true);
+            tp->bytes = total * p->unit_bytes;
+            TRY_HIP(p, hipEventRecord(tp->a, p->st_in), true);
+        }
+        TRY_HIP(p, launch_unpack(C, p->st_in), true);
+        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_in), true);
+    }
     size_t li = 0, ri = 0;
     for (u64 k = 0; k < nslots; ++k) {
         const u64 q0 = k * ups, q1 = std::min(total, q0 + ups);
@@ -863,7 +938,8 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
             const long long j = p->res.n_victims ? p->last_written[ri] : -1;
             if (j >= 0 && p->voff[j + 1] > r0) {
                 const u64 maxpos = p->woff[j] + std::min(r1, p->voff[j + 1]) - p->voff[j] - 1;
-                TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_packed[maxpos / ups], 0), true);
+                const u64 slot = p->direct_out ? 0 : maxpos / ups;   // a direct pack is one launch
+                TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_packed[slot], 0), true);
             }
         }
         C.first = q0;

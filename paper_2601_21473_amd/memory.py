@@ -102,7 +102,7 @@ class PoolMemory:
                     staging_bytes=self.staging.nbytes, ring_slots=self.ring_slots,
                     device=self.device)
 
-    def make_pool(self, timing: bool = False) -> binding.Pool:
+    def make_pool(self, timing: bool = False, direct_bytes: int = 0) -> binding.Pool:
         s = self.spec
         return binding.Pool(capacity_units=s.capacity_units, chunk_bytes=s.chunk_bytes,
                             agent_units=s.agent_units,
@@ -110,7 +110,7 @@ class PoolMemory:
                             host_backing=self.host.ptr, host_bytes=self.host.nbytes,
                             host_off=self.host_off, dev_staging=self.staging.ptr,
                             staging_bytes=self.staging.nbytes, ring_slots=self.ring_slots,
-                            device=self.device, timing=timing)
+                            device=self.device, timing=timing, direct_bytes=direct_bytes)
 
     def host_copy(self, agent: int) -> np.ndarray:
         """View of an agent's host copy (unit-major, planes in order)."""

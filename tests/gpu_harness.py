@@ -76,20 +76,21 @@ def fill_host(mem, content, spec, batch_bytes=256 << 20):
 
 def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_bytes=True,
                slot_units=8, ring_slots=2, sample_units=None, bt_every=1, seed=0, label="",
-               dirty=None, device_inputs=None):
+               dirty=None, device_inputs=None, direct_bytes=0):
     """``device_inputs(t) -> (distances_ptr, active_ptr)`` replaces the uploaded
-    trace on the HIP side (the oracle side always reads ``trace``)."""
+    trace on the HIP side (the oracle side always reads ``trace``).
+    ``direct_bytes``: the pool's direct-transfer limit (0 = always staged)."""
     spec = trace.pools[pool_index]
     ub = spec.unit_bytes
     staging_bytes = 2 * ring_slots * slot_units * ub
     log(f"[parity] {label or trace.name} pool={spec.name} N={trace.n_agents} "
         f"U={spec.capacity_units} unit={ub}B planes={spec.n_planes} theta={theta} "
-        f"budget={budget} slot_units={slot_units} ring={ring_slots}")
+        f"budget={budget} slot_units={slot_units} ring={ring_slots} direct={direct_bytes}")
     mem = PoolMemory(spec, staging_bytes, ring_slots)
     content = W.Content(spec, seed=seed, pool_index=pool_index)
     if check_bytes:
         fill_host(mem, content, spec)
-    pool = mem.make_pool(timing=True)
+    pool = mem.make_pool(timing=True, direct_bytes=direct_bytes)
     opool = OraclePool(spec.capacity_units, spec.agent_units, ub)
     dev = upload_trace(trace) if device_inputs is None else None
     d_dirty = None

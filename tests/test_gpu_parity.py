@@ -9,6 +9,9 @@ and byte movement.  Cases:
     every resident unit);
   * the real unit layouts (64 x 32 KiB KV pages, 448-plane LoRA adapters,
     512 KiB unified units) on agent subsets, with sampled byte checks;
+  * direct transfers (a direction at or below the pool's direct_bytes moves
+    by kernel straight between units and host copies): every step direct,
+    and a limit that sends some steps' directions direct and others staged;
   * edge cases: one-unit ring slots, no prefetch, budgets, an agent count
     that is not a multiple of the wave or block size, lists larger than the
     plan kernel's LDS sort buffer, empty steps, overcommit and call order."""
@@ -44,6 +47,36 @@ def test_tiny_one_unit_slots():
     st = run_parity(W.make_trace("tiny", 1), theta=S, slot_units=1, ring_slots=1,
                     label="tiny one-unit ring")
     assert st["pack_launches"] > 100 and st["unpack_launches"] > 100
+
+
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("theta", [0, S])
+def test_tiny_direct(seed, theta):
+    st = run_parity(W.make_trace("tiny", seed), theta=theta, slot_units=3, ring_slots=2,
+                    direct_bytes=1 << 40, label=f"tiny direct s{seed} t{theta}")
+    assert st["pack_launches"] == 0 and st["unpack_launches"] == 0
+    assert st["direct_out_launches"] > 50 and st["direct_in_launches"] > 50
+    assert st["d2h_bytes"] == 0 and st["h2d_bytes"] == 0
+
+
+@pytest.mark.parametrize("name,n_agents,steps,pool_index,limit_units", [
+    ("bursty", 150, 40, 0, 24),        # 64 x 32 KiB units, lognormal agent sizes
+    ("zipf_lora", 40, 40, 0, 64),      # KV pool, 32-unit agents
+    ("zipf_lora", 40, 40, 1, 2),       # 448-plane LoRA slots
+    ("diffusion", 150, 40, 0, 300),    # 512 KiB unified units
+])
+def test_direct_and_staged_mixed(name, n_agents, steps, pool_index, limit_units):
+    """A limit between small and large steps: each direction of each step
+    goes direct or staged on its own, so both orders of the eviction/load
+    hazard (direct pack then staged unpack and the reverse) occur."""
+    tr = W.subsample_agents(W.make_trace(name, 0), n_agents)
+    spec = tr.pools[pool_index]
+    slot_units = max(1, (64 << 20) // spec.unit_bytes)
+    st = run_parity(tr, pool_index=pool_index, theta=S, steps=steps, slot_units=slot_units,
+                    ring_slots=2, sample_units=48, direct_bytes=limit_units * spec.unit_bytes,
+                    label=f"{name}[{pool_index}] direct<={limit_units}u")
+    assert st["direct_out_launches"] > 0 and st["direct_in_launches"] > 0
+    assert st["pack_launches"] > 0 and st["unpack_launches"] > 0
 
 
 @pytest.mark.parametrize("name,pool_index", [("roundrobin", 0), ("bursty", 0), ("zipf_lora", 0),
