@@ -567,7 +567,7 @@ def main():
 
     def step(t):
         plans = [p.plan_step(dist.ptr + 4 * N * t, act.ptr + N * t, thr, budget, stream,
-                             dirty_ptr) for p in pools]
+                             dirty_ptr, lists=False) for p in pools]
         for p in pools:
             p.evict_pack(stream)
         for p in pools:
@@ -595,15 +595,23 @@ def main():
     moved = out_b + in_b
     stats = [p.stats() for p in pools]
 
-    # plan latency: each plan issued with the device idle
-    lat = []
+    # plan latency: each plan issued with the device idle; wall time of the
+    # Python call (counts only) and the library's own host time of the C call
+    # (stats are read only after a plan, so that nothing is submitted between
+    # the wait for the previous step and the measured call)
+    lat, lat_c = [], []
+    c_prev = sum(sum(p.stats()["plan_host_us"]) for p in pools)
     for k in range(args.plan_steps):
         sync()
         t = args.warmup + args.steps + k
         ts = time.perf_counter()
         for p in pools:
-            p.plan_step(dist.ptr + 4 * N * t, act.ptr + N * t, thr, budget, stream, dirty_ptr)
+            p.plan_step(dist.ptr + 4 * N * t, act.ptr + N * t, thr, budget, stream, dirty_ptr,
+                        lists=False)
         lat.append(time.perf_counter() - ts)
+        c_now = sum(sum(p.stats()["plan_host_us"]) for p in pools)
+        lat_c.append(c_now - c_prev)
+        c_prev = c_now
         for p in pools:
             p.evict_pack(stream)
         for p in pools:
@@ -693,7 +701,13 @@ def main():
     nps = max(args.plan_steps, 1)
     host = [sum(s["plan_host_us"][i] for s in plan_stats) - sum(s["plan_host_us"][i] for s in stats)
             for i in range(3)]
+    phases = [(sum(s["plan_phase_us"][i] for s in plan_stats) -
+               sum(s["plan_phase_us"][i] for s in stats)) / nps for i in range(7)]
     plan = {"median": float(np.median(lat_us)), "p99": float(np.percentile(lat_us, 99)),
+            "c_call_median": float(np.median(lat_c)), "c_call_p99": float(np.percentile(lat_c, 99)),
+            "core_phases_us": dict(zip(("classify", "demand_and_evictable_sorts",
+                                        "candidate_select", "candidate_sort", "acceptance",
+                                        "lists", "free_units"), phases)),
             "gpu_kernels_us": 1e3 * plan_gpu_ms / nps,
             "host_enqueue_us": host[0] / nps, "host_wait_us": host[1] / nps,
             "host_readback_us": host[2] / nps}

@@ -230,6 +230,10 @@ class Pool:
         _check(L.ss_pool_create(C.byref(d), C.byref(h)))
         self._h = h
         self.unit_bytes = int(self._chunk.sum())
+        # reused argument structs of ss_plan_step
+        self._prm, self._out = ss_plan_params(), ss_plan()
+        self._prm_ref, self._out_ref = C.byref(self._prm), C.byref(self._out)
+        self._plan = L.ss_plan_step
 
     def close(self):
         if getattr(self, "_h", None):
@@ -243,14 +247,20 @@ class Pool:
             pass
 
     def plan_step(self, distances_ptr: int, active_ptr: int, threshold: int, budget=None,
-                  stream: int = 0, dirty_ptr: int = 0):
+                  stream: int = 0, dirty_ptr: int = 0, lists: bool = True):
         """``ss_plan_step``; returns a dict with numpy copies of the plan.
-        ``dirty_ptr``: device address of the [N] write-back mask, 0 = none."""
-        prm = ss_plan_params(int(threshold), SS_NO_BUDGET if budget is None else int(budget),
-                             int(dirty_ptr) or None)
-        out = ss_plan()
-        _check(load().ss_plan_step(self._h, int(distances_ptr), int(active_ptr), C.byref(prm),
-                                   C.byref(out), int(stream) or None))
+        ``dirty_ptr``: device address of the [N] write-back mask, 0 = none.
+        ``lists=False`` returns the counts and byte totals only (no copies)."""
+        prm, out = self._prm, self._out
+        prm.threshold = int(threshold)
+        prm.budget_units = SS_NO_BUDGET if budget is None else int(budget)
+        prm.dirty = int(dirty_ptr) or None
+        _check(self._plan(self._h, int(distances_ptr), int(active_ptr), self._prm_ref,
+                          self._out_ref, int(stream) or None))
+        if not lists:
+            return {"units_out": out.units_out, "units_in": out.units_in,
+                    "bytes_out": out.bytes_out, "bytes_in": out.bytes_in,
+                    "n_victims": out.n_victims, "n_loads": out.n_loads}
         nv, nl = out.n_victims, out.n_loads
         victims = (np.ctypeslib.as_array(out.victims, shape=(nv,)).copy() if nv
                    else np.zeros(0, np.uint32))
