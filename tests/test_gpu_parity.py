@@ -127,6 +127,24 @@ def test_write_back_elision(mode):
                label=f"bursty elision {mode}")
 
 
+@pytest.mark.parametrize("mode", ["clean", "mixed"])
+def test_write_back_elision_direct(mode):
+    """Write-back elision with direct transfers: only the dirty victims'
+    units are gathered into their host copies (the per-unit host offsets
+    cover written-back victims only)."""
+    tr = W.make_trace("tiny", 3)
+    rng = np.random.default_rng(12)
+    dirty = (np.zeros(tr.active.shape, np.uint8) if mode == "clean"
+             else (rng.random(tr.active.shape) < 0.4).astype(np.uint8))
+    st = run_parity(tr, theta=S, slot_units=2, ring_slots=2, dirty=dirty, direct_bytes=1 << 40,
+                    label=f"direct elision {mode}")
+    assert st["pack_launches"] == 0 and st["unpack_launches"] == 0
+    if mode == "clean":
+        assert st["direct_out_launches"] == 0 and st["direct_out_bytes"] == 0
+    else:
+        assert st["direct_out_launches"] > 0
+
+
 def test_two_pools_share_streams():
     """The KV and LoRA pools of one workload stepped together (they share the
     device's streams), each against its own oracle, bytes included."""
