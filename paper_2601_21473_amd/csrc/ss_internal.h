@@ -148,7 +148,7 @@ constexpr int kLdsKeys = 16384;                   // 128 KiB of u64 keys in LDS
 // itself), or classification over many workgroups whose last one runs the core.
 hipError_t launch_plan(const PlanArgs& a, hipStream_t st);
 hipError_t launch_bt_update(const BtArgs& a, unsigned n_agents, hipStream_t st);
-constexpr unsigned kFuseAgents = 16384;           // plan core classifies up to this many
+constexpr unsigned kFuseAgents = 4096;            // plan core classifies up to this many
 hipError_t launch_pack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_unpack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_zero_u32(unsigned* p, u64 n, hipStream_t st);

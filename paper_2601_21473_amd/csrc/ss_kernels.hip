@@ -194,75 +194,97 @@ __device__ __forceinline__ void cmp_keep(u64& x, u64 p, bool keep_min) {
     x = keep_min ? (p < x ? p : x) : (p > x ? p : x);
 }
 
-// Compare-exchange of the pairs (r, r | JR) a thread holds in registers
-// (element index i = t + 1024 r; partner i ^ (JR << 10)).
-constexpr unsigned kRegKeys = 8;                  // keys per thread in the register sort
+// Keys per thread in the register stages of the LDS sort (so lists of up to
+// 1024 * kRegKeys keys are sorted in LDS).
+constexpr unsigned kRegKeys = 8;
 
-template <unsigned JR>
-__device__ __forceinline__ void reg_stage(u64 (&x)[kRegKeys], unsigned E, unsigned t, unsigned k) {
+// Ascending sort of lds[0..npad), npad a power of two <= 1024 * kE, by a
+// 1024-thread block, using lds[npad..2 npad) as scratch.  Each wave first
+// sorts runs of 64 keys in registers (thread t holds elements t + 1024 r;
+// 21 compare-exchange stages over wave shuffles, no barrier; waves that hold
+// only padding skip them).  Then runs are merged pairwise, one barrier per
+// round, by merge path (Green, McColl and Bader 2012): thread t writes the
+// kE consecutive outputs starting at t * kE; one binary search over the
+// diagonal of its run pair finds how many of the outputs before it come from
+// the left run, then it merges its kE outputs sequentially with the two run
+// heads in registers.  Ties take the left run first, so the padding keys
+// (all equal) keep a consistent order.
+template <unsigned kE>
+__device__ __forceinline__ void merge_sort_lds_e(u64* lds, unsigned npad) {
+    const unsigned t = threadIdx.x;
+    if ((t & ~63u) < npad) {                         // wave-uniform: the wave holds keys
+        u64 x[kE];
 #pragma unroll
-    for (unsigned r = 0; r < kRegKeys; ++r) {
-        if ((r & JR) == 0 && (r | JR) < E) {
-            const bool asc = ((t + (r << 10)) & k) == 0;
-            const u64 a = x[r], b = x[r | JR];
-            if ((a > b) == asc) {
-                x[r] = b;
-                x[r | JR] = a;
+        for (unsigned r = 0; r < kE; ++r) {
+            const unsigned i = t + (r << 10);
+            x[r] = i < npad ? lds[i] : ~0ull;
+        }
+#pragma unroll
+        for (unsigned k = 2; k <= 64; k <<= 1) {
+#pragma unroll
+            for (unsigned j = k >> 1; j > 0; j >>= 1) {
+#pragma unroll
+                for (unsigned r = 0; r < kE; ++r) {
+                    const unsigned i = t + (r << 10);
+                    const u64 p = __shfl_xor(x[r], (int)j);
+                    // runs below 64 alternate direction (bitonic); each 64-run ends ascending
+                    const bool up = k == 64 || (i & k) == 0;
+                    cmp_keep(x[r], p, ((i & j) == 0) == up);
+                }
             }
         }
+#pragma unroll
+        for (unsigned r = 0; r < kE; ++r) {
+            const unsigned i = t + (r << 10);
+            if (i < npad) lds[i] = x[r];
+        }
+    }
+    __syncthreads();
+    u64* src = lds;
+    u64* dst = lds + npad;
+    for (unsigned L = 64; L < npad; L <<= 1) {
+        const unsigned o = t * kE;                   // first output of this thread
+        if (o < npad) {
+            const unsigned base = o & ~(2 * L - 1);
+            const unsigned d = o - base;             // outputs of the pair before o
+            const u64* A = src + base;
+            const u64* B = src + base + L;
+            unsigned lo = d > L ? d - L : 0, hi = d < L ? d : L;
+            while (lo < hi) {
+                const unsigned mid = (lo + hi) >> 1;
+                if (A[mid] <= B[d - 1 - mid]) lo = mid + 1; else hi = mid;
+            }
+            unsigned i = lo, j = d - lo;
+            u64 a = i < L ? A[i] : ~0ull, b = j < L ? B[j] : ~0ull;
+#pragma unroll
+            for (unsigned k = 0; k < kE; ++k) {
+                const bool takeA = j >= L || (i < L && a <= b);
+                dst[o + k] = takeA ? a : b;
+                if (takeA) {
+                    ++i;
+                    a = i < L ? A[i] : ~0ull;
+                } else {
+                    ++j;
+                    b = j < L ? B[j] : ~0ull;
+                }
+            }
+        }
+        __syncthreads();
+        u64* tmp = src;
+        src = dst;
+        dst = tmp;
+    }
+    if (src != lds) {
+        for (unsigned i = t; i < npad; i += blockDim.x) lds[i] = src[i];
+        __syncthreads();
     }
 }
 
-// Ascending bitonic sort of lds[0..npad), npad a power of two <= 1024 *
-// kRegKeys, by a 1024-thread block.  Thread t keeps elements t + 1024 r in registers:
-// stages with stride >= 1024 stay inside the thread, strides 64..512 go
-// through LDS (two barriers each), strides < 64 are wave shuffles.
-__device__ void bitonic_lds_fast(u64* lds, unsigned npad) {
-    const unsigned t = threadIdx.x;
-    const unsigned E = npad > 1024 ? npad >> 10 : 1;
-    u64 x[kRegKeys];
-#pragma unroll
-    for (unsigned r = 0; r < kRegKeys; ++r) {
-        const unsigned i = t + (r << 10);
-        x[r] = (r < E && i < npad) ? lds[i] : ~0ull;
-    }
-    for (unsigned k = 2; k <= npad; k <<= 1) {
-        for (unsigned j = k >> 1; j > 0; j >>= 1) {
-            if (j >= 1024) {
-                if (j == 1024) reg_stage<1>(x, E, t, k);
-                else if (j == 2048) reg_stage<2>(x, E, t, k);
-                else reg_stage<4>(x, E, t, k);
-            } else if (j >= 64) {
-#pragma unroll
-                for (unsigned r = 0; r < kRegKeys; ++r) {
-                    const unsigned i = t + (r << 10);
-                    if (r < E && i < npad) lds[i] = x[r];
-                }
-                __syncthreads();
-#pragma unroll
-                for (unsigned r = 0; r < kRegKeys; ++r) {
-                    const unsigned i = t + (r << 10);
-                    if (r < E && i < npad) cmp_keep(x[r], lds[i ^ j], ((i & j) == 0) == ((i & k) == 0));
-                }
-                __syncthreads();
-            } else {
-#pragma unroll
-                for (unsigned r = 0; r < kRegKeys; ++r) {
-                    if (r < E) {
-                        const unsigned i = t + (r << 10);
-                        const u64 p = __shfl_xor(x[r], (int)j);
-                        cmp_keep(x[r], p, ((i & j) == 0) == ((i & k) == 0));
-                    }
-                }
-            }
-        }
-    }
-#pragma unroll
-    for (unsigned r = 0; r < kRegKeys; ++r) {
-        const unsigned i = t + (r << 10);
-        if (r < E && i < npad) lds[i] = x[r];
-    }
-    __syncthreads();
+__device__ void merge_sort_lds(u64* lds, unsigned npad) {
+    if (npad <= 1024) merge_sort_lds_e<1>(lds, npad);
+    else if (npad == 2048) merge_sort_lds_e<2>(lds, npad);
+    else if (npad == 4096) merge_sort_lds_e<4>(lds, npad);
+    else merge_sort_lds_e<8>(lds, npad);
 }
 
 // Sort the keys src[i] < kstar (there are exactly m of them) ascending into
@@ -288,7 +310,7 @@ __device__ void select_sort(const u64* src, unsigned n_src, u64 kstar, unsigned 
     }
     for (unsigned i = m + threadIdx.x; i < npad; i += blockDim.x) buf[i] = ~0ull;
     __syncthreads();
-    if (npad <= 1024 * kRegKeys) bitonic_lds_fast(lds, npad);
+    if (npad <= 1024 * kRegKeys) merge_sort_lds(lds, npad);
     else bitonic_asc(buf, npad);
     if (buf == lds) {
         for (unsigned i = threadIdx.x; i < m; i += blockDim.x) dst[i] = lds[i];
@@ -504,7 +526,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
             const unsigned npad = pow2ceil(mprime);
             for (unsigned i = mprime + tid; i < npad; i += blockDim.x) lds[i] = ~0ull;
             __syncthreads();
-            if (npad <= 1024 * kRegKeys) bitonic_lds_fast(lds, npad);
+            if (npad <= 1024 * kRegKeys) merge_sort_lds(lds, npad);
             else bitonic_asc(lds, npad);
             // inclusive prefix of units over the sorted keys; m = count <= cap
             u64 carry = 0;
