@@ -71,7 +71,8 @@ __device__ __forceinline__ void wave_append(bool pred, u64 key, u64* list, unsig
 // Classify agent a (a >= n: no agent) and add it to the lists and sums kept
 // in `cnt` (global memory for the multi-block kernel, LDS in the fused plan
 // core).  Every lane of the wave must call it.
-__device__ __forceinline__ void classify_agent(const PlanArgs& A, unsigned a, PlanCounters* cnt) {
+__device__ __forceinline__ void classify_agent(const PlanArgs& A, unsigned a, PlanCounters* cnt,
+                                               u64* hist) {
     const bool valid = a < A.n;
     unsigned D = 0;
     bool act = false, res = false;
@@ -87,7 +88,7 @@ __device__ __forceinline__ void classify_agent(const PlanArgs& A, unsigned a, Pl
     const bool isE = valid && res && !act;            // evictable resident
     const bool isL = valid && act && !res;            // demand load
     const bool isC = valid && !res && !act && D < A.threshold;   // prefetch candidate
-    if (isC) atomicAdd(&A.hist_w[dist_bucket(D)], s);
+    if (isC) atomicAdd(&hist[dist_bucket(D)], s);
     wave_append(isE, key, A.listE, &cnt->n_E);
     wave_append(isL, key, A.listL, &cnt->n_L);
     wave_append(isC, key, A.listC, &cnt->n_C);
@@ -119,6 +120,7 @@ __device__ __forceinline__ unsigned wave_reserve(bool pred, unsigned* counter) {
 // ---------------------------------------------------------------------------
 
 struct CoreShared {
+    u64 histw[kDistBuckets];        // candidate units per distance bucket (this workgroup)
     PlanCounters cnt;               // fused classification
     u64 wsum[kCoreThreads / 64 + 1];
     u64 hist[256];
@@ -436,16 +438,21 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     const unsigned* units = A.units;
     if (A.fused) {
         if (tid == 0) S.cnt = PlanCounters{};
+        for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) S.histw[b] = 0;
         __syncthreads();
-        for (unsigned base = 0; base < A.n; base += blockDim.x) classify_agent(A, base + tid, &S.cnt);
+        for (unsigned base = 0; base < A.n; base += blockDim.x)
+            classify_agent(A, base + tid, &S.cnt, S.histw);
         __syncthreads();
     }
+    // the candidate histogram: this workgroup's LDS when it classified the
+    // agents itself, else the global sum of all classifying workgroups
+    const u64* histw = A.fused ? S.histw : A.hist_w;
     const PlanCounters c = A.fused ? S.cnt : *A.cnt;
     __syncthreads();
     stamp(1);
 
     if (c.sum_active > A.capacity) {                 // overcommit: change nothing
-        for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
+        if (!A.fused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
         if (tid == 0) {
             PlanResult r = {};
             r.status = 1;
@@ -501,7 +508,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         __syncthreads();
         for (unsigned b0 = 0; b0 < kDistBuckets; b0 += blockDim.x) {
             const unsigned b = b0 + tid;
-            const u64 w = b < kDistBuckets ? A.hist_w[b] : 0;
+            const u64 w = b < kDistBuckets ? histw[b] : 0;
             u64 tw;
             const u64 ew = block_excl_scan(w, S, &tw);
             if (b < kDistBuckets && carry_w + ew <= cap && carry_w + ew + w > cap)
@@ -549,9 +556,9 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
             kstar = weighted_select(A.listC, nC, units, idmask, cap, S, &m);
         }
         // the histogram starts the next step at zero
-        for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
+        if (!A.fused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
     } else {
-        for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
+        if (!A.fused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
     }
     stamp(3);
     if (!sorted) select_sort(A.listC, nC, kstar, m, A.sortC, lds, S);
@@ -688,6 +695,7 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
     __shared__ CoreShared S;
     const unsigned a = blockIdx.x * kCoreThreads + threadIdx.x;
     if (threadIdx.x == 0) S.cnt = PlanCounters{};
+    for (unsigned b = threadIdx.x; b < kDistBuckets; b += kCoreThreads) S.histw[b] = 0;
     __syncthreads();
     const bool valid = a < A.n;
     unsigned D = 0;
@@ -704,7 +712,10 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
     const bool isE = valid && res && !act;            // evictable resident
     const bool isL = valid && act && !res;            // demand load
     const bool isC = valid && !res && !act && D < A.threshold;   // prefetch candidate
-    if (isC) atomicAdd(&A.hist_w[dist_bucket(D)], s);
+    // candidate units per distance bucket: LDS first (distances concentrate on
+    // few buckets, where global atomics would serialize), one global atomic
+    // per non-empty bucket and workgroup below
+    if (isC) atomicAdd(&S.histw[dist_bucket(D)], s);
     const unsigned oE = wave_reserve(isE, &S.cnt.n_E);
     const unsigned oL = wave_reserve(isL, &S.cnt.n_L);
     const unsigned oC = wave_reserve(isC, &S.cnt.n_C);
@@ -737,6 +748,8 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
     if (isE) A.listE[S.uscal[0] + oE] = key;
     if (isL) A.listL[S.uscal[1] + oL] = key;
     if (isC) A.listC[S.uscal[2] + oC] = key;
+    for (unsigned b = threadIdx.x; b < kDistBuckets; b += kCoreThreads)
+        if (S.histw[b]) atomicAdd(&A.hist_w[b], S.histw[b]);
     __threadfence();                                 // release this workgroup's writes
     __syncthreads();
     if (threadIdx.x == 0) S.uscal[3] = atomicAdd(A.done, 1u) == gridDim.x - 1;
