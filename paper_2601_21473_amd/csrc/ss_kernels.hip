@@ -151,19 +151,95 @@ __device__ u64 block_excl_scan(u64 v, CoreShared& S, u64* total) {
 }
 
 // out[0] = 0, out[i+1] = out[i] + f(i) for i < n.
+// Lists longer than the block: each thread takes kPrefixRun consecutive
+// elements per round, so the f(i) of a round (often gathers) are in flight
+// together and a block scan covers 4096 elements (shorter lists keep one
+// element per thread: fewer instructions when most threads would idle).
+constexpr unsigned kPrefixRun = 4;
 template <class F>
 __device__ void block_prefix(unsigned n, F f, u64* out, CoreShared& S) {
     u64 carry = 0;
     if (threadIdx.x == 0) out[0] = 0;
-    for (unsigned base = 0; base < n; base += blockDim.x) {
-        const unsigned i = base + threadIdx.x;
+    if (n <= blockDim.x) {
+        const unsigned i = threadIdx.x;
         const u64 v = (i < n) ? f(i) : 0;
         u64 tot;
         const u64 ex = block_excl_scan(v, S, &tot);
-        if (i < n) out[i + 1] = carry + ex + v;
+        if (i < n) out[i + 1] = ex + v;
+        __syncthreads();
+        return;
+    }
+    for (unsigned base = 0; base < n; base += kPrefixRun * blockDim.x) {
+        const unsigned i0 = base + threadIdx.x * kPrefixRun;
+        u64 v[kPrefixRun];
+        u64 sum = 0;
+#pragma unroll
+        for (unsigned u = 0; u < kPrefixRun; ++u) v[u] = (i0 + u < n) ? f(i0 + u) : 0;
+#pragma unroll
+        for (unsigned u = 0; u < kPrefixRun; ++u) sum += v[u];
+        u64 tot;
+        u64 run = carry + block_excl_scan(sum, S, &tot);
+#pragma unroll
+        for (unsigned u = 0; u < kPrefixRun; ++u) {
+            run += v[u];
+            if (i0 + u < n) out[i0 + u + 1] = run;
+        }
         carry += tot;
     }
     __syncthreads();
+}
+
+// Keys src[i] (i < n) with keep(key) appended to buf[*counter ...] (slots at
+// or beyond cap are counted but not written).  Each thread has kGatherLoads
+// loads in flight before using any, and each wave reserves its slots with
+// one LDS atomic.
+constexpr unsigned kGatherLoads = 8;
+template <class Keep>
+__device__ __forceinline__ void gather_keys(const u64* src, unsigned n, Keep keep, u64* buf,
+                                            unsigned cap, unsigned* counter) {
+    if (n <= blockDim.x) {
+        const unsigned i = threadIdx.x;
+        const u64 k = i < n ? src[i] : ~0ull;
+        const bool take = k != ~0ull && keep(k);
+        const unsigned pos = wave_reserve(take, counter);
+        if (take && pos < cap) buf[pos] = k;
+        return;
+    }
+    for (unsigned i0 = 0; i0 < n; i0 += kGatherLoads * blockDim.x) {
+        u64 k[kGatherLoads];
+#pragma unroll
+        for (unsigned u = 0; u < kGatherLoads; ++u) {
+            const unsigned i = i0 + u * blockDim.x + threadIdx.x;
+            k[u] = i < n ? src[i] : ~0ull;
+        }
+#pragma unroll
+        for (unsigned u = 0; u < kGatherLoads; ++u) {
+            const bool take = k[u] != ~0ull && keep(k[u]);
+            const unsigned pos = wave_reserve(take, counter);
+            if (take && pos < cap) buf[pos] = k[u];
+        }
+    }
+}
+
+// buf[0..n) = src[0..n), kGatherLoads loads in flight per thread.
+__device__ __forceinline__ void copy_keys(const u64* src, unsigned n, u64* buf) {
+    if (n <= blockDim.x) {
+        if (threadIdx.x < n) buf[threadIdx.x] = src[threadIdx.x];
+        return;
+    }
+    for (unsigned i0 = 0; i0 < n; i0 += kGatherLoads * blockDim.x) {
+        u64 k[kGatherLoads];
+#pragma unroll
+        for (unsigned u = 0; u < kGatherLoads; ++u) {
+            const unsigned i = i0 + u * blockDim.x + threadIdx.x;
+            if (i < n) k[u] = src[i];
+        }
+#pragma unroll
+        for (unsigned u = 0; u < kGatherLoads; ++u) {
+            const unsigned i = i0 + u * blockDim.x + threadIdx.x;
+            if (i < n) buf[i] = k[u];
+        }
+    }
 }
 
 __device__ __forceinline__ unsigned pow2ceil(unsigned n) {
@@ -299,17 +375,8 @@ __device__ void select_sort(const u64* src, unsigned n_src, u64 kstar, unsigned 
     u64* buf = (npad <= (unsigned)kLdsKeys) ? lds : dst;
     if (threadIdx.x == 0) S.uscal[7] = 0;
     __syncthreads();
-    if (kstar == ~0ull) {
-        for (unsigned i = threadIdx.x; i < n_src; i += blockDim.x) buf[i] = src[i];
-    } else {
-        for (unsigned i = threadIdx.x; i < n_src; i += blockDim.x) {
-            const u64 k = src[i];
-            if (k < kstar) {
-                const unsigned pos = atomicAdd(&S.uscal[7], 1u);
-                if (pos < m) buf[pos] = k;
-            }
-        }
-    }
+    if (kstar == ~0ull) copy_keys(src, n_src, buf);
+    else gather_keys(src, n_src, [&](u64 k) { return k < kstar; }, buf, m, &S.uscal[7]);
     for (unsigned i = m + threadIdx.x; i < npad; i += blockDim.x) buf[i] = ~0ull;
     __syncthreads();
     if (npad <= 1024 * kRegKeys) merge_sort_lds(lds, npad);
@@ -520,13 +587,9 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         // candidates up to the crossing bucket into LDS (count them on the way)
         if (tid == 0) S.uscal[7] = 0;
         __syncthreads();
-        for (unsigned i = tid; i < nC; i += blockDim.x) {
-            const u64 k = A.listC[i];
-            if (dist_bucket((unsigned)(k >> A.idbits)) <= bstar) {
-                const unsigned pos = atomicAdd(&S.uscal[7], 1u);
-                if (pos < (unsigned)kLdsKeys) lds[pos] = k;
-            }
-        }
+        const unsigned idb = A.idbits;
+        gather_keys(A.listC, nC, [&](u64 k) { return dist_bucket((unsigned)(k >> idb)) <= bstar; },
+                    lds, (unsigned)kLdsKeys, &S.uscal[7]);
         __syncthreads();
         const unsigned mprime = S.uscal[7];
         if (bstar < kDistBuckets && mprime > 0 && mprime <= (unsigned)kLdsKeys) {
@@ -539,12 +602,24 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
             u64 carry = 0;
             if (tid == 0) S.uscal[4] = mprime;
             __syncthreads();
-            for (unsigned b0 = 0; b0 < mprime; b0 += blockDim.x) {
-                const unsigned i = b0 + tid;
-                const u64 w = i < mprime ? (u64)units[lds[i] & idmask] : 0;
+            const unsigned run_len = mprime <= blockDim.x ? 1 : kPrefixRun;
+            for (unsigned b0 = 0; b0 < mprime; b0 += run_len * blockDim.x) {
+                const unsigned i0 = b0 + tid * run_len;
+                u64 w[kPrefixRun];
+                u64 sum = 0;
+#pragma unroll
+                for (unsigned u = 0; u < kPrefixRun; ++u)
+                    w[u] = u < run_len && i0 + u < mprime ? (u64)units[lds[i0 + u] & idmask] : 0;
+#pragma unroll
+                for (unsigned u = 0; u < kPrefixRun; ++u) sum += w[u];
                 u64 tot;
-                const u64 ex = block_excl_scan(w, S, &tot);
-                if (i < mprime && carry + ex <= cap && carry + ex + w > cap) S.uscal[4] = i;
+                u64 run = carry + block_excl_scan(sum, S, &tot);   // units before i0
+#pragma unroll
+                for (unsigned u = 0; u < kPrefixRun; ++u) {
+                    if (u < run_len && i0 + u < mprime && run <= cap && run + w[u] > cap)
+                        S.uscal[4] = i0 + u;
+                    run += w[u];
+                }
                 carry += tot;
             }
             __syncthreads();
