@@ -501,23 +501,37 @@ __device__ __forceinline__ unsigned dist2(short2_t a, short2_t b) {
 __global__ void __launch_bounds__(kPairThreads) k_pair_min(const int* __restrict__ pos,
                                                            unsigned n, unsigned slice,
                                                            unsigned* __restrict__ d2min) {
-    __shared__ short2_t s_p[kPairTile];
+    __shared__ __attribute__((aligned(16))) short2_t s_p[kPairTile];
     const unsigned i = blockIdx.x * kPairThreads + threadIdx.x;
     const unsigned j_lo = blockIdx.y * slice, j_hi = min(j_lo + slice, n);
     short2_t pi = {0, 0};
     if (i < n) pi = short2_t{(short)pos[2 * i], (short)pos[2 * i + 1]};
     unsigned best = kNone;
+    // the next tile's position is loaded while the current tile is compared
+    int2 nxt = make_int2(0, 0);
+    if (j_lo + threadIdx.x < j_hi)
+        nxt = make_int2(pos[2 * (j_lo + threadIdx.x)], pos[2 * (j_lo + threadIdx.x) + 1]);
     for (unsigned j0 = j_lo; j0 < j_hi; j0 += kPairTile) {
         const unsigned j = j0 + threadIdx.x;
-        if (j < j_hi) s_p[threadIdx.x] = short2_t{(short)pos[2 * j], (short)pos[2 * j + 1]};
+        if (j < j_hi) s_p[threadIdx.x] = short2_t{(short)nxt.x, (short)nxt.y};
         __syncthreads();
+        if (j + kPairTile < j_hi) nxt = make_int2(pos[2 * (j + kPairTile)], pos[2 * (j + kPairTile) + 1]);
         const unsigned cnt = min((unsigned)kPairTile, j_hi - j0);
         if (i - j0 < cnt) {                  // this tile holds i itself: skip the self pair
             for (unsigned k = 0; k < cnt; ++k)
                 if (j0 + k != i) best = min(best, dist2(pi, s_p[k]));
         } else if (cnt == kPairTile) {
-#pragma unroll 32
-            for (unsigned k = 0; k < kPairTile; ++k) best = min(best, dist2(pi, s_p[k]));
+            // four positions per 16-byte LDS read (a broadcast: every lane reads
+            // the same address), so the LDS issues a quarter of the reads
+            const uint4* q = reinterpret_cast<const uint4*>(s_p);
+#pragma unroll 8
+            for (unsigned k = 0; k < kPairTile / 4; ++k) {
+                const uint4 v = q[k];
+                best = min(best, dist2(pi, __builtin_bit_cast(short2_t, v.x)));
+                best = min(best, dist2(pi, __builtin_bit_cast(short2_t, v.y)));
+                best = min(best, dist2(pi, __builtin_bit_cast(short2_t, v.z)));
+                best = min(best, dist2(pi, __builtin_bit_cast(short2_t, v.w)));
+            }
         } else {
             for (unsigned k = 0; k < cnt; ++k) best = min(best, dist2(pi, s_p[k]));
         }
