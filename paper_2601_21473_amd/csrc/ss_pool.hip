@@ -910,7 +910,8 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
         if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_in), true);
     }
     size_t li = 0, ri = 0;
-    for (u64 k = 0; k < nslots; ++k) {
+    // host-to-device copies of slot k into the ring
+    auto issue_h2d = [&](u64 k) -> ss_status {
         const u64 q0 = k * ups, q1 = std::min(total, q0 + ups);
         char* slot = p->stage_in + (k % p->ring) * p->slot_bytes;
         TimedPair* tp = nullptr;
@@ -929,6 +930,12 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
                                       p->st_in), true);
         }
         if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_in), true);
+        return SS_OK;
+    };
+    // unpack of slot k
+    auto issue_unpack = [&](u64 k) -> ss_status {
+        const u64 q0 = k * ups, q1 = std::min(total, q0 + ups);
+        char* slot = p->stage_in + (k % p->ring) * p->slot_bytes;
         // units released by victims are overwritten only after the pack read
         // them: released positions [r0, r1) of this slot; the last written-back
         // victim overlapping them gives the last pack slot to wait for
@@ -938,13 +945,19 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
             const long long j = p->res.n_victims ? p->last_written[ri] : -1;
             if (j >= 0 && p->voff[j + 1] > r0) {
                 const u64 maxpos = p->woff[j] + std::min(r1, p->voff[j + 1]) - p->voff[j] - 1;
-                const u64 slot = p->direct_out ? 0 : maxpos / ups;   // a direct pack is one launch
-                TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_packed[slot], 0), true);
+                const u64 ps = p->direct_out ? 0 : maxpos / ups;     // a direct pack is one launch
+                TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_packed[ps], 0), true);
             }
         }
+        // the pack of slot k + 1 becomes ready (its ring slot's device-to-host
+        // copy done) about when this slot's host-to-device copy lands: let it
+        // finish first, so the two HBM-bound kernels do not share HBM
+        if (!p->direct_out && k + 1 < p->n_pack_step)
+            TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_packed[k + 1], 0), true);
         C.first = q0;
         C.count = q1 - q0;
         C.staging = slot;
+        TimedPair* tp = nullptr;
         if (timing) {
             TRY_HIP(p, timed_pair(p->t_unpack, p->n_t_unpack++, &tp), true);
             tp->bytes = (q1 - q0) * p->unit_bytes;
@@ -952,6 +965,25 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
         }
         TRY_HIP(p, launch_unpack(C, p->st_in), true);
         if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_in), true);
+        return SS_OK;
+    };
+    // With two or more ring slots the copy of slot k + 1 is queued before the
+    // unpack of slot k, so the copy engine never waits for an unpack (stream
+    // order still refills a slot only after the unpack that read it, ring
+    // slots earlier).  With one slot they alternate.
+    for (u64 k = 0; k < nslots; ++k) {
+        if (p->ring >= 2) {
+            st = issue_h2d(k);
+            if (!st && k >= 1) st = issue_unpack(k - 1);
+        } else {
+            st = issue_h2d(k);
+            if (!st) st = issue_unpack(k);
+        }
+        if (st) return st;
+    }
+    if (p->ring >= 2 && nslots) {
+        st = issue_unpack(nslots - 1);
+        if (st) return st;
     }
     TRY_HIP(p, hipEventRecord(p->ev_in_done, p->st_in), true);
     TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_in_done, 0), true);
