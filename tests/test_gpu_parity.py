@@ -79,6 +79,22 @@ def test_direct_and_staged_mixed(name, n_agents, steps, pool_index, limit_units)
     assert st["pack_launches"] > 0 and st["unpack_launches"] > 0
 
 
+@pytest.mark.parametrize("case", range(6))
+def test_random_pipeline_shapes(case):
+    """Seeded random ring sizes, slot sizes and direct-transfer limits on a
+    variable-size workload: every ordering of copies, packs and unpacks the
+    pipeline can produce (ring reuse, the release hazard, the wait for the
+    next pack, direct and staged directions mixed) against the oracle."""
+    rng = np.random.default_rng(1000 + case)
+    tr = W.subsample_agents(W.make_trace("bursty", case % 3), 120)
+    tr = W.shrink_planes(tr, lambda p: [32, 16])
+    ring = int(rng.choice([1, 2, 3, 5]))
+    slot_units = int(rng.integers(1, 40))
+    direct = int(rng.choice([0, 0, 8, 64])) * tr.pools[0].unit_bytes
+    run_parity(tr, theta=S, steps=60, slot_units=slot_units, ring_slots=ring, direct_bytes=direct,
+               label=f"random shape {case}: ring {ring}, slot {slot_units}u, direct {direct}B")
+
+
 @pytest.mark.parametrize("name,pool_index", [("roundrobin", 0), ("bursty", 0), ("zipf_lora", 0),
                                              ("zipf_lora", 1), ("diffusion", 0)])
 def test_workload_full_counts(name, pool_index):
