@@ -160,7 +160,7 @@ def parse():
     ap.add_argument("--direct-mib", type=float, default=4,
                     help="directions of a step that move at most this many MiB go by kernel "
                          "straight between units and host copies (0 = always staged)")
-    ap.add_argument("--cpu-steps", type=int, default=2)
+    ap.add_argument("--cpu-steps", type=int, default=8)
     ap.add_argument("--cpu-agents", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true")
@@ -452,12 +452,17 @@ def loader_bench(args, binding, W, spec0, PoolMemory, DeviceBuffer, probe):
     return out
 
 
+CPU_POOL_WINDOW = 1024            # units of the oracle's byte pool in the CPU baseline
+
+
 def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
     """The CPU oracle on a bounded sample: the oracle plan for every agent on
     steps [warmup, warmup + n_steps) (after replaying the earlier steps'
     plans), and the oracle's numpy gather/scatter of the bytes of the first
-    ``n_agents_moved`` victims and loads of each sampled step through warm
-    buffers."""
+    ``n_agents_moved`` written-back victims and loads of each sampled step
+    through warm buffers.  The moved units' rows are taken modulo a window of
+    CPU_POOL_WINDOW units of the oracle's byte pool (same row-gather pattern,
+    memory bounded to the window)."""
     from types import SimpleNamespace
     from oracle import OraclePool, BytePool, apply_step_bytes
     spec = trace.pools[0]
@@ -465,7 +470,10 @@ def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
     opool = OraclePool(spec.capacity_units, spec.agent_units, ub)
     for t in range(warmup):
         opool.plan_step(trace.dist[t], trace.active[t], threshold, budget)
-    bp = BytePool(spec.capacity_units, spec.chunk_bytes)
+    window = min(spec.capacity_units, CPU_POOL_WINDOW)
+    bp = BytePool(window, spec.chunk_bytes)
+    for plane in bp.planes:
+        plane[:] = 1                                  # pages resident before timing
     s = spec.agent_units.astype(np.int64)
     max_agent = int(s.max()) * ub
     stage_out = np.ones(n_agents_moved * max_agent, dtype=np.uint8)
@@ -481,13 +489,11 @@ def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
         Ld = plan.loads[:n_agents_moved]
         nvu = int(s[V].sum())
         nlu = int(s[Ld].sum())
-        sub = SimpleNamespace(victims=V, written=V, loads=Ld, victim_units=plan.written_units[:nvu],
-                              written_units=plan.written_units[:nvu],
-                              load_units=plan.load_units[:nlu])
+        sub = SimpleNamespace(victims=V, written=V, loads=Ld,
+                              victim_units=plan.written_units[:nvu] % window,
+                              written_units=plan.written_units[:nvu] % window,
+                              load_units=plan.load_units[:nlu] % window)
         slot = {int(a): i for i, a in enumerate(list(V) + list(Ld))}
-        for u in np.concatenate([sub.victim_units, sub.load_units]):   # warm the pages
-            for c, plane in enumerate(bp.planes):
-                plane[u] = 1
         t0 = time.perf_counter()
         apply_step_bytes(bp, sub, s, lambda a: host[slot[a]][:s[a] * ub],
                          lambda a, b: host[slot[a]][:len(b)].__setitem__(slice(None), b),
@@ -498,8 +504,9 @@ def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
             "kind": "oracle",
             "sample": f"steps {warmup}-{warmup + n_steps - 1} of the {trace.name} trace: oracle plan "
                       f"of all {trace.n_agents} agents per step ({1e3 * t_plan / n_steps:.2f} ms/step) "
-                      f"+ numpy gather/scatter of the first {n_agents_moved} victims' and loads' "
-                      f"bytes ({moved / 1e9:.2f} GB in {t_move:.2f} s), single thread",
+                      f"+ numpy gather/scatter of the first {n_agents_moved} written-back victims' "
+                      f"and loads' bytes ({moved / 1e9:.2f} GB in {t_move:.2f} s; unit rows taken "
+                      f"modulo a {window}-unit window of the byte pool), single thread",
             "host_threads_available": len(os.sched_getaffinity(0))}
 
 
@@ -574,8 +581,18 @@ def main():
             p.prefetch_unpack(stream)
         return plans
 
+    # the first steps fill the empty pool: timed apart from the steady state
+    fill_steps = min(10, args.warmup)
+    fill_b = 0
+    sync()
+    tf = time.perf_counter()
     for t in range(args.warmup):
-        step(t)
+        plans = step(t)
+        if t < fill_steps:
+            fill_b += sum(pl["bytes_out"] + pl["bytes_in"] for pl in plans)
+        if t == fill_steps - 1:
+            sync()
+            fill_wall = time.perf_counter() - tf
     sync()
     for p in pools:
         p.reset_stats()
@@ -703,7 +720,11 @@ def main():
             for i in range(3)]
     phases = [(sum(s["plan_phase_us"][i] for s in plan_stats) -
                sum(s["plan_phase_us"][i] for s in stats)) / nps for i in range(7)]
+    floor_us = binding.probe_launch(100)
     plan = {"median": float(np.median(lat_us)), "p99": float(np.percentile(lat_us, 99)),
+            "floor_us": floor_us,
+            "floor": "one empty kernel launch, event record and wait (the plan is one launch "
+                     "per pool; its lists come back through mapped host memory)",
             "c_call_median": float(np.median(lat_c)), "c_call_p99": float(np.percentile(lat_c, 99)),
             "core_phases_us": dict(zip(("classify", "demand_and_evictable_sorts",
                                         "candidate_select", "candidate_sort", "acceptance",
@@ -745,6 +766,9 @@ def main():
         "object_distances": objects,
         "estimators": estimators,
         "probe": probe,
+        "fill": ({"steps": fill_steps, "GBps": fill_b / fill_wall / 1e9,
+                  "ms_per_step": 1e3 * fill_wall / fill_steps,
+                  "note": "first steps on the empty pool (not in value)"} if fill_steps else None),
         "step_wall_ms": {"median": 1e3 * float(np.median(step_wall)),
                          "max": 1e3 * float(np.max(step_wall))},
     }

@@ -227,6 +227,12 @@ ss_status ss_reset_stats(ss_pool* pool);
  * to dev[0, bytes) and dev[bytes, 2 bytes) to host[bytes, 2 bytes), so both
  * buffers must hold 2 * bytes; the time is for the pair. */
 ss_status ss_probe_copy(void* dst, const void* src, uint64_t bytes, int iters, float* ms_per_iter);
+/* Host round trip of one empty kernel launch on the current device: launch,
+ * event record, wait for the event; *us_median = the median over `iters`
+ * (>= 1) round trips, in microseconds.  A one-launch plan cannot return
+ * faster than this (the plan's lists come back through mapped host memory,
+ * without a copy). */
+ss_status ss_probe_launch(int iters, float* us_median);
 ss_status ss_probe_link(void* host, void* dev, uint64_t bytes, int dir, int iters,
                         float* ms_per_iter);
 

@@ -27,7 +27,8 @@ SS_FLAG_TIMING = 1
 
 EXPORTS = ["ss_pool_create", "ss_pool_destroy", "ss_plan_step", "ss_evict_pack",
            "ss_prefetch_unpack", "ss_block_table", "ss_block_table_host", "ss_block_table_host_all", "ss_resident_host",
-           "ss_get_stats", "ss_reset_stats", "ss_probe_copy", "ss_probe_link", "ss_sync",
+           "ss_get_stats", "ss_reset_stats", "ss_probe_copy", "ss_probe_launch", "ss_probe_link",
+           "ss_sync",
            "ss_device_count", "ss_device_alloc", "ss_host_alloc", "ss_device_free", "ss_host_free",
            "ss_copy", "ss_last_error", "ss_object_distances_workspace", "ss_object_distances",
            "ss_probe_object_distances", "ss_hop_distances_workspace", "ss_hop_distances",
@@ -124,6 +125,7 @@ def load():
         "ss_get_stats": ([P, C.POINTER(ss_stats)], C.c_int32),
         "ss_reset_stats": ([P], C.c_int32),
         "ss_probe_copy": ([P, P, C.c_uint64, C.c_int, C.POINTER(C.c_float)], C.c_int32),
+        "ss_probe_launch": ([C.c_int, C.POINTER(C.c_float)], C.c_int32),
         "ss_probe_link": ([P, P, C.c_uint64, C.c_int, C.c_int, C.POINTER(C.c_float)], C.c_int32),
         "ss_sync": ([P], C.c_int32),
         "ss_device_count": ([C.POINTER(C.c_int32)], C.c_int32),
@@ -358,6 +360,13 @@ def probe_copy(dst: int, src: int, nbytes: int, iters: int = 10) -> float:
     ms = C.c_float()
     _check(load().ss_probe_copy(int(dst), int(src), int(nbytes), int(iters), C.byref(ms)))
     return ms.value
+
+
+def probe_launch(iters: int = 50) -> float:
+    """Median host round trip (us) of one empty kernel launch and its wait."""
+    us = C.c_float()
+    _check(load().ss_probe_launch(int(iters), C.byref(us)))
+    return us.value
 
 
 def probe_link(host: int, dev: int, nbytes: int, direction: int, iters: int = 5) -> float:

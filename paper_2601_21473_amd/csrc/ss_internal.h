@@ -153,6 +153,7 @@ hipError_t launch_pack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_unpack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_zero_u32(unsigned* p, u64 n, hipStream_t st);
 hipError_t launch_probe_copy(void* dst, const void* src, u64 bytes, hipStream_t st);
+hipError_t launch_nop(hipStream_t st);
 
 // Host helpers defined in ss_pool.hip.
 ss_status set_err(ss_status st, const char* fmt, ...);       // sets ss_last_error

@@ -993,6 +993,8 @@ __global__ void __launch_bounds__(kCopyThreads) k_probe_copy(char* dst, const ch
     wave_copy(dst + off, src + off, rem < kItemBytes ? (unsigned)rem : kItemBytes);
 }
 
+__global__ void k_nop() {}
+
 __global__ void k_zero_u32(unsigned* p, u64 n) {
     for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x)
         p[i] = 0;
@@ -1041,6 +1043,11 @@ hipError_t launch_zero_u32(unsigned* p, u64 n, hipStream_t st) {
     u64 blocks = (n + 255) / 256;
     if (blocks > 4096) blocks = 4096;
     hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)blocks), dim3(256), 0, st, p, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_nop(hipStream_t st) {
+    hipLaunchKernelGGL(k_nop, dim3(1), dim3(64), 0, st);
     return hipGetLastError();
 }
 

@@ -1211,6 +1211,31 @@ ss_status ss_probe_copy(void* dst, const void* src, uint64_t bytes, int iters, f
     return SS_OK;
 }
 
+ss_status ss_probe_launch(int iters, float* us) {
+    if (!us || iters < 1) return set_err(SS_ERR_ARG, "bad probe arguments");
+    hipEvent_t ev;
+    hipStream_t s;
+    TRY_HIP(nullptr, make_event(&ev, false), false);
+    TRY_HIP(nullptr, hipStreamCreateWithFlags(&s, hipStreamNonBlocking), false);
+    std::vector<float> t;
+    hipError_t e = launch_nop(s);                                        // warm-up
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    for (int i = 0; i < iters && e == hipSuccess; ++i) {
+        const auto t0 = std::chrono::steady_clock::now();
+        e = launch_nop(s);
+        if (e == hipSuccess) e = hipEventRecord(ev, s);
+        if (e == hipSuccess) e = hipEventSynchronize(ev);
+        t.push_back(std::chrono::duration<float, std::micro>(std::chrono::steady_clock::now() - t0)
+                        .count());
+    }
+    (void)hipStreamDestroy(s);
+    (void)hipEventDestroy(ev);
+    if (e != hipSuccess) return hip_fail(nullptr, e, "probe launch", false);
+    std::sort(t.begin(), t.end());
+    *us = t[t.size() / 2];
+    return SS_OK;
+}
+
 ss_status ss_probe_link(void* host, void* dev, uint64_t bytes, int dir, int iters, float* ms) {
     if (!host || !dev || !ms || iters < 1 || bytes == 0 || dir < 0 || dir > 2)
         return set_err(SS_ERR_ARG, "bad probe arguments");
