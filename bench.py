@@ -160,8 +160,10 @@ def parse():
     ap.add_argument("--direct-mib", type=float, default=4,
                     help="directions of a step that move at most this many MiB go by kernel "
                          "straight between units and host copies (0 = always staged)")
-    ap.add_argument("--cpu-steps", type=int, default=8)
-    ap.add_argument("--cpu-agents", type=int, default=8)
+    ap.add_argument("--cpu-steps", type=int, default=4)
+    ap.add_argument("--cpu-agents", type=int, default=16)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="sample steps until the CPU oracle's timed work reaches this")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probe", action="store_true")
     ap.add_argument("--clean-evict", action="store_true",
@@ -455,12 +457,13 @@ def loader_bench(args, binding, W, spec0, PoolMemory, DeviceBuffer, probe):
 CPU_POOL_WINDOW = 1024            # units of the oracle's byte pool in the CPU baseline
 
 
-def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
+def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget, min_seconds=0.0):
     """The CPU oracle on a bounded sample: the oracle plan for every agent on
     steps [warmup, warmup + n_steps) (after replaying the earlier steps'
     plans), and the oracle's numpy gather/scatter of the bytes of the first
     ``n_agents_moved`` written-back victims and loads of each sampled step
-    through warm buffers.  The moved units' rows are taken modulo a window of
+    through warm buffers.  Sampling goes on past ``n_steps`` steps until the
+    timed work reaches ``min_seconds`` or the trace ends.  The moved units' rows are taken modulo a window of
     CPU_POOL_WINDOW units of the oracle's byte pool (same row-gather pattern,
     memory bounded to the window)."""
     from types import SimpleNamespace
@@ -478,10 +481,12 @@ def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
     max_agent = int(s.max()) * ub
     stage_out = np.ones(n_agents_moved * max_agent, dtype=np.uint8)
     stage_in = np.ones(n_agents_moved * max_agent, dtype=np.uint8)
-    host = [np.ones(max_agent, dtype=np.uint8) for _ in range(2 * n_agents_moved)]
+    host_out = np.ones(max_agent, dtype=np.uint8)     # one host copy written by every victim
+    host_in = np.ones(max_agent, dtype=np.uint8)      # one host copy read by every load
     t_plan = t_move = 0.0
     moved = 0
-    for t in range(warmup, warmup + n_steps):
+    t = warmup
+    while t < len(trace.dist) and (t < warmup + n_steps or t_plan + t_move < min_seconds):
         t0 = time.perf_counter()
         plan = opool.plan_step(trace.dist[t], trace.active[t], threshold, budget)
         t_plan += time.perf_counter() - t0
@@ -493,16 +498,17 @@ def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget):
                               victim_units=plan.written_units[:nvu] % window,
                               written_units=plan.written_units[:nvu] % window,
                               load_units=plan.load_units[:nlu] % window)
-        slot = {int(a): i for i, a in enumerate(list(V) + list(Ld))}
         t0 = time.perf_counter()
-        apply_step_bytes(bp, sub, s, lambda a: host[slot[a]][:s[a] * ub],
-                         lambda a, b: host[slot[a]][:len(b)].__setitem__(slice(None), b),
+        apply_step_bytes(bp, sub, s, lambda a: host_in[:s[a] * ub],
+                         lambda a, b: host_out[:len(b)].__setitem__(slice(None), b),
                          staging_out=stage_out, staging_in=stage_in)
         t_move += time.perf_counter() - t0
         moved += (nvu + nlu) * ub
+        t += 1
+    n_steps = t - warmup
     return {"value": moved / (t_plan + t_move) / 1e9, "unit": "GB/s", "cores": 1,
             "kind": "oracle",
-            "sample": f"steps {warmup}-{warmup + n_steps - 1} of the {trace.name} trace: oracle plan "
+            "sample": f"steps {warmup}-{t - 1} of the {trace.name} trace: oracle plan "
                       f"of all {trace.n_agents} agents per step ({1e3 * t_plan / n_steps:.2f} ms/step) "
                       f"+ numpy gather/scatter of the first {n_agents_moved} written-back victims' "
                       f"and loads' bytes ({moved / 1e9:.2f} GB in {t_move:.2f} s; unit rows taken "
@@ -741,7 +747,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(trace, args.warmup, args.cpu_steps, args.cpu_agents, thr, budget)
+        cpu = cpu_baseline(trace, args.warmup, args.cpu_steps, args.cpu_agents, thr, budget,
+                           args.cpu_seconds)
 
     rec = {
         "metric": "evict+prefetch GB/s per step (HBM and host-link % of peak); plan latency us/step",
