@@ -157,6 +157,9 @@ def parse():
     ap.add_argument("--host-copies", type=int, default=128,
                     help="distinct host copies shared round-robin by agents; 0 = one per agent")
     ap.add_argument("--plan-steps", type=int, default=20)
+    ap.add_argument("--null-stream", action="store_true",
+                    help="queue the plan and the step on the null stream instead of a stream "
+                         "of the caller's own")
     ap.add_argument("--direct-mib", type=float, default=4,
                     help="directions of a step that move at most this many MiB go by kernel "
                          "straight between units and host copies (0 = always staged)")
@@ -568,7 +571,11 @@ def main():
     dist, act = DeviceBuffer(d_np.nbytes), DeviceBuffer(a_np.nbytes)
     dist.upload(d_np)
     act.upload(a_np)
-    stream = 0
+    # the caller's stream: a non-blocking stream of its own, as a serving loop
+    # would use (--null-stream: the null stream, which adds the runtime's
+    # cross-stream synchronization to every call queued on it)
+    cstream = None if args.null_stream else binding.Stream()
+    stream = 0 if cstream is None else cstream.handle
     clean = DeviceBuffer(N) if args.clean_evict else None
     if clean is not None:
         clean.upload(np.zeros(N, dtype=np.uint8))
@@ -651,6 +658,8 @@ def main():
     for m in mems:
         m.free()
     dist.free()
+    if cstream is not None:
+        cstream.close()
     act.free()
     if clean is not None:
         clean.free()
@@ -760,6 +769,7 @@ def main():
                    "staging_bytes": args.staging_mib << 20, "ring_slots": args.ring,
                    "write_back": "none (clean evictions)" if args.clean_evict else "every eviction",
                    "direct_limit_bytes": int(args.direct_mib * (1 << 20)),
+                   "caller_stream": "null stream" if args.null_stream else "own non-blocking stream",
                    "host_copies": ("one per agent" if args.host_copies == 0 else
                                    f"{args.host_copies} shared round-robin"),
                    "bytes_out": out_b, "bytes_in": in_b},

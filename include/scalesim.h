@@ -140,9 +140,11 @@ typedef struct {                    /* cumulative since create or ss_reset_stats
     uint64_t d2h_bytes, h2d_bytes;
     double   d2h_ms, h2d_ms;               /* per step: first to last copy on its stream */
     double   plan_gpu_ms;                  /* event time of the plan kernels             */
-    double   plan_phase_us[7];             /* plan-core phases (classify, demand and
-                                              evictable sorts, candidate select, candidate
-                                              sort, acceptance, lists, free units)          */
+    double   plan_phase_us[7];             /* plan phases (classify, demand and evictable
+                                              sorts, candidate select, candidate sort,
+                                              acceptance, lists, free units); classify runs
+                                              from the plan kernel's entry (its first
+                                              workgroup when N > 4096)                      */
     double   plan_host_us[3];              /* ss_plan_step on the host: queueing the plan,
                                               waiting for it, reading it back              */
     uint64_t direct_out_launches, direct_in_launches;  /* directions moved by direct_bytes */

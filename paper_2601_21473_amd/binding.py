@@ -430,6 +430,27 @@ def interaction_distances(pos_xy: int, d_action: int, n_agents: int, velocity: i
                                            int(workspace_bytes), int(stream)))
 
 
+class Stream:
+    """A non-blocking HIP stream at the default priority (``handle`` is the
+    hipStream_t to pass as a call's ``stream``)."""
+
+    def __init__(self):
+        self.stream = C.c_void_p()
+        _check(load().ss_stream_create(C.byref(self.stream)))
+
+    @property
+    def handle(self) -> int:
+        return self.stream.value or 0
+
+    def sync(self):
+        _check(load().ss_stream_sync(self.stream))
+
+    def close(self):
+        if self.stream.value:
+            load().ss_stream_destroy(self.stream)
+            self.stream = C.c_void_p()
+
+
 class EventTimer:
     """Event time of work queued on one library stream:
     ``with EventTimer() as t: f(t.stream)`` then ``t.ms``."""

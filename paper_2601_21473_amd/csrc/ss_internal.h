@@ -83,6 +83,9 @@ struct PlanArgs {
     unsigned char* vwritten_host;   // mapped pinned host [N]
     u64* woff;                      // [N+1] prefix units over written-back victims
     unsigned* done;                 // workgroups of k_classify_core finished (0 between steps)
+    unsigned* flag_host;            // mapped pinned host word: `seq` is written there last
+    unsigned seq;                   // this plan's sequence number (never 0)
+    unsigned pad3;
 };
 
 // Candidate distance histogram: bucket(d) = d below 1024, then 32 buckets per
@@ -148,7 +151,7 @@ constexpr int kLdsKeys = 16384;                   // 128 KiB of u64 keys in LDS
 // itself), or classification over many workgroups whose last one runs the core.
 hipError_t launch_plan(const PlanArgs& a, hipStream_t st);
 hipError_t launch_bt_update(const BtArgs& a, unsigned n_agents, hipStream_t st);
-constexpr unsigned kFuseAgents = 4096;            // plan core classifies up to this many
+constexpr unsigned kFuseAgents = 12288;           // plan core classifies up to this many
 hipError_t launch_pack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_unpack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_zero_u32(unsigned* p, u64 n, hipStream_t st);

@@ -56,55 +56,59 @@ __device__ __forceinline__ u64 wave_incl_scan(u64 v) {
 // classification
 // ---------------------------------------------------------------------------
 
-// Append `key` of every lane with `pred` to list[*counter ...]; one atomic per
-// wave, lane order inside the wave (the order between waves is arbitrary and
-// is removed by the sort that follows).
-__device__ __forceinline__ void wave_append(bool pred, u64 key, u64* list, unsigned* counter) {
-    const u64 mask = __ballot(pred);
-    if (mask == 0) return;                           // wave-uniform
-    unsigned base = 0;
-    if (lane_id() == 0) base = atomicAdd(counter, (unsigned)__popcll(mask));
-    base = __shfl(base, 0);
-    if (pred) list[base + mbcnt(mask)] = key;
+// Agents classified per thread and pass: the loads of all of them are issued
+// before any is used, so each thread has that many agents' reads in flight.
+constexpr unsigned kClassBatch = 4;
+
+// The inputs of agents first + u * blockDim.x (u < kClassBatch) below end.
+struct AgentBatch {
+    unsigned D[kClassBatch], s[kClassBatch];
+    unsigned char act[kClassBatch], res[kClassBatch];
+};
+
+__device__ __forceinline__ void load_agents(const PlanArgs& A, unsigned first, unsigned end,
+                                            AgentBatch& b) {
+#pragma unroll
+    for (unsigned u = 0; u < kClassBatch; ++u) {
+        const unsigned a = first + u * blockDim.x;
+        const bool v = a < end;
+        b.D[u] = v ? A.dist[a] : 0u;
+        b.act[u] = v ? A.active[a] : (unsigned char)0;
+        b.res[u] = v ? A.resident[a] : (unsigned char)0;
+        b.s[u] = v ? A.units[a] : 0u;
+    }
 }
 
-// Classify agent a (a >= n: no agent) and add it to the lists and sums kept
-// in `cnt` (global memory for the multi-block kernel, LDS in the fused plan
-// core).  Every lane of the wave must call it.
-__device__ __forceinline__ void classify_agent(const PlanArgs& A, unsigned a, PlanCounters* cnt,
-                                               u64* hist) {
-    const bool valid = a < A.n;
-    unsigned D = 0;
-    bool act = false, res = false;
-    u64 s = 0;
-    if (valid) {
-        D = A.dist[a];
-        act = A.active[a] != 0;
-        res = A.resident[a] != 0;
-        s = A.units[a];
-    }
-    const u64 d = act ? 0ull : (u64)D;               // active agents: distance 0
-    const u64 key = (d << A.idbits) | a;
-    const bool isE = valid && res && !act;            // evictable resident
-    const bool isL = valid && act && !res;            // demand load
-    const bool isC = valid && !res && !act && D < A.threshold;   // prefetch candidate
-    if (isC) atomicAdd(&hist[dist_bucket(D)], s);
-    wave_append(isE, key, A.listE, &cnt->n_E);
-    wave_append(isL, key, A.listL, &cnt->n_L);
-    wave_append(isC, key, A.listC, &cnt->n_C);
-    const u64 s_act = wave_sum(act ? s : 0);
-    const u64 s_res = wave_sum(res ? s : 0);
-    const u64 s_dem = wave_sum(isL ? s : 0);
-    const u64 s_evi = wave_sum(isE ? s : 0);
-    const u64 s_can = wave_sum(isC ? s : 0);
-    if (lane_id() == 0) {
-        if (s_act) atomicAdd(&cnt->sum_active, s_act);
-        if (s_res) atomicAdd(&cnt->sum_resident, s_res);
-        if (s_dem) atomicAdd(&cnt->sum_demand, s_dem);
-        if (s_evi) atomicAdd(&cnt->sum_evictable, s_evi);
-        if (s_can) atomicAdd(&cnt->sum_cand, s_can);
-    }
+// Class of agent a: its key (distance 0 when active, then the id) and its
+// membership of the evictable residents E, the demand loads L and the
+// prefetch candidates C (distance below the threshold).
+struct AgentClass {
+    u64 key;
+    bool isE, isL, isC;
+};
+
+__device__ __forceinline__ AgentClass classify(const PlanArgs& A, unsigned a, bool valid,
+                                               unsigned D, bool act, bool res) {
+    AgentClass c;
+    const u64 d = act ? 0ull : (u64)D;
+    c.key = (d << A.idbits) | a;
+    c.isE = valid && res && !act;
+    c.isL = valid && act && !res;
+    c.isC = valid && !res && !act && D < A.threshold;
+    return c;
 }
+
+// Per-thread unit sums of the classes, added to the block's counters once.
+struct ClassSums {
+    u64 act = 0, res = 0, dem = 0, evi = 0, can = 0;
+    __device__ void add(const AgentClass& c, bool act_, bool res_, u64 s) {
+        act += act_ ? s : 0;
+        res += res_ ? s : 0;
+        dem += c.isL ? s : 0;
+        evi += c.isE ? s : 0;
+        can += c.isC ? s : 0;
+    }
+};
 
 // Block-local slot of this lane in a list (one LDS atomic per wave).
 __device__ __forceinline__ unsigned wave_reserve(bool pred, unsigned* counter) {
@@ -113,6 +117,23 @@ __device__ __forceinline__ unsigned wave_reserve(bool pred, unsigned* counter) {
     unsigned base = 0;
     if (lane_id() == 0) base = atomicAdd(counter, (unsigned)__popcll(mask));
     return __shfl(base, 0) + mbcnt(mask);
+}
+
+// Add every thread's sums to the block counters *cnt (LDS): one reduction per
+// wave and sum, one LDS atomic per wave.
+__device__ __forceinline__ void flush_sums(const ClassSums& t, PlanCounters* cnt) {
+    const u64 s_act = wave_sum(t.act);
+    const u64 s_res = wave_sum(t.res);
+    const u64 s_dem = wave_sum(t.dem);
+    const u64 s_evi = wave_sum(t.evi);
+    const u64 s_can = wave_sum(t.can);
+    if (lane_id() == 0) {
+        if (s_act) atomicAdd(&cnt->sum_active, s_act);
+        if (s_res) atomicAdd(&cnt->sum_resident, s_res);
+        if (s_dem) atomicAdd(&cnt->sum_demand, s_dem);
+        if (s_evi) atomicAdd(&cnt->sum_evictable, s_evi);
+        if (s_can) atomicAdd(&cnt->sum_cand, s_can);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -492,6 +513,45 @@ __device__ u64 weighted_select(const u64* keys, unsigned n, const unsigned* unit
 // k_plan_core
 // ---------------------------------------------------------------------------
 
+// Classification of all agents by the plan core's workgroup: candidate units
+// into the LDS histogram, counts and sums into S.cnt, list entries at their
+// final slots (lane order inside a wave; the order between waves is arbitrary
+// and is removed by the sorts that follow).
+__device__ __forceinline__ void classify_fused(const PlanArgs& A, CoreShared& S) {
+    ClassSums t;
+    for (unsigned base = 0; base < A.n; base += kClassBatch * blockDim.x) {
+        AgentBatch b;
+        load_agents(A, base + threadIdx.x, A.n, b);
+#pragma unroll
+        for (unsigned u = 0; u < kClassBatch; ++u) {
+            const unsigned a = base + u * blockDim.x + threadIdx.x;
+            if (a - lane_id() >= A.n) break;          // wave-uniform: no agent left in this wave
+            const AgentClass c = classify(A, a, a < A.n, b.D[u], b.act[u] != 0, b.res[u] != 0);
+            if (c.isC) atomicAdd(&S.histw[dist_bucket(b.D[u])], (u64)b.s[u]);
+            const unsigned oE = wave_reserve(c.isE, &S.cnt.n_E);
+            const unsigned oL = wave_reserve(c.isL, &S.cnt.n_L);
+            const unsigned oC = wave_reserve(c.isC, &S.cnt.n_C);
+            if (c.isE) A.listE[oE] = c.key;
+            if (c.isL) A.listL[oL] = c.key;
+            if (c.isC) A.listC[oC] = c.key;
+            t.add(c, b.act[u] != 0, b.res[u] != 0, b.s[u]);
+        }
+    }
+    flush_sums(t, &S.cnt);
+}
+
+// Publish the plan to the host: every thread's host-visible writes are made
+// visible at system scope, then one thread writes the plan's sequence number
+// to the mapped flag word, which the host polls.  Last action of the core.
+__device__ __forceinline__ void publish_plan(const PlanArgs& A) {
+    __threadfence_system();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __threadfence_system();
+        __hip_atomic_store(A.flag_host, A.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+}
+
 // The plan core: one workgroup of kCoreThreads threads; `lds` holds kLdsKeys
 // keys.  Inlined into both kernels below so that its LDS accesses stay LDS
 // instructions.
@@ -500,15 +560,14 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     auto stamp = [&](int k) {
         if (A.phase && tid == 0) A.phase[k] = wall_clock64();
     };
-    stamp(0);
+    if (A.fused) stamp(0);                           // else stamped at the classifying kernel's entry
     const u64 idmask = (1ull << A.idbits) - 1;
     const unsigned* units = A.units;
     if (A.fused) {
         if (tid == 0) S.cnt = PlanCounters{};
         for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) S.histw[b] = 0;
         __syncthreads();
-        for (unsigned base = 0; base < A.n; base += blockDim.x)
-            classify_agent(A, base + tid, &S.cnt, S.histw);
+        classify_fused(A, S);
         __syncthreads();
     }
     // the candidate histogram: this workgroup's LDS when it classified the
@@ -527,6 +586,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
             *A.res_host = r;
             if (!A.fused) *A.cnt = PlanCounters{};
         }
+        publish_plan(A);
         return;
     }
     const u64 free_before = A.capacity - c.sum_resident;
@@ -749,6 +809,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         *A.res_host = r;
         if (!A.fused) *A.cnt = PlanCounters{};
     }
+    publish_plan(A);
 }
 
 __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
@@ -758,54 +819,42 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
 }
 
 // Classification over many workgroups, then the plan core in the workgroup
-// that finishes last (N > kFuseAgents).  Each workgroup classifies 1024
-// agents, gathers its counts and sums in LDS and reaches the global counters
-// with one atomic per counter; its list entries go to the ranges those
-// atomics reserve.  Every workgroup then publishes its writes (agent-scope
-// fence) and counts itself done; the one that counts last acquires them all
-// and runs the plan core, so no workgroup ever waits for another and the core
-// starts without a second launch.  It resets the count for the next step.
+// that finishes last (N > kFuseAgents).  Each workgroup classifies
+// kClassBatch * 1024 agents, gathers its counts and sums in LDS and reaches
+// the global counters with one atomic per counter; its list entries go to the
+// ranges those atomics reserve.  Every workgroup then publishes its writes
+// (agent-scope fence) and counts itself done; the one that counts last
+// acquires them all and runs the plan core, so no workgroup ever waits for
+// another and the core starts without a second launch.  It resets the count
+// for the next step.  (Same-address atomics across workgroups serialize, so
+// fewer, larger workgroups reach the core sooner.)
 __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
     __shared__ u64 lds[kLdsKeys];
     __shared__ CoreShared S;
-    const unsigned a = blockIdx.x * kCoreThreads + threadIdx.x;
+    const unsigned first = blockIdx.x * (kClassBatch * kCoreThreads) + threadIdx.x;
+    if (A.phase && blockIdx.x == 0 && threadIdx.x == 0) A.phase[0] = wall_clock64();
     if (threadIdx.x == 0) S.cnt = PlanCounters{};
     for (unsigned b = threadIdx.x; b < kDistBuckets; b += kCoreThreads) S.histw[b] = 0;
     __syncthreads();
-    const bool valid = a < A.n;
-    unsigned D = 0;
-    bool act = false, res = false;
-    u64 s = 0;
-    if (valid) {
-        D = A.dist[a];
-        act = A.active[a] != 0;
-        res = A.resident[a] != 0;
-        s = A.units[a];
+    AgentBatch b;
+    load_agents(A, first, A.n, b);
+    AgentClass c[kClassBatch];
+    unsigned oE[kClassBatch], oL[kClassBatch], oC[kClassBatch];
+    ClassSums t;
+#pragma unroll
+    for (unsigned u = 0; u < kClassBatch; ++u) {
+        const unsigned a = first + u * kCoreThreads;
+        c[u] = classify(A, a, a < A.n, b.D[u], b.act[u] != 0, b.res[u] != 0);
+        // candidate units per distance bucket: LDS first (distances concentrate
+        // on few buckets, where global atomics would serialize), one global
+        // atomic per non-empty bucket and workgroup below
+        if (c[u].isC) atomicAdd(&S.histw[dist_bucket(b.D[u])], (u64)b.s[u]);
+        oE[u] = wave_reserve(c[u].isE, &S.cnt.n_E);
+        oL[u] = wave_reserve(c[u].isL, &S.cnt.n_L);
+        oC[u] = wave_reserve(c[u].isC, &S.cnt.n_C);
+        t.add(c[u], b.act[u] != 0, b.res[u] != 0, b.s[u]);
     }
-    const u64 d = act ? 0ull : (u64)D;               // active agents: distance 0
-    const u64 key = (d << A.idbits) | a;
-    const bool isE = valid && res && !act;            // evictable resident
-    const bool isL = valid && act && !res;            // demand load
-    const bool isC = valid && !res && !act && D < A.threshold;   // prefetch candidate
-    // candidate units per distance bucket: LDS first (distances concentrate on
-    // few buckets, where global atomics would serialize), one global atomic
-    // per non-empty bucket and workgroup below
-    if (isC) atomicAdd(&S.histw[dist_bucket(D)], s);
-    const unsigned oE = wave_reserve(isE, &S.cnt.n_E);
-    const unsigned oL = wave_reserve(isL, &S.cnt.n_L);
-    const unsigned oC = wave_reserve(isC, &S.cnt.n_C);
-    const u64 s_act = wave_sum(act ? s : 0);
-    const u64 s_res = wave_sum(res ? s : 0);
-    const u64 s_dem = wave_sum(isL ? s : 0);
-    const u64 s_evi = wave_sum(isE ? s : 0);
-    const u64 s_can = wave_sum(isC ? s : 0);
-    if (lane_id() == 0) {
-        atomicAdd(&S.cnt.sum_active, s_act);
-        atomicAdd(&S.cnt.sum_resident, s_res);
-        atomicAdd(&S.cnt.sum_demand, s_dem);
-        atomicAdd(&S.cnt.sum_evictable, s_evi);
-        atomicAdd(&S.cnt.sum_cand, s_can);
-    }
+    flush_sums(t, &S.cnt);
     __syncthreads();
     if (threadIdx.x == 0) {
         PlanCounters* g = A.cnt;
@@ -820,11 +869,14 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
         if (lc.sum_cand) atomicAdd(&g->sum_cand, lc.sum_cand);
     }
     __syncthreads();
-    if (isE) A.listE[S.uscal[0] + oE] = key;
-    if (isL) A.listL[S.uscal[1] + oL] = key;
-    if (isC) A.listC[S.uscal[2] + oC] = key;
-    for (unsigned b = threadIdx.x; b < kDistBuckets; b += kCoreThreads)
-        if (S.histw[b]) atomicAdd(&A.hist_w[b], S.histw[b]);
+#pragma unroll
+    for (unsigned u = 0; u < kClassBatch; ++u) {
+        if (c[u].isE) A.listE[S.uscal[0] + oE[u]] = c[u].key;
+        if (c[u].isL) A.listL[S.uscal[1] + oL[u]] = c[u].key;
+        if (c[u].isC) A.listC[S.uscal[2] + oC[u]] = c[u].key;
+    }
+    for (unsigned k = threadIdx.x; k < kDistBuckets; k += kCoreThreads)
+        if (S.histw[k]) atomicAdd(&A.hist_w[k], S.histw[k]);
     __threadfence();                                 // release this workgroup's writes
     __syncthreads();
     if (threadIdx.x == 0) S.uscal[3] = atomicAdd(A.done, 1u) == gridDim.x - 1;
@@ -1008,7 +1060,8 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t st) {
     if (a.fused) {
         hipLaunchKernelGGL(k_plan_core, dim3(1), dim3(kCoreThreads), 0, st, a);
     } else {
-        const unsigned blocks = (a.n + kCoreThreads - 1) / kCoreThreads;
+        const unsigned per = kClassBatch * kCoreThreads;
+        const unsigned blocks = (a.n + per - 1) / per;
         hipLaunchKernelGGL(k_classify_core, dim3(blocks), dim3(kCoreThreads), 0, st, a);
     }
     return hipGetLastError();

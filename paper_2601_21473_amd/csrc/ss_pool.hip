@@ -26,6 +26,10 @@
 // gives a process by default and the two directions never share a queue.
 // Every cross-stream wait refers to an event recorded earlier in host order,
 // so sharing cannot form a cycle.
+//
+// ss_plan_step returns once the plan kernel has written the plan's sequence
+// number into a mapped host word (its last write, after the lists), which the
+// host polls; the runtime's completion event is the fallback.
 #include "scalesim.h"
 #include "ss_internal.h"
 
@@ -44,6 +48,11 @@ using namespace ss;
 
 namespace {
 thread_local std::string g_err;
+
+// How long ss_plan_step polls the plan's mapped flag word before it waits on
+// the plan's event instead (a plan queued behind long work on the caller's
+// stream then costs no spinning host core).
+constexpr long kPlanPollUs = 2000;
 }  // namespace
 
 namespace ss {
@@ -119,6 +128,9 @@ struct ss_pool {
     u64* d_chunk_bytes = nullptr;
 
     // mapped pinned host mirrors of the plan
+    unsigned* h_flag = nullptr;    // the plan kernel's last write: its sequence number
+    unsigned* h_flag_dev = nullptr;
+    unsigned plan_seq = 0;
     PlanResult* h_res = nullptr;
     unsigned* h_victims = nullptr;
     unsigned* h_loads = nullptr;
@@ -241,7 +253,7 @@ void free_pool(ss_pool* p) {
                      p->d_chunk_bytes, p->d_done, p->d_host_off, p->d_whost, p->d_lhost};
     for (void* d : dptrs)
         if (d) (void)hipFree(d);
-    void* hptrs[] = {p->h_res, p->h_victims, p->h_loads, p->h_vwritten};
+    void* hptrs[] = {p->h_flag, p->h_res, p->h_victims, p->h_loads, p->h_vwritten};
     for (void* h : hptrs)
         if (h) (void)hipHostFree(h);
     if (p->st_out) release_streams(p->device);
@@ -360,10 +372,11 @@ ss_status check_usable(ss_pool* p) {
 
 // Fold the previous step's copy events and this plan's event time and phase
 // stamps into the stats (timing mode).  The previous step's loads completed
-// before this plan's kernels ran and the plan kernels before ss_plan_step
-// returned; its evictions are waited for here.
+// before this plan's kernels ran; the plan kernel (which may still be ending
+// when ss_plan_step returns) and the previous evictions are waited for here.
 ss_status collect_plan_timing(ss_pool* p) {
     if (!(p->flags & SS_FLAG_TIMING)) return SS_OK;
+    TRY_HIP(p, hipEventSynchronize(p->ev_planned), true);
     TRY_HIP(p, hipEventSynchronize(p->ev_out_done), true);
     collect_timing(p);
     if (p->phase_pending) {
@@ -564,6 +577,9 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
             khz > 0)
             p->us_per_tick = 1000.0 / khz;
     }
+    CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_flag), 64, hipHostMallocMapped));
+    *p->h_flag = 0;
+    CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_flag_dev), p->h_flag, 0));
     CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_res), sizeof(PlanResult),
                              hipHostMallocMapped));
     CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_victims), N * sizeof(unsigned),
@@ -707,6 +723,9 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     A.vwritten_host = p->h_vwritten_dev;
     A.woff = p->d_woff;
     A.done = p->d_done;
+    if (++p->plan_seq == 0) p->plan_seq = 1;
+    A.flag_host = p->h_flag_dev;
+    A.seq = p->plan_seq;
 
     const bool timing = p->flags & SS_FLAG_TIMING;
     if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.a, caller), true);
@@ -715,7 +734,26 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     TRY_HIP(p, hipEventRecord(p->ev_planned, caller), true);
 
     const auto h1 = std::chrono::steady_clock::now();
-    TRY_HIP(p, hipEventSynchronize(p->ev_planned), true);
+    // The kernel's last write is the sequence number into the mapped flag
+    // word, after its results and lists are visible to the host: poll it for
+    // up to kPlanPollUs, then wait on the plan's event (which also reports a
+    // failed launch or kernel).
+    {
+        bool seen = false;
+        for (;;) {
+            if (__atomic_load_n(p->h_flag, __ATOMIC_ACQUIRE) == p->plan_seq) {
+                seen = true;
+                break;
+            }
+            if (std::chrono::steady_clock::now() - h1 > std::chrono::microseconds(kPlanPollUs)) break;
+            __builtin_ia32_pause();
+        }
+        if (!seen) {
+            TRY_HIP(p, hipEventSynchronize(p->ev_planned), true);
+            if (__atomic_load_n(p->h_flag, __ATOMIC_ACQUIRE) != p->plan_seq)
+                return set_err(SS_ERR_HIP, "plan kernel finished without publishing its plan");
+        }
+    }
     const auto h2 = std::chrono::steady_clock::now();
     // event times of the previous step and of this plan are folded into the
     // stats by ss_evict_pack, off the path that returns the plan
