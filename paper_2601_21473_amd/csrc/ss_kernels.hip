@@ -119,6 +119,22 @@ __device__ __forceinline__ unsigned wave_reserve(bool pred, unsigned* counter) {
     return __shfl(base, 0) + mbcnt(mask);
 }
 
+// Block-local slots of this lane in the three class lists: lane 0 issues the
+// (up to) three LDS atomics back to back and the wave waits once.
+__device__ __forceinline__ void wave_reserve3(const AgentClass& c, PlanCounters* cnt,
+                                              unsigned& oE, unsigned& oL, unsigned& oC) {
+    const u64 mE = __ballot(c.isE), mL = __ballot(c.isL), mC = __ballot(c.isC);
+    unsigned bE = 0, bL = 0, bC = 0;
+    if (lane_id() == 0) {
+        if (mE) bE = atomicAdd(&cnt->n_E, (unsigned)__popcll(mE));
+        if (mL) bL = atomicAdd(&cnt->n_L, (unsigned)__popcll(mL));
+        if (mC) bC = atomicAdd(&cnt->n_C, (unsigned)__popcll(mC));
+    }
+    oE = __shfl(bE, 0) + mbcnt(mE);
+    oL = __shfl(bL, 0) + mbcnt(mL);
+    oC = __shfl(bC, 0) + mbcnt(mC);
+}
+
 // Add every thread's sums to the block counters *cnt (LDS): one reduction per
 // wave and sum, one LDS atomic per wave.
 __device__ __forceinline__ void flush_sums(const ClassSums& t, PlanCounters* cnt) {
@@ -211,9 +227,10 @@ __device__ void block_prefix(unsigned n, F f, u64* out, CoreShared& S) {
 }
 
 // Keys src[i] (i < n) with keep(key) appended to buf[*counter ...] (slots at
-// or beyond cap are counted but not written).  Each thread has kGatherLoads
-// loads in flight before using any, and each wave reserves its slots with
-// one LDS atomic.
+// or beyond cap are counted but not written).  Each thread loads kGatherLoads
+// keys per round, and the next round's loads are issued before this round's
+// keys are placed; each wave reserves the slots of a whole round with one LDS
+// atomic.  The order of the appended keys is arbitrary.
 constexpr unsigned kGatherLoads = 8;
 template <class Keep>
 __device__ __forceinline__ void gather_keys(const u64* src, unsigned n, Keep keep, u64* buf,
@@ -226,40 +243,71 @@ __device__ __forceinline__ void gather_keys(const u64* src, unsigned n, Keep kee
         if (take && pos < cap) buf[pos] = k;
         return;
     }
-    for (unsigned i0 = 0; i0 < n; i0 += kGatherLoads * blockDim.x) {
-        u64 k[kGatherLoads];
+    const unsigned step = kGatherLoads * blockDim.x;
+    u64 k[kGatherLoads];
+#pragma unroll
+    for (unsigned u = 0; u < kGatherLoads; ++u) {
+        const unsigned i = u * blockDim.x + threadIdx.x;
+        k[u] = i < n ? src[i] : ~0ull;
+    }
+    for (unsigned i0 = 0; i0 < n; i0 += step) {
+        u64 kn[kGatherLoads];
 #pragma unroll
         for (unsigned u = 0; u < kGatherLoads; ++u) {
-            const unsigned i = i0 + u * blockDim.x + threadIdx.x;
-            k[u] = i < n ? src[i] : ~0ull;
+            const unsigned i = i0 + step + u * blockDim.x + threadIdx.x;
+            kn[u] = i < n ? src[i] : ~0ull;
         }
+        u64 mask[kGatherLoads];
+        unsigned total = 0;
 #pragma unroll
         for (unsigned u = 0; u < kGatherLoads; ++u) {
-            const bool take = k[u] != ~0ull && keep(k[u]);
-            const unsigned pos = wave_reserve(take, counter);
-            if (take && pos < cap) buf[pos] = k[u];
+            mask[u] = __ballot(k[u] != ~0ull && keep(k[u]));
+            total += (unsigned)__popcll(mask[u]);
         }
+        if (total) {                                 // wave-uniform
+            unsigned off = 0;
+            if (lane_id() == 0) off = atomicAdd(counter, total);
+            off = __shfl(off, 0);
+#pragma unroll
+            for (unsigned u = 0; u < kGatherLoads; ++u) {
+                const unsigned pos = off + mbcnt(mask[u]);
+                if (((mask[u] >> lane_id()) & 1) && pos < cap) buf[pos] = k[u];
+                off += (unsigned)__popcll(mask[u]);
+            }
+        }
+#pragma unroll
+        for (unsigned u = 0; u < kGatherLoads; ++u) k[u] = kn[u];
     }
 }
 
-// buf[0..n) = src[0..n), kGatherLoads loads in flight per thread.
+// buf[0..n) = src[0..n), kGatherLoads loads per thread and round, the next
+// round's loads issued before this round's stores.
 __device__ __forceinline__ void copy_keys(const u64* src, unsigned n, u64* buf) {
     if (n <= blockDim.x) {
         if (threadIdx.x < n) buf[threadIdx.x] = src[threadIdx.x];
         return;
     }
-    for (unsigned i0 = 0; i0 < n; i0 += kGatherLoads * blockDim.x) {
-        u64 k[kGatherLoads];
+    const unsigned step = kGatherLoads * blockDim.x;
+    u64 k[kGatherLoads];
+#pragma unroll
+    for (unsigned u = 0; u < kGatherLoads; ++u) {
+        const unsigned i = u * blockDim.x + threadIdx.x;
+        if (i < n) k[u] = src[i];
+    }
+    for (unsigned i0 = 0; i0 < n; i0 += step) {
+        u64 kn[kGatherLoads];
 #pragma unroll
         for (unsigned u = 0; u < kGatherLoads; ++u) {
-            const unsigned i = i0 + u * blockDim.x + threadIdx.x;
-            if (i < n) k[u] = src[i];
+            const unsigned i = i0 + step + u * blockDim.x + threadIdx.x;
+            if (i < n) kn[u] = src[i];
         }
 #pragma unroll
         for (unsigned u = 0; u < kGatherLoads; ++u) {
             const unsigned i = i0 + u * blockDim.x + threadIdx.x;
             if (i < n) buf[i] = k[u];
         }
+#pragma unroll
+        for (unsigned u = 0; u < kGatherLoads; ++u) k[u] = kn[u];
     }
 }
 
@@ -289,65 +337,106 @@ __device__ void bitonic_asc(u64* buf, unsigned npad) {
     }
 }
 
-__device__ __forceinline__ void cmp_keep(u64& x, u64 p, bool keep_min) {
-    x = keep_min ? (p < x ? p : x) : (p > x ? p : x);
+// Value of lane (lane ^ jl) for jl in {1, 2, 4, 8, 16, 32}, without LDS: DPP
+// quad permutes (1, 2), row rotates (4: by 4 or 12 depending on the lane, 8)
+// and the permlane swaps of 16- and 32-lane halves.
+__device__ __forceinline__ unsigned lane_xor32(unsigned x, unsigned jl) {
+    const unsigned l = lane_id();
+    switch (jl) {
+    case 1: return __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false);     // quad_perm 1,0,3,2
+    case 2: return __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false);     // quad_perm 2,3,0,1
+    case 4: {
+        const unsigned dn = __builtin_amdgcn_mov_dpp(x, 0x124, 0xF, 0xF, false);   // row_ror:4
+        const unsigned up = __builtin_amdgcn_mov_dpp(x, 0x12C, 0xF, 0xF, false);   // row_ror:12
+        return (l & 4) ? dn : up;
+    }
+    case 8: return __builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, false);    // row_ror:8
+    case 16: {
+        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        return (l & 16) ? r[0] : r[1];
+    }
+    default: {
+        const auto q = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        return (l & 32) ? q[0] : q[1];
+    }
+    }
 }
 
-// Keys per thread in the register stages of the LDS sort (so lists of up to
-// 1024 * kRegKeys keys are sorted in LDS).
+__device__ __forceinline__ u64 lane_xor64(u64 v, unsigned jl) {
+    return ((u64)lane_xor32((unsigned)(v >> 32), jl) << 32) | lane_xor32((unsigned)v, jl);
+}
+
+// Largest list sorted in LDS: 1024 threads with up to kRegKeys keys each.
 constexpr unsigned kRegKeys = 8;
 
 // Ascending sort of lds[0..npad), npad a power of two <= 1024 * kE, by a
-// 1024-thread block, using lds[npad..2 npad) as scratch.  Each wave first
-// sorts runs of 64 keys in registers (thread t holds elements t + 1024 r;
-// 21 compare-exchange stages over wave shuffles, no barrier; waves that hold
-// only padding skip them).  Then runs are merged pairwise, one barrier per
-// round, by merge path (Green, McColl and Bader 2012): thread t writes the
-// kE consecutive outputs starting at t * kE; one binary search over the
-// diagonal of its run pair finds how many of the outputs before it come from
-// the left run, then it merges its kE outputs sequentially with the two run
-// heads in registers.  Ties take the left run first, so the padding keys
-// (all equal) keep a consistent order.
+// 1024-thread block, using lds[npad..2 npad) as scratch.
+//
+// Register stage: each wave sorts a run of 64 * kE keys, lane l holding the
+// kE consecutive keys from l * kE, by a bitonic network (Batcher 1968):
+// exchanges between keys of one lane are register moves, exchanges between
+// lanes go through lane_xor64 (no LDS, no barrier); waves that hold only
+// padding skip it.  Merge stage: runs are merged pairwise, one barrier per
+// round, by merge path (Green, McColl and Bader 2012): thread t writes the kE
+// consecutive outputs from t * kE; one binary search over the diagonal of its
+// run pair finds how many of the outputs before it come from the left run,
+// then it merges its kE outputs sequentially with the two run heads in
+// registers.  Ties take the left run first, so the padding keys (all equal)
+// keep a consistent order.
 template <unsigned kE>
 __device__ __forceinline__ void merge_sort_lds_e(u64* lds, unsigned npad) {
-    const unsigned t = threadIdx.x;
-    if ((t & ~63u) < npad) {                         // wave-uniform: the wave holds keys
+    constexpr unsigned W = 64 * kE;                  // keys per wave run
+    const unsigned t = threadIdx.x, l = lane_id();
+    const unsigned base = (t >> 6) * W;
+    if (base < npad) {                               // wave-uniform: the wave holds keys
         u64 x[kE];
 #pragma unroll
         for (unsigned r = 0; r < kE; ++r) {
-            const unsigned i = t + (r << 10);
+            const unsigned i = base + l * kE + r;
             x[r] = i < npad ? lds[i] : ~0ull;
         }
 #pragma unroll
-        for (unsigned k = 2; k <= 64; k <<= 1) {
+        for (unsigned k = 2; k <= W; k <<= 1) {
 #pragma unroll
             for (unsigned j = k >> 1; j > 0; j >>= 1) {
+                if (j < kE) {                        // partner in the same lane
 #pragma unroll
-                for (unsigned r = 0; r < kE; ++r) {
-                    const unsigned i = t + (r << 10);
-                    const u64 p = __shfl_xor(x[r], (int)j);
-                    // runs below 64 alternate direction (bitonic); each 64-run ends ascending
-                    const bool up = k == 64 || (i & k) == 0;
-                    cmp_keep(x[r], p, ((i & j) == 0) == up);
+                    for (unsigned r = 0; r < kE; ++r) {
+                        if (r & j) continue;
+                        const bool up = ((l * kE + r) & k) == 0;
+                        const u64 a = x[r], b = x[r | j];
+                        const bool sw = (a > b) == up;
+                        x[r] = sw ? b : a;
+                        x[r | j] = sw ? a : b;
+                    }
+                } else {                             // partner in lane l ^ (j / kE)
+                    const unsigned i = l * kE;
+                    const bool keep_min = ((i & j) == 0) == ((i & k) == 0);
+#pragma unroll
+                    for (unsigned r = 0; r < kE; ++r) {
+                        const u64 p = lane_xor64(x[r], j / kE);
+                        const bool take = (p < x[r]) == keep_min;
+                        x[r] = take ? p : x[r];
+                    }
                 }
             }
         }
 #pragma unroll
         for (unsigned r = 0; r < kE; ++r) {
-            const unsigned i = t + (r << 10);
+            const unsigned i = base + l * kE + r;
             if (i < npad) lds[i] = x[r];
         }
     }
     __syncthreads();
     u64* src = lds;
     u64* dst = lds + npad;
-    for (unsigned L = 64; L < npad; L <<= 1) {
+    for (unsigned L = W; L < npad; L <<= 1) {
         const unsigned o = t * kE;                   // first output of this thread
         if (o < npad) {
-            const unsigned base = o & ~(2 * L - 1);
-            const unsigned d = o - base;             // outputs of the pair before o
-            const u64* A = src + base;
-            const u64* B = src + base + L;
+            const unsigned b0 = o & ~(2 * L - 1);
+            const unsigned d = o - b0;               // outputs of the pair before o
+            const u64* A = src + b0;
+            const u64* B = src + b0 + L;
             unsigned lo = d > L ? d - L : 0, hi = d < L ? d : L;
             while (lo < hi) {
                 const unsigned mid = (lo + hi) >> 1;
@@ -379,9 +468,12 @@ __device__ __forceinline__ void merge_sort_lds_e(u64* lds, unsigned npad) {
     }
 }
 
+// Keys per lane by list size (measured on one 1024-thread workgroup: longer
+// register runs save merge rounds until the register stage's exchanges cost
+// more than the rounds they save).
 __device__ void merge_sort_lds(u64* lds, unsigned npad) {
-    if (npad <= 1024) merge_sort_lds_e<1>(lds, npad);
-    else if (npad == 2048) merge_sort_lds_e<2>(lds, npad);
+    if (npad <= 512) merge_sort_lds_e<1>(lds, npad);
+    else if (npad <= 2048) merge_sort_lds_e<2>(lds, npad);
     else if (npad == 4096) merge_sort_lds_e<4>(lds, npad);
     else merge_sort_lds_e<8>(lds, npad);
 }
@@ -519,23 +611,26 @@ __device__ u64 weighted_select(const u64* keys, unsigned n, const unsigned* unit
 // and is removed by the sorts that follow).
 __device__ __forceinline__ void classify_fused(const PlanArgs& A, CoreShared& S) {
     ClassSums t;
-    for (unsigned base = 0; base < A.n; base += kClassBatch * blockDim.x) {
-        AgentBatch b;
-        load_agents(A, base + threadIdx.x, A.n, b);
+    const unsigned step = kClassBatch * blockDim.x;
+    AgentBatch b;
+    load_agents(A, threadIdx.x, A.n, b);
+    for (unsigned base = 0; base < A.n; base += step) {
+        AgentBatch nb;                               // next pass's loads in flight
+        load_agents(A, base + step + threadIdx.x, A.n, nb);
 #pragma unroll
         for (unsigned u = 0; u < kClassBatch; ++u) {
             const unsigned a = base + u * blockDim.x + threadIdx.x;
             if (a - lane_id() >= A.n) break;          // wave-uniform: no agent left in this wave
             const AgentClass c = classify(A, a, a < A.n, b.D[u], b.act[u] != 0, b.res[u] != 0);
             if (c.isC) atomicAdd(&S.histw[dist_bucket(b.D[u])], (u64)b.s[u]);
-            const unsigned oE = wave_reserve(c.isE, &S.cnt.n_E);
-            const unsigned oL = wave_reserve(c.isL, &S.cnt.n_L);
-            const unsigned oC = wave_reserve(c.isC, &S.cnt.n_C);
+            unsigned oE, oL, oC;
+            wave_reserve3(c, &S.cnt, oE, oL, oC);
             if (c.isE) A.listE[oE] = c.key;
             if (c.isL) A.listL[oL] = c.key;
             if (c.isC) A.listC[oC] = c.key;
             t.add(c, b.act[u] != 0, b.res[u] != 0, b.s[u]);
         }
+        b = nb;
     }
     flush_sums(t, &S.cnt);
 }
@@ -704,24 +799,59 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     // acceptance: S_i <= budget and S_i <= free1 + (units of the remaining
     // evictable residents with distance strictly larger than d_i)
     if (tid == 0) S.uscal[3] = m;
-    // the evictable keys in LDS for the searches below (the sort buffer is free)
+    // the evictable keys, and their unit prefix when it fits too, in LDS for
+    // the searches below (the sort buffer is free)
     const u64* keysE = sortE;
+    const u64* pref = A.prefE;
     if (nE <= (unsigned)kLdsKeys) {
+        const bool both = 2 * nE + 1 <= (unsigned)kLdsKeys;
         for (unsigned i = tid; i < nE; i += blockDim.x) lds[i] = sortE[i];
+        if (both) for (unsigned i = tid; i <= nE; i += blockDim.x) lds[nE + i] = A.prefE[i];
         keysE = lds;
+        if (both) pref = lds + nE;
     }
     __syncthreads();
-    for (unsigned i = tid; i < m; i += blockDim.x) {
-        const u64 di = sortC[i] >> A.idbits;
-        const u64 Si = A.prefC[i + 1];
-        unsigned lo = 0, hi = nE;                    // first eviction index with d <= di
-        while (lo < hi) {
-            const unsigned mid = (lo + hi) >> 1;
-            if ((keysE[nE - 1 - mid] >> A.idbits) > di) lo = mid + 1; else hi = mid;
+    {
+        // kAccept candidates per thread at once: their binary searches run in
+        // lockstep (ceil(log2(nE + 1)) steps), so the loads of one overlap the
+        // others'
+        constexpr unsigned kAccept = 4;
+        const unsigned steps = nE ? 32u - (unsigned)__clz(nE) : 0u;
+        const u64 base_units = pref[n_d];
+        for (unsigned i0 = tid; i0 < m; i0 += kAccept * blockDim.x) {
+            u64 di[kAccept], Si[kAccept];
+            unsigned lo[kAccept], hi[kAccept];
+#pragma unroll
+            for (unsigned u = 0; u < kAccept; ++u) {
+                const unsigned i = i0 + u * blockDim.x;
+                di[u] = i < m ? sortC[i] >> A.idbits : 0;
+                Si[u] = i < m ? A.prefC[i + 1] : 0;
+                lo[u] = 0;                           // first eviction index with d <= di
+                hi[u] = i < m ? nE : 0;
+            }
+            for (unsigned it = 0; it < steps; ++it) {
+#pragma unroll
+                for (unsigned u = 0; u < kAccept; ++u) {
+                    if (lo[u] < hi[u]) {
+                        const unsigned mid = (lo[u] + hi[u]) >> 1;
+                        if ((keysE[nE - 1 - mid] >> A.idbits) > di[u]) lo[u] = mid + 1;
+                        else hi[u] = mid;
+                    }
+                }
+            }
+#pragma unroll
+            for (unsigned u = 0; u < kAccept; ++u) {
+                // the wave's first failing candidate (lanes hold consecutive
+                // i) goes to one LDS atomic per wave: most candidates past the
+                // accepted prefix fail, and same-address atomics serialize
+                const unsigned i = i0 + u * blockDim.x;
+                const u64 G = lo[u] > n_d ? pref[lo[u]] - base_units : 0;
+                const bool fail = i < m && !(Si[u] <= A.budget && Si[u] <= free1 + G);
+                const u64 fm = __ballot(fail);
+                if (fm && lane_id() == (unsigned)__ffsll((long long)fm) - 1)
+                    atomicMin(&S.uscal[3], i);
+            }
         }
-        const u64 G = lo > n_d ? A.prefE[lo] - A.prefE[n_d] : 0;
-        const bool ok = Si <= A.budget && Si <= free1 + G;
-        if (!ok) atomicMin(&S.uscal[3], i);
     }
     __syncthreads();
     stamp(5);
@@ -849,9 +979,7 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
         // on few buckets, where global atomics would serialize), one global
         // atomic per non-empty bucket and workgroup below
         if (c[u].isC) atomicAdd(&S.histw[dist_bucket(b.D[u])], (u64)b.s[u]);
-        oE[u] = wave_reserve(c[u].isE, &S.cnt.n_E);
-        oL[u] = wave_reserve(c[u].isL, &S.cnt.n_L);
-        oC[u] = wave_reserve(c[u].isC, &S.cnt.n_C);
+        wave_reserve3(c[u], &S.cnt, oE[u], oL[u], oC[u]);
         t.add(c[u], b.act[u] != 0, b.res[u] != 0, b.s[u]);
     }
     flush_sums(t, &S.cnt);
