@@ -223,6 +223,18 @@ def test_lists_beyond_lds_sort_buffer():
                label="global sort path")
 
 
+@pytest.mark.parametrize("n_agents", [4097, 12288, 12289])
+def test_classification_batch_edges(n_agents):
+    # agent counts around the plan's one-workgroup limit (12,288) and one past
+    # a 4,096-agent classification batch, with ragged sizes and noisy distances
+    rng = np.random.default_rng(n_agents)
+    units = rng.integers(1, 4, size=n_agents).astype(np.uint32)
+    tr = synthetic_trace(n_agents, n_agents // 3, 20, n_agents // 50, seed=n_agents, units=units,
+                         chunk_bytes=(16,), noisy=True)
+    run_parity(tr, theta=S, slot_units=2048, ring_slots=2, sample_units=3000,
+               label=f"classification edges {n_agents}")
+
+
 def test_empty_steps_and_idle_pool():
     tr = synthetic_trace(100, 40, 30, lambda t, r: 0 if t % 3 else r.integers(0, 30), seed=2)
     run_parity(tr, theta=S, slot_units=5, ring_slots=2, label="empty steps")
