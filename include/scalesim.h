@@ -144,7 +144,7 @@ typedef struct {                    /* cumulative since create or ss_reset_stats
                                               sorts, candidate select, candidate sort,
                                               acceptance, lists, free units); classify runs
                                               from the plan kernel's entry (its first
-                                              workgroup when N > 4096)                      */
+                                              workgroup when N > 12288)                     */
     double   plan_host_us[3];              /* ss_plan_step on the host: queueing the plan,
                                               waiting for it, reading it back              */
     uint64_t direct_out_launches, direct_in_launches;  /* directions moved by direct_bytes */
@@ -170,8 +170,11 @@ void ss_pool_destroy(ss_pool* pool);
  * the block table.  `distances` [N] uint32 and `active` [N] uint8 (0/1) are
  * DEVICE pointers read during the call's kernels, which run on `stream`
  * after the work queued there before the call and after the previous step's
- * loads.  The call returns after the plan is known on the host (one
- * device-to-host readback).  The block-table
+ * loads.  The call returns once the plan is known on the host: the plan
+ * kernel writes its lists into mapped host memory and, last, a sequence
+ * number that the call polls (for up to 2 ms, then it waits on the kernel's
+ * completion event); by then the kernel has finished reading `distances`
+ * and `active`, though it may still be ending on the device.  The block-table
  * update that the plan implies is queued on the device by the next call that
  * needs it (ss_evict_pack, ss_block_table*, ss_resident_host, ss_sync) and is
  * ordered before the copy kernels.
