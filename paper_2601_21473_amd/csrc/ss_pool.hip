@@ -118,9 +118,13 @@ struct ss_pool {
     u64* d_host_off = nullptr;     // direct mode: [N] host-copy offsets
     u64 *d_whost = nullptr, *d_lhost = nullptr;   // direct mode: [U] per moved unit
     PlanResult* d_res = nullptr;
-    u64* d_phase = nullptr;
+    // timing mode: two plans' phase stamps in mapped host memory (the kernel
+    // writes them, the host reads them directly) and two plans' event pairs,
+    // so a plan's timing is folded one step later, when it is long complete
+    u64* h_phase = nullptr;        // [2][kPlanPhases]
+    u64* h_phase_dev = nullptr;
     u64* d_hist_w = nullptr;
-    bool phase_pending = false;
+    bool plan_pending[2] = {false, false};
     double us_per_tick = 0.01;     // device wall clock
     CopyItem* d_items = nullptr;
     unsigned n_items = 0;
@@ -150,8 +154,7 @@ struct ss_pool {
     // timing (SS_FLAG_TIMING): one pair per launch or per slot's copies
     std::vector<TimedPair> t_pack, t_unpack, t_d2h, t_h2d, t_dout, t_din;
     size_t n_t_pack = 0, n_t_unpack = 0, n_t_d2h = 0, n_t_h2d = 0, n_t_dout = 0, n_t_din = 0;
-    TimedPair t_plan;
-    bool t_plan_used = false;
+    TimedPair t_plan[2];
     ss_stats stats{};
 
     // plan of the current step (host)
@@ -248,17 +251,17 @@ void free_pool(ss_pool* p) {
     void* dptrs[] = {p->d_units, p->d_agent_off, p->d_bt, p->d_resident, p->d_occ, p->d_cnt,
                      p->d_listE, p->d_listC, p->d_listL, p->d_sortE, p->d_sortC, p->d_sortL,
                      p->d_prefE, p->d_prefC, p->d_loff, p->d_victims, p->d_loads, p->d_vunits,
-                     p->d_lunits, p->d_free_old, p->d_res, p->d_phase, p->d_hist_w,
+                     p->d_lunits, p->d_free_old, p->d_res, p->d_hist_w,
                      p->d_wunits, p->d_vwritten, p->d_woff, p->d_items, p->d_plane_base,
                      p->d_chunk_bytes, p->d_done, p->d_host_off, p->d_whost, p->d_lhost};
     for (void* d : dptrs)
         if (d) (void)hipFree(d);
-    void* hptrs[] = {p->h_flag, p->h_res, p->h_victims, p->h_loads, p->h_vwritten};
+    void* hptrs[] = {p->h_flag, p->h_phase, p->h_res, p->h_victims, p->h_loads, p->h_vwritten};
     for (void* h : hptrs)
         if (h) (void)hipHostFree(h);
     if (p->st_out) release_streams(p->device);
     hipEvent_t evs[] = {p->ev_planned, p->ev_bt, p->ev_caller, p->ev_out_done, p->ev_in_done,
-                        p->t_plan.a, p->t_plan.b};
+                        p->t_plan[0].a, p->t_plan[0].b, p->t_plan[1].a, p->t_plan[1].b};
     for (hipEvent_t e : evs)
         if (e) (void)hipEventDestroy(e);
     for (hipEvent_t e : p->ev_packed)
@@ -311,11 +314,21 @@ void collect_timing(ss_pool* p) {
          &p->stats.direct_out_launches);
     fold(p->t_din, p->n_t_din, &p->stats.direct_in_ms, &p->stats.direct_in_bytes,
          &p->stats.direct_in_launches);
-    float ms = 0.f;
-    if (p->t_plan_used && hipEventElapsedTime(&ms, p->t_plan.a, p->t_plan.b) == hipSuccess)
-        p->stats.plan_gpu_ms += ms;
     p->n_t_pack = p->n_t_unpack = p->n_t_d2h = p->n_t_h2d = p->n_t_dout = p->n_t_din = 0;
-    p->t_plan_used = false;
+}
+
+// Fold plan slot k (its event time and phase stamps) into the stats; its
+// kernel must have completed.
+void fold_plan(ss_pool* p, int k) {
+    if (!p->plan_pending[k]) return;
+    p->plan_pending[k] = false;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, p->t_plan[k].a, p->t_plan[k].b) == hipSuccess)
+        p->stats.plan_gpu_ms += ms;
+    const volatile u64* ph = p->h_phase + k * kPlanPhases;
+    for (int i = 1; i < 8; ++i)
+        if (ph[i] >= ph[i - 1])
+            p->stats.plan_phase_us[i - 1] += (double)(ph[i] - ph[i - 1]) * p->us_per_tick;
 }
 
 }  // namespace
@@ -370,23 +383,28 @@ ss_status check_usable(ss_pool* p) {
     return SS_OK;
 }
 
-// Fold the previous step's copy events and this plan's event time and phase
-// stamps into the stats (timing mode).  The previous step's loads completed
-// before this plan's kernels ran; the plan kernel (which may still be ending
-// when ss_plan_step returns) and the previous evictions are waited for here.
+// Fold the previous step's copy events and the previous plan's event time and
+// phase stamps into the stats (timing mode; called before this step's pack).
+// The previous step's loads completed before this plan's kernel ran, and so
+// did the previous plan; the previous evictions are waited for here.  This
+// plan is folded at the next step, or by ss_get_stats.
 ss_status collect_plan_timing(ss_pool* p) {
+    if (!(p->flags & SS_FLAG_TIMING)) return SS_OK;
+    TRY_HIP(p, hipEventSynchronize(p->ev_out_done), true);
+    collect_timing(p);
+    fold_plan(p, (int)((p->plan_seq + 1) & 1));      // the previous plan's slot
+    return SS_OK;
+}
+
+// Everything pending, the current plan included (its kernel is waited for).
+ss_status collect_all_timing(ss_pool* p) {
     if (!(p->flags & SS_FLAG_TIMING)) return SS_OK;
     TRY_HIP(p, hipEventSynchronize(p->ev_planned), true);
     TRY_HIP(p, hipEventSynchronize(p->ev_out_done), true);
+    TRY_HIP(p, hipEventSynchronize(p->ev_in_done), true);
     collect_timing(p);
-    if (p->phase_pending) {
-        p->phase_pending = false;
-        u64 ph[kPlanPhases];
-        TRY_HIP(p, hipMemcpy(ph, p->d_phase, sizeof ph, hipMemcpyDeviceToHost), true);
-        for (int k = 1; k < 8; ++k)
-            if (ph[k] >= ph[k - 1])
-                p->stats.plan_phase_us[k - 1] += (double)(ph[k] - ph[k - 1]) * p->us_per_tick;
-    }
+    fold_plan(p, 0);
+    fold_plan(p, 1);
     return SS_OK;
 }
 
@@ -569,7 +587,10 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(dalloc(&p->d_vwritten, N));
     CREATE_TRY(dalloc(&p->d_woff, N + 1));
     CREATE_TRY(dalloc(&p->d_res, 1));
-    CREATE_TRY(dalloc(&p->d_phase, kPlanPhases));
+    CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_phase), 2 * kPlanPhases * sizeof(u64),
+                             hipHostMallocMapped));
+    std::memset(p->h_phase, 0, 2 * kPlanPhases * sizeof(u64));
+    CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_phase_dev), p->h_phase, 0));
     CREATE_TRY(dalloc(&p->d_hist_w, kDistBuckets));
     {
         int khz = 0;
@@ -646,8 +667,10 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
                            &p->ev_in_done})
         CREATE_TRY(make_event(ev, false));
     if (p->flags & SS_FLAG_TIMING) {
-        CREATE_TRY(make_event(&p->t_plan.a, true));
-        CREATE_TRY(make_event(&p->t_plan.b, true));
+        for (TimedPair& tp : p->t_plan) {
+            CREATE_TRY(make_event(&tp.a, true));
+            CREATE_TRY(make_event(&tp.b, true));
+        }
     }
     CREATE_TRY(hipEventRecord(p->ev_out_done, p->st_out));
     CREATE_TRY(hipEventRecord(p->ev_in_done, p->st_in));
@@ -716,7 +739,7 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     A.victims_host = p->h_victims_dev;
     A.loads_host = p->h_loads_dev;
     A.fused = p->N <= kFuseAgents ? 1u : 0u;
-    A.phase = (p->flags & SS_FLAG_TIMING) ? p->d_phase : nullptr;
+
     A.hist_w = p->d_hist_w;
     A.dirty = params->dirty;
     A.vwritten = p->d_vwritten;
@@ -726,11 +749,16 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     if (++p->plan_seq == 0) p->plan_seq = 1;
     A.flag_host = p->h_flag_dev;
     A.seq = p->plan_seq;
+    const int tslot = (int)(p->plan_seq & 1);
+    A.phase = (p->flags & SS_FLAG_TIMING) ? p->h_phase_dev + tslot * kPlanPhases : nullptr;
 
     const bool timing = p->flags & SS_FLAG_TIMING;
-    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.a, caller), true);
+    if (timing) {
+        fold_plan(p, tslot);             // a plan two steps back that was never folded
+        TRY_HIP(p, hipEventRecord(p->t_plan[tslot].a, caller), true);
+    }
     TRY_HIP(p, launch_plan(A, caller), true);
-    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan.b, caller), true);
+    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan[tslot].b, caller), true);
     TRY_HIP(p, hipEventRecord(p->ev_planned, caller), true);
 
     const auto h1 = std::chrono::steady_clock::now();
@@ -755,12 +783,9 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
         }
     }
     const auto h2 = std::chrono::steady_clock::now();
-    // event times of the previous step and of this plan are folded into the
-    // stats by ss_evict_pack, off the path that returns the plan
-    if (timing) {
-        p->t_plan_used = true;
-        p->phase_pending = true;
-    }
+    // this plan's event time and phase stamps are folded into the stats one
+    // step later (or by ss_get_stats), off the path that returns the plan
+    if (timing) p->plan_pending[tslot] = true;
 
     const PlanResult r = *p->h_res;
     if (r.status == 1) {
@@ -1093,7 +1118,7 @@ ss_status ss_get_stats(ss_pool* p, ss_stats* out) {
     DeviceGuard g(p->device);
     for (hipStream_t s : {p->st_out, p->st_in})
         TRY_HIP(p, hipStreamSynchronize(s), false);
-    ss_status st = collect_plan_timing(p);
+    ss_status st = collect_all_timing(p);
     if (st) return st;
     *out = p->stats;
     return SS_OK;
@@ -1104,7 +1129,7 @@ ss_status ss_reset_stats(ss_pool* p) {
     DeviceGuard g(p->device);
     for (hipStream_t s : {p->st_out, p->st_in})
         TRY_HIP(p, hipStreamSynchronize(s), false);
-    ss_status st = collect_plan_timing(p);
+    ss_status st = collect_all_timing(p);
     if (st) return st;
     p->stats = ss_stats{};
     return SS_OK;
