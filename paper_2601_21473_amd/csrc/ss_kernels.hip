@@ -6,13 +6,16 @@
 //                into evictable residents / demand loads / prefetch
 //                candidates, wave64 ballot + mbcnt stream compaction of each
 //                class, and the unit sums the plan needs;
-//   plan core    one workgroup of 1024 threads: LDS bitonic sorts, weighted
-//                radix select of the candidate prefix that can possibly fit,
+//   plan core    one workgroup of 1024 threads: register/LDS merge sorts,
+//                the distance-histogram cut (weighted radix select as the
+//                fallback) of the candidate prefix that can possibly fit,
 //                prefix sums, the prefetch acceptance rule in closed form,
 //                the victim count, the free-unit list, and the plan written
-//                to a mapped host mirror.
-//   k_plan_core      the plan core, classifying the agents itself (N <= 16,384);
-//   k_classify_core  classification over N / 1024 workgroups, the last of
+//                to a mapped host mirror, published by a sequence number
+//                written last.
+//   k_plan_core      the plan core, classifying the agents itself
+//                    (N <= kFuseAgents = 12,288);
+//   k_classify_core  classification over N / 4096 workgroups, the last of
 //                    which runs the plan core (larger N), in one launch.
 //   k_bt_victims / k_bt_loads   block-table release and allocation.
 // Data movement:
