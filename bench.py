@@ -524,7 +524,19 @@ def cpu_baseline(trace, warmup, n_steps, n_agents_moved, threshold, budget, min_
                       f"+ numpy gather/scatter of the first {n_agents_moved} written-back victims' "
                       f"and loads' bytes ({moved / 1e9:.2f} GB in {t_move:.2f} s; unit rows taken "
                       f"modulo a {window}-unit window of the byte pool), single thread",
-            "host_threads_available": len(os.sched_getaffinity(0))}
+            "host_threads_available": len(os.sched_getaffinity(0)), "cpu_model": cpu_model()}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name as the kernel reports it (empty if unknown)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
 
 
 def main():
