@@ -208,11 +208,13 @@ def probes(binding, host=None):
     ms = binding.probe_copy(b.ptr, a.ptr, n, iters=10)
     out["hbm_copy_GBps"] = 2 * n / ms / 1e6
     # the runtime's own device-to-device copy of the same buffers, for
-    # reference (synchronous call, best host wall time of five)
+    # reference (it may return before the copy ends: each is followed by a
+    # wait for the null stream; best host wall time of five)
     walls = []
     for _ in range(5):
         t0 = time.perf_counter()
         binding.copy(b.ptr, a.ptr, n)
+        binding.null_stream_sync()
         walls.append(time.perf_counter() - t0)
     out["runtime_dtod_copy_GBps"] = 2 * n / min(walls) / 1e9
     a.free()

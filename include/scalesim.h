@@ -438,6 +438,7 @@ ss_status ss_copy(void* dst, const void* src, uint64_t bytes);
  * the calls above without a framework:
  *   ss_stream_create   non-blocking stream at the default priority on the
  *                      current device; ss_stream_destroy / ss_stream_sync
+ *                      (ss_stream_sync(NULL) waits for the null stream)
  *   ss_event_create    timing event; ss_event_record on a stream;
  *   ss_event_elapsed   waits for `end`, then milliseconds from start to end */
 ss_status ss_stream_create(void** stream);

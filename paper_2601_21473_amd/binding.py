@@ -356,6 +356,11 @@ def copy(dst: int, src: int, nbytes: int):
     _check(load().ss_copy(int(dst), int(src), int(nbytes)))
 
 
+def null_stream_sync():
+    """Wait for the work queued on the null stream."""
+    _check(load().ss_stream_sync(None))
+
+
 def probe_copy(dst: int, src: int, nbytes: int, iters: int = 10) -> float:
     ms = C.c_float()
     _check(load().ss_probe_copy(int(dst), int(src), int(nbytes), int(iters), C.byref(ms)))
