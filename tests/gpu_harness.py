@@ -76,10 +76,12 @@ def fill_host(mem, content, spec, batch_bytes=256 << 20):
 
 def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_bytes=True,
                slot_units=8, ring_slots=2, sample_units=None, bt_every=1, seed=0, label="",
-               dirty=None, device_inputs=None, direct_bytes=0):
+               dirty=None, device_inputs=None, direct_bytes=0, stream=0, before_plan=None):
     """``device_inputs(t) -> (distances_ptr, active_ptr)`` replaces the uploaded
     trace on the HIP side (the oracle side always reads ``trace``).
-    ``direct_bytes``: the pool's direct-transfer limit (0 = always staged)."""
+    ``direct_bytes``: the pool's direct-transfer limit (0 = always staged).
+    ``stream``: the caller's stream of every call; ``before_plan(t, stream)``
+    may queue work there before step t's plan."""
     spec = trace.pools[pool_index]
     ub = spec.unit_bytes
     staging_bytes = 2 * ring_slots * slot_units * ub
@@ -99,13 +101,14 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
         d_dirty = DeviceBuffer(dm.nbytes)
         d_dirty.upload(dm)
     T = trace.n_steps if steps is None else steps
-    stream = 0
     rng = np.random.default_rng(seed + 99)
     units_i64 = spec.agent_units.astype(np.int64)
     moved = 0
     t0 = time.time()
     for t in range(T):
         d_ptr, a_ptr = (dev.dist(t), dev.active(t)) if dev is not None else device_inputs(t)
+        if before_plan is not None:
+            before_plan(t, stream)
         g = pool.plan_step(d_ptr, a_ptr, theta, budget, stream,
                            0 if d_dirty is None else d_dirty.ptr + trace.n_agents * t)
         o = opool.plan_step(trace.dist[t], trace.active[t], theta, budget,

@@ -21,7 +21,7 @@ import pytest
 import workloads as W
 from gpu_harness import run_parity, synthetic_trace, upload_trace, log
 from paper_2601_21473_amd import binding as B
-from paper_2601_21473_amd.memory import PoolMemory
+from paper_2601_21473_amd.memory import DeviceBuffer, PoolMemory
 
 pytestmark = pytest.mark.gpu
 S = W.SENTINEL
@@ -233,6 +233,38 @@ def test_classification_batch_edges(n_agents):
                          chunk_bytes=(16,), noisy=True)
     run_parity(tr, theta=S, slot_units=2048, ring_slots=2, sample_units=3000,
                label=f"classification edges {n_agents}")
+
+
+def test_plan_queued_behind_long_work():
+    # Work queued on the caller's stream before a plan holds its kernel back
+    # for longer than the host polls the plan's flag (2 ms), so the call falls
+    # back to the plan's event; the plans must match the oracle either way.
+    n = 50_000
+    rng = np.random.default_rng(21)
+    pos = np.ascontiguousarray(rng.integers(0, 4096, size=(n, 2)).astype(np.int32))
+    p = DeviceBuffer(pos.nbytes)
+    p.upload(pos)
+    d = DeviceBuffer(4 * n)
+    d.upload(rng.integers(0, 1000, size=n).astype(np.uint32))
+    out = DeviceBuffer(4 * n)
+    wsb = B.interaction_distances_workspace(n)
+    ws = DeviceBuffer(max(wsb, 4))
+    s = B.Stream()
+
+    def busy(t, stream):
+        if t % 3 == 0:                       # about 16 x 0.2 ms of kernels
+            for _ in range(16):
+                B.interaction_distances(p.ptr, d.ptr, n, 3, 2, out.ptr, ws.ptr, wsb, stream)
+
+    try:
+        tr = synthetic_trace(600, 250, 12, 40, seed=21, chunk_bytes=(16,))
+        run_parity(tr, theta=S, slot_units=64, ring_slots=2, stream=s.handle,
+                   before_plan=busy, label="plan behind long work")
+    finally:
+        s.sync()
+        s.close()
+        for b in (p, d, out, ws):
+            b.free()
 
 
 def test_empty_steps_and_idle_pool():
