@@ -778,8 +778,10 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
         }
         if (!seen) {
             TRY_HIP(p, hipEventSynchronize(p->ev_planned), true);
-            if (__atomic_load_n(p->h_flag, __ATOMIC_ACQUIRE) != p->plan_seq)
+            if (__atomic_load_n(p->h_flag, __ATOMIC_ACQUIRE) != p->plan_seq) {
+                p->poisoned = true;              // the device state is unknown
                 return set_err(SS_ERR_HIP, "plan kernel finished without publishing its plan");
+            }
         }
     }
     const auto h2 = std::chrono::steady_clock::now();
