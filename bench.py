@@ -551,8 +551,9 @@ def main():
                                        args.summarize_pmc[2], args.pmc_commands), indent=1))
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU: this build has no multi-GPU path "
-              f"(--gpus {args.gpus} requested)", file=sys.stderr)
+        print(f"bench.py measures one GPU only (--gpus {args.gpus} requested): the library "
+              f"has no multi-GPU path; agents would shard across GPUs, each GPU planning "
+              f"and moving its own agents with no exchange", file=sys.stderr)
         sys.exit(2)
     import workloads as W
     from paper_2601_21473_amd import binding
