@@ -728,17 +728,18 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     u64 kstar = ~0ull;
     bool sorted = false;
     if (c.sum_cand > cap) {
-        u64 carry_w = 0;
+        // thread t holds buckets 2t and 2t+1: one block scan finds the
+        // crossing bucket (the unique one with the units before it <= cap
+        // and the units up to it > cap)
+        static_assert(kDistBuckets == 2 * kCoreThreads, "two buckets per thread");
         if (tid == 0) S.uscal[5] = kDistBuckets;
         __syncthreads();
-        for (unsigned b0 = 0; b0 < kDistBuckets; b0 += blockDim.x) {
-            const unsigned b = b0 + tid;
-            const u64 w = b < kDistBuckets ? histw[b] : 0;
+        {
+            const u64 w0 = histw[2 * tid], w1 = histw[2 * tid + 1];
             u64 tw;
-            const u64 ew = block_excl_scan(w, S, &tw);
-            if (b < kDistBuckets && carry_w + ew <= cap && carry_w + ew + w > cap)
-                S.uscal[5] = b;                       // crossing bucket (unique)
-            carry_w += tw;
+            const u64 ew = block_excl_scan(w0 + w1, S, &tw);
+            if (ew <= cap && ew + w0 > cap) S.uscal[5] = 2 * tid;
+            else if (ew + w0 <= cap && ew + w0 + w1 > cap) S.uscal[5] = 2 * tid + 1;
         }
         __syncthreads();
         const unsigned bstar = S.uscal[5];
