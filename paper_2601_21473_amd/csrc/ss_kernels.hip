@@ -39,19 +39,63 @@ __device__ __forceinline__ unsigned mbcnt(u64 mask) {
                                      __builtin_amdgcn_mbcnt_lo((unsigned)mask, 0u));
 }
 
+// Value of lane (lane ^ jl) for jl in {1, 2, 4, 8, 16, 32}, without LDS: DPP
+// quad permutes (1, 2), row rotates (4: by 4 or 12 depending on the lane, 8)
+// and the permlane swaps of 16- and 32-lane halves.
+__device__ __forceinline__ unsigned lane_xor32(unsigned x, unsigned jl) {
+    const unsigned l = lane_id();
+    switch (jl) {
+    case 1: return __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false);     // quad_perm 1,0,3,2
+    case 2: return __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false);     // quad_perm 2,3,0,1
+    case 4: {
+        const unsigned dn = __builtin_amdgcn_mov_dpp(x, 0x124, 0xF, 0xF, false);   // row_ror:4
+        const unsigned up = __builtin_amdgcn_mov_dpp(x, 0x12C, 0xF, 0xF, false);   // row_ror:12
+        return (l & 4) ? dn : up;
+    }
+    case 8: return __builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, false);    // row_ror:8
+    case 16: {
+        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        return (l & 16) ? r[0] : r[1];
+    }
+    default: {
+        const auto q = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        return (l & 32) ? q[0] : q[1];
+    }
+    }
+}
+
+__device__ __forceinline__ u64 lane_xor64(u64 v, unsigned jl) {
+    return ((u64)lane_xor32((unsigned)(v >> 32), jl) << 32) | lane_xor32((unsigned)v, jl);
+}
+
+// Sum over the wave, in every lane (butterfly over lane_xor64).
 __device__ __forceinline__ u64 wave_sum(u64 v) {
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    for (unsigned o = 32; o > 0; o >>= 1) v += lane_xor64(v, o);
     return v;
 }
 
+// v of the lane `ctrl` selects (DPP row shift or row broadcast), 0 in lanes
+// the move does not reach and in rows outside row_mask.
+template <int ctrl, int row_mask>
+__device__ __forceinline__ u64 dpp_move64(u64 v) {
+    const unsigned lo = __builtin_amdgcn_update_dpp(0u, (unsigned)v, ctrl, row_mask, 0xF, false);
+    const unsigned hi = __builtin_amdgcn_update_dpp(0u, (unsigned)(v >> 32), ctrl, row_mask, 0xF,
+                                                    false);
+    return ((u64)hi << 32) | lo;
+}
+
+// Inclusive scan over the wave (all lanes active): row-wise by DPP row shifts
+// of 1, 2, 4 and 8 lanes, then row 0's total into row 1 and row 2's into row 3
+// (row_bcast:15), then the first two rows' total into rows 2 and 3
+// (row_bcast:31).  No LDS.
 __device__ __forceinline__ u64 wave_incl_scan(u64 v) {
-    const unsigned l = lane_id();
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        u64 t = __shfl_up(v, o);
-        if (l >= (unsigned)o) v += t;
-    }
+    v += dpp_move64<0x111, 0xF>(v);                  // row_shr:1
+    v += dpp_move64<0x112, 0xF>(v);                  // row_shr:2
+    v += dpp_move64<0x114, 0xF>(v);                  // row_shr:4
+    v += dpp_move64<0x118, 0xF>(v);                  // row_shr:8
+    v += dpp_move64<0x142, 0xA>(v);                  // row_bcast:15 into rows 1 and 3
+    v += dpp_move64<0x143, 0xC>(v);                  // row_bcast:31 into rows 2 and 3
     return v;
 }
 
@@ -338,35 +382,6 @@ __device__ void bitonic_asc(u64* buf, unsigned npad) {
             __syncthreads();
         }
     }
-}
-
-// Value of lane (lane ^ jl) for jl in {1, 2, 4, 8, 16, 32}, without LDS: DPP
-// quad permutes (1, 2), row rotates (4: by 4 or 12 depending on the lane, 8)
-// and the permlane swaps of 16- and 32-lane halves.
-__device__ __forceinline__ unsigned lane_xor32(unsigned x, unsigned jl) {
-    const unsigned l = lane_id();
-    switch (jl) {
-    case 1: return __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false);     // quad_perm 1,0,3,2
-    case 2: return __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false);     // quad_perm 2,3,0,1
-    case 4: {
-        const unsigned dn = __builtin_amdgcn_mov_dpp(x, 0x124, 0xF, 0xF, false);   // row_ror:4
-        const unsigned up = __builtin_amdgcn_mov_dpp(x, 0x12C, 0xF, 0xF, false);   // row_ror:12
-        return (l & 4) ? dn : up;
-    }
-    case 8: return __builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, false);    // row_ror:8
-    case 16: {
-        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
-        return (l & 16) ? r[0] : r[1];
-    }
-    default: {
-        const auto q = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-        return (l & 32) ? q[0] : q[1];
-    }
-    }
-}
-
-__device__ __forceinline__ u64 lane_xor64(u64 v, unsigned jl) {
-    return ((u64)lane_xor32((unsigned)(v >> 32), jl) << 32) | lane_xor32((unsigned)v, jl);
 }
 
 // Largest list sorted in LDS: 1024 threads with up to kRegKeys keys each.
