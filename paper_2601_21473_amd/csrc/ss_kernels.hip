@@ -34,6 +34,12 @@ typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ unsigned lane_id() { return __lane_id(); }
 
+// Lane 0's value in every lane (a scalar read: every caller has all lanes
+// active, so lane 0 is the first active lane).
+__device__ __forceinline__ unsigned lane0(unsigned v) {
+    return (unsigned)__builtin_amdgcn_readfirstlane((int)v);
+}
+
 __device__ __forceinline__ unsigned mbcnt(u64 mask) {
     return __builtin_amdgcn_mbcnt_hi((unsigned)(mask >> 32),
                                      __builtin_amdgcn_mbcnt_lo((unsigned)mask, 0u));
@@ -163,7 +169,7 @@ __device__ __forceinline__ unsigned wave_reserve(bool pred, unsigned* counter) {
     if (mask == 0) return 0;                         // wave-uniform
     unsigned base = 0;
     if (lane_id() == 0) base = atomicAdd(counter, (unsigned)__popcll(mask));
-    return __shfl(base, 0) + mbcnt(mask);
+    return lane0(base) + mbcnt(mask);
 }
 
 // Block-local slots of this lane in the three class lists: lane 0 issues the
@@ -177,9 +183,9 @@ __device__ __forceinline__ void wave_reserve3(const AgentClass& c, PlanCounters*
         if (mL) bL = atomicAdd(&cnt->n_L, (unsigned)__popcll(mL));
         if (mC) bC = atomicAdd(&cnt->n_C, (unsigned)__popcll(mC));
     }
-    oE = __shfl(bE, 0) + mbcnt(mE);
-    oL = __shfl(bL, 0) + mbcnt(mL);
-    oC = __shfl(bC, 0) + mbcnt(mC);
+    oE = lane0(bE) + mbcnt(mE);
+    oL = lane0(bL) + mbcnt(mL);
+    oC = lane0(bC) + mbcnt(mC);
 }
 
 // Add every thread's sums to the block counters *cnt (LDS): one reduction per
@@ -314,7 +320,7 @@ __device__ __forceinline__ void gather_keys(const u64* src, unsigned n, Keep kee
         if (total) {                                 // wave-uniform
             unsigned off = 0;
             if (lane_id() == 0) off = atomicAdd(counter, total);
-            off = __shfl(off, 0);
+            off = lane0(off);
 #pragma unroll
             for (unsigned u = 0; u < kGatherLoads; ++u) {
                 const unsigned pos = off + mbcnt(mask[u]);
