@@ -45,7 +45,9 @@
  * library owns its internal HIP streams (all at the default priority).  Work
  * of a call starts after the work the caller has queued on `stream` before
  * the call; ss_prefetch_unpack makes `stream` wait for the whole step (both
- * directions of the copy) before the caller's later work on it.
+ * directions of the copy) before the caller's later work on it.  A step
+ * whose moves are all direct transfers (ss_pool_desc.direct_bytes) queues
+ * its kernels on `stream` itself. 
  *
  * Errors.  No C++ exception crosses this boundary.  Every call returns an
  * ss_status; ss_last_error() gives a message for the calling thread.

@@ -19,7 +19,9 @@
 // pinned host copy over the host link, at the addresses the block-table
 // kernels record per moved unit.  Small steps are latency-bound, and one
 // launch costs less than the copy commands of every agent.  A direct unpack
-// that overwrites released units waits for the step's last pack.
+// that overwrites released units waits for the step's last pack.  A step
+// whose moves are all direct runs on the caller's stream (block-table update,
+// pack, unpack), so it crosses no hardware queue after the plan.
 //
 // The two streams are shared by all pools of a device, so any number of pools
 // (plus the caller's stream) fits in the four hardware queues the HIP runtime
@@ -150,6 +152,7 @@ struct ss_pool {
     std::vector<hipEvent_t> ev_packed;            // per eviction slot index in the step
     unsigned n_pack_step = 0;                     // pack launches of the current step
     bool direct_out = false;                      // this step's eviction went direct
+    bool inline_step = false;                     // this step runs on the caller's stream
 
     // timing (SS_FLAG_TIMING): one pair per launch or per slot's copies
     std::vector<TimedPair> t_pack, t_unpack, t_d2h, t_h2d, t_dout, t_din;
@@ -248,6 +251,9 @@ void free_pool(ss_pool* p) {
     hipStream_t sts[] = {p->st_out, p->st_in};
     for (hipStream_t s : sts)
         if (s) (void)hipStreamSynchronize(s);
+    // work of steps that ran on a caller's stream
+    for (hipEvent_t e : {p->ev_planned, p->ev_bt, p->ev_out_done, p->ev_in_done})
+        if (e) (void)hipEventSynchronize(e);
     void* dptrs[] = {p->d_units, p->d_agent_off, p->d_bt, p->d_resident, p->d_occ, p->d_cnt,
                      p->d_listE, p->d_listC, p->d_listL, p->d_sortE, p->d_sortC, p->d_sortL,
                      p->d_prefE, p->d_prefC, p->d_loff, p->d_victims, p->d_loads, p->d_vunits,
@@ -408,8 +414,10 @@ ss_status collect_all_timing(ss_pool* p) {
     return SS_OK;
 }
 
-// Queue the block-table update of the last plan on the out stream (once).
-ss_status flush_bt(ss_pool* p) {
+// Queue the block-table update of the last plan (once): on the out stream, or
+// on `s` for a step that runs on the caller's stream.
+ss_status flush_bt(ss_pool* p, hipStream_t s = nullptr) {
+    if (!s) s = p->st_out;
     if (!p->bt_pending) return SS_OK;
     BtArgs B{};
     B.res = p->d_res;
@@ -433,9 +441,9 @@ ss_status flush_bt(ss_pool* p) {
     B.whost = p->d_whost;
     B.lhost = p->d_lhost;
     p->bt_pending = false;
-    TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_planned, 0), true);
-    TRY_HIP(p, launch_bt_update(B, p->N, p->st_out), true);
-    TRY_HIP(p, hipEventRecord(p->ev_bt, p->st_out), true);
+    TRY_HIP(p, hipStreamWaitEvent(s, p->ev_planned, 0), true);
+    TRY_HIP(p, launch_bt_update(B, p->N, s), true);
+    TRY_HIP(p, hipEventRecord(p->ev_bt, s), true);
     return SS_OK;
 }
 
@@ -844,18 +852,32 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
     if (st) return st;
     if (p->state != kPlanned) return set_err(SS_ERR_ORDER, "ss_evict_pack must follow ss_plan_step");
     DeviceGuard g(p->device);
-    st = flush_bt(p);
-    if (st) return st;
-    st = collect_plan_timing(p);
-    if (st) return st;
     hipStream_t caller = static_cast<hipStream_t>(stream);
-    const bool timing = p->flags & SS_FLAG_TIMING;
-    TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_caller, 0), true);
-
     const u64 total = p->res.units_written;
     const u64 ups = p->units_per_slot;
     const bool direct = p->direct_bytes && total && total * p->unit_bytes <= p->direct_bytes;
+    // A step whose moves are all direct (or empty) runs on the caller's
+    // stream: block-table update, pack and unpack queue behind the plan on one
+    // hardware queue, without the cross-queue waits that cost more than such
+    // a step's kernels.
+    const u64 total_in = p->res.units_in;
+    const bool direct_in = p->direct_bytes && total_in &&
+                           total_in * p->unit_bytes <= p->direct_bytes;
+    p->inline_step = p->direct_bytes && (total == 0 || direct) && (total_in == 0 || direct_in);
+    hipStream_t so = p->inline_step ? caller : p->st_out;
+    st = flush_bt(p, so);
+    if (st) return st;
+    st = collect_plan_timing(p);
+    if (st) return st;
+    const bool timing = p->flags & SS_FLAG_TIMING;
+    if (p->inline_step) {
+        // after a block-table update queued earlier on the out stream
+        TRY_HIP(p, hipStreamWaitEvent(so, p->ev_bt, 0), true);
+    } else {
+        TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
+        TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_caller, 0), true);
+    }
+
     const u64 nslots = direct ? 1 : (total + ups - 1) / ups;
     while (p->ev_packed.size() < nslots) {
         hipEvent_t ev;
@@ -884,11 +906,11 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
         if (timing) {
             TRY_HIP(p, timed_pair(p->t_dout, p->n_t_dout++, &tp), true);
             tp->bytes = total * p->unit_bytes;
-            TRY_HIP(p, hipEventRecord(tp->a, p->st_out), true);
+            TRY_HIP(p, hipEventRecord(tp->a, so), true);
         }
-        TRY_HIP(p, launch_pack(C, p->st_out), true);
-        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_out), true);
-        TRY_HIP(p, hipEventRecord(p->ev_packed[0], p->st_out), true);
+        TRY_HIP(p, launch_pack(C, so), true);
+        if (timing) TRY_HIP(p, hipEventRecord(tp->b, so), true);
+        TRY_HIP(p, hipEventRecord(p->ev_packed[0], so), true);
     }
     size_t vi = 0;
     for (u64 k = 0; !direct && k < nslots; ++k) {
@@ -924,7 +946,7 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
         }
         if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_out), true);
     }
-    TRY_HIP(p, hipEventRecord(p->ev_out_done, p->st_out), true);
+    TRY_HIP(p, hipEventRecord(p->ev_out_done, so), true);
     p->state = kPacked;
     return SS_OK;
 }
@@ -937,9 +959,12 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
     DeviceGuard g(p->device);
     hipStream_t caller = static_cast<hipStream_t>(stream);
     const bool timing = p->flags & SS_FLAG_TIMING;
-    TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_caller, 0), true);
-    TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_bt, 0), true);
+    hipStream_t si = p->inline_step ? caller : p->st_in;
+    if (!p->inline_step) {
+        TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
+        TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_caller, 0), true);
+    }
+    TRY_HIP(p, hipStreamWaitEvent(si, p->ev_bt, 0), true);
 
     const u64 total = p->res.units_in;
     const u64 ups = p->units_per_slot;
@@ -960,7 +985,7 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
         // one launch scatters every load straight from its host copy; units
         // released this step are overwritten only after the packs read them
         if (total > nF && p->n_pack_step)
-            TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_packed[p->n_pack_step - 1], 0), true);
+            TRY_HIP(p, hipStreamWaitEvent(si, p->ev_packed[p->n_pack_step - 1], 0), true);
         C.first = 0;
         C.count = total;
         C.staging = p->host_dev;
@@ -969,10 +994,10 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
         if (timing) {
             TRY_HIP(p, timed_pair(p->t_din, p->n_t_din++, &tp), true);
             tp->bytes = total * p->unit_bytes;
-            TRY_HIP(p, hipEventRecord(tp->a, p->st_in), true);
+            TRY_HIP(p, hipEventRecord(tp->a, si), true);
         }
-        TRY_HIP(p, launch_unpack(C, p->st_in), true);
-        if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_in), true);
+        TRY_HIP(p, launch_unpack(C, si), true);
+        if (timing) TRY_HIP(p, hipEventRecord(tp->b, si), true);
     }
     size_t li = 0, ri = 0;
     // host-to-device copies of slot k into the ring
@@ -1050,9 +1075,14 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
         st = issue_unpack(nslots - 1);
         if (st) return st;
     }
-    TRY_HIP(p, hipEventRecord(p->ev_in_done, p->st_in), true);
-    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_in_done, 0), true);
-    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_out_done, 0), true);
+    TRY_HIP(p, hipEventRecord(p->ev_in_done, si), true);
+    if (!p->inline_step) {
+        TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_in_done, 0), true);
+        TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_out_done, 0), true);
+    } else {
+        // an eviction queued on another caller stream
+        TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_out_done, 0), true);
+    }
     p->state = kIdle;
     return SS_OK;
 }
@@ -1082,6 +1112,7 @@ ss_status ss_block_table_host(ss_pool* p, uint32_t agent, int32_t* out, uint32_t
     u64 off = 0;
     for (uint32_t a = 0; a < agent; ++a) off += p->s[a];
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
+    TRY_HIP(p, hipEventSynchronize(p->ev_bt), false);     // an update queued on a caller's stream
     TRY_HIP(p, hipMemcpy(out, p->d_bt + off, s * sizeof(int32_t), hipMemcpyDeviceToHost), false);
     return SS_OK;
 }
@@ -1099,6 +1130,7 @@ ss_status ss_block_table_host_all(ss_pool* p, int32_t* out, uint64_t cap, uint64
     st = flush_bt(p);
     if (st) return st;
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
+    TRY_HIP(p, hipEventSynchronize(p->ev_bt), false);     // an update queued on a caller's stream
     TRY_HIP(p, hipMemcpy(out, p->d_bt, total * sizeof(int32_t), hipMemcpyDeviceToHost), false);
     return SS_OK;
 }
@@ -1111,6 +1143,7 @@ ss_status ss_resident_host(ss_pool* p, uint8_t* out) {
     st = flush_bt(p);
     if (st) return st;
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
+    TRY_HIP(p, hipEventSynchronize(p->ev_bt), false);     // an update queued on a caller's stream
     TRY_HIP(p, hipMemcpy(out, p->d_resident, p->N, hipMemcpyDeviceToHost), false);
     return SS_OK;
 }
@@ -1145,6 +1178,9 @@ ss_status ss_sync(ss_pool* p) {
     if (st) return st;
     for (hipStream_t s : {p->st_out, p->st_in})
         TRY_HIP(p, hipStreamSynchronize(s), true);
+    // work of a step that ran on a caller's stream
+    for (hipEvent_t e : {p->ev_planned, p->ev_bt, p->ev_out_done, p->ev_in_done})
+        TRY_HIP(p, hipEventSynchronize(e), true);
     return SS_OK;
 }
 
