@@ -711,11 +711,13 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     hipStream_t caller = static_cast<hipStream_t>(stream);
 
     // The plan kernels run on the caller's stream, after the caller's earlier
-    // work (which may produce the distances) and after the previous step's
-    // loads (which read the plan buffers this plan rewrites; that step's
-    // block-table update precedes them).  The block-table update of this plan
-    // is queued on the out stream behind ev_planned (flush_bt).
+    // work (which may produce the distances), after the previous step's loads
+    // (which read the plan buffers this plan rewrites) and after the previous
+    // plan's block-table update (which an overcommitted plan's successor on
+    // another stream must not overtake).  This plan's block-table update is
+    // queued behind it on the same stream.
     TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_in_done, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_bt, 0), true);
 
     PlanArgs A{};
     A.dist = distances;
@@ -768,6 +770,15 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     TRY_HIP(p, launch_plan(A, caller), true);
     if (timing) TRY_HIP(p, hipEventRecord(p->t_plan[tslot].b, caller), true);
     TRY_HIP(p, hipEventRecord(p->ev_planned, caller), true);
+    // The block-table update queues right behind the plan kernel, on the same
+    // stream, while the host waits for the plan: it needs nothing from the
+    // host, and the step's first transfer then finds it done.  (After an
+    // overcommitted plan its kernels see the status and change nothing.)
+    p->bt_pending = true;
+    {
+        const ss_status sb = flush_bt(p, caller);
+        if (sb) return sb;
+    }
 
     const auto h1 = std::chrono::steady_clock::now();
     // The kernel's last write is the sequence number into the mapped flag
@@ -803,7 +814,6 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
                        (unsigned long long)p->U);
     }
     p->res = r;
-    p->bt_pending = true;
     p->voff.resize(r.n_victims + 1);
     p->loff.resize(r.n_loads + 1);
     p->voff[0] = 0;
@@ -870,13 +880,13 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
     st = collect_plan_timing(p);
     if (st) return st;
     const bool timing = p->flags & SS_FLAG_TIMING;
-    if (p->inline_step) {
-        // after a block-table update queued earlier on the out stream
-        TRY_HIP(p, hipStreamWaitEvent(so, p->ev_bt, 0), true);
-    } else {
+    if (!p->inline_step) {
         TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
         TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_caller, 0), true);
     }
+    // The packs read the unit lists the block-table update writes; it was
+    // queued on the plan's stream, which need not be this call's.
+    TRY_HIP(p, hipStreamWaitEvent(so, p->ev_bt, 0), true);
 
     const u64 nslots = direct ? 1 : (total + ups - 1) / ups;
     while (p->ev_packed.size() < nslots) {

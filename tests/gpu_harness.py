@@ -76,12 +76,14 @@ def fill_host(mem, content, spec, batch_bytes=256 << 20):
 
 def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_bytes=True,
                slot_units=8, ring_slots=2, sample_units=None, bt_every=1, seed=0, label="",
-               dirty=None, device_inputs=None, direct_bytes=0, stream=0, before_plan=None):
+               dirty=None, device_inputs=None, direct_bytes=0, stream=0, before_plan=None,
+               move_stream=None):
     """``device_inputs(t) -> (distances_ptr, active_ptr)`` replaces the uploaded
     trace on the HIP side (the oracle side always reads ``trace``).
     ``direct_bytes``: the pool's direct-transfer limit (0 = always staged).
     ``stream``: the caller's stream of every call; ``before_plan(t, stream)``
-    may queue work there before step t's plan."""
+    may queue work there before step t's plan.  ``move_stream``: the caller's
+    stream of ``evict_pack`` and ``prefetch_unpack`` if not ``stream``."""
     spec = trace.pools[pool_index]
     ub = spec.unit_bytes
     staging_bytes = 2 * ring_slots * slot_units * ub
@@ -126,8 +128,9 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
         assert g["n_demand_victims"] == o.n_demand_victims, (label, t)
         assert g["units_out"] == o.units_out and g["units_in"] == o.units_in, (label, t)
         assert g["bytes_out"] == o.bytes_out and g["bytes_in"] == o.bytes_in, (label, t)
-        pool.evict_pack(stream)
-        pool.prefetch_unpack(stream)
+        ms = stream if move_stream is None else move_stream
+        pool.evict_pack(ms)
+        pool.prefetch_unpack(ms)
         pool.sync()
         moved += o.units_in + o.units_out
         if t % bt_every == 0 or t == T - 1:

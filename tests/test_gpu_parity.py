@@ -267,6 +267,42 @@ def test_plan_queued_behind_long_work():
             b.free()
 
 
+@pytest.mark.parametrize("direct", [0, 1 << 20])
+def test_moves_on_another_stream_than_the_plan(direct):
+    # The plan runs on one caller stream (behind kernels queued there every
+    # other step) and the step's moves on another: the packs and unpacks must
+    # still follow the plan's block-table update, queued on the plan's stream.
+    n = 50_000
+    rng = np.random.default_rng(23)
+    pos = np.ascontiguousarray(rng.integers(0, 4096, size=(n, 2)).astype(np.int32))
+    p = DeviceBuffer(pos.nbytes)
+    p.upload(pos)
+    d = DeviceBuffer(4 * n)
+    d.upload(rng.integers(0, 1000, size=n).astype(np.uint32))
+    out = DeviceBuffer(4 * n)
+    wsb = B.interaction_distances_workspace(n)
+    ws = DeviceBuffer(max(wsb, 4))
+    s_plan, s_move = B.Stream(), B.Stream()
+
+    def busy(t, stream):
+        if t % 2 == 0:
+            for _ in range(4):
+                B.interaction_distances(p.ptr, d.ptr, n, 3, 2, out.ptr, ws.ptr, wsb, stream)
+
+    try:
+        tr = synthetic_trace(300, 120, 12, 25, seed=23, chunk_bytes=(16,))
+        run_parity(tr, theta=S, slot_units=32, ring_slots=2, stream=s_plan.handle,
+                   move_stream=s_move.handle, before_plan=busy, direct_bytes=direct,
+                   label=f"moves on another stream, direct={direct}")
+    finally:
+        s_plan.sync()
+        s_move.sync()
+        s_plan.close()
+        s_move.close()
+        for b in (p, d, out, ws):
+            b.free()
+
+
 def test_empty_steps_and_idle_pool():
     tr = synthetic_trace(100, 40, 30, lambda t, r: 0 if t % 3 else r.integers(0, 30), seed=2)
     run_parity(tr, theta=S, slot_units=5, ring_slots=2, label="empty steps")
