@@ -172,14 +172,15 @@ void ss_pool_destroy(ss_pool* pool);
  * the block table.  `distances` [N] uint32 and `active` [N] uint8 (0/1) are
  * DEVICE pointers read during the call's kernels, which run on `stream`
  * after the work queued there before the call and after the previous step's
- * loads.  The call returns once the plan is known on the host: the plan
- * kernel writes its lists into mapped host memory and, last, a sequence
- * number that the call polls (for up to 2 ms, then it waits on the kernel's
- * completion event); by then the kernel has finished reading `distances`
- * and `active`, though it may still be ending on the device.  The block-table
- * update that the plan implies is queued on the device by the next call that
- * needs it (ss_evict_pack, ss_block_table*, ss_resident_host, ss_sync) and is
- * ordered before the copy kernels.
+ * loads and block-table update.  The call returns once the plan is known on
+ * the host: the plan kernel writes its lists into mapped host memory and,
+ * last, a sequence number that the call polls (for up to 2 ms, then it waits
+ * on the kernel's completion event); by then the kernel has finished reading
+ * `distances` and `active`, though it may still be ending on the device.  The
+ * block-table update that the plan implies is queued on `stream` right behind
+ * the plan kernel (after an overcommitted plan it changes nothing); the copy
+ * kernels of ss_evict_pack and ss_prefetch_unpack wait for it whatever
+ * stream those calls are given.
  * SS_ERR_OVERCOMMIT if the active agents need more than capacity_units
  * (pool unchanged).  SS_ERR_ORDER if the previous step was not completed with
  * ss_evict_pack and ss_prefetch_unpack. */
@@ -204,9 +205,9 @@ ss_status ss_prefetch_unpack(ss_pool* pool, void* stream);
 
 /* The device block table in CSR form: agent a's logical unit j is physical
  * unit (*d_units)[(*d_agent_off)[a] + j], or -1 when a is not resident.
- * Pool-owned device memory, valid until ss_pool_destroy.  The call queues any
- * pending block-table update; the table is current once that work has run
- * (for instance after ss_sync). */
+ * Pool-owned device memory, valid until ss_pool_destroy.  The table is
+ * current once the update queued by the last ss_plan_step has run (for
+ * instance after ss_sync). */
 ss_status ss_block_table(ss_pool* pool, const int32_t** d_units, const uint64_t** d_agent_off);
 
 /* Copy agent's block-table row to host (synchronous).  *n = agent's units;
