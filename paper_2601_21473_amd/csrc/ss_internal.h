@@ -43,6 +43,29 @@ struct CopyItem {
     u64 unit_off;
 };
 
+struct BtArgs {
+    const PlanResult* res;
+    const unsigned* victims;
+    const unsigned* loads;
+    const unsigned* units;          // s[a]
+    const u64* agent_off;           // [N+1] block-table CSR offsets
+    int* bt;                        // [sum s]
+    unsigned* occ;
+    const u64* voff;                // = prefE: prefix units over victims
+    const u64* loff;
+    const int* free_old;
+    int* vunits;                    // [U] victims' old units, victim then j order
+    int* lunits;                    // [U] loads' new units, load then j order
+    u64 capacity;                   // U
+    const unsigned char* vwritten;  // [N] per victim: written back
+    const u64* woff;                // [N+1] prefix units over written-back victims
+    int* wunits;                    // [U] written-back victims' units (pack source)
+    const u64* host_off;            // [N] host-copy byte offset per agent (direct mode, else null)
+    u64 unit_bytes;
+    u64* whost;                     // [U] host byte offset of each written-back unit (or null)
+    u64* lhost;                     // [U] host byte offset of each loaded unit (or null)
+};
+
 struct PlanArgs {
     const unsigned* dist;           // [N] caller distances (device)
     const unsigned char* active;    // [N] caller mask (device)
@@ -86,6 +109,7 @@ struct PlanArgs {
     unsigned* flag_host;            // mapped pinned host word: `seq` is written there last
     unsigned seq;                   // this plan's sequence number (never 0)
     unsigned pad3;
+    const BtArgs* bt;               // block-table update (device copy), run in the fused core's tail
 };
 
 // Candidate distance histogram: bucket(d) = d below 1024, then 32 buckets per
@@ -99,28 +123,6 @@ __host__ __device__ inline unsigned dist_bucket(unsigned d) {
 
 constexpr int kPlanPhases = 10;
 
-struct BtArgs {
-    const PlanResult* res;
-    const unsigned* victims;
-    const unsigned* loads;
-    const unsigned* units;          // s[a]
-    const u64* agent_off;           // [N+1] block-table CSR offsets
-    int* bt;                        // [sum s]
-    unsigned* occ;
-    const u64* voff;                // = prefE: prefix units over victims
-    const u64* loff;
-    const int* free_old;
-    int* vunits;                    // [U] victims' old units, victim then j order
-    int* lunits;                    // [U] loads' new units, load then j order
-    u64 capacity;                   // U
-    const unsigned char* vwritten;  // [N] per victim: written back
-    const u64* woff;                // [N+1] prefix units over written-back victims
-    int* wunits;                    // [U] written-back victims' units (pack source)
-    const u64* host_off;            // [N] host-copy byte offset per agent (direct mode, else null)
-    u64 unit_bytes;
-    u64* whost;                     // [U] host byte offset of each written-back unit (or null)
-    u64* lhost;                     // [U] host byte offset of each loaded unit (or null)
-};
 
 struct CopyArgs {
     const int* units_list;          // vunits (pack) or lunits (unpack)

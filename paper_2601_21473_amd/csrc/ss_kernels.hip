@@ -14,10 +14,12 @@
 //                to a mapped host mirror, published by a sequence number
 //                written last.
 //   k_plan_core      the plan core, classifying the agents itself
-//                    (N <= kFuseAgents = 12,288);
+//                    (N <= kFuseAgents = 12,288) and, after publishing the
+//                    plan, updating the block table;
 //   k_classify_core  classification over N / 4096 workgroups, the last of
 //                    which runs the plan core (larger N), in one launch.
-//   k_bt_victims / k_bt_loads   block-table release and allocation.
+//   k_bt_victims / k_bt_loads   block-table release and allocation after
+//                    k_classify_core.
 // Data movement:
 //   k_copy<pack>  gathers (pack) or scatters (unpack) whole units between the
 //                pool's planes and a contiguous staging slot, one wave per
@@ -662,6 +664,104 @@ __device__ __forceinline__ void classify_fused(const PlanArgs& A, CoreShared& S)
 // Publish the plan to the host: every thread's host-visible writes are made
 // visible at system scope, then one thread writes the plan's sequence number
 // to the mapped flag word, which the host polls.  Last action of the core.
+// Release one victim's units j0, j0 + jstep, ... < s (block-table row at
+// `base`, eviction-order offset o, written-back offset ow, host-copy offset
+// hoff): record them in eviction order for the loads (and, for a victim that
+// is written back, for the pack), clear the block-table entries and the
+// units' occupancy bits.
+__device__ __forceinline__ void bt_release_units(const BtArgs& B, u64 base, unsigned s, u64 o,
+                                                 bool written, u64 ow, u64 hoff, unsigned j0,
+                                                 unsigned jstep) {
+    for (unsigned j = j0; j < s; j += jstep) {
+        const int u = B.bt[base + j];
+        B.vunits[o + j] = u;
+        if (written) {
+            B.wunits[ow + j] = u;
+            if (B.whost) B.whost[ow + j] = hoff + (u64)j * B.unit_bytes;
+        }
+        B.bt[base + j] = -1;
+        if ((u64)(unsigned)u < B.capacity)
+            atomicAnd(&B.occ[(unsigned)u >> 5], ~(1u << ((unsigned)u & 31u)));
+    }
+}
+
+// Hand one load its units j0, j0 + jstep, ... < s (row at `base`, load-order
+// offset o): the pre-step free units first, then the victims' units in
+// eviction order (nF = free units used).
+__device__ __forceinline__ void bt_assign_units(const BtArgs& B, u64 base, unsigned s, u64 o,
+                                                u64 hoff, u64 nF, unsigned j0, unsigned jstep) {
+    for (unsigned j = j0; j < s; j += jstep) {
+        const u64 q = o + j;
+        const int u = q < nF ? B.free_old[q] : B.vunits[q - nF];
+        B.bt[base + j] = u;
+        B.lunits[q] = u;
+        if (B.lhost) B.lhost[q] = hoff + (u64)j * B.unit_bytes;
+        if ((u64)(unsigned)u < B.capacity)
+            atomicOr(&B.occ[(unsigned)u >> 5], 1u << ((unsigned)u & 31u));
+    }
+}
+
+__device__ __forceinline__ unsigned lane_bcast(unsigned x, unsigned k) {
+    return (unsigned)__builtin_amdgcn_readlane((int)x, (int)k);
+}
+__device__ __forceinline__ u64 lane_bcast(u64 x, unsigned k) {
+    return ((u64)lane_bcast((unsigned)(x >> 32), k) << 32) | lane_bcast((unsigned)x, k);
+}
+
+// The block-table update inside one workgroup.  Wave w takes victims (then
+// loads) w, w + nw, ...; lane k of a batch loads the k-th of them first, so
+// the item-level loads of up to 64 items are in flight at once and each item
+// then costs one dependent load (its row or its units).
+__device__ __forceinline__ void bt_update_block(const BtArgs& B, unsigned n_v, unsigned n_l,
+                                                u64 nF) {
+    const unsigned wid = threadIdx.x >> 6, nw = blockDim.x >> 6, lane = lane_id();
+    for (unsigned i0 = wid; i0 < n_v; i0 += 64 * nw) {
+        const unsigned ik = i0 + lane * nw;
+        unsigned v = 0, w = 0, s = 0;
+        u64 o = 0, ow = 0, base = 0, hoff = 0;
+        if (ik < n_v) {
+            v = B.victims[ik];
+            o = B.voff[ik];
+            ow = B.woff[ik];
+            w = B.vwritten[ik];
+            base = B.agent_off[v];
+            s = B.units[v];
+            if (B.whost) hoff = B.host_off[v];
+        }
+        const unsigned rounds = min(64u, (n_v - i0 + nw - 1) / nw);
+        for (unsigned k = 0; k < rounds; ++k)
+            bt_release_units(B, lane_bcast(base, k), lane_bcast(s, k), lane_bcast(o, k),
+                             lane_bcast(w, k) != 0, lane_bcast(ow, k), lane_bcast(hoff, k),
+                             lane, 64u);
+    }
+    __syncthreads();                                 // the victims' units, before the loads take them
+    for (unsigned i0 = wid; i0 < n_l; i0 += 64 * nw) {
+        const unsigned ik = i0 + lane * nw;
+        unsigned s = 0;
+        u64 o = 0, base = 0, hoff = 0;
+        if (ik < n_l) {
+            const unsigned a = B.loads[ik];
+            o = B.loff[ik];
+            base = B.agent_off[a];
+            s = B.units[a];
+            if (B.lhost) hoff = B.host_off[a];
+        }
+        const unsigned rounds = min(64u, (n_l - i0 + nw - 1) / nw);
+        for (unsigned k = 0; k < rounds; ++k)
+            bt_assign_units(B, lane_bcast(base, k), lane_bcast(s, k), lane_bcast(o, k),
+                            lane_bcast(hoff, k), nF, lane, 64u);
+    }
+}
+
+// The fused plan core's tail, compiled apart (not inlined) so that its
+// registers do not weigh on the core's own allocation; its arguments come from
+// the pool's device copy, not from the kernel's.
+__device__ __attribute__((noinline)) void bt_tail(const BtArgs* Bp, unsigned n_v, unsigned n_l,
+                                                  u64 nF) {
+    const BtArgs B = *Bp;
+    bt_update_block(B, n_v, n_l, nF);
+}
+
 __device__ __forceinline__ void publish_plan(const PlanArgs& A) {
     __threadfence_system();
     __syncthreads();
@@ -673,16 +773,20 @@ __device__ __forceinline__ void publish_plan(const PlanArgs& A) {
 
 // The plan core: one workgroup of kCoreThreads threads; `lds` holds kLdsKeys
 // keys.  Inlined into both kernels below so that its LDS accesses stay LDS
-// instructions.
+// instructions.  kFused: the core classifies the agents itself and, after
+// publishing the plan, updates the block table (k_plan_core); otherwise it
+// runs in the last classifying workgroup of k_classify_core and the update is
+// left to k_bt_victims and k_bt_loads.
+template <bool kFused>
 __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShared& S) {
     const unsigned tid = threadIdx.x;
     auto stamp = [&](int k) {
         if (A.phase && tid == 0) A.phase[k] = wall_clock64();
     };
-    if (A.fused) stamp(0);                           // else stamped at the classifying kernel's entry
+    if (kFused) stamp(0);                           // else stamped at the classifying kernel's entry
     const u64 idmask = (1ull << A.idbits) - 1;
     const unsigned* units = A.units;
-    if (A.fused) {
+    if (kFused) {
         if (tid == 0) S.cnt = PlanCounters{};
         for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) S.histw[b] = 0;
         __syncthreads();
@@ -691,19 +795,19 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     }
     // the candidate histogram: this workgroup's LDS when it classified the
     // agents itself, else the global sum of all classifying workgroups
-    const u64* histw = A.fused ? S.histw : A.hist_w;
-    const PlanCounters c = A.fused ? S.cnt : *A.cnt;
+    const u64* histw = kFused ? S.histw : A.hist_w;
+    const PlanCounters c = kFused ? S.cnt : *A.cnt;
     __syncthreads();
     stamp(1);
 
     if (c.sum_active > A.capacity) {                 // overcommit: change nothing
-        if (!A.fused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
+        if (!kFused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
         if (tid == 0) {
             PlanResult r = {};
             r.status = 1;
             *A.res = r;
             *A.res_host = r;
-            if (!A.fused) *A.cnt = PlanCounters{};
+            if (!kFused) *A.cnt = PlanCounters{};
         }
         publish_plan(A);
         return;
@@ -811,9 +915,9 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
             kstar = weighted_select(A.listC, nC, units, idmask, cap, S, &m);
         }
         // the histogram starts the next step at zero
-        if (!A.fused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
+        if (!kFused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
     } else {
-        if (!A.fused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
+        if (!kFused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
     }
     stamp(3);
     if (!sorted) select_sort(A.listC, nC, kstar, m, A.sortC, lds, S);
@@ -962,15 +1066,21 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         r.units_written = A.woff[n_v];
         *A.res = r;
         *A.res_host = r;
-        if (!A.fused) *A.cnt = PlanCounters{};
+        if (!kFused) *A.cnt = PlanCounters{};
     }
     publish_plan(A);
+    if (!kFused) return;
+    // The host has the plan; the workgroup goes on to update the block table
+    // (waves over victims, then over loads), which saves the step two launches.
+    // Every list it reads was written above by this workgroup; the barrier
+    // inside publish_plan ordered those writes before these reads.
+    bt_tail(A.bt, n_v, n_l, n_free_used);
 }
 
 __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
     __shared__ u64 lds[kLdsKeys];
     __shared__ CoreShared S;
-    plan_core(A, lds, S);
+    plan_core<true>(A, lds, S);
 }
 
 // Classification over many workgroups, then the plan core in the workgroup
@@ -1038,60 +1148,33 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
     __threadfence();                                 // acquire every workgroup's writes
     if (threadIdx.x == 0) *A.done = 0;
     __syncthreads();
-    plan_core(A, lds, S);
+    plan_core<false>(A, lds, S);
 }
 
 // ---------------------------------------------------------------------------
 // block table
 // ---------------------------------------------------------------------------
 
-// Release the victims' units (one block per victim): record them in eviction
-// order for the loads (and, for victims that are written back, for the pack),
-// clear the block-table entries and the occupancy bits.
+// Standalone update (plans whose core did not classify the agents itself):
+// one block per victim, then, in a second launch, one block per load.
 __global__ void __launch_bounds__(256) k_bt_victims(BtArgs B) {
     if (B.res->status != 0) return;
     const unsigned nv = B.res->n_victims;
     for (unsigned i = blockIdx.x; i < nv; i += gridDim.x) {
         const unsigned v = B.victims[i];
-        const u64 base = B.agent_off[v];
-        const unsigned s = B.units[v];
-        const u64 o = B.voff[i];
-        const bool written = B.vwritten[i] != 0;
-        const u64 ow = B.woff[i];
-        for (unsigned j = threadIdx.x; j < s; j += blockDim.x) {
-            const int u = B.bt[base + j];
-            B.vunits[o + j] = u;
-            if (written) {
-                B.wunits[ow + j] = u;
-                if (B.whost) B.whost[ow + j] = B.host_off[v] + (u64)j * B.unit_bytes;
-            }
-            B.bt[base + j] = -1;
-            if ((u64)(unsigned)u < B.capacity)
-                atomicAnd(&B.occ[(unsigned)u >> 5], ~(1u << ((unsigned)u & 31u)));
-        }
+        bt_release_units(B, B.agent_off[v], B.units[v], B.voff[i], B.vwritten[i] != 0, B.woff[i],
+                         B.whost ? B.host_off[v] : 0, threadIdx.x, blockDim.x);
     }
 }
 
-// Hand units to the loads (one block per load): the pre-step free units
-// first, then the victims' units in eviction order.
 __global__ void __launch_bounds__(256) k_bt_loads(BtArgs B) {
     if (B.res->status != 0) return;
     const unsigned nl = B.res->n_loads;
     const u64 nF = B.res->n_free_used;
     for (unsigned i = blockIdx.x; i < nl; i += gridDim.x) {
         const unsigned a = B.loads[i];
-        const u64 base = B.agent_off[a];
-        const unsigned s = B.units[a];
-        const u64 o = B.loff[i];
-        for (unsigned j = threadIdx.x; j < s; j += blockDim.x) {
-            const u64 q = o + j;
-            const int u = q < nF ? B.free_old[q] : B.vunits[q - nF];
-            B.bt[base + j] = u;
-            B.lunits[q] = u;
-            if (B.lhost) B.lhost[q] = B.host_off[a] + (u64)j * B.unit_bytes;
-            if ((u64)(unsigned)u < B.capacity)
-                atomicOr(&B.occ[(unsigned)u >> 5], 1u << ((unsigned)u & 31u));
-        }
+        bt_assign_units(B, B.agent_off[a], B.units[a], B.loff[i], B.lhost ? B.host_off[a] : 0, nF,
+                        threadIdx.x, blockDim.x);
     }
 }
 

@@ -120,6 +120,7 @@ struct ss_pool {
     u64* d_host_off = nullptr;     // direct mode: [N] host-copy offsets
     u64 *d_whost = nullptr, *d_lhost = nullptr;   // direct mode: [U] per moved unit
     PlanResult* d_res = nullptr;
+    BtArgs* d_btargs = nullptr;    // the block-table update's arguments (pool constants)
     // timing mode: two plans' phase stamps in mapped host memory (the kernel
     // writes them, the host reads them directly) and two plans' event pairs,
     // so a plan's timing is folded one step later, when it is long complete
@@ -168,7 +169,6 @@ struct ss_pool {
 
     State state = kIdle;
     bool poisoned = false;
-    bool bt_pending = false;     // block-table update of the last plan not yet queued
 };
 
 namespace {
@@ -259,7 +259,8 @@ void free_pool(ss_pool* p) {
                      p->d_prefE, p->d_prefC, p->d_loff, p->d_victims, p->d_loads, p->d_vunits,
                      p->d_lunits, p->d_free_old, p->d_res, p->d_hist_w,
                      p->d_wunits, p->d_vwritten, p->d_woff, p->d_items, p->d_plane_base,
-                     p->d_chunk_bytes, p->d_done, p->d_host_off, p->d_whost, p->d_lhost};
+                     p->d_chunk_bytes, p->d_done, p->d_host_off, p->d_whost, p->d_lhost,
+                     p->d_btargs};
     for (void* d : dptrs)
         if (d) (void)hipFree(d);
     void* hptrs[] = {p->h_flag, p->h_phase, p->h_res, p->h_victims, p->h_loads, p->h_vwritten};
@@ -414,11 +415,8 @@ ss_status collect_all_timing(ss_pool* p) {
     return SS_OK;
 }
 
-// Queue the block-table update of the last plan (once): on the out stream, or
-// on `s` for a step that runs on the caller's stream.
-ss_status flush_bt(ss_pool* p, hipStream_t s = nullptr) {
-    if (!s) s = p->st_out;
-    if (!p->bt_pending) return SS_OK;
+// Arguments of the block-table update that follows each plan.
+BtArgs bt_args(const ss_pool* p) {
     BtArgs B{};
     B.res = p->d_res;
     B.victims = p->d_victims;
@@ -440,11 +438,7 @@ ss_status flush_bt(ss_pool* p, hipStream_t s = nullptr) {
     B.unit_bytes = p->unit_bytes;
     B.whost = p->d_whost;
     B.lhost = p->d_lhost;
-    p->bt_pending = false;
-    TRY_HIP(p, hipStreamWaitEvent(s, p->ev_planned, 0), true);
-    TRY_HIP(p, launch_bt_update(B, p->N, s), true);
-    TRY_HIP(p, hipEventRecord(p->ev_bt, s), true);
-    return SS_OK;
+    return B;
 }
 
 }  // namespace
@@ -680,6 +674,12 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
             CREATE_TRY(make_event(&tp.b, true));
         }
     }
+    {
+        // every pointer the block-table update uses is fixed from here on
+        const BtArgs B = bt_args(p);
+        CREATE_TRY(dalloc(&p->d_btargs, 1));
+        CREATE_TRY(hipMemcpy(p->d_btargs, &B, sizeof(BtArgs), hipMemcpyHostToDevice));
+    }
     CREATE_TRY(hipEventRecord(p->ev_out_done, p->st_out));
     CREATE_TRY(hipEventRecord(p->ev_in_done, p->st_in));
     CREATE_TRY(hipStreamSynchronize(p->st_out));
@@ -756,6 +756,7 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     A.vwritten_host = p->h_vwritten_dev;
     A.woff = p->d_woff;
     A.done = p->d_done;
+    A.bt = p->d_btargs;
     if (++p->plan_seq == 0) p->plan_seq = 1;
     A.flag_host = p->h_flag_dev;
     A.seq = p->plan_seq;
@@ -770,15 +771,13 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     TRY_HIP(p, launch_plan(A, caller), true);
     if (timing) TRY_HIP(p, hipEventRecord(p->t_plan[tslot].b, caller), true);
     TRY_HIP(p, hipEventRecord(p->ev_planned, caller), true);
-    // The block-table update queues right behind the plan kernel, on the same
-    // stream, while the host waits for the plan: it needs nothing from the
-    // host, and the step's first transfer then finds it done.  (After an
-    // overcommitted plan its kernels see the status and change nothing.)
-    p->bt_pending = true;
-    {
-        const ss_status sb = flush_bt(p, caller);
-        if (sb) return sb;
-    }
+    // The block-table update: a fused plan core runs it in its own tail,
+    // after publishing the plan; otherwise two kernels queue right behind the
+    // plan kernel on the same stream, while the host waits for the plan.
+    // Either way it needs nothing from the host, and it changes nothing after
+    // an overcommitted plan.
+    if (!A.fused) TRY_HIP(p, launch_bt_update(bt_args(p), p->N, caller), true);
+    TRY_HIP(p, hipEventRecord(p->ev_bt, caller), true);
 
     const auto h1 = std::chrono::steady_clock::now();
     // The kernel's last write is the sequence number into the mapped flag
@@ -875,8 +874,6 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
                            total_in * p->unit_bytes <= p->direct_bytes;
     p->inline_step = p->direct_bytes && (total == 0 || direct) && (total_in == 0 || direct_in);
     hipStream_t so = p->inline_step ? caller : p->st_out;
-    st = flush_bt(p, so);
-    if (st) return st;
     st = collect_plan_timing(p);
     if (st) return st;
     const bool timing = p->flags & SS_FLAG_TIMING;
@@ -1099,11 +1096,6 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
 
 ss_status ss_block_table(ss_pool* p, const int32_t** d_units, const uint64_t** d_agent_off) {
     if (!p || !d_units || !d_agent_off) return set_err(SS_ERR_ARG, "NULL argument");
-    if (!p->poisoned) {
-        DeviceGuard g(p->device);
-        ss_status st = flush_bt(p);
-        if (st) return st;
-    }
     *d_units = p->d_bt;
     *d_agent_off = reinterpret_cast<const uint64_t*>(p->d_agent_off);
     return SS_OK;
@@ -1117,8 +1109,6 @@ ss_status ss_block_table_host(ss_pool* p, uint32_t agent, int32_t* out, uint32_t
     *n = s;
     if (cap < s) return set_err(SS_ERR_ARG, "cap %u < %u units", cap, s);
     DeviceGuard g(p->device);
-    st = flush_bt(p);
-    if (st) return st;
     u64 off = 0;
     for (uint32_t a = 0; a < agent; ++a) off += p->s[a];
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
@@ -1137,8 +1127,6 @@ ss_status ss_block_table_host_all(ss_pool* p, int32_t* out, uint64_t cap, uint64
     if (cap < total) return set_err(SS_ERR_ARG, "cap %llu < %llu entries", (unsigned long long)cap,
                                     (unsigned long long)total);
     DeviceGuard g(p->device);
-    st = flush_bt(p);
-    if (st) return st;
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
     TRY_HIP(p, hipEventSynchronize(p->ev_bt), false);     // an update queued on a caller's stream
     TRY_HIP(p, hipMemcpy(out, p->d_bt, total * sizeof(int32_t), hipMemcpyDeviceToHost), false);
@@ -1150,8 +1138,6 @@ ss_status ss_resident_host(ss_pool* p, uint8_t* out) {
     if (st) return st;
     if (!out) return set_err(SS_ERR_ARG, "NULL output");
     DeviceGuard g(p->device);
-    st = flush_bt(p);
-    if (st) return st;
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
     TRY_HIP(p, hipEventSynchronize(p->ev_bt), false);     // an update queued on a caller's stream
     TRY_HIP(p, hipMemcpy(out, p->d_resident, p->N, hipMemcpyDeviceToHost), false);
@@ -1184,8 +1170,6 @@ ss_status ss_sync(ss_pool* p) {
     ss_status st = check_usable(p);
     if (st) return st;
     DeviceGuard g(p->device);
-    st = flush_bt(p);
-    if (st) return st;
     for (hipStream_t s : {p->st_out, p->st_in})
         TRY_HIP(p, hipStreamSynchronize(s), true);
     // work of a step that ran on a caller's stream
