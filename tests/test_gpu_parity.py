@@ -223,6 +223,20 @@ def test_lists_beyond_lds_sort_buffer():
                label="global sort path")
 
 
+@pytest.mark.parametrize("direct", [0, 1 << 20])
+def test_block_table_tail_many_items(direct):
+    # 1,190-1,790 victims and 1,190-4,400 loads per step among 12,001 agents
+    # (the fused plan core's limit is 12,288): more than the 16 waves x 64
+    # items that its block-table tail takes in one batch, so every wave runs
+    # more than one batch.
+    rng = np.random.default_rng(31)
+    n = 12001
+    units = rng.integers(1, 3, size=n).astype(np.uint32)
+    tr = synthetic_trace(n, 9000, 8, 4400, seed=31, units=units, chunk_bytes=(16,))
+    run_parity(tr, theta=0, slot_units=1024, ring_slots=2, direct_bytes=direct,
+               label=f"tail batches, direct={direct}")
+
+
 @pytest.mark.parametrize("n_agents", [4097, 12288, 12289])
 def test_classification_batch_edges(n_agents):
     # agent counts around the plan's one-workgroup limit (12,288) and one past
