@@ -236,6 +236,7 @@ class Pool:
         self._prm, self._out = ss_plan_params(), ss_plan()
         self._prm_ref, self._out_ref = C.byref(self._prm), C.byref(self._out)
         self._plan = L.ss_plan_step
+        self._views = {}            # numpy views of the pool-owned host lists, by address
 
     def close(self):
         if getattr(self, "_h", None):
@@ -264,16 +265,27 @@ class Pool:
                     "bytes_out": out.bytes_out, "bytes_in": out.bytes_in,
                     "n_victims": out.n_victims, "n_loads": out.n_loads}
         nv, nl = out.n_victims, out.n_loads
-        victims = (np.ctypeslib.as_array(out.victims, shape=(nv,)).copy() if nv
-                   else np.zeros(0, np.uint32))
-        loads = (np.ctypeslib.as_array(out.loads, shape=(nl,)).copy() if nl
-                 else np.zeros(0, np.uint32))
-        written = (np.ctypeslib.as_array(out.victim_written, shape=(nv,)).copy() if nv
-                   else np.zeros(0, np.uint8))
+        victims = self._host_list(out.victims, np.uint32)[:nv].copy()
+        loads = self._host_list(out.loads, np.uint32)[:nl].copy()
+        written = self._host_list(out.victim_written, np.uint8)[:nv].copy()
         return {"victims": victims, "loads": loads, "n_demand": out.n_demand,
                 "n_demand_victims": out.n_demand_victims, "units_out": out.units_out,
                 "units_in": out.units_in, "bytes_out": out.bytes_out, "bytes_in": out.bytes_in,
                 "units_written": out.units_written, "victim_written": written}
+
+    def _host_list(self, ptr, dtype) -> np.ndarray:
+        """A numpy view of N entries of one of the plan's host lists.  The
+        lists live in pool-owned host memory that keeps its address for the
+        pool's life, so the view is made once per address."""
+        addr = C.cast(ptr, C.c_void_p).value
+        if not addr:
+            return np.zeros(0, dtype)
+        v = self._views.get((addr, dtype))
+        if v is None:
+            ctype = C.c_uint32 if dtype == np.uint32 else C.c_uint8
+            v = np.ctypeslib.as_array((ctype * self.n_agents).from_address(addr))
+            self._views[(addr, dtype)] = v
+        return v
 
     def evict_pack(self, stream: int = 0):
         _check(load().ss_evict_pack(self._h, int(stream) or None))

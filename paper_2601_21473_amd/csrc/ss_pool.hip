@@ -154,6 +154,7 @@ struct ss_pool {
     unsigned n_pack_step = 0;                     // pack launches of the current step
     bool direct_out = false;                      // this step's eviction went direct
     bool inline_step = false;                     // this step runs on the caller's stream
+    hipStream_t bt_stream = nullptr;              // stream of the last plan's block-table update
 
     // timing (SS_FLAG_TIMING): one pair per launch or per slot's copies
     std::vector<TimedPair> t_pack, t_unpack, t_d2h, t_h2d, t_dout, t_din;
@@ -414,6 +415,11 @@ ss_status collect_all_timing(ss_pool* p) {
     fold_plan(p, 1);
     return SS_OK;
 }
+
+// The event that follows the last plan's block-table update: the plan's own
+// event when the plan kernel runs the update in its tail (N <= kFuseAgents,
+// fixed for a pool), else the event after the update's kernels.
+hipEvent_t bt_event(const ss_pool* p) { return p->N <= kFuseAgents ? p->ev_planned : p->ev_bt; }
 
 // Arguments of the block-table update that follows each plan.
 BtArgs bt_args(const ss_pool* p) {
@@ -717,7 +723,7 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     // another stream must not overtake).  This plan's block-table update is
     // queued behind it on the same stream.
     TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_in_done, 0), true);
-    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_bt, 0), true);
+    TRY_HIP(p, hipStreamWaitEvent(caller, bt_event(p), 0), true);
 
     PlanArgs A{};
     A.dist = distances;
@@ -776,8 +782,11 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     // plan kernel on the same stream, while the host waits for the plan.
     // Either way it needs nothing from the host, and it changes nothing after
     // an overcommitted plan.
-    if (!A.fused) TRY_HIP(p, launch_bt_update(bt_args(p), p->N, caller), true);
-    TRY_HIP(p, hipEventRecord(p->ev_bt, caller), true);
+    if (!A.fused) {
+        TRY_HIP(p, launch_bt_update(bt_args(p), p->N, caller), true);
+        TRY_HIP(p, hipEventRecord(p->ev_bt, caller), true);
+    }
+    p->bt_stream = caller;
 
     const auto h1 = std::chrono::steady_clock::now();
     // The kernel's last write is the sequence number into the mapped flag
@@ -881,9 +890,12 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
         TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
         TRY_HIP(p, hipStreamWaitEvent(p->st_out, p->ev_caller, 0), true);
     }
-    // The packs read the unit lists the block-table update writes; it was
-    // queued on the plan's stream, which need not be this call's.
-    TRY_HIP(p, hipStreamWaitEvent(so, p->ev_bt, 0), true);
+    // The packs read the unit lists the block-table update writes.  It was
+    // queued on the plan's stream: when that is this call's stream, the packs
+    // already follow it (on that stream, or behind ev_caller); otherwise they
+    // wait for it.  (A wait on another stream's pending event costs the host
+    // about 16 us.)
+    if (caller != p->bt_stream) TRY_HIP(p, hipStreamWaitEvent(so, bt_event(p), 0), true);
 
     const u64 nslots = direct ? 1 : (total + ups - 1) / ups;
     while (p->ev_packed.size() < nslots) {
@@ -971,7 +983,9 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
         TRY_HIP(p, hipEventRecord(p->ev_caller, caller), true);
         TRY_HIP(p, hipStreamWaitEvent(p->st_in, p->ev_caller, 0), true);
     }
-    TRY_HIP(p, hipStreamWaitEvent(si, p->ev_bt, 0), true);
+    // the unpacks write units the block-table update assigns (as in
+    // ss_evict_pack, the wait is implied when the plan ran on this stream)
+    if (caller != p->bt_stream) TRY_HIP(p, hipStreamWaitEvent(si, bt_event(p), 0), true);
 
     const u64 total = p->res.units_in;
     const u64 ups = p->units_per_slot;
@@ -1112,7 +1126,7 @@ ss_status ss_block_table_host(ss_pool* p, uint32_t agent, int32_t* out, uint32_t
     u64 off = 0;
     for (uint32_t a = 0; a < agent; ++a) off += p->s[a];
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
-    TRY_HIP(p, hipEventSynchronize(p->ev_bt), false);     // an update queued on a caller's stream
+    TRY_HIP(p, hipEventSynchronize(bt_event(p)), false);  // an update queued on a caller's stream
     TRY_HIP(p, hipMemcpy(out, p->d_bt + off, s * sizeof(int32_t), hipMemcpyDeviceToHost), false);
     return SS_OK;
 }
@@ -1128,7 +1142,7 @@ ss_status ss_block_table_host_all(ss_pool* p, int32_t* out, uint64_t cap, uint64
                                     (unsigned long long)total);
     DeviceGuard g(p->device);
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
-    TRY_HIP(p, hipEventSynchronize(p->ev_bt), false);     // an update queued on a caller's stream
+    TRY_HIP(p, hipEventSynchronize(bt_event(p)), false);  // an update queued on a caller's stream
     TRY_HIP(p, hipMemcpy(out, p->d_bt, total * sizeof(int32_t), hipMemcpyDeviceToHost), false);
     return SS_OK;
 }
@@ -1139,7 +1153,7 @@ ss_status ss_resident_host(ss_pool* p, uint8_t* out) {
     if (!out) return set_err(SS_ERR_ARG, "NULL output");
     DeviceGuard g(p->device);
     TRY_HIP(p, hipStreamSynchronize(p->st_out), false);
-    TRY_HIP(p, hipEventSynchronize(p->ev_bt), false);     // an update queued on a caller's stream
+    TRY_HIP(p, hipEventSynchronize(bt_event(p)), false);  // an update queued on a caller's stream
     TRY_HIP(p, hipMemcpy(out, p->d_resident, p->N, hipMemcpyDeviceToHost), false);
     return SS_OK;
 }
