@@ -177,10 +177,11 @@ void ss_pool_destroy(ss_pool* pool);
  * last, a sequence number that the call polls (for up to 2 ms, then it waits
  * on the kernel's completion event); by then the kernel has finished reading
  * `distances` and `active`, though it may still be ending on the device.  The
- * block-table update that the plan implies is queued on `stream` right behind
- * the plan kernel (after an overcommitted plan it changes nothing); the copy
- * kernels of ss_evict_pack and ss_prefetch_unpack wait for it whatever
- * stream those calls are given.
+ * block-table update that the plan implies runs on `stream` after the plan is
+ * published: in the plan kernel's own tail up to 12,288 agents, else as two
+ * kernels queued right behind it (after an overcommitted plan it changes
+ * nothing); the copy kernels of ss_evict_pack and ss_prefetch_unpack follow
+ * it whatever stream those calls are given.
  * SS_ERR_OVERCOMMIT if the active agents need more than capacity_units
  * (pool unchanged).  SS_ERR_ORDER if the previous step was not completed with
  * ss_evict_pack and ss_prefetch_unpack. */
