@@ -20,6 +20,7 @@ import pytest
 
 import workloads as W
 from gpu_harness import run_parity, synthetic_trace, upload_trace, log
+from oracle import OraclePool, OvercommitError
 from paper_2601_21473_amd import binding as B
 from paper_2601_21473_amd.memory import DeviceBuffer, PoolMemory
 
@@ -371,6 +372,54 @@ def test_overcommit_and_call_order():
     pool.close()
     dev.free()
     mem.free()
+
+
+@pytest.mark.parametrize("n_agents", [64, 12289])
+def test_overcommit_between_streams(n_agents):
+    # Overcommitted steps between good ones, each step's calls on another
+    # caller stream, with the plan core classifying the agents itself (64)
+    # and after the multi-workgroup classification (12,289, where the
+    # block-table update runs as kernels that must see the overcommit and
+    # change nothing): plans, block table and residency match the oracle.
+    cap = 40 if n_agents < 100 else 100
+    # active agents per step (unit-size agents): over capacity at steps 1 and
+    # 3, exactly at capacity at step 5
+    counts = [cap * 6 // 10, cap * 13 // 10, cap * 4 // 10, cap + 1, cap * 7 // 10, cap, cap // 2]
+    tr = synthetic_trace(n_agents, cap, len(counts), lambda t, r: counts[t], seed=n_agents,
+                         chunk_bytes=(16,))
+    spec = tr.pools[0]
+    mem = PoolMemory(spec, 2 * 2 * 16 * spec.unit_bytes, 2)
+    pool = mem.make_pool()
+    opool = OraclePool(spec.capacity_units, spec.agent_units, spec.unit_bytes)
+    dev = upload_trace(tr)
+    streams = [B.Stream(), B.Stream()]
+    try:
+        for t in range(tr.n_steps):
+            st = streams[t % 2].handle
+            log(f"[overcommit] N={n_agents} step {t} active={counts[t]}")
+            if counts[t] > spec.capacity_units:
+                with pytest.raises(B.OvercommitError):
+                    pool.plan_step(dev.dist(t), dev.active(t), S, None, st)
+                with pytest.raises(OvercommitError):
+                    opool.plan_step(tr.dist[t], tr.active[t], S)
+            else:
+                g = pool.plan_step(dev.dist(t), dev.active(t), S, None, st)
+                o = opool.plan_step(tr.dist[t], tr.active[t], S)
+                assert g["victims"].tolist() == o.victims.tolist(), (n_agents, t)
+                assert g["loads"].tolist() == o.loads.tolist(), (n_agents, t)
+                pool.evict_pack(st)
+                pool.prefetch_unpack(st)
+            pool.sync()
+            obt = np.concatenate(opool.bt).astype(np.int32)
+            assert np.array_equal(pool.block_table_host_all(), obt), (n_agents, t)
+            assert np.array_equal(pool.resident_host().astype(bool), opool.resident), (n_agents, t)
+    finally:
+        for s_ in streams:
+            s_.sync()
+            s_.close()
+        pool.close()
+        dev.free()
+        mem.free()
 
 
 def test_host_pointer_for_distances_is_rejected():
