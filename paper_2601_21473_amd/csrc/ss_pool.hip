@@ -720,8 +720,8 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     // work (which may produce the distances), after the previous step's loads
     // (which read the plan buffers this plan rewrites) and after the previous
     // plan's block-table update (which an overcommitted plan's successor on
-    // another stream must not overtake).  This plan's block-table update is
-    // queued behind it on the same stream.
+    // another stream must not overtake).  This plan's block-table update runs
+    // after the plan on the same stream.
     TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_in_done, 0), true);
     TRY_HIP(p, hipStreamWaitEvent(caller, bt_event(p), 0), true);
 
