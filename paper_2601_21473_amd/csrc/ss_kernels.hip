@@ -1004,8 +1004,18 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     const u64 units_out = A.prefE[n_v];
     const u64 units_in = c.sum_demand + A.prefC[n_p];
 
-    // plan lists, load offsets, residency
-    for (unsigned i = tid; i < n_v; i += blockDim.x) {
+    // plan lists, load offsets, residency (victims and loads are disjoint)
+    for (unsigned i = tid; i < n_l; i += blockDim.x) {
+        const unsigned a = (unsigned)((i < nL ? A.sortL[i] : sortC[i - nL]) & idmask);
+        A.loads[i] = a;
+        A.loads_host[i] = a;
+        A.resident[a] = 1;
+        if (i >= nL) A.loff[i + 1] = c.sum_demand + A.prefC[i - nL + 1];
+    }
+    // the victims, and the offsets of the written-back victims' units (all of
+    // them without a mask): with at most one victim per thread, from the same
+    // loads in one pass
+    auto victim = [&](unsigned i, u64* wunits) {
         const unsigned v = (unsigned)(sortE[nE - 1 - i] & idmask);
         const unsigned char w = (!A.dirty || A.dirty[v]) ? 1 : 0;
         A.victims[i] = v;
@@ -1013,19 +1023,23 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         A.vwritten[i] = w;
         A.vwritten_host[i] = w;
         A.resident[v] = 0;
-    }
-    // offsets of the written-back victims' units (all of them without a mask)
-    block_prefix(n_v, [&](unsigned i) {
-        const unsigned v = (unsigned)(sortE[nE - 1 - i] & idmask);
-        return (!A.dirty || A.dirty[v]) ? (u64)units[v] : 0ull;
-    }, A.woff, S);
-
-    for (unsigned i = tid; i < n_l; i += blockDim.x) {
-        const unsigned a = (unsigned)((i < nL ? A.sortL[i] : sortC[i - nL]) & idmask);
-        A.loads[i] = a;
-        A.loads_host[i] = a;
-        A.resident[a] = 1;
-        if (i >= nL) A.loff[i + 1] = c.sum_demand + A.prefC[i - nL + 1];
+        *wunits = w ? (u64)units[v] : 0ull;
+    };
+    if (n_v <= blockDim.x) {
+        u64 wv = 0;
+        if (tid < n_v) victim(tid, &wv);
+        u64 tot;
+        const u64 ex = block_excl_scan(wv, S, &tot);
+        if (tid == 0) A.woff[0] = 0;
+        if (tid < n_v) A.woff[tid + 1] = ex + wv;
+        __syncthreads();
+    } else {
+        u64 wv;
+        for (unsigned i = tid; i < n_v; i += blockDim.x) victim(i, &wv);
+        block_prefix(n_v, [&](unsigned i) {
+            const unsigned v = (unsigned)(sortE[nE - 1 - i] & idmask);
+            return (!A.dirty || A.dirty[v]) ? (u64)units[v] : 0ull;
+        }, A.woff, S);
     }
 
     stamp(6);
