@@ -9,9 +9,9 @@ and byte movement.  Cases:
     every resident unit);
   * the real unit layouts (64 x 32 KiB KV pages, 448-plane LoRA adapters,
     512 KiB unified units) on agent subsets, with sampled byte checks;
-  * the round-robin workload in the benchmark's own launch configuration
-    (full size, 2 MiB units, 1 GiB slots, shared host copies), plans every
-    step and bytes on sampled units;
+  * the round-robin and Zipf-LoRA workloads in the benchmark's own launch
+    configuration (full size, 2 MiB units and 80 MiB adapter slots, 1 GiB
+    slots, shared host copies), plans every step and bytes on sampled units;
   * direct transfers (a direction at or below the pool's direct_bytes moves
     by kernel straight between units and host copies): every step direct,
     and a limit that sends some steps' directions direct and others staged;
@@ -108,31 +108,36 @@ def test_workload_full_counts(name, pool_index):
                sample_units=sample, label=f"{name}[{pool_index}] full counts")
 
 
-def test_bench_configuration_sampled():
-    # The round-robin workload as bench.py times it: 1,000 agents, a 40 GB pool
-    # of 2 MiB units (64 planes x 32 KiB), 8 GiB of staging in four 1 GiB
-    # slots per direction, a 4 MiB direct limit, 128 host copies shared
-    # round-robin by the agents and a stream of the caller's own.  Plans,
-    # block table and residency match the oracle at every step.  Bytes are
-    # checked where one step fixes them, on sampled units every tenth step: a
-    # victim whose host copy no other agent moving in the step shares must
-    # leave its device bytes there, and such a load must receive the bytes its
-    # host copy held before the step.
-    tr = W.make_trace("roundrobin", 0)
-    spec = tr.pools[0]
-    ub = spec.unit_bytes
+@pytest.mark.parametrize("name", ["roundrobin", "zipf_lora"])
+def test_bench_configuration_sampled(name):
+    # A workload as bench.py times it: full size, real unit layouts (2 MiB
+    # units of 64 x 32 KiB; for the LoRA workload also 80 MiB adapter slots of
+    # 448 planes in a second pool planned with the same inputs), 8 GiB of
+    # staging per pool in four slots per direction, a 4 MiB direct limit, 128
+    # host copies per pool shared round-robin by the agents and a stream of
+    # the caller's own.  Plans, block tables and residency match the oracle at
+    # every step.  Bytes are checked where one step fixes them, on sampled
+    # units every tenth step: a victim whose host copy no other agent moving
+    # in the step shares must leave its device bytes there, and such a load
+    # must receive the bytes its host copy held before the step.
+    tr = W.make_trace(name, 0)
     n_host = 128
-    mem = PoolMemory(spec, 8192 << 20, 4, host_slots=n_host)
-    words = int(spec.agent_units.max()) * ub // 8
-    pattern = np.arange(words, dtype=np.uint64)
-    host64 = mem.host_np.view(np.uint64)
-    for k in range(n_host):       # every 8-byte word of the host copies distinct
-        host64[k * words:(k + 1) * words] = pattern + np.uint64((k + 1) << 40)
-    pool = mem.make_pool(timing=True, direct_bytes=4 << 20)
-    opool = OraclePool(spec.capacity_units, spec.agent_units, ub)
+    ctx = []
+    for pi, spec in enumerate(tr.pools):
+        ub = spec.unit_bytes
+        mem = PoolMemory(spec, 8192 << 20, 4, host_slots=n_host)
+        words = int(spec.agent_units.max()) * ub // 8
+        pattern = np.arange(words, dtype=np.uint64)
+        host64 = mem.host_np.view(np.uint64)
+        for k in range(n_host):   # every 8-byte word of both pools' host copies distinct
+            host64[k * words:(k + 1) * words] = pattern + np.uint64((pi << 56) | ((k + 1) << 40))
+        del pattern, host64
+        units = spec.agent_units.astype(np.int64)
+        ctx.append(dict(spec=spec, ub=ub, mem=mem, units=units,
+                        row=np.concatenate([[0], np.cumsum(units)]),
+                        pool=mem.make_pool(timing=True, direct_bytes=4 << 20),
+                        opool=OraclePool(spec.capacity_units, spec.agent_units, ub)))
     dev = upload_trace(tr)
-    units = spec.agent_units.astype(np.int64)
-    row = np.concatenate([[0], np.cumsum(units)])
     stream = B.Stream()
     rng = np.random.default_rng(7)
     checked_v = checked_l = 0
@@ -142,60 +147,81 @@ def test_bench_configuration_sampled():
         counts = np.bincount(slots, minlength=n_host)
         return [int(a) for a in group if counts[int(a) % n_host] == 1]
 
+    def sample_units(units, a):
+        return sorted({0, int(units[a]) // 2, int(units[a]) - 1})
+
+    def read_units(mem, phys):
+        # the sampled units' chunks only (whole-plane reads would move GBs)
+        out = np.empty((len(phys), mem.spec.unit_bytes), dtype=np.uint8)
+        off = 0
+        for c, cb in enumerate(mem.spec.chunk_bytes):
+            for k, u in enumerate(phys):
+                out[k, off:off + cb] = mem.planes[c].download(int(u) * cb, cb)
+            off += cb
+        return out
+
     try:
         for t in range(tr.n_steps):
             check = t % 10 == 5
             if check:
-                pool.sync()
-                bt_before = pool.block_table_host_all().copy()
-            g = pool.plan_step(dev.dist(t), dev.active(t), S, None, stream.handle)
-            o = opool.plan_step(tr.dist[t], tr.active[t], S)
-            assert g["victims"].tolist() == o.victims.tolist(), t
-            assert g["loads"].tolist() == o.loads.tolist(), t
-            assert g["bytes_out"] == o.bytes_out and g["bytes_in"] == o.bytes_in, t
+                for c in ctx:
+                    c["pool"].sync()
+                    c["bt_before"] = c["pool"].block_table_host_all().copy()
+            for c in ctx:
+                g = c["pool"].plan_step(dev.dist(t), dev.active(t), S, None, stream.handle)
+                o = c["opool"].plan_step(tr.dist[t], tr.active[t], S)
+                assert g["victims"].tolist() == o.victims.tolist(), (name, t)
+                assert g["loads"].tolist() == o.loads.tolist(), (name, t)
+                assert g["bytes_out"] == o.bytes_out and g["bytes_in"] == o.bytes_in, (name, t)
+                c["v_before"], c["l_before"] = {}, {}
+                if check:
+                    movers = np.concatenate([o.victims, o.loads])
+                    vs = unique_movers(o.victims, movers)
+                    ls = unique_movers(o.loads, movers)
+                    for v in [vs[i] for i in rng.permutation(len(vs))[:2]]:
+                        js = sample_units(c["units"], v)
+                        rows = c["bt_before"][c["row"][v] + np.asarray(js)]
+                        assert (rows >= 0).all(), (name, t, v)
+                        c["v_before"][v] = (js, read_units(c["mem"], rows))
+                    for a in [ls[i] for i in rng.permutation(len(ls))[:2]]:
+                        js = sample_units(c["units"], a)
+                        hc = c["mem"].host_copy(a).reshape(-1, c["ub"])
+                        c["l_before"][a] = (js, hc[js].copy())
+            for c in ctx:
+                c["pool"].evict_pack(stream.handle)
+            for c in ctx:
+                c["pool"].prefetch_unpack(stream.handle)
             if check:
-                movers = np.concatenate([o.victims, o.loads])
-                vs = unique_movers(o.victims, movers)
-                ls = unique_movers(o.loads, movers)
-                vs = [vs[i] for i in rng.permutation(len(vs))[:2]]
-                ls = [ls[i] for i in rng.permutation(len(ls))[:2]]
-                v_before, l_before = {}, {}
-                for v in vs:
-                    js = sorted({0, int(units[v]) // 2, int(units[v]) - 1})
-                    rows = bt_before[row[v] + np.asarray(js)]
-                    assert (rows >= 0).all(), (t, v)
-                    v_before[v] = (js, mem.units_bytes(rows))
-                for a in ls:
-                    js = sorted({0, int(units[a]) // 2, int(units[a]) - 1})
-                    hc = mem.host_copy(a).reshape(-1, ub)
-                    l_before[a] = (js, hc[js].copy())
-            pool.evict_pack(stream.handle)
-            pool.prefetch_unpack(stream.handle)
-            if check:
-                pool.sync()
-                bt = pool.block_table_host_all()
-                assert np.array_equal(bt, np.concatenate(opool.bt).astype(np.int32)), t
-                assert np.array_equal(pool.resident_host().astype(bool), opool.resident), t
-                for v, (js, exp) in v_before.items():
-                    got = mem.host_copy(v).reshape(-1, ub)[js]
-                    assert np.array_equal(got, exp), (t, "victim host copy", v)
-                    checked_v += len(js)
-                for a, (js, exp) in l_before.items():
-                    got = mem.units_bytes(bt[row[a] + np.asarray(js)])
-                    assert np.array_equal(got, exp), (t, "loaded units", a)
-                    checked_l += len(js)
-        pool.sync()
-        assert np.array_equal(pool.block_table_host_all(),
-                              np.concatenate(opool.bt).astype(np.int32))
-        log(f"[bench config] {tr.n_steps} steps, {checked_v} victim and {checked_l} "
+                for c in ctx:
+                    pool, mem, ub = c["pool"], c["mem"], c["ub"]
+                    pool.sync()
+                    bt = pool.block_table_host_all()
+                    assert np.array_equal(bt, np.concatenate(c["opool"].bt).astype(np.int32)), \
+                        (name, t)
+                    assert np.array_equal(pool.resident_host().astype(bool),
+                                          c["opool"].resident), (name, t)
+                    for v, (js, exp) in c["v_before"].items():
+                        got = mem.host_copy(v).reshape(-1, ub)[js]
+                        assert np.array_equal(got, exp), (name, t, "victim host copy", v)
+                        checked_v += len(js)
+                    for a, (js, exp) in c["l_before"].items():
+                        got = read_units(mem, bt[c["row"][a] + np.asarray(js)])
+                        assert np.array_equal(got, exp), (name, t, "loaded units", a)
+                        checked_l += len(js)
+        for c in ctx:
+            c["pool"].sync()
+            assert np.array_equal(c["pool"].block_table_host_all(),
+                                  np.concatenate(c["opool"].bt).astype(np.int32)), name
+        log(f"[bench config] {name}: {tr.n_steps} steps, {checked_v} victim and {checked_l} "
             f"load units checked")
         assert checked_v > 0 and checked_l > 0
     finally:
         stream.sync()
         stream.close()
-        pool.close()
+        for c in ctx:
+            c["pool"].close()
+            c["mem"].free()
         dev.free()
-        mem.free()
 
 
 @pytest.mark.parametrize("name,theta,budget", [("roundrobin", 0, None), ("bursty", 0, None),
