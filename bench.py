@@ -2,7 +2,8 @@
 """Benchmark of one simulation step of the invocation-distance memory manager
 on one MI355X: plan (distances + activation mask -> victims, loads, block
 table), evict (pack + device-to-host copy) and prefetch (host-to-device copy
-+ unpack), on the 1,000-agent round-robin workload by default.
++ unpack), on the 50,000-agent diffusion workload (one 160 GB pool) by
+default.
 
 Prints one JSON line.  ``value`` is evict+prefetch bytes moved per second of
 wall time over the timed steps (inputs -- the per-step distances and masks --
@@ -55,6 +56,19 @@ def kernel_source_hash():
     return hashlib.sha256(text[a:b].encode()).hexdigest()[:16]
 
 
+def launch_units(kind, blocks, n_items, n_planes):
+    """Units one copy launch of ``blocks`` workgroups covers: the pack, and the
+    unpack of pools whose chunks hold several items, take ceil(n_items / 8)
+    workgroups per unit; the unpack of pools with one item per plane (run
+    order) takes n_items workgroups per 8 units (the last group may be
+    partial, so this is an upper bound there)."""
+    waves = COPY_BLOCK // 64
+    groups = (n_items + waves - 1) // waves
+    if kind == "pack" or n_items != n_planes:
+        return blocks // groups
+    return blocks // n_items * waves
+
+
 def summarize_pmc(fetch_csv, write_csv, workload, out_json, commands):
     """HBM traffic of the copy kernels from two rocprofv3 --pmc runs
     (FETCH_SIZE, WRITE_SIZE in KiB per dispatch), each scaled by the ratio of
@@ -89,7 +103,7 @@ def summarize_pmc(fetch_csv, write_csv, workload, out_json, commands):
         f = [v for v, g in f if g == grid]
         w = [v for v, g in w if g == grid]
         blocks = grid // COPY_BLOCK
-        units = blocks // groups if short == "pack" else blocks // n_items * waves
+        units = launch_units(short, blocks, n_items, len(spec.chunk_bytes))
         alg = 2 * units * spec.unit_bytes
         fetch_b = np.mean(f) * 1024 * factor["FETCH_SIZE"]
         write_b = np.mean(w) * 1024 * factor["WRITE_SIZE"]
@@ -103,10 +117,13 @@ def summarize_pmc(fetch_csv, write_csv, workload, out_json, commands):
     return out
 
 
-def summarize_trace(trace_csv, out_md, title, command, note=""):
+def summarize_trace(trace_csv, out_md, title, command, note="", workload=None):
     """Markdown table of per-kernel launch counts and durations from a
     rocprofv3 --kernel-trace CSV (every kernel, plus the copy kernels split
-    into full-slot launches and the rest)."""
+    into full-slot launches and the rest).  With ``workload``, also each copy
+    kernel's algorithmic bytes over all its launches (units per launch from
+    the grid) divided by its summed durations, the figure ``roofline`` gives
+    from HIP events."""
     import csv
     import collections
     rows = list(csv.DictReader(open(trace_csv)))
@@ -137,8 +154,111 @@ def summarize_trace(trace_csv, out_md, title, command, note=""):
     for n, v in full.items():
         lines.append(f"| `{PMC_KERNELS[n]}` | {grid_full[n]:,} | {len(v)} | {np.mean(v):.1f} | "
                      f"{np.median(v):.1f} | {min(v):.1f} |")
+    if workload:
+        import workloads as W
+        spec = W.make_trace(workload, 0).pools[0]
+        n_items = sum((c + COPY_ITEM_BYTES - 1) // COPY_ITEM_BYTES for c in spec.chunk_bytes)
+        lines += ["", f"Copy kernels over all launches ({workload} layout: {spec.unit_bytes:,} B "
+                  f"units, {n_items} items per unit; algorithmic bytes = 2 x units x unit bytes, "
+                  "units from the grid):", "",
+                  "| Kernel | Launches | Algorithmic GB | Summed us | Achieved TB/s | Of 8 TB/s |",
+                  "|---|---|---|---|---|---|"]
+        for n, short in PMC_KERNELS.items():
+            alg = us = 0.0
+            k = 0
+            for r in rows:
+                if r["Kernel_Name"] != n:
+                    continue
+                blocks = int(r["Grid_Size_X"]) // COPY_BLOCK
+                alg += 2.0 * launch_units(short, blocks, n_items, len(spec.chunk_bytes)) * \
+                    spec.unit_bytes
+                us += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+                k += 1
+            if k:
+                tbs = alg / us / 1e6
+                lines.append(f"| `{short}` | {k} | {alg / 1e9:.1f} | {us:,.0f} | {tbs:.2f} | "
+                             f"{tbs / 8.0:.3f} |")
     if note:
         lines += ["", note]
+    open(out_md, "w").write("\n".join(lines) + "\n")
+    return "\n".join(lines)
+
+
+def summarize_copies(copy_csv, steps_jsonl, bench_json, out_md, title, command):
+    """Host-link summary from a rocprofv3 --memory-copy-trace CSV.  The trace
+    holds no sizes, so bytes come from the benchmark's per-step record of the
+    same run (``--jsonl``): every staged step's written-back bytes crossed
+    device to host, its loaded bytes host to device.  The step copies are those
+    on the stream with the most copies of each direction (the pool's pair;
+    the probes use streams of their own).  Per direction: copies, mean
+    duration, busy time (union of the copies' intervals) and bytes / busy time
+    against the one-way probe of the same run; both directions together:
+    bytes / the union of all their intervals against the two-way probe."""
+    import csv
+    import collections
+    rows = list(csv.DictReader(open(copy_csv)))
+    recs = [json.loads(l) for l in open(steps_jsonl) if l.strip()]
+    bench = json.loads([l for l in open(bench_json) if l.strip().startswith("{")][-1])
+    probe = bench.get("probe") or {}
+    by = collections.defaultdict(list)
+    for r in rows:
+        d = r["Direction"].replace("MEMORY_COPY_", "")
+        by[(d, r["Stream_Id"])].append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+
+    def union(iv):
+        iv = sorted(iv)
+        tot, cs, ce = 0, None, None
+        for a, b in iv:
+            if ce is None or a > ce:
+                if ce is not None:
+                    tot += ce - cs
+                cs, ce = a, b
+            else:
+                ce = max(ce, b)
+        return tot + (ce - cs if ce is not None else 0)
+
+    step_bytes = {"DEVICE_TO_HOST": sum(r["bytes_out"] - r.get("direct_out_bytes", 0) for r in recs),
+                  "HOST_TO_DEVICE": sum(r["bytes_in"] - r.get("direct_in_bytes", 0) for r in recs)}
+    one_way = {"DEVICE_TO_HOST": probe.get("d2h_GBps"), "HOST_TO_DEVICE": probe.get("h2d_GBps")}
+    lines = [f"# {title}", "", "Command (repository root = `$REPO`, on one MI355X):", "",
+             f"    {command}", "",
+             f"Summary of `{os.path.basename(copy_csv)}` and of the per-step record "
+             f"`{os.path.basename(steps_jsonl)}` ({len(recs)} steps: warm-up, timed and "
+             "plan-latency steps) written by `python bench.py --summarize-copies`.  Bytes are "
+             "the steps' staged write-back and load bytes; the probes' copies run on streams "
+             "of their own and are left out.", "",
+             "| Direction | Copies | Mean us | Busy ms | GB | GB/s while busy | One-way probe GB/s | "
+             "Of probe |", "|---|---|---|---|---|---|---|---|"]
+    all_iv = []
+    out = {}
+    for d in ("DEVICE_TO_HOST", "HOST_TO_DEVICE"):
+        cands = [(len(v), k) for k, v in by.items() if k[0] == d]
+        if not cands:
+            continue
+        _, key = max(cands)
+        iv = by[key]
+        all_iv += iv
+        busy = union(iv) / 1e9
+        mean_us = np.mean([b - a for a, b in iv]) / 1e3
+        gb = step_bytes[d] / 1e9
+        rate = gb / busy if busy else 0.0
+        pw = one_way[d]
+        out[d] = rate
+        lines.append(f"| {d.replace('_', ' ').lower()} | {len(iv):,} | {mean_us:.1f} | "
+                     f"{1e3 * busy:,.1f} | {gb:.2f} | {rate:.1f} | "
+                     f"{pw:.1f} | {rate / pw:.3f} |" if pw else
+                     f"| {d} | {len(iv):,} | {mean_us:.1f} | {1e3 * busy:,.1f} | {gb:.2f} | "
+                     f"{rate:.1f} | - | - |")
+    busy_all = union(all_iv) / 1e9
+    tot = sum(step_bytes.values()) / 1e9
+    dup = probe.get("duplex_GBps")
+    lines += ["", f"Both directions: {tot:.2f} GB over {1e3 * busy_all:,.1f} ms in which at least "
+              f"one direction copied = {tot / busy_all:.1f} GB/s" +
+              (f" against the two-way probe's {dup:.1f} GB/s ({tot / busy_all / dup:.3f})."
+               if dup else "."),
+              "", f"Benchmark line of the same run: value {bench.get('value', 0):.1f} GB/s "
+              f"(wall time of the timed steps), dma.frac_of_measured_link "
+              f"{(bench.get('dma') or {}).get('frac_of_measured_link', float('nan')):.3f}."]
     open(out_md, "w").write("\n".join(lines) + "\n")
     return "\n".join(lines)
 
@@ -148,7 +268,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="roundrobin", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--workload", default="diffusion", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--threshold", type=int, default=0xFFFFFFFF)
     ap.add_argument("--budget", type=int, default=None)
@@ -191,7 +311,17 @@ def parse():
                     help="write the copy kernels' HBM traffic from two rocprofv3 --pmc runs")
     ap.add_argument("--pmc-commands", nargs="*", default=[])
     ap.add_argument("--summarize-trace", nargs=4, metavar=("TRACE_CSV", "OUT_MD", "TITLE", "COMMAND"),
-                    help="write a markdown summary of a rocprofv3 --kernel-trace CSV")
+                    help="write a markdown summary of a rocprofv3 --kernel-trace CSV (with "
+                         "--workload: the copy kernels' achieved rate over all launches too)")
+    ap.add_argument("--trace-workload", default=None,
+                    help="workload whose unit layout --summarize-trace uses for the copy kernels")
+    ap.add_argument("--summarize-copies", nargs=6,
+                    metavar=("COPY_CSV", "STEPS_JSONL", "BENCH_JSON", "OUT_MD", "TITLE", "COMMAND"),
+                    help="write a host-link summary of a rocprofv3 --memory-copy-trace CSV")
+    ap.add_argument("--jsonl", default=None,
+                    help="write one JSON record per step (warm-up, timed and plan-latency steps) "
+                         "to this file; the host then waits for each step before the next "
+                         "(the next plan waits for it on the device anyway)")
     return ap.parse_args()
 
 
@@ -544,7 +674,10 @@ def cpu_model() -> str:
 def main():
     args = parse()
     if args.summarize_trace:
-        print(summarize_trace(*args.summarize_trace))
+        print(summarize_trace(*args.summarize_trace, workload=args.trace_workload))
+        return
+    if args.summarize_copies:
+        print(summarize_copies(*args.summarize_copies))
         return
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc[:2], args.workload,
@@ -575,9 +708,9 @@ def main():
                                                  pr), "probe": pr}), flush=True)
         return
     trace = W.make_trace(args.workload, args.seed)
-    T_need = args.warmup + args.steps + args.plan_steps
+    T_need = args.warmup + args.steps
     if T_need > trace.n_steps:
-        sys.exit(f"warmup + steps + plan-steps = {T_need} exceeds the trace's {trace.n_steps} steps")
+        sys.exit(f"warmup + steps = {T_need} exceeds the trace's {trace.n_steps} steps")
     budget = args.budget
     thr = args.threshold
 
@@ -608,13 +741,47 @@ def main():
         for p in pools:
             p.sync()
 
-    def step(t):
+    # per-step record (--jsonl): the step's plan, bytes and, from the pools'
+    # timing counters, its plan, pack, copy and unpack times
+    jl = open(args.jsonl, "w") if args.jsonl else None
+    jl_prev = [None]
+    stat_keys = ("pack_ms", "unpack_ms", "d2h_ms", "h2d_ms", "plan_gpu_ms", "direct_out_ms",
+                 "direct_in_ms", "pack_launches", "unpack_launches", "direct_out_bytes",
+                 "direct_in_bytes")
+
+    def record(t, phase, plans, t_call):
+        if jl is None:
+            return
+        cur = [p.stats() for p in pools]           # waits for the step
+        tot = {k: sum(c[k] for c in cur) for k in stat_keys}
+        tot["plan_host_us"] = sum(sum(c["plan_host_us"]) for c in cur)
+        prev = jl_prev[0] or {k: 0 for k in tot}
+        d = {k: tot[k] - prev[k] for k in tot}
+        jl_prev[0] = tot
+        jl.write(json.dumps({
+            "t": t, "phase": phase, "n_victims": sum(pl["n_victims"] for pl in plans),
+            "n_loads": sum(pl["n_loads"] for pl in plans),
+            "units_out": sum(pl["units_out"] for pl in plans),
+            "units_in": sum(pl["units_in"] for pl in plans),
+            "bytes_out": sum(pl["bytes_out"] for pl in plans),
+            "bytes_in": sum(pl["bytes_in"] for pl in plans),
+            "t_step_call_ms": 1e3 * t_call, "t_plan_us": d["plan_host_us"],
+            "t_plan_gpu_us": 1e3 * d["plan_gpu_ms"], "t_pack_ms": d["pack_ms"],
+            "t_d2h_ms": d["d2h_ms"], "t_h2d_ms": d["h2d_ms"], "t_unpack_ms": d["unpack_ms"],
+            "t_direct_out_ms": d["direct_out_ms"], "t_direct_in_ms": d["direct_in_ms"],
+            "pack_launches": d["pack_launches"], "unpack_launches": d["unpack_launches"],
+            "direct_out_bytes": d["direct_out_bytes"], "direct_in_bytes": d["direct_in_bytes"]})
+            + "\n")
+
+    def step(t, phase="timed"):
+        ts = time.perf_counter()
         plans = [p.plan_step(dist.ptr + 4 * N * t, act.ptr + N * t, thr, budget, stream,
                              dirty_ptr, lists=False) for p in pools]
         for p in pools:
             p.evict_pack(stream)
         for p in pools:
             p.prefetch_unpack(stream)
+        record(t, phase, plans, time.perf_counter() - ts)
         return plans
 
     # the first steps fill the empty pool: timed apart from the steady state
@@ -623,7 +790,7 @@ def main():
     sync()
     tf = time.perf_counter()
     for t in range(args.warmup):
-        plans = step(t)
+        plans = step(t, "warmup")
         if t < fill_steps:
             fill_b += sum(pl["bytes_out"] + pl["bytes_in"] for pl in plans)
         if t == fill_steps - 1:
@@ -651,26 +818,45 @@ def main():
     # plan latency: each plan issued with the device idle; wall time of the
     # Python call (counts only) and the library's own host time of the C call
     # (stats are read only after a plan, so that nothing is submitted between
-    # the wait for the previous step and the measured call)
-    lat, lat_c = [], []
-    c_prev = sum(sum(p.stats()["plan_host_us"]) for p in pools)
-    for k in range(args.plan_steps):
+    # the wait for the previous step and the measured call).  First with the
+    # inputs in device memory, then with the same kind of inputs in host
+    # memory (numpy arrays, copied by the call into pinned memory that the
+    # plan kernel reads over the host link).  The latency steps follow the
+    # timed ones and wrap around at the trace's end (any step's inputs are a
+    # valid plan input).
+    def plan_latency(host_inputs, first):
+        lat, lat_c = [], []
+        c_prev = sum(sum(p.stats()["plan_host_us"]) for p in pools)
+        for k in range(args.plan_steps):
+            sync()
+            t = (first + k) % trace.n_steps
+            if host_inputs:
+                d_ptr, a_ptr = d_np[t].ctypes.data, a_np[t].ctypes.data
+            else:
+                d_ptr, a_ptr = dist.ptr + 4 * N * t, act.ptr + N * t
+            ts = time.perf_counter()
+            plans = [p.plan_step(d_ptr, a_ptr, thr, budget, stream, dirty_ptr, lists=False)
+                     for p in pools]
+            lat.append(time.perf_counter() - ts)
+            c_now = sum(sum(p.stats()["plan_host_us"]) for p in pools)
+            lat_c.append(c_now - c_prev)
+            c_prev = c_now
+            for p in pools:
+                p.evict_pack(stream)
+            for p in pools:
+                p.prefetch_unpack(stream)
+            record(t, "plan_host_inputs" if host_inputs else "plan", plans, lat[-1])
         sync()
-        t = args.warmup + args.steps + k
-        ts = time.perf_counter()
-        for p in pools:
-            p.plan_step(dist.ptr + 4 * N * t, act.ptr + N * t, thr, budget, stream, dirty_ptr,
-                        lists=False)
-        lat.append(time.perf_counter() - ts)
-        c_now = sum(sum(p.stats()["plan_host_us"]) for p in pools)
-        lat_c.append(c_now - c_prev)
-        c_prev = c_now
-        for p in pools:
-            p.evict_pack(stream)
-        for p in pools:
-            p.prefetch_unpack(stream)
-    sync()
+        lat_us = np.array(lat) * 1e6
+        return {"median": float(np.median(lat_us)), "p99": float(np.percentile(lat_us, 99)),
+                "c_call_median": float(np.median(lat_c)),
+                "c_call_p99": float(np.percentile(lat_c, 99))}
+
+    lat_dev = plan_latency(False, args.warmup + args.steps)
     plan_stats = [p.stats() for p in pools]
+    lat_host = plan_latency(True, args.warmup + args.steps + args.plan_steps)
+    if jl is not None:
+        jl.close()
     if probe:
         # a second probe after the timed steps: each direction keeps its better
         # reading
@@ -751,7 +937,6 @@ def main():
         dma["ideal_s"] = ideal
         dma["frac_of_measured_link"] = ideal / wall
         dma["duplex_overlap_measured"] = duplex
-    lat_us = np.array(lat) * 1e6
     plan_gpu_ms = sum(s["plan_gpu_ms"] for s in plan_stats) - sum(s["plan_gpu_ms"] for s in stats)
     nps = max(args.plan_steps, 1)
     host = [sum(s["plan_host_us"][i] for s in plan_stats) - sum(s["plan_host_us"][i] for s in stats)
@@ -759,11 +944,15 @@ def main():
     phases = [(sum(s["plan_phase_us"][i] for s in plan_stats) -
                sum(s["plan_phase_us"][i] for s in stats)) / nps for i in range(7)]
     floor_us = binding.probe_launch(100)
-    plan = {"median": float(np.median(lat_us)), "p99": float(np.percentile(lat_us, 99)),
+    plan = {"median": lat_dev["median"], "p99": lat_dev["p99"],
             "floor_us": floor_us,
             "floor": "one empty kernel launch, event record and wait (the plan is one launch "
                      "per pool; its lists come back through mapped host memory)",
-            "c_call_median": float(np.median(lat_c)), "c_call_p99": float(np.percentile(lat_c, 99)),
+            "c_call_median": lat_dev["c_call_median"], "c_call_p99": lat_dev["c_call_p99"],
+            "inputs": "device memory (distances and masks already in HBM)",
+            "host_inputs": dict(lat_host, inputs="host memory (numpy arrays; the call copies "
+                                "them into pinned memory the plan kernel reads over the host "
+                                "link)"),
             "core_phases_us": dict(zip(("classify", "demand_and_evictable_sorts",
                                         "candidate_select", "candidate_sort", "acceptance",
                                         "lists", "free_units"), phases)),

@@ -45,9 +45,11 @@
  * library owns its internal HIP streams (all at the default priority).  Work
  * of a call starts after the work the caller has queued on `stream` before
  * the call; ss_prefetch_unpack makes `stream` wait for the whole step (both
- * directions of the copy) before the caller's later work on it.  A step
- * whose moves are all direct transfers (ss_pool_desc.direct_bytes) queues
- * its kernels on `stream` itself. 
+ * directions of the copy) before the caller's later work on it, and the next
+ * ss_plan_step's kernels start after the previous step's loads, evictions and
+ * block-table update whatever stream each call is given.  A step whose moves
+ * are all direct transfers (ss_pool_desc.direct_bytes) queues its kernels on
+ * `stream` itself.
  *
  * Errors.  No C++ exception crosses this boundary.  Every call returns an
  * ss_status; ss_last_error() gives a message for the calling thread.
@@ -112,7 +114,7 @@ typedef struct {
 typedef struct {
     uint32_t threshold;             /* prefetch agents with distance < threshold (0 = off) */
     uint64_t budget_units;          /* max prefetched units per step; SS_NO_BUDGET = none  */
-    const uint8_t* dirty;           /* [N] DEVICE, optional: 1 = the agent's memory changed
+    const uint8_t* dirty;           /* [N] host or device, optional: 1 = the agent's memory changed
                                        since it was loaded, so an eviction writes it back;
                                        0 = its host copy is current and its units are
                                        released without a copy.  NULL = every eviction
@@ -132,6 +134,12 @@ typedef struct {
     uint64_t        bytes_out, bytes_in;   /* bytes written back / loaded           */
     uint64_t        units_written;         /* victims' units written back (<= units_out) */
     const uint8_t*  victim_written;        /* [n_victims] host: 1 = written back     */
+    const uint32_t* d_victims;      /* [n_victims] DEVICE mirror of `victims`; pool-owned.
+                                       Written by the plan kernel on the call's stream:
+                                       work queued on that stream after the call (or any
+                                       work after ss_sync) may read it until the next
+                                       ss_plan_step's kernel rewrites it               */
+    const uint32_t* d_loads;        /* [n_loads] DEVICE mirror of `loads`, same terms    */
 } ss_plan;
 
 typedef struct {                    /* cumulative since create or ss_reset_stats          */
@@ -169,22 +177,33 @@ void ss_pool_destroy(ss_pool* pool);
 
 /* Plan one step (Section 3.3 and Appendix A, Evict + DispatchLoadTasks):
  * turns distances and the activation mask into victims and loads and updates
- * the block table.  `distances` [N] uint32 and `active` [N] uint8 (0/1) are
- * DEVICE pointers read during the call's kernels, which run on `stream`
+ * the block table.  `distances` [N] uint32 and `active` [N] uint8 (0/1), and
+ * params->dirty [N] when given, are each either host memory (pageable or
+ * pinned; the call copies them into pool-owned mapped pinned memory, which the
+ * plan kernel reads over the host link, so the caller may reuse them once the
+ * call returns) or device memory of the pool's device (read in place by the
+ * call's kernels, which must not race with writers).  The kernels run on `stream`
  * after the work queued there before the call and after the previous step's
- * loads and block-table update.  The call returns once the plan is known on
+ * loads, evictions (packs and device-to-host copies) and block-table update
+ * (when `stream` is the stream the previous ss_prefetch_unpack was given,
+ * stream order already implies this and no wait is added; a stream handle is
+ * identified by its value).  The call returns once the plan is known on
  * the host: the plan kernel writes its lists into mapped host memory and,
  * last, a sequence number that the call polls (for up to 2 ms, then it waits
  * on the kernel's completion event); by then the kernel has finished reading
- * `distances` and `active`, though it may still be ending on the device.  The
+ * its inputs, though it may still be ending on the device.  The
  * block-table update that the plan implies runs on `stream` after the plan is
  * published: in the plan kernel's own tail up to 12,288 agents, else as two
  * kernels queued right behind it (after an overcommitted plan it changes
  * nothing); the copy kernels of ss_evict_pack and ss_prefetch_unpack follow
- * it whatever stream those calls are given.
+ * it whatever stream those calls are given.  Host inputs must hold N
+ * readable elements; their copy into the mirrors is part of the call's host
+ * time.  `out` receives the host lists and their device mirrors (ss_plan).
  * SS_ERR_OVERCOMMIT if the active agents need more than capacity_units
- * (pool unchanged).  SS_ERR_ORDER if the previous step was not completed with
- * ss_evict_pack and ss_prefetch_unpack. */
+ * (pool unchanged).  SS_ERR_ARG (pool unchanged) if an input is device memory
+ * of another device or a device range shorter than N elements.  SS_ERR_ORDER
+ * if the previous step was not completed with ss_evict_pack and
+ * ss_prefetch_unpack. */
 ss_status ss_plan_step(ss_pool* pool, const uint32_t* distances, const uint8_t* active,
                        const ss_plan_params* params, ss_plan* out, void* stream);
 
@@ -455,6 +474,16 @@ ss_status ss_event_elapsed(void* start, void* end, float* ms);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char* ss_last_error(void);
+
+/* Failure injection, for callers that test their handling of SS_ERR_HIP and
+ * SS_ERR_POISONED (a failing HIP call cannot otherwise be provoked without
+ * harming the device).  Counting from this call, the n-th copy command issued
+ * by ss_evict_pack, ss_prefetch_unpack or ss_loader_pump, in any pool or
+ * loader of the process, is not issued and fails as a HIP error would: that
+ * call returns SS_ERR_HIP and its pool or loader is poisoned.  n = 0 disarms;
+ * the hook disarms itself once it has fired.  Work queued before the failing
+ * copy still runs, so ss_pool_destroy and ss_loader_destroy stay clean. */
+void ss_debug_fail_copy(uint32_t n);
 
 #ifdef __cplusplus
 }

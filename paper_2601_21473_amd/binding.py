@@ -36,7 +36,7 @@ EXPORTS = ["ss_pool_create", "ss_pool_destroy", "ss_plan_step", "ss_evict_pack",
            "ss_stream_create", "ss_stream_destroy", "ss_stream_sync", "ss_event_create",
            "ss_event_destroy", "ss_event_record", "ss_event_elapsed", "ss_loader_create",
            "ss_loader_destroy", "ss_loader_submit", "ss_loader_pump", "ss_loader_pending",
-           "ss_loader_sync", "ss_loader_get_stats"]
+           "ss_loader_sync", "ss_loader_get_stats", "ss_debug_fail_copy"]
 
 
 class ss_load_task(C.Structure):
@@ -73,7 +73,8 @@ class ss_plan(C.Structure):
                 ("n_demand_victims", C.c_uint32), ("victims", C.POINTER(C.c_uint32)),
                 ("loads", C.POINTER(C.c_uint32)), ("units_out", C.c_uint64),
                 ("units_in", C.c_uint64), ("bytes_out", C.c_uint64), ("bytes_in", C.c_uint64),
-                ("units_written", C.c_uint64), ("victim_written", C.POINTER(C.c_uint8))]
+                ("units_written", C.c_uint64), ("victim_written", C.POINTER(C.c_uint8)),
+                ("d_victims", C.c_void_p), ("d_loads", C.c_void_p)]
 
 
 class ss_stats(C.Structure):
@@ -159,6 +160,7 @@ def load():
         "ss_hop_distances_workspace": ([C.c_uint32], C.c_uint64),
         "ss_hop_distances": ([P, P, C.c_uint32, C.c_uint32, P, C.c_uint32, C.c_uint32, P, P,
                               C.c_uint64, P], C.c_int32),
+        "ss_debug_fail_copy": ([C.c_uint32], None),
         "ss_interaction_distances_workspace": ([C.c_uint32], C.c_uint64),
         "ss_interaction_distances": ([P, P, C.c_uint32, C.c_uint32, C.c_uint32, P, P, C.c_uint64,
                                       P], C.c_int32),
@@ -251,8 +253,10 @@ class Pool:
 
     def plan_step(self, distances_ptr: int, active_ptr: int, threshold: int, budget=None,
                   stream: int = 0, dirty_ptr: int = 0, lists: bool = True):
-        """``ss_plan_step``; returns a dict with numpy copies of the plan.
-        ``dirty_ptr``: device address of the [N] write-back mask, 0 = none.
+        """``ss_plan_step``; returns a dict with numpy copies of the plan and
+        the device addresses of its device mirrors (``d_victims``, ``d_loads``).
+        ``distances_ptr``, ``active_ptr`` and ``dirty_ptr`` (the [N] write-back
+        mask, 0 = none) are addresses of device or host memory.
         ``lists=False`` returns the counts and byte totals only (no copies)."""
         prm, out = self._prm, self._out
         prm.threshold = int(threshold)
@@ -271,7 +275,8 @@ class Pool:
         return {"victims": victims, "loads": loads, "n_demand": out.n_demand,
                 "n_demand_victims": out.n_demand_victims, "units_out": out.units_out,
                 "units_in": out.units_in, "bytes_out": out.bytes_out, "bytes_in": out.bytes_in,
-                "units_written": out.units_written, "victim_written": written}
+                "units_written": out.units_written, "victim_written": written,
+                "d_victims": out.d_victims or 0, "d_loads": out.d_loads or 0}
 
     def _host_list(self, ptr, dtype) -> np.ndarray:
         """A numpy view of N entries of one of the plan's host lists.  The
@@ -338,6 +343,12 @@ class Pool:
         _check(load().ss_reset_stats(self._h))
 
 
+def debug_fail_copy(n: int):
+    """Arm (n >= 1) or disarm (0) the failure of the n-th copy command issued
+    from now by the pools' and loaders' data movement (``ss_debug_fail_copy``)."""
+    load().ss_debug_fail_copy(int(n))
+
+
 def device_count() -> int:
     n = C.c_int32()
     _check(load().ss_device_count(C.byref(n)))
@@ -371,6 +382,11 @@ def copy(dst: int, src: int, nbytes: int):
 def null_stream_sync():
     """Wait for the work queued on the null stream."""
     _check(load().ss_stream_sync(None))
+
+
+def stream_sync(stream: int = 0):
+    """Wait for the work queued on a stream (hipStream_t handle, 0 = null)."""
+    _check(load().ss_stream_sync(int(stream) or None))
 
 
 def probe_copy(dst: int, src: int, nbytes: int, iters: int = 10) -> float:

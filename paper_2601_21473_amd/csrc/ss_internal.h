@@ -67,8 +67,8 @@ struct BtArgs {
 };
 
 struct PlanArgs {
-    const unsigned* dist;           // [N] caller distances (device)
-    const unsigned char* active;    // [N] caller mask (device)
+    const unsigned* dist;           // [N] caller distances (device, or mapped pinned mirror)
+    const unsigned char* active;    // [N] caller mask (device, or mapped pinned mirror)
     unsigned char* resident;        // [N] state
     const unsigned* units;          // [N] s[a]
     unsigned n;
@@ -101,7 +101,7 @@ struct PlanArgs {
     unsigned pad2;
     u64* phase;                     // [kPlanPhases] wall-clock stamps of the plan core, or null
     u64* hist_w;                    // [kDistBuckets] candidate units per distance bucket
-    const unsigned char* dirty;     // [N] optional write-back mask (device)
+    const unsigned char* dirty;     // [N] optional write-back mask (device, or mapped mirror)
     unsigned char* vwritten;        // [N] per victim: written back (device)
     unsigned char* vwritten_host;   // mapped pinned host [N]
     u64* woff;                      // [N+1] prefix units over written-back victims
@@ -162,6 +162,9 @@ hipError_t launch_nop(hipStream_t st);
 
 // Host helpers defined in ss_pool.hip.
 ss_status set_err(ss_status st, const char* fmt, ...);       // sets ss_last_error
+// hipMemcpyAsync of the data-movement paths (pool steps, loader chunks); a
+// copy armed to fail by ss_debug_fail_copy returns hipErrorUnknown unissued.
+hipError_t copy_async(void* dst, const void* src, u64 bytes, hipMemcpyKind kind, hipStream_t st);
 bool device_range_ok(const void* ptr, u64 bytes, int device); // one device allocation
 bool pinned_range_ok(const void* ptr, u64 bytes);             // pinned host memory
 

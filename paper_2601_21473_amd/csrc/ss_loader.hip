@@ -366,8 +366,8 @@ ss_status ss_loader_pump(ss_loader* L, uint32_t max_chunks, ss_load_log* log, ui
         char* stage = m.staging + (u64)slot * m.slot_bytes;
         // the copy refills the slot only after the unpack that last read it
         if (m.slot_used[slot]) L_TRY(L, hipStreamWaitEvent(L->cp, m.slot_free[slot], 0));
-        L_TRY(L, hipMemcpyAsync(stage, m.host + m.host_off[a] + (u64)T.cursor * m.unit_bytes,
-                                (u64)cnt * m.unit_bytes, hipMemcpyHostToDevice, L->cp));
+        L_TRY(L, copy_async(stage, m.host + m.host_off[a] + (u64)T.cursor * m.unit_bytes,
+                            (u64)cnt * m.unit_bytes, hipMemcpyHostToDevice, L->cp));
         L_TRY(L, hipEventRecord(L->copied, L->cp));
         L_TRY(L, hipStreamWaitEvent(L->st, L->copied, 0));
         CopyArgs C{};

@@ -11,7 +11,8 @@
 // that writes units released by this step's victims waits for the pack that
 // read them.  Loads take the pre-step free units first and then the released
 // units in eviction order, so slot k of the loads depends on a single pack
-// slot.  The next step's plan waits for both streams.
+// slot.  The next step's plan waits for the previous step's loads, its
+// evictions (packs and device-to-host copies) and its block-table update.
 //
 // Direct transfers (direct_bytes): a direction whose bytes in the step are at
 // most the pool's limit skips the staging ring and the copy commands; one
@@ -36,6 +37,7 @@
 #include "ss_internal.h"
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <cstdarg>
 #include <cstdio>
@@ -57,7 +59,20 @@ thread_local std::string g_err;
 constexpr long kPlanPollUs = 2000;
 }  // namespace
 
+namespace {
+// Copies left before the armed one fails (0 = disarmed); see ss_debug_fail_copy.
+std::atomic<uint32_t> g_fail_copy{0};
+}  // namespace
+
 namespace ss {
+hipError_t copy_async(void* dst, const void* src, u64 bytes, hipMemcpyKind kind, hipStream_t st) {
+    uint32_t n = g_fail_copy.load(std::memory_order_relaxed);
+    while (n != 0 && !g_fail_copy.compare_exchange_weak(n, n - 1, std::memory_order_relaxed)) {
+    }
+    if (n == 1) return hipErrorUnknown;              // this is the armed copy: not issued
+    return hipMemcpyAsync(dst, src, bytes, kind, st);
+}
+
 ss_status set_err(ss_status st, const char* fmt, ...) {
     char buf[512];
     va_list ap;
@@ -146,6 +161,14 @@ struct ss_pool {
     unsigned* h_victims_dev = nullptr;
     unsigned* h_loads_dev = nullptr;
     unsigned char* h_vwritten_dev = nullptr;
+    // mapped pinned mirrors of host-memory plan inputs (distances, mask, dirty
+    // mask): the plan kernel reads them over the host link
+    unsigned* h_in_dist = nullptr;
+    unsigned char* h_in_act = nullptr;
+    unsigned char* h_in_dirty = nullptr;
+    unsigned* h_in_dist_dev = nullptr;
+    unsigned char* h_in_act_dev = nullptr;
+    unsigned char* h_in_dirty_dev = nullptr;
 
     hipStream_t st_out = nullptr, st_in = nullptr;
     hipEvent_t ev_planned = nullptr, ev_bt = nullptr, ev_caller = nullptr,
@@ -155,6 +178,9 @@ struct ss_pool {
     bool direct_out = false;                      // this step's eviction went direct
     bool inline_step = false;                     // this step runs on the caller's stream
     hipStream_t bt_stream = nullptr;              // stream of the last plan's block-table update
+    hipStream_t joined_stream = nullptr;          // caller stream that the last ss_prefetch_unpack
+                                                  // made wait for the whole step
+    bool joined_valid = false;
 
     // timing (SS_FLAG_TIMING): one pair per launch or per slot's copies
     std::vector<TimedPair> t_pack, t_unpack, t_d2h, t_h2d, t_dout, t_din;
@@ -264,7 +290,8 @@ void free_pool(ss_pool* p) {
                      p->d_btargs};
     for (void* d : dptrs)
         if (d) (void)hipFree(d);
-    void* hptrs[] = {p->h_flag, p->h_phase, p->h_res, p->h_victims, p->h_loads, p->h_vwritten};
+    void* hptrs[] = {p->h_flag, p->h_phase, p->h_res, p->h_victims, p->h_loads, p->h_vwritten,
+                     p->h_in_dist, p->h_in_act, p->h_in_dirty};
     for (void* h : hptrs)
         if (h) (void)hipHostFree(h);
     if (p->st_out) release_streams(p->device);
@@ -385,6 +412,21 @@ bool pinned_range_ok(const void* ptr, u64 bytes) {
 
 namespace {
 
+// Where a plan input of `bytes` bytes lives: device memory of `device`
+// (kInDevice, read by the kernel in place), host memory (kInHost: pageable or
+// pinned; copied into the pool's mapped mirror), or neither (kInBad: device
+// memory of another device, or a device range that is too short).
+enum InputKind { kInDevice, kInHost, kInBad };
+InputKind input_kind(const void* ptr, u64 bytes, int device) {
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, ptr) != hipSuccess) {
+        (void)hipGetLastError();
+        return kInHost;                              // memory the runtime does not know: pageable
+    }
+    if (attr.type == hipMemoryTypeHost || attr.type == hipMemoryTypeUnregistered) return kInHost;
+    return device_range_ok(ptr, bytes, device) ? kInDevice : kInBad;
+}
+
 ss_status check_usable(ss_pool* p) {
     if (!p) return set_err(SS_ERR_ARG, "pool is NULL");
     if (p->poisoned) return set_err(SS_ERR_POISONED, "pool is poisoned by an earlier HIP failure");
@@ -452,6 +494,8 @@ BtArgs bt_args(const ss_pool* p) {
 extern "C" {
 
 const char* ss_last_error(void) { return g_err.c_str(); }
+
+void ss_debug_fail_copy(uint32_t n) { g_fail_copy.store(n, std::memory_order_relaxed); }
 
 ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     if (!d || !out) return set_err(SS_ERR_ARG, "desc and out must not be NULL");
@@ -620,6 +664,13 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_loads_dev), p->h_loads, 0));
     CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_vwritten), N, hipHostMallocMapped));
     CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_vwritten_dev), p->h_vwritten, 0));
+    CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_in_dist), N * sizeof(unsigned),
+                             hipHostMallocMapped));
+    CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_in_dist_dev), p->h_in_dist, 0));
+    CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_in_act), N, hipHostMallocMapped));
+    CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_in_act_dev), p->h_in_act, 0));
+    CREATE_TRY(hipHostMalloc(reinterpret_cast<void**>(&p->h_in_dirty), N, hipHostMallocMapped));
+    CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_in_dirty_dev), p->h_in_dirty, 0));
 
     // copy items: pieces of at most kItemBytes, plane by plane
     std::vector<CopyItem> items;
@@ -708,26 +759,54 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
                                      "ss_prefetch_unpack before the next ss_plan_step");
     DeviceGuard g(p->device);
     const auto h0 = std::chrono::steady_clock::now();
-    if (!device_range_ok(distances, (u64)p->N * 4, p->device) ||
-        !device_range_ok(active, (u64)p->N, p->device))
-        return set_err(SS_ERR_ARG, "distances [N] and active [N] must be device memory of "
-                                   "device %d", p->device);
-    if (params->dirty && !device_range_ok(params->dirty, (u64)p->N, p->device))
-        return set_err(SS_ERR_ARG, "dirty [N] must be device memory of device %d", p->device);
+    const InputKind kd = input_kind(distances, (u64)p->N * 4, p->device);
+    const InputKind ka = input_kind(active, (u64)p->N, p->device);
+    const InputKind kw = params->dirty ? input_kind(params->dirty, (u64)p->N, p->device) : kInDevice;
+    if (kd == kInBad || ka == kInBad || kw == kInBad)
+        return set_err(SS_ERR_ARG, "distances, active and dirty must be host memory or device "
+                                   "memory of device %d holding N elements", p->device);
+    // Host inputs go to the pool's mapped pinned mirrors, which the plan
+    // kernel reads over the host link.  The previous plan's kernel read its
+    // inputs before it published that plan, so the mirrors are free again.
+    const unsigned* in_dist = distances;
+    const unsigned char* in_act = active;
+    const unsigned char* in_dirty = params->dirty;
+    if (kd == kInHost) {
+        std::memcpy(p->h_in_dist, distances, (size_t)p->N * 4);
+        in_dist = p->h_in_dist_dev;
+    }
+    if (ka == kInHost) {
+        std::memcpy(p->h_in_act, active, p->N);
+        in_act = p->h_in_act_dev;
+    }
+    if (params->dirty && kw == kInHost) {
+        std::memcpy(p->h_in_dirty, params->dirty, p->N);
+        in_dirty = p->h_in_dirty_dev;
+    }
     hipStream_t caller = static_cast<hipStream_t>(stream);
 
     // The plan kernels run on the caller's stream, after the caller's earlier
     // work (which may produce the distances), after the previous step's loads
-    // (which read the plan buffers this plan rewrites) and after the previous
-    // plan's block-table update (which an overcommitted plan's successor on
-    // another stream must not overtake).  This plan's block-table update runs
+    // and evictions, and after the previous plan's block-table update (which
+    // an overcommitted plan's successor on another stream must not overtake).
+    // The evictions matter as much as the loads: this plan's block-table
+    // update rewrites the unit lists the previous packs read, this step's
+    // unpacks into pre-step free units may overwrite units the previous
+    // step released before its packs read them, and this step's
+    // host-to-device copies may read a host copy that the previous step's
+    // device-to-host copies still write.  When the caller's stream is the one
+    // the previous ss_prefetch_unpack made wait for the whole step, stream
+    // order already gives all of this.  This plan's block-table update runs
     // after the plan on the same stream.
-    TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_in_done, 0), true);
+    if (!(p->joined_valid && p->joined_stream == caller)) {
+        TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_in_done, 0), true);
+        TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_out_done, 0), true);
+    }
     TRY_HIP(p, hipStreamWaitEvent(caller, bt_event(p), 0), true);
 
     PlanArgs A{};
-    A.dist = distances;
-    A.active = active;
+    A.dist = in_dist;
+    A.active = in_act;
     A.resident = p->d_resident;
     A.units = p->d_units;
     A.n = p->N;
@@ -757,7 +836,7 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     A.fused = p->N <= kFuseAgents ? 1u : 0u;
 
     A.hist_w = p->d_hist_w;
-    A.dirty = params->dirty;
+    A.dirty = in_dirty;
     A.vwritten = p->d_vwritten;
     A.vwritten_host = p->h_vwritten_dev;
     A.woff = p->d_woff;
@@ -850,6 +929,8 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     pl.bytes_in = r.units_in * p->unit_bytes;
     pl.units_written = r.units_written;
     pl.victim_written = p->h_vwritten;
+    pl.d_victims = p->d_victims;
+    pl.d_loads = p->d_loads;
     *out = pl;
     p->state = kPlanned;
     p->stats.steps++;
@@ -960,7 +1041,7 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
             const unsigned v = p->h_victims[i];
             char* dst = p->host + p->host_off[v] + (lo - p->woff[i]) * p->unit_bytes;
             const char* src = slot + (lo - p0) * p->unit_bytes;
-            TRY_HIP(p, hipMemcpyAsync(dst, src, (hi - lo) * p->unit_bytes, hipMemcpyDeviceToHost,
+            TRY_HIP(p, copy_async(dst, src, (hi - lo) * p->unit_bytes, hipMemcpyDeviceToHost,
                                       p->st_out), true);
         }
         if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_out), true);
@@ -1037,7 +1118,7 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
             const unsigned a = p->h_loads[i];
             const char* src = p->host + p->host_off[a] + (lo - p->loff[i]) * p->unit_bytes;
             char* dst = slot + (lo - q0) * p->unit_bytes;
-            TRY_HIP(p, hipMemcpyAsync(dst, src, (hi - lo) * p->unit_bytes, hipMemcpyHostToDevice,
+            TRY_HIP(p, copy_async(dst, src, (hi - lo) * p->unit_bytes, hipMemcpyHostToDevice,
                                       p->st_in), true);
         }
         if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_in), true);
@@ -1104,6 +1185,9 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
         // an eviction queued on another caller stream
         TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_out_done, 0), true);
     }
+    // `caller` now follows the whole step (both directions)
+    p->joined_stream = caller;
+    p->joined_valid = true;
     p->state = kIdle;
     return SS_OK;
 }

@@ -77,13 +77,24 @@ def fill_host(mem, content, spec, batch_bytes=256 << 20):
 def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_bytes=True,
                slot_units=8, ring_slots=2, sample_units=None, bt_every=1, seed=0, label="",
                dirty=None, device_inputs=None, direct_bytes=0, stream=0, before_plan=None,
-               move_stream=None):
+               move_stream=None, sync_every=1, host_inputs=False, check_mirrors=False):
     """``device_inputs(t) -> (distances_ptr, active_ptr)`` replaces the uploaded
     trace on the HIP side (the oracle side always reads ``trace``).
     ``direct_bytes``: the pool's direct-transfer limit (0 = always staged).
     ``stream``: the caller's stream of every call; ``before_plan(t, stream)``
     may queue work there before step t's plan.  ``move_stream``: the caller's
-    stream of ``evict_pack`` and ``prefetch_unpack`` if not ``stream``."""
+    stream of ``evict_pack`` and ``prefetch_unpack`` if not ``stream``.
+    ``sync_every``: the host waits for the pool only every that many steps
+    (and after the last), so a step's plan and copies overlap the previous
+    step's copies in between; plans are still compared every step, the block
+    table, residency and bytes at the steps that wait.  At each of those, the
+    host copy of every agent that is not resident must hold its content.
+    ``host_inputs``: distances and masks (and the dirty mask) are passed as
+    host arrays (pageable numpy memory) instead of device pointers.
+    ``check_mirrors``: the plan's device lists are read back and compared
+    each step too."""
+    assert sync_every >= 1
+    assert sync_every == 1 or dirty is None, "the dirty-mask checks write host copies each step"
     spec = trace.pools[pool_index]
     ub = spec.unit_bytes
     staging_bytes = 2 * ring_slots * slot_units * ub
@@ -96,23 +107,35 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
         fill_host(mem, content, spec)
     pool = mem.make_pool(timing=True, direct_bytes=direct_bytes)
     opool = OraclePool(spec.capacity_units, spec.agent_units, ub)
-    dev = upload_trace(trace) if device_inputs is None else None
+    dev = upload_trace(trace) if device_inputs is None and not host_inputs else None
+    if host_inputs:
+        h_dist = np.ascontiguousarray(trace.dist, dtype=np.uint32)
+        h_act = np.ascontiguousarray(trace.active, dtype=np.uint8)
     d_dirty = None
     if dirty is not None:
         dm = np.ascontiguousarray(dirty, dtype=np.uint8)
-        d_dirty = DeviceBuffer(dm.nbytes)
-        d_dirty.upload(dm)
+        if not host_inputs:
+            d_dirty = DeviceBuffer(dm.nbytes)
+            d_dirty.upload(dm)
     T = trace.n_steps if steps is None else steps
     rng = np.random.default_rng(seed + 99)
     units_i64 = spec.agent_units.astype(np.int64)
     moved = 0
     t0 = time.time()
     for t in range(T):
-        d_ptr, a_ptr = (dev.dist(t), dev.active(t)) if dev is not None else device_inputs(t)
+        if host_inputs:
+            d_ptr, a_ptr = h_dist[t].ctypes.data, h_act[t].ctypes.data
+        else:
+            d_ptr, a_ptr = (dev.dist(t), dev.active(t)) if dev is not None else device_inputs(t)
         if before_plan is not None:
             before_plan(t, stream)
-        g = pool.plan_step(d_ptr, a_ptr, theta, budget, stream,
-                           0 if d_dirty is None else d_dirty.ptr + trace.n_agents * t)
+        if dirty is None:
+            w_ptr = 0
+        elif host_inputs:
+            w_ptr = dm[t].ctypes.data
+        else:
+            w_ptr = d_dirty.ptr + trace.n_agents * t
+        g = pool.plan_step(d_ptr, a_ptr, theta, budget, stream, w_ptr)
         o = opool.plan_step(trace.dist[t], trace.active[t], theta, budget,
                             None if dirty is None else dirty[t])
         assert g["units_written"] == o.units_written, (label, t)
@@ -128,11 +151,25 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
         assert g["n_demand_victims"] == o.n_demand_victims, (label, t)
         assert g["units_out"] == o.units_out and g["units_in"] == o.units_in, (label, t)
         assert g["bytes_out"] == o.bytes_out and g["bytes_in"] == o.bytes_in, (label, t)
+        if check_mirrors:
+            # the plan's device lists, read on the plan's stream after the call
+            nv, nl = len(o.victims), len(o.loads)
+            dv = np.empty(max(nv, 1), np.uint32)
+            dl = np.empty(max(nl, 1), np.uint32)
+            B.stream_sync(stream)
+            if nv:
+                B.copy(dv.ctypes.data, g["d_victims"], 4 * nv)
+            if nl:
+                B.copy(dl.ctypes.data, g["d_loads"], 4 * nl)
+            assert dv[:nv].tolist() == o.victims.tolist(), (label, t, "device victims")
+            assert dl[:nl].tolist() == o.loads.tolist(), (label, t, "device loads")
         ms = stream if move_stream is None else move_stream
         pool.evict_pack(ms)
         pool.prefetch_unpack(ms)
-        pool.sync()
         moved += o.units_in + o.units_out
+        if t % sync_every != 0 and t != T - 1:
+            continue
+        pool.sync()
         if t % bt_every == 0 or t == T - 1:
             bt = pool.block_table_host_all()
             obt = np.concatenate(opool.bt)
@@ -155,6 +192,19 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
                 exp = content.units_bytes(A, J)
                 bad = np.flatnonzero((got != exp).any(axis=1))
                 assert len(bad) == 0, (label, t, "device bytes", A[bad[:4]], J[bad[:4]])
+            if sync_every > 1:
+                # steps since the last wait wrote back victims the host never
+                # saw: every agent that is not resident now must have its
+                # content in its host copy (its initial copy, or the bytes
+                # written back when it was last evicted after a poisoning)
+                off = np.flatnonzero(~opool.resident)
+                if sample_units is not None and len(off) > sample_units:
+                    off = rng.choice(off, sample_units, replace=False)
+                for a in off:
+                    a = int(a)
+                    exp = content.units_bytes(np.full(units_i64[a], a), np.arange(units_i64[a]))
+                    assert np.array_equal(mem.host_copy(a), exp.reshape(-1)), \
+                        (label, t, "host copy of an offloaded agent", a)
             if dirty is None:
                 for a in o.loads:         # a resident agent's host copy is stale by design
                     mem.host_copy(int(a))[:] = POISON

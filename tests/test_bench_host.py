@@ -91,3 +91,85 @@ def test_summarize_pmc_scales_by_the_probe(tmp_path):
         assert k["units_per_launch"] == 512 and k["dispatches"] == 1
         assert abs(k["traffic_over_algorithmic"] - 1.0) < 1e-12
     assert out["kernel_source_sha256_16"] == bench.kernel_source_hash()
+
+
+def test_launch_units_by_layout():
+    # pack: ceil(items / 8) workgroups per unit.  Unpack with one item per
+    # plane (64 x 32 KiB KV pages) runs n_items workgroups per 8 units; with
+    # several items per plane (one 512 KiB plane = 16 items) it takes the pack
+    # order.
+    import bench
+    assert bench.launch_units("pack", 4096, 64, 64) == 512
+    assert bench.launch_units("unpack", 4096, 64, 64) == 512
+    assert bench.launch_units("pack", 4096, 16, 1) == 2048
+    assert bench.launch_units("unpack", 4096, 16, 1) == 2048
+
+
+def test_summarize_pmc_diffusion_layout(tmp_path):
+    # a whole 1 GiB slot of the diffusion layout is 2,048 units of 512 KiB:
+    # 4,096 workgroups for the pack and (pack order) for the unpack
+    import bench
+    pack, unpack = list(bench.PMC_KERNELS)
+    kib = bench.PROBE_BYTES / 1024
+    slot_kib = 2048 * (512 << 10) / 1024
+    grid = 4096 * bench.COPY_BLOCK
+    hdr = ["Kernel_Name", "Counter_Name", "Counter_Value", "Grid_Size"]
+    _write_csv(tmp_path / "f.csv", hdr, [(bench.PROBE_KERNEL, "FETCH_SIZE", kib / 2, 1 << 20),
+                                         (pack, "FETCH_SIZE", slot_kib / 2, grid),
+                                         (unpack, "FETCH_SIZE", 1.01 * slot_kib / 2, grid)])
+    _write_csv(tmp_path / "w.csv", hdr, [(bench.PROBE_KERNEL, "WRITE_SIZE", kib, 1 << 20),
+                                         (pack, "WRITE_SIZE", slot_kib, grid),
+                                         (unpack, "WRITE_SIZE", 1.01 * slot_kib, grid)])
+    out = bench.summarize_pmc(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "diffusion",
+                              str(tmp_path / "pmc.json"), ["cmd"])
+    assert out["kernels"]["pack"]["units_per_launch"] == 2048
+    assert out["kernels"]["unpack"]["units_per_launch"] == 2048
+    assert abs(out["kernels"]["pack"]["traffic_over_algorithmic"] - 1.0) < 1e-12
+    assert abs(out["kernels"]["unpack"]["traffic_over_algorithmic"] - 1.01) < 1e-12
+
+
+def test_summarize_trace_all_launch_rate(tmp_path):
+    # two whole-slot packs of the diffusion layout (2 GiB algorithmic bytes
+    # each) in 250 + 286.9 us, and a half-slot one in 250 us: 5 GiB / 786.9 us
+    import bench
+    pack, _ = list(bench.PMC_KERNELS)
+    rows = [(pack, 0, 250_000, 4096 * 512), (pack, 0, 286_900, 4096 * 512),
+            (pack, 0, 250_000, 2048 * 512)]
+    csv_path = tmp_path / "run_kernel_trace.csv"
+    _write_csv(csv_path, ["Kernel_Name", "Start_Timestamp", "End_Timestamp", "Grid_Size_X"], rows)
+    md = bench.summarize_trace(str(csv_path), str(tmp_path / "out.md"), "T", "cmd",
+                               workload="diffusion")
+    tbs = 5 * (1 << 30) / 786.9e-6 / 1e12
+    assert f"| `pack` | 3 | {5 * (1 << 30) / 1e9:.1f} | 787 | {tbs:.2f} | {tbs / 8:.3f} |" in md
+
+
+def test_summarize_copies(tmp_path):
+    # device-to-host copies on two streams (the probe's one copy, the step
+    # stream's three), host-to-device on one; busy time is the union of each
+    # stream's intervals, bytes come from the step records
+    import json
+    import bench
+    hdr = ["Kind", "Direction", "Stream_Id", "Source_Agent_Id", "Destination_Agent_Id",
+           "Correlation_Id", "Start_Timestamp", "End_Timestamp"]
+    D, H = "MEMORY_COPY_DEVICE_TO_HOST", "MEMORY_COPY_HOST_TO_DEVICE"
+    rows = [("MEMORY_COPY", D, 9, "a", "b", 1, 0, 50_000_000),                 # probe
+            ("MEMORY_COPY", D, 3, "a", "b", 2, 100_000_000, 110_000_000),
+            ("MEMORY_COPY", D, 3, "a", "b", 3, 105_000_000, 120_000_000),     # overlaps
+            ("MEMORY_COPY", D, 3, "a", "b", 4, 130_000_000, 140_000_000),
+            ("MEMORY_COPY", H, 4, "a", "b", 5, 100_000_000, 125_000_000)]
+    _write_csv(tmp_path / "mc.csv", hdr, rows)
+    with open(tmp_path / "steps.jsonl", "w") as f:
+        f.write(json.dumps({"t": 0, "bytes_out": 1_000_000_000, "bytes_in": 2_000_000_000}) + "\n")
+        f.write(json.dumps({"t": 1, "bytes_out": 500_000_000, "bytes_in": 0,
+                            "direct_out_bytes": 0}) + "\n")
+    with open(tmp_path / "bench.json", "w") as f:
+        f.write(json.dumps({"value": 90.0, "probe": {"d2h_GBps": 60.0, "h2d_GBps": 100.0,
+                                                    "duplex_GBps": 120.0},
+                            "dma": {"frac_of_measured_link": 0.9}}) + "\n")
+    md = bench.summarize_copies(str(tmp_path / "mc.csv"), str(tmp_path / "steps.jsonl"),
+                                str(tmp_path / "bench.json"), str(tmp_path / "o.md"), "T", "cmd")
+    # D2H: 1.5 GB over 30 ms busy = 50 GB/s, 0.833 of 60; H2D: 2 GB over 25 ms = 80 GB/s
+    assert "| device to host | 3 | 11666.7 | 30.0 | 1.50 | 50.0 | 60.0 | 0.833 |" in md
+    assert "| host to device | 1 | 25000.0 | 25.0 | 2.00 | 80.0 | 100.0 | 0.800 |" in md
+    # both: 3.5 GB over the union [100, 125] + [130, 140] = 35 ms = 100 GB/s
+    assert "3.50 GB over 35.0 ms" in md and "= 100.0 GB/s" in md and "(0.833)" in md

@@ -9,9 +9,13 @@ and byte movement.  Cases:
     every resident unit);
   * the real unit layouts (64 x 32 KiB KV pages, 448-plane LoRA adapters,
     512 KiB unified units) on agent subsets, with sampled byte checks;
-  * the round-robin and Zipf-LoRA workloads in the benchmark's own launch
-    configuration (full size, 2 MiB units and 80 MiB adapter slots, 1 GiB
-    slots, shared host copies), plans every step and bytes on sampled units;
+  * every workload but the tiny one in the benchmark's own launch
+    configuration (full size, real unit layouts, 1 GiB slots, shared host
+    copies, no host wait between steps), plans every step, block tables every
+    tenth step and bytes on sampled units;
+  * distances and masks from host memory, and the plan's device lists;
+  * the plan on one stream and the moves on another without host waits, so
+    that a step's plan overlaps the previous step's copies;
   * direct transfers (a direction at or below the pool's direct_bytes moves
     by kernel straight between units and host copies): every step direct,
     and a limit that sends some steps' directions direct and others staged;
@@ -108,19 +112,25 @@ def test_workload_full_counts(name, pool_index):
                sample_units=sample, label=f"{name}[{pool_index}] full counts")
 
 
-@pytest.mark.parametrize("name", ["roundrobin", "zipf_lora"])
-def test_bench_configuration_sampled(name):
+@pytest.mark.parametrize("name,steps", [("roundrobin", None), ("zipf_lora", None),
+                                        ("bursty", 150), ("diffusion", 60)])
+def test_bench_configuration_sampled(name, steps):
     # A workload as bench.py times it: full size, real unit layouts (2 MiB
     # units of 64 x 32 KiB; for the LoRA workload also 80 MiB adapter slots of
-    # 448 planes in a second pool planned with the same inputs), 8 GiB of
-    # staging per pool in four slots per direction, a 4 MiB direct limit, 128
-    # host copies per pool shared round-robin by the agents and a stream of
-    # the caller's own.  Plans, block tables and residency match the oracle at
-    # every step.  Bytes are checked where one step fixes them, on sampled
+    # 448 planes in a second pool planned with the same inputs; 512 KiB units
+    # in one 160 GB pool for the 50,000-agent workload), 8 GiB of staging per
+    # pool in four slots per direction, a 4 MiB direct limit, 128 host copies
+    # per pool shared round-robin by the agents and a stream of the caller's
+    # own; the host waits for the pool only every tenth step.  Plans match the
+    # oracle at every step; block tables and residency every tenth step and
+    # after the last.  Bytes are checked where one step fixes them, on sampled
     # units every tenth step: a victim whose host copy no other agent moving
     # in the step shares must leave its device bytes there, and such a load
     # must receive the bytes its host copy held before the step.
     tr = W.make_trace(name, 0)
+    if steps is not None:
+        tr = W.Trace(tr.name, tr.n_agents, steps, tr.pools, tr.active[:steps], tr.dist[:steps],
+                     tr.dist_true[:steps], tr.meta)
     n_host = 128
     ctx = []
     for pi, spec in enumerate(tr.pools):
@@ -427,7 +437,7 @@ def test_moves_on_another_stream_than_the_plan(direct):
         tr = synthetic_trace(300, 120, 12, 25, seed=23, chunk_bytes=(16,))
         run_parity(tr, theta=S, slot_units=32, ring_slots=2, stream=s_plan.handle,
                    move_stream=s_move.handle, before_plan=busy, direct_bytes=direct,
-                   label=f"moves on another stream, direct={direct}")
+                   sync_every=3, label=f"moves on another stream, direct={direct}")
     finally:
         s_plan.sync()
         s_move.sync()
@@ -541,15 +551,87 @@ def test_overcommit_between_streams(n_agents):
         mem.free()
 
 
-def test_host_pointer_for_distances_is_rejected():
-    tr = synthetic_trace(16, 8, 1, 2, seed=0)
+@pytest.mark.parametrize("name", ["tiny", "roundrobin", "diffusion"])
+def test_host_inputs(name):
+    # Distances and masks passed as host arrays (pageable numpy memory): the
+    # call copies them into pinned memory that the plan kernel reads over the
+    # host link.  One workgroup plans the 64- and 1,000-agent workloads, the
+    # classification over many workgroups the 50,000-agent one.  The plan's
+    # device lists are compared with the oracle every step too.
+    if name == "tiny":
+        tr, slot, sample, steps = W.make_trace("tiny", 0), 3, None, None
+    else:
+        tr, slot = small(W.make_trace(name, 0)), 4096
+        sample, steps = (20000, 120) if name == "diffusion" else (None, None)
+    run_parity(tr, theta=S, steps=steps, slot_units=slot, ring_slots=2, sample_units=sample,
+               host_inputs=True, check_mirrors=True, label=f"{name} host inputs")
+
+
+def test_mixed_host_and_device_inputs():
+    # host distances with a device mask, on the multi-workgroup plan path
+    tr = synthetic_trace(12289, 4000, 12, 150, seed=41, chunk_bytes=(16,), noisy=True)
+    dev = upload_trace(tr)
+    h_dist = np.ascontiguousarray(tr.dist, dtype=np.uint32)
+    try:
+        run_parity(tr, theta=S, slot_units=1024, ring_slots=2, sample_units=2000,
+                   device_inputs=lambda t: (h_dist[t].ctypes.data, dev.active(t)),
+                   check_mirrors=True, label="host distances, device mask")
+    finally:
+        dev.free()
+
+
+def test_write_back_elision_host_mask():
+    tr = W.make_trace("tiny", 2)
+    rng = np.random.default_rng(13)
+    dirty = (rng.random(tr.active.shape) < 0.4).astype(np.uint8)
+    run_parity(tr, theta=S, slot_units=2, ring_slots=2, dirty=dirty, host_inputs=True,
+               label="elision, host mask")
+
+
+def test_short_device_input_is_rejected():
+    # a device pointer with fewer than N elements left in its allocation is
+    # refused before any work, and the pool is unchanged
+    tr = synthetic_trace(16, 8, 2, 2, seed=0)
     spec = tr.pools[0]
     mem = PoolMemory(spec, 4 * spec.unit_bytes, 1)
     pool = mem.make_pool()
-    d = np.ascontiguousarray(tr.dist[0])
-    a = np.ascontiguousarray(tr.active[0])
-    with pytest.raises(B.ScaleSimError) as e:
-        pool.plan_step(d.ctypes.data, a.ctypes.data, S)
-    assert e.value.status == B.SS_ERR_ARG
-    pool.close()
-    mem.free()
+    dev = upload_trace(tr)
+    try:
+        last = dev.d.ptr + dev.d.nbytes - 4 * 15          # 15 of 16 elements left
+        with pytest.raises(B.ScaleSimError) as e:
+            pool.plan_step(last, dev.active(0), S)
+        assert e.value.status == B.SS_ERR_ARG
+        g = pool.plan_step(dev.dist(0), dev.active(0), S)
+        o = OraclePool(spec.capacity_units, spec.agent_units).plan_step(tr.dist[0], tr.active[0], S)
+        assert g["loads"].tolist() == o.loads.tolist()
+        pool.evict_pack(0)
+        pool.prefetch_unpack(0)
+        pool.sync()
+    finally:
+        pool.close()
+        dev.free()
+        mem.free()
+
+
+@pytest.mark.parametrize("direct", [0, 1 << 20])
+def test_plan_and_moves_on_two_streams_without_waits(direct):
+    # Ordering between a step's evictions and the next step's plan: the plan
+    # runs on one caller stream, the moves on another, and the host waits for
+    # the pool only every eighth step.  Many small ring slots keep a step's
+    # packs and device-to-host copies running while the next plan is queued;
+    # that plan's block-table update rewrites the lists those packs read, its
+    # unpacks may overwrite units the packs have not read yet, and its
+    # host-to-device copies may read host copies still being written, unless
+    # the plan waits for the evictions.  Block table, residency, resident bytes
+    # and the host copy of every offloaded agent are compared at each wait.
+    tr = W.shrink_planes(W.make_trace("bursty", 0), lambda p: [2048, 2048])
+    s_plan, s_move = B.Stream(), B.Stream()
+    try:
+        run_parity(tr, theta=S, steps=120, slot_units=48, ring_slots=2, sample_units=3000,
+                   stream=s_plan.handle, move_stream=s_move.handle, sync_every=8,
+                   direct_bytes=direct, label=f"two streams, no waits, direct={direct}")
+    finally:
+        s_plan.sync()
+        s_move.sync()
+        s_plan.close()
+        s_move.close()
