@@ -958,7 +958,11 @@ def main():
                                         "lists", "free_units"), phases)),
             "gpu_kernels_us": 1e3 * plan_gpu_ms / nps,
             "host_enqueue_us": host[0] / nps, "host_wait_us": host[1] / nps,
-            "host_readback_us": host[2] / nps}
+            "host_readback_us": host[2] / nps,
+            "host_enqueue_parts_us": dict(zip(
+                ("inputs", "stream_waits", "plan_launch", "other"),
+                [(sum(s["plan_enqueue_us"][i] for s in plan_stats) -
+                  sum(s["plan_enqueue_us"][i] for s in stats)) / nps for i in range(4)]))}
 
     rr = trace.pools[0] if args.workload == "roundrobin" else W.make_trace("roundrobin", 0).pools[0]
     loader = (None if args.no_loader else

@@ -161,6 +161,10 @@ typedef struct {                    /* cumulative since create or ss_reset_stats
     uint64_t direct_out_bytes, direct_in_bytes;        /* (not counted in pack/unpack or
                                                           d2h/h2d above)                  */
     double   direct_out_ms, direct_in_ms;              /* event time of those launches    */
+    double   plan_enqueue_us[4];           /* plan_host_us[0] in parts: checking (and
+                                              copying) the inputs, queueing the stream
+                                              waits, queueing the plan kernel and its
+                                              events, the rest                             */
 } ss_stats;
 
 /* Create a pool (Appendix A: register a memory module).  Validates every
@@ -193,10 +197,9 @@ void ss_pool_destroy(ss_pool* pool);
  * on the kernel's completion event); by then the kernel has finished reading
  * its inputs, though it may still be ending on the device.  The
  * block-table update that the plan implies runs on `stream` after the plan is
- * published: in the plan kernel's own tail up to 12,288 agents, else as two
- * kernels queued right behind it (after an overcommitted plan it changes
- * nothing); the copy kernels of ss_evict_pack and ss_prefetch_unpack follow
- * it whatever stream those calls are given.  Host inputs must hold N
+ * published, in the plan kernel's own tail (after an overcommitted plan it
+ * changes nothing); the copy kernels of ss_evict_pack and ss_prefetch_unpack
+ * follow it whatever stream those calls are given.  Host inputs must hold N
  * readable elements; their copy into the mirrors is part of the call's host
  * time.  `out` receives the host lists and their device mirrors (ss_plan).
  * SS_ERR_OVERCOMMIT if the active agents need more than capacity_units

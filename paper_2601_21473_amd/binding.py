@@ -86,7 +86,8 @@ class ss_stats(C.Structure):
                 ("plan_phase_us", C.c_double * 7), ("plan_host_us", C.c_double * 3),
                 ("direct_out_launches", C.c_uint64), ("direct_in_launches", C.c_uint64),
                 ("direct_out_bytes", C.c_uint64), ("direct_in_bytes", C.c_uint64),
-                ("direct_out_ms", C.c_double), ("direct_in_ms", C.c_double)]
+                ("direct_out_ms", C.c_double), ("direct_in_ms", C.c_double),
+                ("plan_enqueue_us", C.c_double * 4)]
 
 
 class ScaleSimError(RuntimeError):
@@ -272,7 +273,8 @@ class Pool:
         victims = self._host_list(out.victims, np.uint32)[:nv].copy()
         loads = self._host_list(out.loads, np.uint32)[:nl].copy()
         written = self._host_list(out.victim_written, np.uint8)[:nv].copy()
-        return {"victims": victims, "loads": loads, "n_demand": out.n_demand,
+        return {"victims": victims, "loads": loads, "n_victims": nv, "n_loads": nl,
+                "n_demand": out.n_demand,
                 "n_demand_victims": out.n_demand_victims, "units_out": out.units_out,
                 "units_in": out.units_in, "bytes_out": out.bytes_out, "bytes_in": out.bytes_in,
                 "units_written": out.units_written, "victim_written": written,
@@ -337,6 +339,7 @@ class Pool:
         out = {k: getattr(s, k) for k, _ in ss_stats._fields_}
         out["plan_phase_us"] = list(out["plan_phase_us"])
         out["plan_host_us"] = list(out["plan_host_us"])
+        out["plan_enqueue_us"] = list(out["plan_enqueue_us"])
         return out
 
     def reset_stats(self):

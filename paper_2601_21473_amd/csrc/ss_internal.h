@@ -11,6 +11,22 @@ namespace ss {
 
 typedef unsigned long long u64;
 
+// Prefetch candidates are listed in kCandLists sub-lists by distance range:
+// sub-list k holds the candidates whose distance bucket (dist_bucket below)
+// lies in [cand_list_start(k), cand_list_start(k + 1)), so a plan that can
+// accept only near candidates reads only the first sub-lists.
+constexpr unsigned kCandLists = 8;
+__host__ __device__ inline unsigned cand_list(unsigned bucket) {
+    if (bucket < 4u) return 0u;
+    if (bucket < 64u) return (31u - (unsigned)__builtin_clz(bucket)) - 1u;   // 4, 8, 16, 32 ...
+    if (bucket < 256u) return 5u;
+    if (bucket < 1024u) return 6u;
+    return 7u;
+}
+__host__ __device__ inline unsigned cand_list_start(unsigned k) {   // 0 4 8 16 32 64 256 1024
+    return k == 0 ? 0u : k <= 5 ? (2u << k) : k == 6 ? 256u : 1024u;
+}
+
 // Per-step accumulators written by the classify kernel.  The plan-core
 // kernel consumes and re-zeroes them, so they are zero between steps.
 struct PlanCounters {
@@ -19,7 +35,8 @@ struct PlanCounters {
     u64 sum_demand;      // units of active, non-resident agents
     u64 sum_evictable;   // units of inactive, resident agents
     u64 sum_cand;        // units of prefetch candidates
-    unsigned n_E, n_C, n_L, pad;
+    unsigned n_E, n_L;
+    unsigned n_C[kCandLists];   // candidates per distance sub-list
 };
 
 // Outcome of a plan, written by the plan-core kernel to device memory and to
@@ -74,12 +91,12 @@ struct PlanArgs {
     unsigned n;
     unsigned idbits;                // key = (d << idbits) | id
     unsigned threshold;
-    unsigned pad0;
+    unsigned smax;                  // largest agent size in units (pool constant)
     u64 budget;
     u64 capacity;
     PlanCounters* cnt;
     u64* listE;                     // [N] unsorted keys from classify
-    u64* listC;
+    u64* listC;                     // [kCandLists][N] candidate sub-lists by distance range
     u64* listL;
     u64* sortE;                     // [pow2 >= N] sorted keys (ascending), also global sort scratch
     u64* sortC;
@@ -101,6 +118,8 @@ struct PlanArgs {
     unsigned pad2;
     u64* phase;                     // [kPlanPhases] wall-clock stamps of the plan core, or null
     u64* hist_w;                    // [kDistBuckets] candidate units per distance bucket
+    unsigned* hist_e;               // [kDistBuckets] evictable residents' units per bucket
+                                    // (both global: multi-workgroup classification only)
     const unsigned char* dirty;     // [N] optional write-back mask (device, or mapped mirror)
     unsigned char* vwritten;        // [N] per victim: written back (device)
     unsigned char* vwritten_host;   // mapped pinned host [N]
@@ -109,7 +128,7 @@ struct PlanArgs {
     unsigned* flag_host;            // mapped pinned host word: `seq` is written there last
     unsigned seq;                   // this plan's sequence number (never 0)
     unsigned pad3;
-    const BtArgs* bt;               // block-table update (device copy), run in the fused core's tail
+    const BtArgs* bt;               // block-table update (device copy), run in the core's tail
 };
 
 // Candidate distance histogram: bucket(d) = d below 1024, then 32 buckets per
@@ -152,7 +171,6 @@ constexpr int kLdsKeys = 16384;                   // 128 KiB of u64 keys in LDS
 // The plan kernels: the plan core alone (fused: it classifies the agents
 // itself), or classification over many workgroups whose last one runs the core.
 hipError_t launch_plan(const PlanArgs& a, hipStream_t st);
-hipError_t launch_bt_update(const BtArgs& a, unsigned n_agents, hipStream_t st);
 constexpr unsigned kFuseAgents = 12288;           // plan core classifies up to this many
 hipError_t launch_pack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_unpack(const CopyArgs& a, hipStream_t st);

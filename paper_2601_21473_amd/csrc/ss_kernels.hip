@@ -14,12 +14,11 @@
 //                to a mapped host mirror, published by a sequence number
 //                written last.
 //   k_plan_core      the plan core, classifying the agents itself
-//                    (N <= kFuseAgents = 12,288) and, after publishing the
-//                    plan, updating the block table;
+//                    (N <= kFuseAgents = 12,288);
 //   k_classify_core  classification over N / 4096 workgroups, the last of
 //                    which runs the plan core (larger N), in one launch.
-//   k_bt_victims / k_bt_loads   block-table release and allocation after
-//                    k_classify_core.
+//   Either way the core's workgroup updates the block table (release of the
+//   victims' units, assignment of the loads' units) after publishing the plan.
 // Data movement:
 //   k_copy<pack>  gathers (pack) or scatters (unpack) whole units between the
 //                pool's planes and a contiguous staging slot, one wave per
@@ -134,12 +133,14 @@ __device__ __forceinline__ void load_agents(const PlanArgs& A, unsigned first, u
     }
 }
 
-// Class of agent a: its key (distance 0 when active, then the id) and its
+// Class of agent a: its key (distance 0 when active, then the id), its
 // membership of the evictable residents E, the demand loads L and the
-// prefetch candidates C (distance below the threshold).
+// prefetch candidates C (distance below the threshold), the distance bucket
+// of an inactive agent and a candidate's sub-list.
 struct AgentClass {
     u64 key;
     bool isE, isL, isC;
+    unsigned bucket, kl;
 };
 
 __device__ __forceinline__ AgentClass classify(const PlanArgs& A, unsigned a, bool valid,
@@ -150,6 +151,8 @@ __device__ __forceinline__ AgentClass classify(const PlanArgs& A, unsigned a, bo
     c.isE = valid && res && !act;
     c.isL = valid && act && !res;
     c.isC = valid && !res && !act && D < A.threshold;
+    c.bucket = dist_bucket(D);
+    c.kl = cand_list(c.bucket);
     return c;
 }
 
@@ -174,20 +177,33 @@ __device__ __forceinline__ unsigned wave_reserve(bool pred, unsigned* counter) {
     return lane0(base) + mbcnt(mask);
 }
 
-// Block-local slots of this lane in the three class lists: lane 0 issues the
-// (up to) three LDS atomics back to back and the wave waits once.
-__device__ __forceinline__ void wave_reserve3(const AgentClass& c, PlanCounters* cnt,
-                                              unsigned& oE, unsigned& oL, unsigned& oC) {
-    const u64 mE = __ballot(c.isE), mL = __ballot(c.isL), mC = __ballot(c.isC);
-    unsigned bE = 0, bL = 0, bC = 0;
+// Block-local slots of this lane in the E and L lists and in its candidate
+// sub-list: one ballot per list, then lane 0 issues the LDS atomics of every
+// non-empty list back to back and the wave waits once.
+__device__ __forceinline__ void wave_reserve_lists(const AgentClass& c, PlanCounters* cnt,
+                                                   unsigned& oE, unsigned& oL, unsigned& oC) {
+    const u64 mE = __ballot(c.isE), mL = __ballot(c.isL);
+    u64 mC[kCandLists];
+#pragma unroll
+    for (unsigned k = 0; k < kCandLists; ++k) mC[k] = __ballot(c.isC && c.kl == k);
+    unsigned bE = 0, bL = 0, bC[kCandLists];
+#pragma unroll
+    for (unsigned k = 0; k < kCandLists; ++k) bC[k] = 0;
     if (lane_id() == 0) {
         if (mE) bE = atomicAdd(&cnt->n_E, (unsigned)__popcll(mE));
         if (mL) bL = atomicAdd(&cnt->n_L, (unsigned)__popcll(mL));
-        if (mC) bC = atomicAdd(&cnt->n_C, (unsigned)__popcll(mC));
+#pragma unroll
+        for (unsigned k = 0; k < kCandLists; ++k)
+            if (mC[k]) bC[k] = atomicAdd(&cnt->n_C[k], (unsigned)__popcll(mC[k]));
     }
     oE = lane0(bE) + mbcnt(mE);
     oL = lane0(bL) + mbcnt(mL);
-    oC = lane0(bC) + mbcnt(mC);
+    oC = 0;
+#pragma unroll
+    for (unsigned k = 0; k < kCandLists; ++k) {
+        const unsigned b = lane0(bC[k]) + mbcnt(mC[k]);
+        if (c.isC && c.kl == k) oC = b;
+    }
 }
 
 // Add every thread's sums to the block counters *cnt (LDS): one reduction per
@@ -213,12 +229,11 @@ __device__ __forceinline__ void flush_sums(const ClassSums& t, PlanCounters* cnt
 
 struct CoreShared {
     u64 histw[kDistBuckets];        // candidate units per distance bucket (this workgroup)
-    PlanCounters cnt;               // fused classification
+    PlanCounters cnt;               // this workgroup's classification
     u64 wsum[kCoreThreads / 64 + 1];
-    u64 hist[256];
-    unsigned hcnt[256];
     u64 scal[8];
     unsigned uscal[8];
+    unsigned cbase[kCandLists];     // multi-workgroup classification: sub-list bases
 };
 
 // Exclusive block scan of one value per thread; returns the prefix and sets
@@ -504,6 +519,39 @@ __device__ void merge_sort_lds(u64* lds, unsigned npad) {
     else merge_sort_lds_e<8>(lds, npad);
 }
 
+// The keys that gather(buf, cap, counter) appends (its calls of gather_keys
+// with one LDS counter), sorted ascending into dst[0..m); returns m.  They are
+// gathered into LDS and sorted there when they fit; otherwise they are
+// gathered again, into dst (room for pow2ceil(N) keys), and sorted there.
+template <class Gather>
+__device__ unsigned gather_sorted(Gather gather, u64* dst, u64* lds, CoreShared& S) {
+    if (threadIdx.x == 0) S.uscal[7] = 0;
+    __syncthreads();
+    gather(lds, (unsigned)kLdsKeys, &S.uscal[7]);
+    __syncthreads();
+    const unsigned m = S.uscal[7];
+    __syncthreads();                                 // every thread has m before the reuse below
+    if (m == 0) return 0;
+    const unsigned npad = pow2ceil(m);
+    u64* buf = lds;
+    if (m > (unsigned)kLdsKeys) {
+        if (threadIdx.x == 0) S.uscal[7] = 0;
+        __syncthreads();
+        gather(dst, m, &S.uscal[7]);
+        buf = dst;
+        __syncthreads();
+    }
+    for (unsigned i = m + threadIdx.x; i < npad; i += blockDim.x) buf[i] = ~0ull;
+    __syncthreads();
+    if (buf == lds && npad <= 1024 * kRegKeys) merge_sort_lds(lds, npad);
+    else bitonic_asc(buf, npad);
+    if (buf == lds) {
+        for (unsigned i = threadIdx.x; i < m; i += blockDim.x) dst[i] = lds[i];
+        __syncthreads();
+    }
+    return m;
+}
+
 // Sort the keys src[i] < kstar (there are exactly m of them) ascending into
 // dst[0..m).  dst has room for pow2ceil(N) keys and doubles as the sort buffer
 // when m exceeds the LDS budget.
@@ -526,116 +574,16 @@ __device__ void select_sort(const u64* src, unsigned n_src, u64 kstar, unsigned 
     }
 }
 
-// Add (bin, w) of every lane with `valid` to the LDS histogram.  Lanes that
-// share a bin are summed first (a few rounds of leader election), so heavily
-// concentrated digits cost one atomic per bin and wave; whatever is left after
-// four rounds (spread digits) goes through plain atomics.
-__device__ __forceinline__ void hist_add(CoreShared& S, bool valid, unsigned bin, u64 w) {
-    const unsigned l = lane_id();
-    u64 active = __ballot(valid);
-    for (int round = 0; round < 4 && active; ++round) {
-        const unsigned leader = (unsigned)__ffsll((long long)active) - 1;
-        const unsigned lb = __shfl(bin, leader);
-        const u64 same = __ballot(valid && bin == lb) & active;
-        const u64 sum = wave_sum(((same >> l) & 1) ? w : 0);
-        if (l == leader) {
-            atomicAdd(&S.hist[lb], sum);
-            atomicAdd(&S.hcnt[lb], (unsigned)__popcll(same));
-        }
-        active &= ~same;
-    }
-    if ((active >> l) & 1) {
-        atomicAdd(&S.hist[bin], w);
-        atomicAdd(&S.hcnt[bin], 1u);
-    }
-}
-
-// Weighted radix select over the candidate keys: the smallest key k* such that
-// the units of all candidates with key <= k* exceed `cap`.  Candidates with
-// key < k* are the only ones whose cumulative prefix can stay within `cap`.
-// Returns k* and the number of keys below it in *m.  Requires the total
-// weight to exceed cap.
-__device__ u64 weighted_select(const u64* keys, unsigned n, const unsigned* units, u64 idmask,
-                               u64 cap, CoreShared& S, unsigned* m_out) {
-    // highest set bit over all keys bounds the digits that can differ
-    u64 orv = 0;
-    for (unsigned i = threadIdx.x; i < n; i += blockDim.x) orv |= keys[i];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) orv |= __shfl_xor(orv, o);
-    if (threadIdx.x == 0) S.scal[0] = 0;
-    __syncthreads();
-    if (lane_id() == 0) atomicOr(&S.scal[0], orv);
-    __syncthreads();
-    orv = S.scal[0];
-    const int top = orv ? 63 - __clzll(orv) : 0;
-    int shift = (top / 8) * 8;
-    u64 prefix = 0, pmask = 0, below = 0;
-    unsigned below_cnt = 0;
-    for (; shift >= 0; shift -= 8) {
-        for (unsigned b = threadIdx.x; b < 256; b += blockDim.x) {
-            S.hist[b] = 0;
-            S.hcnt[b] = 0;
-        }
-        __syncthreads();
-        for (unsigned base = 0; base < n; base += blockDim.x) {
-            const unsigned i = base + threadIdx.x;
-            const u64 k = i < n ? keys[i] : 0;
-            const bool in = i < n && (k & pmask) == prefix;
-            hist_add(S, in, (unsigned)(k >> shift) & 255u, in ? (u64)units[k & idmask] : 0);
-        }
-        __syncthreads();
-        if (threadIdx.x < 64) {
-            // lane l owns bins 4l..4l+3
-            const unsigned l = threadIdx.x;
-            u64 w4 = 0;
-            unsigned c4 = 0;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                w4 += S.hist[4 * l + q];
-                c4 += S.hcnt[4 * l + q];
-            }
-            const u64 wi = wave_incl_scan(w4);
-            const u64 ci = wave_incl_scan((u64)c4);
-            const u64 over = __ballot(below + wi > cap);
-            const unsigned L = over ? (unsigned)__ffsll((long long)over) - 1 : 63;
-            if (l == L) {
-                u64 acc = below + wi - w4;
-                unsigned cacc = below_cnt + (unsigned)(ci - c4);
-                unsigned bsel = 4 * l + 3;
-                for (int q = 0; q < 4; ++q) {
-                    const u64 h = S.hist[4 * l + q];
-                    if (acc + h > cap) {
-                        bsel = 4 * l + q;
-                        break;
-                    }
-                    acc += h;
-                    cacc += S.hcnt[4 * l + q];
-                }
-                S.scal[1] = acc;
-                S.uscal[0] = cacc;
-                S.uscal[1] = bsel;
-            }
-        }
-        __syncthreads();
-        below = S.scal[1];
-        below_cnt = S.uscal[0];
-        prefix |= (u64)S.uscal[1] << shift;
-        pmask |= 255ull << shift;
-        __syncthreads();
-    }
-    *m_out = below_cnt;
-    return prefix;
-}
-
 // ---------------------------------------------------------------------------
 // k_plan_core
 // ---------------------------------------------------------------------------
 
 // Classification of all agents by the plan core's workgroup: candidate units
-// into the LDS histogram, counts and sums into S.cnt, list entries at their
-// final slots (lane order inside a wave; the order between waves is arbitrary
-// and is removed by the sorts that follow).
-__device__ __forceinline__ void classify_fused(const PlanArgs& A, CoreShared& S) {
+// into the LDS histogram S.histw, evictable residents' units into the LDS
+// histogram `he`, counts and sums into S.cnt, list entries at their final
+// slots (lane order inside a wave; the order between waves is arbitrary and
+// is removed by the sorts that follow).
+__device__ __forceinline__ void classify_fused(const PlanArgs& A, CoreShared& S, unsigned* he) {
     ClassSums t;
     const unsigned step = kClassBatch * blockDim.x;
     AgentBatch b;
@@ -648,12 +596,13 @@ __device__ __forceinline__ void classify_fused(const PlanArgs& A, CoreShared& S)
             const unsigned a = base + u * blockDim.x + threadIdx.x;
             if (a - lane_id() >= A.n) break;          // wave-uniform: no agent left in this wave
             const AgentClass c = classify(A, a, a < A.n, b.D[u], b.act[u] != 0, b.res[u] != 0);
-            if (c.isC) atomicAdd(&S.histw[dist_bucket(b.D[u])], (u64)b.s[u]);
+            if (c.isC) atomicAdd(&S.histw[c.bucket], (u64)b.s[u]);
+            if (c.isE) atomicAdd(&he[c.bucket], b.s[u]);
             unsigned oE, oL, oC;
-            wave_reserve3(c, &S.cnt, oE, oL, oC);
+            wave_reserve_lists(c, &S.cnt, oE, oL, oC);
             if (c.isE) A.listE[oE] = c.key;
             if (c.isL) A.listL[oL] = c.key;
-            if (c.isC) A.listC[oC] = c.key;
+            if (c.isC) A.listC[(u64)c.kl * A.n + oC] = c.key;
             t.add(c, b.act[u] != 0, b.res[u] != 0, b.s[u]);
         }
         b = nb;
@@ -773,10 +722,34 @@ __device__ __forceinline__ void publish_plan(const PlanArgs& A) {
 
 // The plan core: one workgroup of kCoreThreads threads; `lds` holds kLdsKeys
 // keys.  Inlined into both kernels below so that its LDS accesses stay LDS
-// instructions.  kFused: the core classifies the agents itself and, after
-// publishing the plan, updates the block table (k_plan_core); otherwise it
-// runs in the last classifying workgroup of k_classify_core and the update is
-// left to k_bt_victims and k_bt_loads.
+// instructions.  kFused: the core classifies the agents itself (k_plan_core);
+// otherwise it runs in the last classifying workgroup of k_classify_core.
+// After publishing the plan it updates the block table.
+//
+// Only the keys that can take part in the plan are sorted.  Write need for the
+// units the demand loads lack (demand units minus free units), HC[b] and HE[b]
+// for the units of the candidates and of the evictable residents whose
+// distance falls in bucket b (dist_bucket is monotone in the distance).
+//  * Candidates.  The capacity a candidate of distance x may use is
+//    free1 + G(x) = max(P(lo), P(n_d)) - need, with P the unit prefix over the
+//    eviction order, lo the evictable residents farther than x and n_d the
+//    demand victims; P(lo) <= HEsuf(b) (units of buckets >= b) and
+//    P(n_d) < need + smax when need > 0 (0 otherwise).  A candidate of bucket b
+//    uses at least HCbefore(b) + 1 units, so if that exceeds
+//    min(budget, max(HEsuf(b) - need, free1 bound)) no candidate of bucket b
+//    or later is accepted (the left side grows with b, the right side
+//    shrinks).  The buckets below b_cut, the first such bucket, hold every
+//    accepted candidate; only they are gathered and sorted.
+//  * Evictable residents.  Accepted candidates use at most
+//    Cmax = min(budget, HCbefore(b_cut)) units, so every victim has less than
+//    R = need + Cmax units of evictable residents before it in eviction order.
+//    With b_E the last bucket whose HEsuf reaches R, all victims lie in the
+//    buckets >= b_E (T): a resident of a lower bucket comes after all of T,
+//    whose units reach R.  T is gathered and sorted instead of all residents.
+//    The acceptance test stays exact: a candidate nearer than every key of T
+//    has free1 + G >= units(T) - need >= Cmax, which is what the test then
+//    computes from T as well.  (R <= 0: no victims, T is empty; HEsuf(0) < R:
+//    T is every evictable resident.)
 template <bool kFused>
 __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShared& S) {
     const unsigned tid = threadIdx.x;
@@ -785,23 +758,40 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     };
     if (kFused) stamp(0);                           // else stamped at the classifying kernel's entry
     const u64 idmask = (1ull << A.idbits) - 1;
+    const unsigned idb = A.idbits;
     const unsigned* units = A.units;
+    unsigned* he_lds = reinterpret_cast<unsigned*>(lds);
     if (kFused) {
         if (tid == 0) S.cnt = PlanCounters{};
-        for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) S.histw[b] = 0;
+        for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) {
+            S.histw[b] = 0;
+            he_lds[b] = 0;
+        }
         __syncthreads();
-        classify_fused(A, S);
+        classify_fused(A, S, he_lds);
         __syncthreads();
     }
-    // the candidate histogram: this workgroup's LDS when it classified the
-    // agents itself, else the global sum of all classifying workgroups
+    // the histograms and counters: this workgroup's LDS when it classified the
+    // agents itself, else the global sums of all classifying workgroups (the
+    // counters copied into LDS)
     const u64* histw = kFused ? S.histw : A.hist_w;
-    const PlanCounters c = kFused ? S.cnt : *A.cnt;
+    const unsigned* histe = kFused ? he_lds : A.hist_e;
+    if (!kFused && tid == 0) S.cnt = *A.cnt;
     __syncthreads();
+    const PlanCounters& c = S.cnt;
     stamp(1);
 
+    static_assert(kDistBuckets == 2 * kCoreThreads, "two buckets per thread");
+    const unsigned b0 = 2 * tid;
+    const u64 hc0 = histw[b0], hc1 = histw[b0 + 1];
+    const u64 he0 = histe[b0], he1 = histe[b0 + 1];
+    if (!kFused) {                                   // each thread clears what it read
+        A.hist_w[b0] = 0;
+        A.hist_w[b0 + 1] = 0;
+        A.hist_e[b0] = 0;
+        A.hist_e[b0 + 1] = 0;
+    }
     if (c.sum_active > A.capacity) {                 // overcommit: change nothing
-        if (!kFused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
         if (tid == 0) {
             PlanResult r = {};
             r.status = 1;
@@ -813,114 +803,80 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         return;
     }
     const u64 free_before = A.capacity - c.sum_resident;
-    const unsigned nE = c.n_E, nL = c.n_L, nC = c.n_C;
+    const long long need = (long long)c.sum_demand - (long long)free_before;
+    const unsigned nE = c.n_E, nL = c.n_L;
+
+    // the cuts (see above), from one scan of each histogram
+    u64 tot_c, tot_e;
+    const u64 hcb = block_excl_scan(hc0 + hc1, S, &tot_c);     // HCbefore(b0)
+    const u64 heb = block_excl_scan(he0 + he1, S, &tot_e);     // HEbefore(b0)
+    const long long f1ub = need > 0 ? (long long)A.smax - 1 : -need;
+    auto fails = [&](u64 hc_before, u64 he_before) {
+        long long lim = (long long)(tot_e - he_before) - need;  // HEsuf(b) - need
+        if (lim < f1ub) lim = f1ub;
+        const u64 cap = A.budget < (u64)lim ? A.budget : (u64)lim;
+        return hc_before >= cap;                                // hc_before + 1 > cap
+    };
+    // the buckets that do not fail form the prefix [0, b_cut): count them and
+    // sum their candidate units in one reduction (count in the low 12 bits)
+    const u64 keep0 = fails(hcb, heb) ? 0 : ((hc0 << 12) | 1);
+    const u64 keep1 = fails(hcb + hc0, heb + he0) ? 0 : ((hc1 << 12) | 1);
+    u64 kept;
+    (void)block_excl_scan(keep0 + keep1, S, &kept);
+    const unsigned b_cut = (unsigned)(kept & 4095u);
+    const u64 cmax = A.budget < (kept >> 12) ? A.budget : (kept >> 12);
+    const long long R = need + (long long)cmax;
+    unsigned b_E = kDistBuckets;                     // R <= 0: no victims
+    if (R > 0) {
+        const u64 r = (u64)R;
+        u64 reach;
+        (void)block_excl_scan((u64)(tot_e - heb >= r) + (u64)(tot_e - heb - he0 >= r), S, &reach);
+        b_E = reach ? (unsigned)reach - 1 : 0;       // none reaches R: every evictable resident
+    }
 
     // demand loads by id (their distance is 0, so key order is id order)
     select_sort(A.listL, nL, ~0ull, nL, A.sortL, lds, S);
-    // evictable residents; eviction order is descending key = reversed array
-    select_sort(A.listE, nE, ~0ull, nE, A.sortE, lds, S);
+    // the evictable residents of buckets >= b_E, ascending; eviction order is
+    // descending key = the reversed array
+    const unsigned nT = b_E >= kDistBuckets ? 0u : gather_sorted(
+        [&](u64* buf, unsigned cap, unsigned* counter) {
+            gather_keys(A.listE, nE, [&](u64 k) { return dist_bucket((unsigned)(k >> idb)) >= b_E; },
+                        buf, cap, counter);
+        }, A.sortE, lds, S);
     const u64* sortE = A.sortE;
-    block_prefix(nE, [&](unsigned i) { return (u64)units[sortE[nE - 1 - i] & idmask]; },
+    block_prefix(nT, [&](unsigned i) { return (u64)units[sortE[nT - 1 - i] & idmask]; },
                  A.prefE, S);
     block_prefix(nL, [&](unsigned i) { return (u64)units[A.sortL[i] & idmask]; }, A.loff, S);
     stamp(2);
 
     // demand victims: shortest prefix of the eviction order covering `need`
     if (tid == 0) {
-        const long long need = (long long)c.sum_demand - (long long)free_before;
         unsigned n_d = 0;
         if (need > 0) {
-            unsigned lo = 1, hi = nE;                // prefE[hi] >= need holds
+            unsigned lo = 1, hi = nT;                // prefE[nT] >= R >= need holds
             while (lo < hi) {
                 const unsigned mid = (lo + hi) >> 1;
                 if ((long long)A.prefE[mid] >= need) hi = mid; else lo = mid + 1;
             }
-            n_d = lo < nE ? lo : nE;
+            n_d = lo < nT ? lo : nT;
         }
         S.uscal[2] = n_d;
     }
     __syncthreads();
     const unsigned n_d = S.uscal[2];
     const u64 free1 = free_before + A.prefE[n_d] - c.sum_demand;
-    const u64 avail = free1 + (A.prefE[nE] - A.prefE[n_d]);
-    const u64 cap = A.budget < avail ? A.budget : avail;
 
-    // candidates whose cumulative units can stay within cap, sorted by key:
-    // the distance histogram gives the bucket where the cumulative units pass
-    // cap; the candidates up to that bucket are sorted and the prefix that
-    // fits is kept (radix select when that set is larger than the LDS buffer)
-    unsigned m = nC;
-    u64 kstar = ~0ull;
-    bool sorted = false;
-    if (c.sum_cand > cap) {
-        // thread t holds buckets 2t and 2t+1: one block scan finds the
-        // crossing bucket (the unique one with the units before it <= cap
-        // and the units up to it > cap)
-        static_assert(kDistBuckets == 2 * kCoreThreads, "two buckets per thread");
-        if (tid == 0) S.uscal[5] = kDistBuckets;
-        __syncthreads();
-        {
-            const u64 w0 = histw[2 * tid], w1 = histw[2 * tid + 1];
-            u64 tw;
-            const u64 ew = block_excl_scan(w0 + w1, S, &tw);
-            if (ew <= cap && ew + w0 > cap) S.uscal[5] = 2 * tid;
-            else if (ew + w0 <= cap && ew + w0 + w1 > cap) S.uscal[5] = 2 * tid + 1;
-        }
-        __syncthreads();
-        const unsigned bstar = S.uscal[5];
-        // candidates up to the crossing bucket into LDS (count them on the way)
-        if (tid == 0) S.uscal[7] = 0;
-        __syncthreads();
-        const unsigned idb = A.idbits;
-        gather_keys(A.listC, nC, [&](u64 k) { return dist_bucket((unsigned)(k >> idb)) <= bstar; },
-                    lds, (unsigned)kLdsKeys, &S.uscal[7]);
-        __syncthreads();
-        const unsigned mprime = S.uscal[7];
-        if (bstar < kDistBuckets && mprime > 0 && mprime <= (unsigned)kLdsKeys) {
-            const unsigned npad = pow2ceil(mprime);
-            for (unsigned i = mprime + tid; i < npad; i += blockDim.x) lds[i] = ~0ull;
-            __syncthreads();
-            if (npad <= 1024 * kRegKeys) merge_sort_lds(lds, npad);
-            else bitonic_asc(lds, npad);
-            // inclusive prefix of units over the sorted keys; m = count <= cap
-            u64 carry = 0;
-            if (tid == 0) S.uscal[4] = mprime;
-            __syncthreads();
-            const unsigned run_len = mprime <= blockDim.x ? 1 : kPrefixRun;
-            for (unsigned b0 = 0; b0 < mprime; b0 += run_len * blockDim.x) {
-                const unsigned i0 = b0 + tid * run_len;
-                u64 w[kPrefixRun];
-                u64 sum = 0;
-#pragma unroll
-                for (unsigned u = 0; u < kPrefixRun; ++u)
-                    w[u] = u < run_len && i0 + u < mprime ? (u64)units[lds[i0 + u] & idmask] : 0;
-#pragma unroll
-                for (unsigned u = 0; u < kPrefixRun; ++u) sum += w[u];
-                u64 tot;
-                u64 run = carry + block_excl_scan(sum, S, &tot);   // units before i0
-#pragma unroll
-                for (unsigned u = 0; u < kPrefixRun; ++u) {
-                    if (u < run_len && i0 + u < mprime && run <= cap && run + w[u] > cap)
-                        S.uscal[4] = i0 + u;
-                    run += w[u];
-                }
-                carry += tot;
-            }
-            __syncthreads();
-            m = S.uscal[4];
-            for (unsigned i = tid; i < m; i += blockDim.x) A.sortC[i] = lds[i];
-            __syncthreads();
-            sorted = true;
-        } else {
-            kstar = weighted_select(A.listC, nC, units, idmask, cap, S, &m);
-        }
-        // the histogram starts the next step at zero
-        if (!kFused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
-    } else {
-        if (!kFused) for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) A.hist_w[b] = 0;
-    }
+    // the candidates of buckets < b_cut, from the sub-lists whose distance
+    // range starts below b_cut, sorted by key
+    const unsigned m = gather_sorted(
+        [&](u64* buf, unsigned cap, unsigned* counter) {
+            for (unsigned k = 0; k < kCandLists; ++k)
+                if (cand_list_start(k) < b_cut && c.n_C[k])
+                    gather_keys(A.listC + (u64)k * A.n, c.n_C[k],
+                                [&](u64 key) { return dist_bucket((unsigned)(key >> idb)) < b_cut; },
+                                buf, cap, counter);
+        }, A.sortC, lds, S);
     stamp(3);
-    if (!sorted) select_sort(A.listC, nC, kstar, m, A.sortC, lds, S);
     const u64* sortC = A.sortC;
     block_prefix(m, [&](unsigned i) { return (u64)units[sortC[i] & idmask]; }, A.prefC, S);
     stamp(4);
@@ -932,20 +888,20 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     // the searches below (the sort buffer is free)
     const u64* keysE = sortE;
     const u64* pref = A.prefE;
-    if (nE <= (unsigned)kLdsKeys) {
-        const bool both = 2 * nE + 1 <= (unsigned)kLdsKeys;
-        for (unsigned i = tid; i < nE; i += blockDim.x) lds[i] = sortE[i];
-        if (both) for (unsigned i = tid; i <= nE; i += blockDim.x) lds[nE + i] = A.prefE[i];
+    if (nT <= (unsigned)kLdsKeys) {
+        const bool both = 2 * nT + 1 <= (unsigned)kLdsKeys;
+        for (unsigned i = tid; i < nT; i += blockDim.x) lds[i] = sortE[i];
+        if (both) for (unsigned i = tid; i <= nT; i += blockDim.x) lds[nT + i] = A.prefE[i];
         keysE = lds;
-        if (both) pref = lds + nE;
+        if (both) pref = lds + nT;
     }
     __syncthreads();
     {
         // kAccept candidates per thread at once: their binary searches run in
-        // lockstep (ceil(log2(nE + 1)) steps), so the loads of one overlap the
+        // lockstep (ceil(log2(nT + 1)) steps), so the loads of one overlap the
         // others'
         constexpr unsigned kAccept = 4;
-        const unsigned steps = nE ? 32u - (unsigned)__clz(nE) : 0u;
+        const unsigned steps = nT ? 32u - (unsigned)__clz(nT) : 0u;
         const u64 base_units = pref[n_d];
         for (unsigned i0 = tid; i0 < m; i0 += kAccept * blockDim.x) {
             u64 di[kAccept], Si[kAccept];
@@ -953,17 +909,17 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
 #pragma unroll
             for (unsigned u = 0; u < kAccept; ++u) {
                 const unsigned i = i0 + u * blockDim.x;
-                di[u] = i < m ? sortC[i] >> A.idbits : 0;
+                di[u] = i < m ? sortC[i] >> idb : 0;
                 Si[u] = i < m ? A.prefC[i + 1] : 0;
                 lo[u] = 0;                           // first eviction index with d <= di
-                hi[u] = i < m ? nE : 0;
+                hi[u] = i < m ? nT : 0;
             }
             for (unsigned it = 0; it < steps; ++it) {
 #pragma unroll
                 for (unsigned u = 0; u < kAccept; ++u) {
                     if (lo[u] < hi[u]) {
                         const unsigned mid = (lo[u] + hi[u]) >> 1;
-                        if ((keysE[nE - 1 - mid] >> A.idbits) > di[u]) lo[u] = mid + 1;
+                        if ((keysE[nT - 1 - mid] >> idb) > di[u]) lo[u] = mid + 1;
                         else hi[u] = mid;
                     }
                 }
@@ -989,12 +945,12 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         unsigned n_v = n_d;
         if (n_p > 0 && A.prefC[n_p] > free1) {
             const u64 target = A.prefE[n_d] + (A.prefC[n_p] - free1);
-            unsigned lo = n_d + 1, hi = nE;
+            unsigned lo = n_d + 1, hi = nT;
             while (lo < hi) {
                 const unsigned mid = (lo + hi) >> 1;
                 if (A.prefE[mid] >= target) hi = mid; else lo = mid + 1;
             }
-            n_v = lo < nE ? lo : nE;
+            n_v = lo < nT ? lo : nT;
         }
         S.uscal[4] = n_v;
     }
@@ -1016,7 +972,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     // them without a mask): with at most one victim per thread, from the same
     // loads in one pass
     auto victim = [&](unsigned i, u64* wunits) {
-        const unsigned v = (unsigned)(sortE[nE - 1 - i] & idmask);
+        const unsigned v = (unsigned)(sortE[nT - 1 - i] & idmask);
         const unsigned char w = (!A.dirty || A.dirty[v]) ? 1 : 0;
         A.victims[i] = v;
         A.victims_host[i] = v;
@@ -1037,7 +993,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         u64 wv;
         for (unsigned i = tid; i < n_v; i += blockDim.x) victim(i, &wv);
         block_prefix(n_v, [&](unsigned i) {
-            const unsigned v = (unsigned)(sortE[nE - 1 - i] & idmask);
+            const unsigned v = (unsigned)(sortE[nT - 1 - i] & idmask);
             return (!A.dirty || A.dirty[v]) ? (u64)units[v] : 0ull;
         }, A.woff, S);
     }
@@ -1083,11 +1039,12 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         if (!kFused) *A.cnt = PlanCounters{};
     }
     publish_plan(A);
-    if (!kFused) return;
     // The host has the plan; the workgroup goes on to update the block table
-    // (waves over victims, then over loads), which saves the step two launches.
-    // Every list it reads was written above by this workgroup; the barrier
-    // inside publish_plan ordered those writes before these reads.
+    // (waves over victims, then over loads), which saves the step the launches
+    // of separate update kernels (queueing those two kernels behind the
+    // multi-workgroup plan kernel cost the host about 0.1 ms per call).  Every
+    // list it reads was written above by this workgroup; the barrier inside
+    // publish_plan ordered those writes before these reads.
     bt_tail(A.bt, n_v, n_l, n_free_used);
 }
 
@@ -1112,8 +1069,12 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
     __shared__ CoreShared S;
     const unsigned first = blockIdx.x * (kClassBatch * kCoreThreads) + threadIdx.x;
     if (A.phase && blockIdx.x == 0 && threadIdx.x == 0) A.phase[0] = wall_clock64();
+    unsigned* he = reinterpret_cast<unsigned*>(lds);  // evictable units per bucket (this workgroup)
     if (threadIdx.x == 0) S.cnt = PlanCounters{};
-    for (unsigned b = threadIdx.x; b < kDistBuckets; b += kCoreThreads) S.histw[b] = 0;
+    for (unsigned b = threadIdx.x; b < kDistBuckets; b += kCoreThreads) {
+        S.histw[b] = 0;
+        he[b] = 0;
+    }
     __syncthreads();
     AgentBatch b;
     load_agents(A, first, A.n, b);
@@ -1124,36 +1085,49 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
     for (unsigned u = 0; u < kClassBatch; ++u) {
         const unsigned a = first + u * kCoreThreads;
         c[u] = classify(A, a, a < A.n, b.D[u], b.act[u] != 0, b.res[u] != 0);
-        // candidate units per distance bucket: LDS first (distances concentrate
-        // on few buckets, where global atomics would serialize), one global
-        // atomic per non-empty bucket and workgroup below
-        if (c[u].isC) atomicAdd(&S.histw[dist_bucket(b.D[u])], (u64)b.s[u]);
-        wave_reserve3(c[u], &S.cnt, oE[u], oL[u], oC[u]);
+        // candidate and evictable units per distance bucket: LDS first
+        // (distances concentrate on few buckets, where global atomics would
+        // serialize), one global atomic per non-empty bucket and workgroup
+        // below
+        if (c[u].isC) atomicAdd(&S.histw[c[u].bucket], (u64)b.s[u]);
+        if (c[u].isE) atomicAdd(&he[c[u].bucket], b.s[u]);
+        wave_reserve_lists(c[u], &S.cnt, oE[u], oL[u], oC[u]);
         t.add(c[u], b.act[u] != 0, b.res[u] != 0, b.s[u]);
     }
     flush_sums(t, &S.cnt);
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (threadIdx.x < 64) {
+        // the workgroup's list ranges and sums: one lane per global counter, so
+        // each kind is one vector atomic and the wave waits for one round trip
         PlanCounters* g = A.cnt;
         const PlanCounters& lc = S.cnt;
-        S.uscal[0] = lc.n_E ? atomicAdd(&g->n_E, lc.n_E) : 0;
-        S.uscal[1] = lc.n_L ? atomicAdd(&g->n_L, lc.n_L) : 0;
-        S.uscal[2] = lc.n_C ? atomicAdd(&g->n_C, lc.n_C) : 0;
-        if (lc.sum_active) atomicAdd(&g->sum_active, lc.sum_active);
-        if (lc.sum_resident) atomicAdd(&g->sum_resident, lc.sum_resident);
-        if (lc.sum_demand) atomicAdd(&g->sum_demand, lc.sum_demand);
-        if (lc.sum_evictable) atomicAdd(&g->sum_evictable, lc.sum_evictable);
-        if (lc.sum_cand) atomicAdd(&g->sum_cand, lc.sum_cand);
+        const unsigned l = threadIdx.x;
+        unsigned* ctr = l < kCandLists ? &g->n_C[l] : l == kCandLists ? &g->n_E : &g->n_L;
+        const unsigned val = l < kCandLists ? lc.n_C[l] : l == kCandLists ? lc.n_E : lc.n_L;
+        unsigned base = 0;
+        if (l < kCandLists + 2 && val) base = atomicAdd(ctr, val);
+        u64* sctr = &g->sum_active;
+        u64 sval = lc.sum_active;
+        if (l == 1) { sctr = &g->sum_resident; sval = lc.sum_resident; }
+        if (l == 2) { sctr = &g->sum_demand; sval = lc.sum_demand; }
+        if (l == 3) { sctr = &g->sum_evictable; sval = lc.sum_evictable; }
+        if (l == 4) { sctr = &g->sum_cand; sval = lc.sum_cand; }
+        if (l < 5 && sval) atomicAdd(sctr, sval);
+        if (l < kCandLists) S.cbase[l] = base;
+        if (l == kCandLists) S.uscal[0] = base;
+        if (l == kCandLists + 1) S.uscal[1] = base;
     }
     __syncthreads();
 #pragma unroll
     for (unsigned u = 0; u < kClassBatch; ++u) {
         if (c[u].isE) A.listE[S.uscal[0] + oE[u]] = c[u].key;
         if (c[u].isL) A.listL[S.uscal[1] + oL[u]] = c[u].key;
-        if (c[u].isC) A.listC[S.uscal[2] + oC[u]] = c[u].key;
+        if (c[u].isC) A.listC[(u64)c[u].kl * A.n + S.cbase[c[u].kl] + oC[u]] = c[u].key;
     }
-    for (unsigned k = threadIdx.x; k < kDistBuckets; k += kCoreThreads)
+    for (unsigned k = threadIdx.x; k < kDistBuckets; k += kCoreThreads) {
         if (S.histw[k]) atomicAdd(&A.hist_w[k], S.histw[k]);
+        if (he[k]) atomicAdd(&A.hist_e[k], he[k]);
+    }
     __threadfence();                                 // release this workgroup's writes
     __syncthreads();
     if (threadIdx.x == 0) S.uscal[3] = atomicAdd(A.done, 1u) == gridDim.x - 1;
@@ -1163,33 +1137,6 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
     if (threadIdx.x == 0) *A.done = 0;
     __syncthreads();
     plan_core<false>(A, lds, S);
-}
-
-// ---------------------------------------------------------------------------
-// block table
-// ---------------------------------------------------------------------------
-
-// Standalone update (plans whose core did not classify the agents itself):
-// one block per victim, then, in a second launch, one block per load.
-__global__ void __launch_bounds__(256) k_bt_victims(BtArgs B) {
-    if (B.res->status != 0) return;
-    const unsigned nv = B.res->n_victims;
-    for (unsigned i = blockIdx.x; i < nv; i += gridDim.x) {
-        const unsigned v = B.victims[i];
-        bt_release_units(B, B.agent_off[v], B.units[v], B.voff[i], B.vwritten[i] != 0, B.woff[i],
-                         B.whost ? B.host_off[v] : 0, threadIdx.x, blockDim.x);
-    }
-}
-
-__global__ void __launch_bounds__(256) k_bt_loads(BtArgs B) {
-    if (B.res->status != 0) return;
-    const unsigned nl = B.res->n_loads;
-    const u64 nF = B.res->n_free_used;
-    for (unsigned i = blockIdx.x; i < nl; i += gridDim.x) {
-        const unsigned a = B.loads[i];
-        bt_assign_units(B, B.agent_off[a], B.units[a], B.loff[i], B.lhost ? B.host_off[a] : 0, nF,
-                        threadIdx.x, blockDim.x);
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1314,15 +1261,6 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t st) {
         const unsigned blocks = (a.n + per - 1) / per;
         hipLaunchKernelGGL(k_classify_core, dim3(blocks), dim3(kCoreThreads), 0, st, a);
     }
-    return hipGetLastError();
-}
-
-hipError_t launch_bt_update(const BtArgs& b, unsigned n_agents, hipStream_t st) {
-    const unsigned blocks = n_agents < 1024 ? n_agents : 1024;
-    hipLaunchKernelGGL(k_bt_victims, dim3(blocks), dim3(256), 0, st, b);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_bt_loads, dim3(blocks), dim3(256), 0, st, b);
     return hipGetLastError();
 }
 

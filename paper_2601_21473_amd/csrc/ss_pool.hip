@@ -142,6 +142,8 @@ struct ss_pool {
     u64* h_phase = nullptr;        // [2][kPlanPhases]
     u64* h_phase_dev = nullptr;
     u64* d_hist_w = nullptr;
+    unsigned* d_hist_e = nullptr;
+    uint32_t smax = 1;             // largest agent size in units
     bool plan_pending[2] = {false, false};
     double us_per_tick = 0.01;     // device wall clock
     CopyItem* d_items = nullptr;
@@ -171,7 +173,7 @@ struct ss_pool {
     unsigned char* h_in_dirty_dev = nullptr;
 
     hipStream_t st_out = nullptr, st_in = nullptr;
-    hipEvent_t ev_planned = nullptr, ev_bt = nullptr, ev_caller = nullptr,
+    hipEvent_t ev_planned = nullptr, ev_caller = nullptr,
                ev_out_done = nullptr, ev_in_done = nullptr;
     std::vector<hipEvent_t> ev_packed;            // per eviction slot index in the step
     unsigned n_pack_step = 0;                     // pack launches of the current step
@@ -279,12 +281,12 @@ void free_pool(ss_pool* p) {
     for (hipStream_t s : sts)
         if (s) (void)hipStreamSynchronize(s);
     // work of steps that ran on a caller's stream
-    for (hipEvent_t e : {p->ev_planned, p->ev_bt, p->ev_out_done, p->ev_in_done})
+    for (hipEvent_t e : {p->ev_planned, p->ev_out_done, p->ev_in_done})
         if (e) (void)hipEventSynchronize(e);
     void* dptrs[] = {p->d_units, p->d_agent_off, p->d_bt, p->d_resident, p->d_occ, p->d_cnt,
                      p->d_listE, p->d_listC, p->d_listL, p->d_sortE, p->d_sortC, p->d_sortL,
                      p->d_prefE, p->d_prefC, p->d_loff, p->d_victims, p->d_loads, p->d_vunits,
-                     p->d_lunits, p->d_free_old, p->d_res, p->d_hist_w,
+                     p->d_lunits, p->d_free_old, p->d_res, p->d_hist_w, p->d_hist_e,
                      p->d_wunits, p->d_vwritten, p->d_woff, p->d_items, p->d_plane_base,
                      p->d_chunk_bytes, p->d_done, p->d_host_off, p->d_whost, p->d_lhost,
                      p->d_btargs};
@@ -295,7 +297,7 @@ void free_pool(ss_pool* p) {
     for (void* h : hptrs)
         if (h) (void)hipHostFree(h);
     if (p->st_out) release_streams(p->device);
-    hipEvent_t evs[] = {p->ev_planned, p->ev_bt, p->ev_caller, p->ev_out_done, p->ev_in_done,
+    hipEvent_t evs[] = {p->ev_planned, p->ev_caller, p->ev_out_done, p->ev_in_done,
                         p->t_plan[0].a, p->t_plan[0].b, p->t_plan[1].a, p->t_plan[1].b};
     for (hipEvent_t e : evs)
         if (e) (void)hipEventDestroy(e);
@@ -459,9 +461,8 @@ ss_status collect_all_timing(ss_pool* p) {
 }
 
 // The event that follows the last plan's block-table update: the plan's own
-// event when the plan kernel runs the update in its tail (N <= kFuseAgents,
-// fixed for a pool), else the event after the update's kernels.
-hipEvent_t bt_event(const ss_pool* p) { return p->N <= kFuseAgents ? p->ev_planned : p->ev_bt; }
+// event (the plan kernel runs the update in its tail).
+hipEvent_t bt_event(const ss_pool* p) { return p->ev_planned; }
 
 // Arguments of the block-table update that follows each plan.
 BtArgs bt_args(const ss_pool* p) {
@@ -608,7 +609,7 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(dalloc(&p->d_cnt, 1));
     CREATE_TRY(dalloc(&p->d_done, 1));
     CREATE_TRY(dalloc(&p->d_listE, N));
-    CREATE_TRY(dalloc(&p->d_listC, N));
+    CREATE_TRY(dalloc(&p->d_listC, N * kCandLists));
     CREATE_TRY(dalloc(&p->d_listL, N));
     CREATE_TRY(dalloc(&p->d_sortE, npad));
     CREATE_TRY(dalloc(&p->d_sortC, npad));
@@ -644,6 +645,8 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     std::memset(p->h_phase, 0, 2 * kPlanPhases * sizeof(u64));
     CREATE_TRY(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_phase_dev), p->h_phase, 0));
     CREATE_TRY(dalloc(&p->d_hist_w, kDistBuckets));
+    CREATE_TRY(dalloc(&p->d_hist_e, kDistBuckets));
+    for (uint32_t a = 0; a < p->N; ++a) p->smax = std::max(p->smax, p->s[a]);
     {
         int khz = 0;
         if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, p->device) == hipSuccess &&
@@ -714,6 +717,8 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     {
         std::vector<u64> zw(kDistBuckets, 0);
         CREATE_TRY(hipMemcpy(p->d_hist_w, zw.data(), kDistBuckets * sizeof(u64), hipMemcpyHostToDevice));
+        CREATE_TRY(hipMemcpy(p->d_hist_e, zw.data(), kDistBuckets * sizeof(unsigned),
+                             hipMemcpyHostToDevice));
     }
     CREATE_TRY(hipMemcpy(p->d_items, items.data(), items.size() * sizeof(CopyItem),
                          hipMemcpyHostToDevice));
@@ -722,8 +727,7 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
                          hipMemcpyHostToDevice));
 
     CREATE_TRY(acquire_streams(p->device, &p->st_out, &p->st_in));
-    for (hipEvent_t* ev : {&p->ev_planned, &p->ev_bt, &p->ev_caller, &p->ev_out_done,
-                           &p->ev_in_done})
+    for (hipEvent_t* ev : {&p->ev_planned, &p->ev_caller, &p->ev_out_done, &p->ev_in_done})
         CREATE_TRY(make_event(ev, false));
     if (p->flags & SS_FLAG_TIMING) {
         for (TimedPair& tp : p->t_plan) {
@@ -784,6 +788,7 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
         in_dirty = p->h_in_dirty_dev;
     }
     hipStream_t caller = static_cast<hipStream_t>(stream);
+    const auto e0 = std::chrono::steady_clock::now();     // inputs checked (and copied)
 
     // The plan kernels run on the caller's stream, after the caller's earlier
     // work (which may produce the distances), after the previous step's loads
@@ -803,6 +808,7 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
         TRY_HIP(p, hipStreamWaitEvent(caller, p->ev_out_done, 0), true);
     }
     TRY_HIP(p, hipStreamWaitEvent(caller, bt_event(p), 0), true);
+    const auto e1 = std::chrono::steady_clock::now();     // stream waits queued
 
     PlanArgs A{};
     A.dist = in_dist;
@@ -836,6 +842,8 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     A.fused = p->N <= kFuseAgents ? 1u : 0u;
 
     A.hist_w = p->d_hist_w;
+    A.hist_e = p->d_hist_e;
+    A.smax = p->smax;
     A.dirty = in_dirty;
     A.vwritten = p->d_vwritten;
     A.vwritten_host = p->h_vwritten_dev;
@@ -856,15 +864,10 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     TRY_HIP(p, launch_plan(A, caller), true);
     if (timing) TRY_HIP(p, hipEventRecord(p->t_plan[tslot].b, caller), true);
     TRY_HIP(p, hipEventRecord(p->ev_planned, caller), true);
-    // The block-table update: a fused plan core runs it in its own tail,
-    // after publishing the plan; otherwise two kernels queue right behind the
-    // plan kernel on the same stream, while the host waits for the plan.
-    // Either way it needs nothing from the host, and it changes nothing after
-    // an overcommitted plan.
-    if (!A.fused) {
-        TRY_HIP(p, launch_bt_update(bt_args(p), p->N, caller), true);
-        TRY_HIP(p, hipEventRecord(p->ev_bt, caller), true);
-    }
+    const auto e2 = std::chrono::steady_clock::now();     // plan kernel and its events queued
+    // The block-table update runs in the plan kernel's own tail, after the
+    // plan is published; it needs nothing from the host, and it changes
+    // nothing after an overcommitted plan.
     p->bt_stream = caller;
 
     const auto h1 = std::chrono::steady_clock::now();
@@ -942,6 +945,10 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
         p->stats.plan_host_us[0] += us(h1 - h0);
         p->stats.plan_host_us[1] += us(h2 - h1);
         p->stats.plan_host_us[2] += us(h3 - h2);
+        p->stats.plan_enqueue_us[0] += us(e0 - h0);
+        p->stats.plan_enqueue_us[1] += us(e1 - e0);
+        p->stats.plan_enqueue_us[2] += us(e2 - e1);
+        p->stats.plan_enqueue_us[3] += us(h1 - e2);
     }
     return SS_OK;
 }
@@ -1042,7 +1049,7 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
             char* dst = p->host + p->host_off[v] + (lo - p->woff[i]) * p->unit_bytes;
             const char* src = slot + (lo - p0) * p->unit_bytes;
             TRY_HIP(p, copy_async(dst, src, (hi - lo) * p->unit_bytes, hipMemcpyDeviceToHost,
-                                      p->st_out), true);
+                                  p->st_out), true);
         }
         if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_out), true);
     }
@@ -1119,7 +1126,7 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
             const char* src = p->host + p->host_off[a] + (lo - p->loff[i]) * p->unit_bytes;
             char* dst = slot + (lo - q0) * p->unit_bytes;
             TRY_HIP(p, copy_async(dst, src, (hi - lo) * p->unit_bytes, hipMemcpyHostToDevice,
-                                      p->st_in), true);
+                                  p->st_in), true);
         }
         if (timing) TRY_HIP(p, hipEventRecord(tp->b, p->st_in), true);
         return SS_OK;
@@ -1271,7 +1278,7 @@ ss_status ss_sync(ss_pool* p) {
     for (hipStream_t s : {p->st_out, p->st_in})
         TRY_HIP(p, hipStreamSynchronize(s), true);
     // work of a step that ran on a caller's stream
-    for (hipEvent_t e : {p->ev_planned, p->ev_bt, p->ev_out_done, p->ev_in_done})
+    for (hipEvent_t e : {p->ev_planned, p->ev_out_done, p->ev_in_done})
         TRY_HIP(p, hipEventSynchronize(e), true);
     return SS_OK;
 }

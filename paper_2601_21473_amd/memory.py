@@ -70,7 +70,8 @@ class PoolMemory:
     ``host_slots`` bounds the host copies: ``None`` gives every agent its own
     copy; an integer ``k`` gives agents ``k`` distinct copies of the largest
     agent size, agent ``a`` using copy ``a % k`` (many logical agents behind one
-    physical copy, as the paper does for adapters)."""
+    physical copy, as the paper does for adapters); an array gives agent ``a``
+    copy ``host_slots[a]`` of the largest agent size."""
 
     def __init__(self, spec, staging_bytes: int, ring_slots: int, host_slots=None,
                  device: int = 0):
@@ -84,9 +85,13 @@ class PoolMemory:
             host_bytes = int(units.sum()) * ub
         else:
             slot = int(units.max()) * ub
-            self.host_off = (np.arange(len(units), dtype=np.uint64) % np.uint64(host_slots)) * \
-                np.uint64(slot)
-            host_bytes = int(host_slots) * slot
+            if np.ndim(host_slots) == 0:
+                slot_of = np.arange(len(units), dtype=np.uint64) % np.uint64(host_slots)
+            else:
+                slot_of = np.asarray(host_slots, dtype=np.uint64)
+                assert len(slot_of) == len(units)
+            self.host_off = slot_of * np.uint64(slot)
+            host_bytes = (int(slot_of.max()) + 1) * slot
         self.host = HostBuffer(host_bytes)
         self.host_np = self.host.np
         self.ring_slots = ring_slots

@@ -112,9 +112,9 @@ def test_workload_full_counts(name, pool_index):
                sample_units=sample, label=f"{name}[{pool_index}] full counts")
 
 
-@pytest.mark.parametrize("name,steps", [("roundrobin", None), ("zipf_lora", None),
-                                        ("bursty", 150), ("diffusion", 60)])
-def test_bench_configuration_sampled(name, steps):
+@pytest.mark.parametrize("name,steps,watched", [("roundrobin", None, 0), ("zipf_lora", None, 0),
+                                                ("bursty", 150, 0), ("diffusion", 60, 64)])
+def test_bench_configuration_sampled(name, steps, watched):
     # A workload as bench.py times it: full size, real unit layouts (2 MiB
     # units of 64 x 32 KiB; for the LoRA workload also 80 MiB adapter slots of
     # 448 planes in a second pool planned with the same inputs; 512 KiB units
@@ -126,20 +126,27 @@ def test_bench_configuration_sampled(name, steps):
     # after the last.  Bytes are checked where one step fixes them, on sampled
     # units every tenth step: a victim whose host copy no other agent moving
     # in the step shares must leave its device bytes there, and such a load
-    # must receive the bytes its host copy held before the step.
+    # must receive the bytes its host copy held before the step.  Where a step
+    # moves so many agents that every shared copy has several movers (the
+    # 50,000-agent workload), `watched` sampled agents get private host copies.
     tr = W.make_trace(name, 0)
     if steps is not None:
         tr = W.Trace(tr.name, tr.n_agents, steps, tr.pools, tr.active[:steps], tr.dist[:steps],
                      tr.dist_true[:steps], tr.meta)
     n_host = 128
+    slot_of = np.arange(tr.n_agents, dtype=np.int64) % n_host
+    if watched:
+        watch = np.random.default_rng(5).choice(tr.n_agents, watched, replace=False)
+        slot_of[watch] = n_host + np.arange(watched)
+    n_slots = int(slot_of.max()) + 1
     ctx = []
     for pi, spec in enumerate(tr.pools):
         ub = spec.unit_bytes
-        mem = PoolMemory(spec, 8192 << 20, 4, host_slots=n_host)
+        mem = PoolMemory(spec, 8192 << 20, 4, host_slots=slot_of)
         words = int(spec.agent_units.max()) * ub // 8
         pattern = np.arange(words, dtype=np.uint64)
         host64 = mem.host_np.view(np.uint64)
-        for k in range(n_host):   # every 8-byte word of both pools' host copies distinct
+        for k in range(n_slots):  # every 8-byte word of both pools' host copies distinct
             host64[k * words:(k + 1) * words] = pattern + np.uint64((pi << 56) | ((k + 1) << 40))
         del pattern, host64
         units = spec.agent_units.astype(np.int64)
@@ -153,9 +160,8 @@ def test_bench_configuration_sampled(name, steps):
     checked_v = checked_l = 0
 
     def unique_movers(group, movers):
-        slots = np.asarray(movers, dtype=np.int64) % n_host
-        counts = np.bincount(slots, minlength=n_host)
-        return [int(a) for a in group if counts[int(a) % n_host] == 1]
+        counts = np.bincount(slot_of[np.asarray(movers, dtype=np.int64)], minlength=n_slots)
+        return [int(a) for a in group if counts[slot_of[int(a)]] == 1]
 
     def sample_units(units, a):
         return sorted({0, int(units[a]) // 2, int(units[a]) - 1})
@@ -351,6 +357,38 @@ def test_lists_beyond_lds_sort_buffer():
     tr = synthetic_trace(40000, 20000, 25, 600, seed=11, chunk_bytes=(16,))
     run_parity(tr, theta=S, slot_units=8192, ring_slots=2, sample_units=4000,
                label="global sort path")
+
+
+def test_cut_sets_beyond_lds():
+    # 40,000 unit-size agents, room for 20,000.  Step 0 fills the pool with
+    # agents that never run again; at step 1 the other 20,000 agents are one
+    # step away, so the plan swaps the whole pool: the evictable residents it
+    # must sort (20,000) and the candidates it may accept (20,000) both exceed
+    # the plan kernel's 16,384-key LDS buffer and take the global-memory sorts.
+    n, cap = 40000, 20000
+    active = np.zeros((4, n), np.uint8)
+    active[0, :cap] = 1
+    active[2, cap:] = 1
+    dist = W.exact_distances(active)
+    pool = W.PoolSpec("syn", cap, [16], np.ones(n, np.uint32))
+    tr = W.Trace("swap40000", n, 4, [pool], active, dist, dist.copy(), {})
+    run_parity(tr, theta=S, slot_units=8192, ring_slots=2, sample_units=4000,
+               label="cut sets beyond LDS")
+
+
+@pytest.mark.parametrize("n_agents", [40000, 50000])
+@pytest.mark.parametrize("theta,budget", [(S, None), (3, None), (S, 300)])
+def test_many_agents_variable_sizes(n_agents, theta, budget):
+    # the multi-workgroup plan path with ragged sizes, noisy distances, a
+    # pool of about a tenth of all units and several hundred activations per
+    # step: candidate cuts, evictable cuts, thresholds and budgets
+    rng = np.random.default_rng(n_agents)
+    units = rng.integers(1, 9, size=n_agents).astype(np.uint32)
+    cap = int(units.sum()) // 10
+    tr = synthetic_trace(n_agents, cap, 24, lambda t, r: r.integers(200, 600), seed=n_agents,
+                         units=units, chunk_bytes=(16,), noisy=True)
+    run_parity(tr, theta=theta, budget=budget, slot_units=8192, ring_slots=2, sample_units=3000,
+               label=f"{n_agents} agents t{theta} b{budget}")
 
 
 @pytest.mark.parametrize("direct", [0, 1 << 20])
