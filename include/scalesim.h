@@ -362,6 +362,21 @@ ss_status ss_interaction_distances(const int32_t* pos_xy, const uint32_t* d_acti
                                    uint32_t* out, void* workspace, uint64_t workspace_bytes,
                                    void* stream);
 
+/* The same computation for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the partial minima live in a static device array of the
+ * library instead of a workspace, so the call allocates nothing.  At most
+ * 1,048,576 agents (SS_ERR_ARG beyond, nothing queued).  The array holds
+ * 4 MiB on each device the library runs on until the process ends; its
+ * device address is looked up on the first call on a device.  Every call on
+ * one device shares that array and clears it on `stream` before use: calls
+ * whose work overlaps on one device (other streams, other threads) race and
+ * give unspecified results.  Other arguments, errors and results as
+ * ss_interaction_distances. */
+ss_status ss_interaction_distances_static(const int32_t* pos_xy, const uint32_t* d_action,
+                                          uint32_t n_agents, uint32_t velocity, uint32_t radius,
+                                          uint32_t* out, void* stream);
+
 /* ---- Load-task scheduler (Appendix A, "Load task scheduler" and
  * "Preemption support") ------------------------------------------------------
  *

@@ -36,7 +36,8 @@ EXPORTS = ["ss_pool_create", "ss_pool_destroy", "ss_plan_step", "ss_evict_pack",
            "ss_stream_create", "ss_stream_destroy", "ss_stream_sync", "ss_event_create",
            "ss_event_destroy", "ss_event_record", "ss_event_elapsed", "ss_loader_create",
            "ss_loader_destroy", "ss_loader_submit", "ss_loader_pump", "ss_loader_pending",
-           "ss_loader_sync", "ss_loader_get_stats", "ss_debug_fail_copy"]
+           "ss_loader_sync", "ss_loader_get_stats", "ss_debug_fail_copy",
+           "ss_interaction_distances_static"]
 
 
 class ss_load_task(C.Structure):
@@ -162,6 +163,8 @@ def load():
         "ss_hop_distances": ([P, P, C.c_uint32, C.c_uint32, P, C.c_uint32, C.c_uint32, P, P,
                               C.c_uint64, P], C.c_int32),
         "ss_debug_fail_copy": ([C.c_uint32], None),
+        "ss_interaction_distances_static": ([P, P, C.c_uint32, C.c_uint32, C.c_uint32, P, P],
+                                            C.c_int32),
         "ss_interaction_distances_workspace": ([C.c_uint32], C.c_uint64),
         "ss_interaction_distances": ([P, P, C.c_uint32, C.c_uint32, C.c_uint32, P, P, C.c_uint64,
                                       P], C.c_int32),
@@ -464,6 +467,15 @@ def interaction_distances(pos_xy: int, d_action: int, n_agents: int, velocity: i
     _check(load().ss_interaction_distances(int(pos_xy), int(d_action), int(n_agents),
                                            int(velocity), int(radius), int(out), int(workspace),
                                            int(workspace_bytes), int(stream)))
+
+
+def interaction_distances_static(pos_xy: int, d_action: int, n_agents: int, velocity: int,
+                                 radius: int, out: int, stream: int = 0):
+    """Queue ``ss_interaction_distances_static`` (device addresses; no
+    workspace: the library's static scratch, at most 1,048,576 agents)."""
+    _check(load().ss_interaction_distances_static(int(pos_xy), int(d_action), int(n_agents),
+                                                  int(velocity), int(radius), int(out),
+                                                  int(stream)))
 
 
 class Stream:

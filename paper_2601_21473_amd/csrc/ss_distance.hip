@@ -53,6 +53,7 @@
 #include "ss_internal.h"
 
 #include <algorithm>
+#include <mutex>
 
 namespace ss {
 namespace {
@@ -781,31 +782,43 @@ ss_status ss_hop_distances(const uint32_t* row_off, const uint32_t* col, uint32_
 
 uint64_t ss_interaction_distances_workspace(uint32_t n_agents) { return (uint64_t)n_agents * 4; }
 
-ss_status ss_interaction_distances(const int32_t* pos_xy, const uint32_t* d_action,
-                                   uint32_t n_agents, uint32_t velocity, uint32_t radius,
-                                   uint32_t* out, void* workspace, uint64_t workspace_bytes,
-                                   void* stream) {
+}  // extern "C"
+
+// Partial minima of ss_interaction_distances_static (4 MiB): one array per
+// device, held from the library's load until the process ends, shared by
+// every call on that device.  Host code never uses its name as an address:
+// the device address is looked up once per device (scratch_addr) and kept.
+static __device__ __align__(256) unsigned scratch[1u << 20];
+
+namespace {
+
+// Checks the arrays of an interaction-distance call (not its workspace) and
+// returns the current device in *dev.
+ss_status interaction_args(const int32_t* pos_xy, const uint32_t* d_action, uint32_t n_agents,
+                           uint32_t velocity, const uint32_t* out, int* dev) {
     if (n_agents >= (1u << 31)) return set_err(SS_ERR_ARG, "n_agents must be below 2^31");
     if (velocity == 0) return set_err(SS_ERR_ARG, "velocity must be >= 1");
     if (n_agents == 0) return SS_OK;
-    if (!pos_xy || !d_action || !out || !workspace) return set_err(SS_ERR_ARG, "NULL argument");
-    const u64 need = ss_interaction_distances_workspace(n_agents);
-    if (workspace_bytes < need)
-        return set_err(SS_ERR_ARG, "workspace_bytes %llu < %llu", (unsigned long long)workspace_bytes,
-                       (unsigned long long)need);
-    int dev = -1;
-    if (hipGetDevice(&dev) != hipSuccess) {
+    if (!pos_xy || !d_action || !out) return set_err(SS_ERR_ARG, "NULL argument");
+    if (hipGetDevice(dev) != hipSuccess) {
         (void)hipGetLastError();
         return set_err(SS_ERR_ARG, "no current device");
     }
-    if (!device_range_ok(pos_xy, (u64)n_agents * 8, dev) ||
-        !device_range_ok(d_action, (u64)n_agents * 4, dev) ||
-        !device_range_ok(out, (u64)n_agents * 4, dev) || !device_range_ok(workspace, need, dev))
+    if (!device_range_ok(pos_xy, (u64)n_agents * 8, *dev) ||
+        !device_range_ok(d_action, (u64)n_agents * 4, *dev) ||
+        !device_range_ok(out, (u64)n_agents * 4, *dev))
         return set_err(SS_ERR_ARG, "every array must be device memory of the current device (%d)",
-                       dev);
+                       *dev);
+    return SS_OK;
+}
+
+// The three interaction kernels on `st`, with d2min [n_agents] as the
+// partial minima (cleared by the first kernel).
+ss_status interaction_launch(const int32_t* pos_xy, const uint32_t* d_action, uint32_t n_agents,
+                             uint32_t velocity, uint32_t radius, uint32_t* out, unsigned* d2min,
+                             int dev, hipStream_t st) {
     int cus = 256;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 256;
-    unsigned* d2min = static_cast<unsigned*>(workspace);
     const unsigned iblocks = (n_agents + kPairThreads - 1) / kPairThreads;
     // split the other agents into slices so that about 8 workgroups run per CU
     const unsigned want = (unsigned)std::max<u64>(1, (u64)cus * 8 / iblocks);
@@ -813,7 +826,6 @@ ss_status ss_interaction_distances(const int32_t* pos_xy, const uint32_t* d_acti
     const unsigned slices = std::min(want, tiles);
     const unsigned slice = (tiles + slices - 1) / slices * kPairTile;
     const unsigned nslice = (n_agents + slice - 1) / slice;
-    hipStream_t st = static_cast<hipStream_t>(stream);
     const unsigned b256 = (n_agents + 255) / 256;
     hipLaunchKernelGGL(k_pair_init, dim3(b256), dim3(256), 0, st, d2min, n_agents);
     hipError_t e = hipGetLastError();
@@ -830,6 +842,70 @@ ss_status ss_interaction_distances(const int32_t* pos_xy, const uint32_t* d_acti
     if (e != hipSuccess)
         return set_err(SS_ERR_HIP, "interaction distance kernels: %s", hipGetErrorString(e));
     return SS_OK;
+}
+
+constexpr uint32_t kStaticPairAgents = 1u << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+unsigned* g_scratch_addr[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev` (current), looked up on the
+// first call per device.
+ss_status scratch_addr(int dev, unsigned** out) {
+    if (dev < 0 || dev >= kMaxDevices) return set_err(SS_ERR_ARG, "device %d out of range", dev);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr)
+            return set_err(SS_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                           hipGetErrorString(e));
+        g_scratch_addr[dev] = static_cast<unsigned*>(ptr);
+    }
+    *out = g_scratch_addr[dev];
+    return SS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ss_status ss_interaction_distances(const int32_t* pos_xy, const uint32_t* d_action,
+                                   uint32_t n_agents, uint32_t velocity, uint32_t radius,
+                                   uint32_t* out, void* workspace, uint64_t workspace_bytes,
+                                   void* stream) {
+    int dev = -1;
+    ss_status st = interaction_args(pos_xy, d_action, n_agents, velocity, out, &dev);
+    if (st != SS_OK || n_agents == 0) return st;
+    if (!workspace) return set_err(SS_ERR_ARG, "NULL argument");
+    const u64 need = ss_interaction_distances_workspace(n_agents);
+    if (workspace_bytes < need)
+        return set_err(SS_ERR_ARG, "workspace_bytes %llu < %llu", (unsigned long long)workspace_bytes,
+                       (unsigned long long)need);
+    if (!device_range_ok(workspace, need, dev))
+        return set_err(SS_ERR_ARG, "every array must be device memory of the current device (%d)",
+                       dev);
+    return interaction_launch(pos_xy, d_action, n_agents, velocity, radius, out,
+                              static_cast<unsigned*>(workspace), dev,
+                              static_cast<hipStream_t>(stream));
+}
+
+ss_status ss_interaction_distances_static(const int32_t* pos_xy, const uint32_t* d_action,
+                                          uint32_t n_agents, uint32_t velocity, uint32_t radius,
+                                          uint32_t* out, void* stream) {
+    static_assert(sizeof(scratch) == kStaticPairAgents * sizeof(unsigned), "scratch size");
+    if (n_agents > kStaticPairAgents)
+        return set_err(SS_ERR_ARG, "n_agents %u exceeds the %u agents of the static scratch "
+                                   "(use ss_interaction_distances with a workspace)",
+                       n_agents, kStaticPairAgents);
+    int dev = -1;
+    ss_status st = interaction_args(pos_xy, d_action, n_agents, velocity, out, &dev);
+    if (st != SS_OK || n_agents == 0) return st;
+    unsigned* d2min = nullptr;
+    st = scratch_addr(dev, &d2min);
+    if (st != SS_OK) return st;
+    return interaction_launch(pos_xy, d_action, n_agents, velocity, radius, out, d2min, dev,
+                              static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"
