@@ -320,8 +320,12 @@ def parse():
                     help="write a host-link summary of a rocprofv3 --memory-copy-trace CSV")
     ap.add_argument("--jsonl", default=None,
                     help="write one JSON record per step (warm-up, timed and plan-latency steps) "
-                         "to this file; the host then waits for each step before the next "
-                         "(the next plan waits for it on the device anyway)")
+                         "to this file: the plan's counts and bytes and the host time of the "
+                         "step's calls (no extra waits)")
+    ap.add_argument("--jsonl-timing", action="store_true",
+                    help="with --jsonl, add each step's plan, pack, copy and unpack times from "
+                         "the pools' timing counters (the host then waits for every step before "
+                         "queueing the next)")
     return ap.parse_args()
 
 
@@ -752,26 +756,35 @@ def main():
     def record(t, phase, plans, t_call):
         if jl is None:
             return
-        cur = [p.stats() for p in pools]           # waits for the step
-        tot = {k: sum(c[k] for c in cur) for k in stat_keys}
-        tot["plan_host_us"] = sum(sum(c["plan_host_us"]) for c in cur)
-        prev = jl_prev[0] or {k: 0 for k in tot}
-        d = {k: tot[k] - prev[k] for k in tot}
-        jl_prev[0] = tot
-        jl.write(json.dumps({
-            "t": t, "phase": phase, "n_victims": sum(pl["n_victims"] for pl in plans),
-            "n_loads": sum(pl["n_loads"] for pl in plans),
-            "units_out": sum(pl["units_out"] for pl in plans),
-            "units_in": sum(pl["units_in"] for pl in plans),
-            "bytes_out": sum(pl["bytes_out"] for pl in plans),
-            "bytes_in": sum(pl["bytes_in"] for pl in plans),
-            "t_step_call_ms": 1e3 * t_call, "t_plan_us": d["plan_host_us"],
-            "t_plan_gpu_us": 1e3 * d["plan_gpu_ms"], "t_pack_ms": d["pack_ms"],
-            "t_d2h_ms": d["d2h_ms"], "t_h2d_ms": d["h2d_ms"], "t_unpack_ms": d["unpack_ms"],
-            "t_direct_out_ms": d["direct_out_ms"], "t_direct_in_ms": d["direct_in_ms"],
-            "pack_launches": d["pack_launches"], "unpack_launches": d["unpack_launches"],
-            "direct_out_bytes": d["direct_out_bytes"], "direct_in_bytes": d["direct_in_bytes"]})
-            + "\n")
+        direct = int(args.direct_mib * (1 << 20))
+        out_b = sum(pl["bytes_out"] for pl in plans)
+        in_b = sum(pl["bytes_in"] for pl in plans)
+        rec = {"t": t, "phase": phase, "n_victims": sum(pl["n_victims"] for pl in plans),
+               "n_loads": sum(pl["n_loads"] for pl in plans),
+               "units_out": sum(pl["units_out"] for pl in plans),
+               "units_in": sum(pl["units_in"] for pl in plans),
+               "bytes_out": out_b, "bytes_in": in_b,
+               # a direction at or below the direct limit moves by kernel, not by copies
+               "direct_out_bytes": sum(pl["bytes_out"] for pl in plans
+                                       if 0 < pl["bytes_out"] <= direct),
+               "direct_in_bytes": sum(pl["bytes_in"] for pl in plans
+                                      if 0 < pl["bytes_in"] <= direct),
+               "t_step_call_ms": 1e3 * t_call}
+        if args.jsonl_timing:
+            cur = [p.stats() for p in pools]       # waits for the step
+            tot = {k: sum(c[k] for c in cur) for k in stat_keys}
+            tot["plan_host_us"] = sum(sum(c["plan_host_us"]) for c in cur)
+            prev = jl_prev[0] or {k: 0 for k in tot}
+            d = {k: tot[k] - prev[k] for k in tot}
+            jl_prev[0] = tot
+            rec.update({"t_plan_us": d["plan_host_us"], "t_plan_gpu_us": 1e3 * d["plan_gpu_ms"],
+                        "t_pack_ms": d["pack_ms"], "t_d2h_ms": d["d2h_ms"],
+                        "t_h2d_ms": d["h2d_ms"], "t_unpack_ms": d["unpack_ms"],
+                        "t_direct_out_ms": d["direct_out_ms"],
+                        "t_direct_in_ms": d["direct_in_ms"],
+                        "pack_launches": d["pack_launches"],
+                        "unpack_launches": d["unpack_launches"]})
+        jl.write(json.dumps(rec) + "\n")
 
     def step(t, phase="timed"):
         ts = time.perf_counter()

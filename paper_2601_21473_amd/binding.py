@@ -12,7 +12,10 @@ import os
 
 import numpy as np
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libscalesim.so")
+# SCALESIM_LIB names another build of the library to load instead (for
+# example the one with host-side sanitizers, build.build(sanitize=True)).
+LIB_PATH = os.environ.get("SCALESIM_LIB") or \
+    os.path.join(os.path.dirname(os.path.abspath(__file__)), "libscalesim.so")
 
 SS_OK = 0
 SS_ERR_ARG = -1

@@ -106,7 +106,7 @@ struct PlanArgs {
     u64* loff;                      // [N+1] prefix units over loads
     unsigned* victims;              // [N] device copy of the plan
     unsigned* loads;                // [N]
-    const unsigned* occ;            // occupancy bitmap, bit u = unit u in use
+    unsigned* occ;                  // occupancy bitmap, bit u = unit u in use
     unsigned occ_words;
     unsigned pad1;
     int* free_old;                  // [U] pre-step free units, ascending

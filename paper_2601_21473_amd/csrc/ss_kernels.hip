@@ -613,40 +613,62 @@ __device__ __forceinline__ void classify_fused(const PlanArgs& A, CoreShared& S,
 // Publish the plan to the host: every thread's host-visible writes are made
 // visible at system scope, then one thread writes the plan's sequence number
 // to the mapped flag word, which the host polls.  Last action of the core.
-// Release one victim's units j0, j0 + jstep, ... < s (block-table row at
-// `base`, eviction-order offset o, written-back offset ow, host-copy offset
-// hoff): record them in eviction order for the loads (and, for a victim that
-// is written back, for the pack), clear the block-table entries and the
-// units' occupancy bits.
-__device__ __forceinline__ void bt_release_units(const BtArgs& B, u64 base, unsigned s, u64 o,
-                                                 bool written, u64 ow, u64 hoff, unsigned j0,
-                                                 unsigned jstep) {
-    for (unsigned j = j0; j < s; j += jstep) {
-        const int u = B.bt[base + j];
-        B.vunits[o + j] = u;
-        if (written) {
-            B.wunits[ow + j] = u;
-            if (B.whost) B.whost[ow + j] = hoff + (u64)j * B.unit_bytes;
+// Items (victims or loads) of the block-table update handled together: every
+// lane loads its entries of all of them before it stores any, so a group
+// costs one memory round trip per 64 of its logical units.
+constexpr unsigned kBtGroup = 4;
+
+// Release the units of a group of victims (block-table row base[g], s[g]
+// units, eviction-order offset o[g], written back w[g] at offset ow[g], host
+// copy at hoff[g]); lanes take logical units j: record each unit in eviction
+// order for the loads (and, for a victim that is written back, for the pack)
+// and clear its block-table entry.  (Occupancy bits: see bt_update_block.)
+__device__ __forceinline__ void bt_release_group(const BtArgs& B, const u64 (&base)[kBtGroup],
+                                                 const unsigned (&s)[kBtGroup],
+                                                 const u64 (&o)[kBtGroup],
+                                                 const bool (&w)[kBtGroup],
+                                                 const u64 (&ow)[kBtGroup],
+                                                 const u64 (&hoff)[kBtGroup], unsigned smax) {
+    for (unsigned j = lane_id(); j < smax; j += 64) {
+        int u[kBtGroup];
+#pragma unroll
+        for (unsigned g = 0; g < kBtGroup; ++g) u[g] = j < s[g] ? B.bt[base[g] + j] : -1;
+#pragma unroll
+        for (unsigned g = 0; g < kBtGroup; ++g) {
+            if (j >= s[g]) continue;
+            B.vunits[o[g] + j] = u[g];
+            if (w[g]) {
+                B.wunits[ow[g] + j] = u[g];
+                if (B.whost) B.whost[ow[g] + j] = hoff[g] + (u64)j * B.unit_bytes;
+            }
+            B.bt[base[g] + j] = -1;
         }
-        B.bt[base + j] = -1;
-        if ((u64)(unsigned)u < B.capacity)
-            atomicAnd(&B.occ[(unsigned)u >> 5], ~(1u << ((unsigned)u & 31u)));
     }
 }
 
-// Hand one load its units j0, j0 + jstep, ... < s (row at `base`, load-order
-// offset o): the pre-step free units first, then the victims' units in
-// eviction order (nF = free units used).
-__device__ __forceinline__ void bt_assign_units(const BtArgs& B, u64 base, unsigned s, u64 o,
-                                                u64 hoff, u64 nF, unsigned j0, unsigned jstep) {
-    for (unsigned j = j0; j < s; j += jstep) {
-        const u64 q = o + j;
-        const int u = q < nF ? B.free_old[q] : B.vunits[q - nF];
-        B.bt[base + j] = u;
-        B.lunits[q] = u;
-        if (B.lhost) B.lhost[q] = hoff + (u64)j * B.unit_bytes;
-        if ((u64)(unsigned)u < B.capacity)
-            atomicOr(&B.occ[(unsigned)u >> 5], 1u << ((unsigned)u & 31u));
+// Hand a group of loads their units (row base[g], s[g] units, load-order
+// offset o[g], host copy at hoff[g]): the pre-step free units first, then the
+// victims' units in eviction order (nF = free units used).
+__device__ __forceinline__ void bt_assign_group(const BtArgs& B, const u64 (&base)[kBtGroup],
+                                                const unsigned (&s)[kBtGroup],
+                                                const u64 (&o)[kBtGroup],
+                                                const u64 (&hoff)[kBtGroup], u64 nF,
+                                                unsigned smax) {
+    for (unsigned j = lane_id(); j < smax; j += 64) {
+        int u[kBtGroup];
+#pragma unroll
+        for (unsigned g = 0; g < kBtGroup; ++g) {
+            const u64 q = o[g] + j;
+            u[g] = j >= s[g] ? -1 : q < nF ? B.free_old[q] : B.vunits[q - nF];
+        }
+#pragma unroll
+        for (unsigned g = 0; g < kBtGroup; ++g) {
+            if (j >= s[g]) continue;
+            const u64 q = o[g] + j;
+            B.bt[base[g] + j] = u[g];
+            B.lunits[q] = u[g];
+            if (B.lhost) B.lhost[q] = hoff[g] + (u64)j * B.unit_bytes;
+        }
     }
 }
 
@@ -659,10 +681,16 @@ __device__ __forceinline__ u64 lane_bcast(u64 x, unsigned k) {
 
 // The block-table update inside one workgroup.  Wave w takes victims (then
 // loads) w, w + nw, ...; lane k of a batch loads the k-th of them first, so
-// the item-level loads of up to 64 items are in flight at once and each item
-// then costs one dependent load (its row or its units).
+// the item-level loads of up to 64 items are in flight at once; the wave then
+// takes the batch's items kBtGroup at a time, lanes over their units.
+// Occupancy: the plan core already marked the pre-step free units the loads
+// take; the released units that no load takes, released positions
+// [units_in - nF, units_out), are freed here.  (Clearing every released unit's
+// bit and setting every loaded unit's bit had cost about 0.4 ms at 50,000
+// agents: consecutive units share a 32-bit word, so a wave's atomics
+// serialized on two or three addresses.)
 __device__ __forceinline__ void bt_update_block(const BtArgs& B, unsigned n_v, unsigned n_l,
-                                                u64 nF) {
+                                                u64 nF, u64 units_in, u64 units_out) {
     const unsigned wid = threadIdx.x >> 6, nw = blockDim.x >> 6, lane = lane_id();
     for (unsigned i0 = wid; i0 < n_v; i0 += 64 * nw) {
         const unsigned ik = i0 + lane * nw;
@@ -678,12 +706,31 @@ __device__ __forceinline__ void bt_update_block(const BtArgs& B, unsigned n_v, u
             if (B.whost) hoff = B.host_off[v];
         }
         const unsigned rounds = min(64u, (n_v - i0 + nw - 1) / nw);
-        for (unsigned k = 0; k < rounds; ++k)
-            bt_release_units(B, lane_bcast(base, k), lane_bcast(s, k), lane_bcast(o, k),
-                             lane_bcast(w, k) != 0, lane_bcast(ow, k), lane_bcast(hoff, k),
-                             lane, 64u);
+        for (unsigned k0 = 0; k0 < rounds; k0 += kBtGroup) {
+            u64 gb[kBtGroup], go[kBtGroup], gow[kBtGroup], gh[kBtGroup];
+            unsigned gs[kBtGroup], smax = 0;
+            bool gw[kBtGroup];
+#pragma unroll
+            for (unsigned g = 0; g < kBtGroup; ++g) {
+                const bool in = k0 + g < rounds;
+                const unsigned k = in ? k0 + g : k0;       // a lane of the batch either way
+                gb[g] = lane_bcast(base, k);
+                gs[g] = in ? lane_bcast(s, k) : 0u;
+                go[g] = lane_bcast(o, k);
+                gw[g] = lane_bcast(w, k) != 0;
+                gow[g] = lane_bcast(ow, k);
+                gh[g] = lane_bcast(hoff, k);
+                smax = max(smax, gs[g]);
+            }
+            bt_release_group(B, gb, gs, go, gw, gow, gh, smax);
+        }
     }
     __syncthreads();                                 // the victims' units, before the loads take them
+    for (u64 q = (units_in > nF ? units_in - nF : 0) + threadIdx.x; q < units_out; q += blockDim.x) {
+        const int u = B.vunits[q];
+        if ((u64)(unsigned)u < B.capacity)
+            atomicAnd(&B.occ[(unsigned)u >> 5], ~(1u << ((unsigned)u & 31u)));
+    }
     for (unsigned i0 = wid; i0 < n_l; i0 += 64 * nw) {
         const unsigned ik = i0 + lane * nw;
         unsigned s = 0;
@@ -696,19 +743,31 @@ __device__ __forceinline__ void bt_update_block(const BtArgs& B, unsigned n_v, u
             if (B.lhost) hoff = B.host_off[a];
         }
         const unsigned rounds = min(64u, (n_l - i0 + nw - 1) / nw);
-        for (unsigned k = 0; k < rounds; ++k)
-            bt_assign_units(B, lane_bcast(base, k), lane_bcast(s, k), lane_bcast(o, k),
-                            lane_bcast(hoff, k), nF, lane, 64u);
+        for (unsigned k0 = 0; k0 < rounds; k0 += kBtGroup) {
+            u64 gb[kBtGroup], go[kBtGroup], gh[kBtGroup];
+            unsigned gs[kBtGroup], smax = 0;
+#pragma unroll
+            for (unsigned g = 0; g < kBtGroup; ++g) {
+                const bool in = k0 + g < rounds;
+                const unsigned k = in ? k0 + g : k0;
+                gb[g] = lane_bcast(base, k);
+                gs[g] = in ? lane_bcast(s, k) : 0u;
+                go[g] = lane_bcast(o, k);
+                gh[g] = lane_bcast(hoff, k);
+                smax = max(smax, gs[g]);
+            }
+            bt_assign_group(B, gb, gs, go, gh, nF, smax);
+        }
     }
 }
 
-// The fused plan core's tail, compiled apart (not inlined) so that its
+// The plan core's tail, compiled apart (not inlined) so that its
 // registers do not weigh on the core's own allocation; its arguments come from
 // the pool's device copy, not from the kernel's.
 __device__ __attribute__((noinline)) void bt_tail(const BtArgs* Bp, unsigned n_v, unsigned n_l,
-                                                  u64 nF) {
+                                                  u64 nF, u64 units_in, u64 units_out) {
     const BtArgs B = *Bp;
-    bt_update_block(B, n_v, n_l, nF);
+    bt_update_block(B, n_v, n_l, nF, units_in, units_out);
 }
 
 __device__ __forceinline__ void publish_plan(const PlanArgs& A) {
@@ -999,7 +1058,11 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     }
 
     stamp(6);
-    // pre-step free units in ascending order, as many as the loads can use
+    // pre-step free units in ascending order, as many as the loads can use;
+    // they all go to this step's loads, so the thread that owns their
+    // occupancy word marks them in use there (plain stores: one owner per
+    // word).  The block-table update then only frees the released units that
+    // no load takes.
     const u64 n_free_used = units_in < free_before ? units_in : free_before;
     if (n_free_used > 0) {
         const unsigned W = A.occ_words;
@@ -1011,12 +1074,15 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         u64 tot;
         u64 pos = block_excl_scan(cnt, S, &tot);
         for (unsigned w = w0; w < w1 && pos < n_free_used; ++w) {
-            unsigned bits = ~A.occ[w];
+            const unsigned word = A.occ[w];
+            unsigned bits = ~word, used = 0;
             while (bits && pos < n_free_used) {
                 const unsigned b = __ffs(bits) - 1;
                 bits &= bits - 1;
+                used |= 1u << b;
                 A.free_old[pos++] = (int)(w * 32u + b);
             }
+            if (used) A.occ[w] = word | used;
         }
     }
 
@@ -1045,7 +1111,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     // multi-workgroup plan kernel cost the host about 0.1 ms per call).  Every
     // list it reads was written above by this workgroup; the barrier inside
     // publish_plan ordered those writes before these reads.
-    bt_tail(A.bt, n_v, n_l, n_free_used);
+    bt_tail(A.bt, n_v, n_l, n_free_used, units_in, units_out);
 }
 
 __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
