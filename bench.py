@@ -227,8 +227,8 @@ def summarize_copies(copy_csv, steps_jsonl, bench_json, out_md, title, command):
              "plan-latency steps) written by `python bench.py --summarize-copies`.  Bytes are "
              "the steps' staged write-back and load bytes; the probes' copies run on streams "
              "of their own and are left out.", "",
-             "| Direction | Copies | Mean us | Busy ms | GB | GB/s while busy | One-way probe GB/s | "
-             "Of probe |", "|---|---|---|---|---|---|---|---|"]
+             "| Direction | Copies | Mean us | Median gap us | Busy ms | GB | GB/s while busy | "
+             "One-way probe GB/s | Of probe |", "|---|---|---|---|---|---|---|---|---|"]
     all_iv = []
     out = {}
     for d in ("DEVICE_TO_HOST", "HOST_TO_DEVICE"):
@@ -240,15 +240,20 @@ def summarize_copies(copy_csv, steps_jsonl, bench_json, out_md, title, command):
         all_iv += iv
         busy = union(iv) / 1e9
         mean_us = np.mean([b - a for a, b in iv]) / 1e3
+        sv = sorted(iv)
+        # idle time between successive copies of the stream, within a step
+        gaps = [sv[i][0] - sv[i - 1][1] for i in range(1, len(sv))
+                if 0 <= sv[i][0] - sv[i - 1][1] < 1_000_000]
+        gap_us = float(np.median(gaps)) / 1e3 if gaps else float("nan")
         gb = step_bytes[d] / 1e9
         rate = gb / busy if busy else 0.0
         pw = one_way[d]
         out[d] = rate
-        lines.append(f"| {d.replace('_', ' ').lower()} | {len(iv):,} | {mean_us:.1f} | "
+        lines.append(f"| {d.replace('_', ' ').lower()} | {len(iv):,} | {mean_us:.1f} | {gap_us:.1f} | "
                      f"{1e3 * busy:,.1f} | {gb:.2f} | {rate:.1f} | "
                      f"{pw:.1f} | {rate / pw:.3f} |" if pw else
-                     f"| {d} | {len(iv):,} | {mean_us:.1f} | {1e3 * busy:,.1f} | {gb:.2f} | "
-                     f"{rate:.1f} | - | - |")
+                     f"| {d} | {len(iv):,} | {mean_us:.1f} | {gap_us:.1f} | {1e3 * busy:,.1f} | "
+                     f"{gb:.2f} | {rate:.1f} | - | - |")
     busy_all = union(all_iv) / 1e9
     tot = sum(step_bytes.values()) / 1e9
     dup = probe.get("duplex_GBps")

@@ -155,7 +155,7 @@ def test_summarize_copies(tmp_path):
     rows = [("MEMORY_COPY", D, 9, "a", "b", 1, 0, 50_000_000),                 # probe
             ("MEMORY_COPY", D, 3, "a", "b", 2, 100_000_000, 110_000_000),
             ("MEMORY_COPY", D, 3, "a", "b", 3, 105_000_000, 120_000_000),     # overlaps
-            ("MEMORY_COPY", D, 3, "a", "b", 4, 130_000_000, 140_000_000),
+            ("MEMORY_COPY", D, 3, "a", "b", 4, 120_500_000, 130_500_000),
             ("MEMORY_COPY", H, 4, "a", "b", 5, 100_000_000, 125_000_000)]
     _write_csv(tmp_path / "mc.csv", hdr, rows)
     with open(tmp_path / "steps.jsonl", "w") as f:
@@ -169,7 +169,10 @@ def test_summarize_copies(tmp_path):
     md = bench.summarize_copies(str(tmp_path / "mc.csv"), str(tmp_path / "steps.jsonl"),
                                 str(tmp_path / "bench.json"), str(tmp_path / "o.md"), "T", "cmd")
     # D2H: 1.5 GB over 30 ms busy = 50 GB/s, 0.833 of 60; H2D: 2 GB over 25 ms = 80 GB/s
-    assert "| device to host | 3 | 11666.7 | 30.0 | 1.50 | 50.0 | 60.0 | 0.833 |" in md
-    assert "| host to device | 1 | 25000.0 | 25.0 | 2.00 | 80.0 | 100.0 | 0.800 |" in md
-    # both: 3.5 GB over the union [100, 125] + [130, 140] = 35 ms = 100 GB/s
-    assert "3.50 GB over 35.0 ms" in md and "= 100.0 GB/s" in md and "(0.833)" in md
+    # median idle gap between successive step copies: the second overlaps the
+    # first (skipped), the third starts 0.5 ms after the second ends; H2D has
+    # one copy (no gap)
+    assert "| device to host | 3 | 11666.7 | 500.0 | 30.0 | 1.50 | 50.0 | 60.0 | 0.833 |" in md
+    assert "| host to device | 1 | 25000.0 | nan | 25.0 | 2.00 | 80.0 | 100.0 | 0.800 |" in md
+    # both: 3.5 GB over the union [100, 130.5] = 30.5 ms = 114.8 GB/s
+    assert "3.50 GB over 30.5 ms" in md and "= 114.8 GB/s" in md and "(0.956)" in md
