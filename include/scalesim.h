@@ -149,7 +149,9 @@ typedef struct {                    /* cumulative since create or ss_reset_stats
     double   pack_ms, unpack_ms;           /* sum of per-launch event durations         */
     uint64_t d2h_bytes, h2d_bytes;
     double   d2h_ms, h2d_ms;               /* per step: first to last copy on its stream */
-    double   plan_gpu_ms;                  /* event time of the plan kernels             */
+    double   plan_gpu_ms;                  /* plan kernels, from the first workgroup's
+                                              entry to the end of the block-table update,
+                                              by the kernels' own wall-clock stamps       */
     double   plan_phase_us[7];             /* plan phases (classify, demand and evictable
                                               sorts, candidate select, candidate sort,
                                               acceptance, lists, free units); classify runs

@@ -859,6 +859,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
             if (!kFused) *A.cnt = PlanCounters{};
         }
         publish_plan(A);
+        stamp(8);
         return;
     }
     const u64 free_before = A.capacity - c.sum_resident;
@@ -1112,6 +1113,10 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     // list it reads was written above by this workgroup; the barrier inside
     // publish_plan ordered those writes before these reads.
     bt_tail(A.bt, n_v, n_l, n_free_used, units_in, units_out);
+    if (A.phase) {                                   // kernel-uniform
+        __syncthreads();
+        stamp(8);                                    // the whole plan kernel, tail included
+    }
 }
 
 __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {

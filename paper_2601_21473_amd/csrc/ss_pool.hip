@@ -187,7 +187,6 @@ struct ss_pool {
     // timing (SS_FLAG_TIMING): one pair per launch or per slot's copies
     std::vector<TimedPair> t_pack, t_unpack, t_d2h, t_h2d, t_dout, t_din;
     size_t n_t_pack = 0, n_t_unpack = 0, n_t_d2h = 0, n_t_h2d = 0, n_t_dout = 0, n_t_din = 0;
-    TimedPair t_plan[2];
     ss_stats stats{};
 
     // plan of the current step (host)
@@ -297,8 +296,7 @@ void free_pool(ss_pool* p) {
     for (void* h : hptrs)
         if (h) (void)hipHostFree(h);
     if (p->st_out) release_streams(p->device);
-    hipEvent_t evs[] = {p->ev_planned, p->ev_caller, p->ev_out_done, p->ev_in_done,
-                        p->t_plan[0].a, p->t_plan[0].b, p->t_plan[1].a, p->t_plan[1].b};
+    hipEvent_t evs[] = {p->ev_planned, p->ev_caller, p->ev_out_done, p->ev_in_done};
     for (hipEvent_t e : evs)
         if (e) (void)hipEventDestroy(e);
     for (hipEvent_t e : p->ev_packed)
@@ -354,15 +352,15 @@ void collect_timing(ss_pool* p) {
     p->n_t_pack = p->n_t_unpack = p->n_t_d2h = p->n_t_h2d = p->n_t_dout = p->n_t_din = 0;
 }
 
-// Fold plan slot k (its event time and phase stamps) into the stats; its
-// kernel must have completed.
+// Fold plan slot k (its phase stamps: the kernel's wall clock at its entry,
+// at each phase's end, and after its block-table tail) into the stats; its
+// kernel must have completed.  No event pair brackets the plan kernel, so a
+// timed plan call queues what an untimed one does.
 void fold_plan(ss_pool* p, int k) {
     if (!p->plan_pending[k]) return;
     p->plan_pending[k] = false;
-    float ms = 0.f;
-    if (hipEventElapsedTime(&ms, p->t_plan[k].a, p->t_plan[k].b) == hipSuccess)
-        p->stats.plan_gpu_ms += ms;
     const volatile u64* ph = p->h_phase + k * kPlanPhases;
+    if (ph[8] >= ph[0]) p->stats.plan_gpu_ms += (double)(ph[8] - ph[0]) * p->us_per_tick * 1e-3;
     for (int i = 1; i < 8; ++i)
         if (ph[i] >= ph[i - 1])
             p->stats.plan_phase_us[i - 1] += (double)(ph[i] - ph[i - 1]) * p->us_per_tick;
@@ -729,12 +727,6 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     CREATE_TRY(acquire_streams(p->device, &p->st_out, &p->st_in));
     for (hipEvent_t* ev : {&p->ev_planned, &p->ev_caller, &p->ev_out_done, &p->ev_in_done})
         CREATE_TRY(make_event(ev, false));
-    if (p->flags & SS_FLAG_TIMING) {
-        for (TimedPair& tp : p->t_plan) {
-            CREATE_TRY(make_event(&tp.a, true));
-            CREATE_TRY(make_event(&tp.b, true));
-        }
-    }
     {
         // every pointer the block-table update uses is fixed from here on
         const BtArgs B = bt_args(p);
@@ -857,12 +849,8 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
     A.phase = (p->flags & SS_FLAG_TIMING) ? p->h_phase_dev + tslot * kPlanPhases : nullptr;
 
     const bool timing = p->flags & SS_FLAG_TIMING;
-    if (timing) {
-        fold_plan(p, tslot);             // a plan two steps back that was never folded
-        TRY_HIP(p, hipEventRecord(p->t_plan[tslot].a, caller), true);
-    }
+    if (timing) fold_plan(p, tslot);     // a plan two steps back that was never folded
     TRY_HIP(p, launch_plan(A, caller), true);
-    if (timing) TRY_HIP(p, hipEventRecord(p->t_plan[tslot].b, caller), true);
     TRY_HIP(p, hipEventRecord(p->ev_planned, caller), true);
     const auto e2 = std::chrono::steady_clock::now();     // plan kernel and its events queued
     // The block-table update runs in the plan kernel's own tail, after the
