@@ -4,8 +4,9 @@
 //   classification  one pass over the agents: distance of active agents
 //                forced to 0, 64-bit priority keys (d, id), classification
 //                into evictable residents / demand loads / prefetch
-//                candidates, wave64 ballot + mbcnt stream compaction of each
-//                class, and the unit sums the plan needs;
+//                candidates, stream compaction of each class (wave64 ballot
+//                + mbcnt ranks, one DPP scan per list over the waves' counts),
+//                and the unit sums the plan needs;
 //   plan core    one workgroup of 1024 threads: register/LDS merge sorts,
 //                the distance-histogram cut (weighted radix select as the
 //                fallback) of the candidate prefix that can possibly fit,
@@ -114,7 +115,7 @@ __device__ __forceinline__ u64 wave_incl_scan(u64 v) {
 // before any is used, so each thread has that many agents' reads in flight.
 constexpr unsigned kClassBatch = 4;
 
-// The inputs of agents first + u * blockDim.x (u < kClassBatch) below end.
+// The inputs of agents first + u * kCoreThreads (u < kClassBatch) below end.
 struct AgentBatch {
     unsigned D[kClassBatch], s[kClassBatch];
     unsigned char act[kClassBatch], res[kClassBatch];
@@ -124,7 +125,7 @@ __device__ __forceinline__ void load_agents(const PlanArgs& A, unsigned first, u
                                             AgentBatch& b) {
 #pragma unroll
     for (unsigned u = 0; u < kClassBatch; ++u) {
-        const unsigned a = first + u * blockDim.x;
+        const unsigned a = first + u * kCoreThreads;
         const bool v = a < end;
         b.D[u] = v ? A.dist[a] : 0u;
         b.act[u] = v ? A.active[a] : (unsigned char)0;
@@ -177,33 +178,88 @@ __device__ __forceinline__ unsigned wave_reserve(bool pred, unsigned* counter) {
     return lane0(base) + mbcnt(mask);
 }
 
-// Block-local slots of this lane in the E and L lists and in its candidate
-// sub-list: one ballot per list, then lane 0 issues the LDS atomics of every
-// non-empty list back to back and the wave waits once.
-__device__ __forceinline__ void wave_reserve_lists(const AgentClass& c, PlanCounters* cnt,
-                                                   unsigned& oE, unsigned& oL, unsigned& oC) {
-    const u64 mE = __ballot(c.isE), mL = __ballot(c.isL);
-    u64 mC[kCandLists];
+// List ids of the classification: the candidate sub-lists 0 .. kCandLists-1,
+// then the evictable residents E and the demand loads L (an agent is in at
+// most one of them).
+constexpr unsigned kListE = kCandLists, kListL = kCandLists + 1, kLists = kCandLists + 2;
+constexpr unsigned kNoList = 0xFFu;
+// Counts of one pass (kClassBatch agents per thread): one per wave, agent
+// slot and list; a list's counts fill one wave, which scans them.
+constexpr unsigned kPassSlots = (kCoreThreads / 64) * kClassBatch;
+static_assert(kPassSlots == 64, "one wave scans a list's counts");
+constexpr unsigned kPassTab = kLists * kPassSlots;     // u32 entries per pass table
+
+__device__ __forceinline__ unsigned list_of(const AgentClass& c) {
+    return c.isC ? c.kl : c.isE ? kListE : c.isL ? kListL : kNoList;
+}
+
+__device__ __forceinline__ unsigned* list_counter(PlanCounters* c, unsigned k) {
+    return k < kCandLists ? &c->n_C[k] : k == kListE ? &c->n_E : &c->n_L;
+}
+
+__device__ __forceinline__ u64* list_ptr(const PlanArgs& A, unsigned k) {
+    return k < kCandLists ? A.listC + (u64)k * A.n : k == kListE ? A.listE : A.listL;
+}
+
+// Slots of one pass's agents in their lists (the whole workgroup, one agent
+// per thread and u).  No atomic sits in the waves' path: each wave ranks its
+// lanes within every list (ballot, mbcnt) and stores its per-list counts in
+// tab[list][wave, u]; after a barrier wave k scans list k's 64 counts (DPP)
+// and adds the list's base, which is this workgroup's running count of the
+// list (kGlobal false) or the range that one device-wide atomic reserves for
+// the workgroup's whole list (kGlobal true: one pass per workgroup); after a
+// second barrier every agent's slot is its table entry plus its rank.  Slots
+// follow (wave, u, lane) order within a pass.  Callers alternate between two
+// tables on consecutive passes, so a pass never overwrites a table that a
+// thread of the previous pass has still to read.
+template <bool kGlobal>
+__device__ __forceinline__ void reserve_pass(const unsigned (&lst)[kClassBatch],
+                                             unsigned (&slot)[kClassBatch], unsigned* tab,
+                                             PlanCounters* local, PlanCounters* global) {
+    const unsigned w = threadIdx.x >> 6, l = lane_id();
+    // this wave's column of the table: zero, then the count of every list
+    // present in the wave (in order behind the zeros: one wave's LDS accesses
+    // complete in order)
+    if (l < kLists * kClassBatch)
+        tab[(l / kClassBatch) * kPassSlots + w * kClassBatch + l % kClassBatch] = 0;
+    unsigned rank[kClassBatch];
 #pragma unroll
-    for (unsigned k = 0; k < kCandLists; ++k) mC[k] = __ballot(c.isC && c.kl == k);
-    unsigned bE = 0, bL = 0, bC[kCandLists];
-#pragma unroll
-    for (unsigned k = 0; k < kCandLists; ++k) bC[k] = 0;
-    if (lane_id() == 0) {
-        if (mE) bE = atomicAdd(&cnt->n_E, (unsigned)__popcll(mE));
-        if (mL) bL = atomicAdd(&cnt->n_L, (unsigned)__popcll(mL));
-#pragma unroll
-        for (unsigned k = 0; k < kCandLists; ++k)
-            if (mC[k]) bC[k] = atomicAdd(&cnt->n_C[k], (unsigned)__popcll(mC[k]));
+    for (unsigned u = 0; u < kClassBatch; ++u) {
+        // one round per distinct list among the wave's lanes (usually one to
+        // three), instead of one ballot per list: every instruction of this
+        // single-workgroup path is on the plan's critical path
+        u64 rest = __ballot(lst[u] != kNoList);
+        unsigned r = 0;
+        while (rest) {                               // wave-uniform
+            const unsigned k = (unsigned)__builtin_amdgcn_readlane((int)lst[u], (int)__builtin_ctzll(rest));
+            const u64 m = __ballot(lst[u] == k);
+            r = lst[u] == k ? mbcnt(m) : r;
+            if (l == 0) tab[k * kPassSlots + w * kClassBatch + u] = (unsigned)__popcll(m);
+            rest &= ~m;
+        }
+        rank[u] = r;
     }
-    oE = lane0(bE) + mbcnt(mE);
-    oL = lane0(bL) + mbcnt(mL);
-    oC = 0;
-#pragma unroll
-    for (unsigned k = 0; k < kCandLists; ++k) {
-        const unsigned b = lane0(bC[k]) + mbcnt(mC[k]);
-        if (c.isC && c.kl == k) oC = b;
+    __syncthreads();
+    if (w < kLists) {                                // wave-uniform
+        const unsigned v = tab[w * kPassSlots + l];
+        const unsigned incl = (unsigned)wave_incl_scan((u64)v);
+        const unsigned total = (unsigned)__builtin_amdgcn_readlane((int)incl, 63);
+        unsigned base;
+        if (kGlobal) {
+            unsigned b = 0;
+            if (l == 0 && total) b = atomicAdd(list_counter(global, w), total);
+            base = lane0(b);
+        } else {
+            unsigned* ctr = list_counter(local, w);
+            base = *ctr;                             // only this wave touches list w
+            if (l == 0) *ctr = base + total;
+        }
+        tab[w * kPassSlots + l] = base + incl - v;
     }
+    __syncthreads();
+#pragma unroll
+    for (unsigned u = 0; u < kClassBatch; ++u)
+        slot[u] = lst[u] == kNoList ? 0u : tab[lst[u] * kPassSlots + w * kClassBatch + u] + rank[u];
 }
 
 // Add every thread's sums to the block counters *cnt (LDS): one reduction per
@@ -233,7 +289,6 @@ struct CoreShared {
     u64 wsum[kCoreThreads / 64 + 1];
     u64 scal[8];
     unsigned uscal[8];
-    unsigned cbase[kCandLists];     // multi-workgroup classification: sub-list bases
 };
 
 // Exclusive block scan of one value per thread; returns the prefix and sets
@@ -580,31 +635,34 @@ __device__ void select_sort(const u64* src, unsigned n_src, u64 kstar, unsigned 
 
 // Classification of all agents by the plan core's workgroup: candidate units
 // into the LDS histogram S.histw, evictable residents' units into the LDS
-// histogram `he`, counts and sums into S.cnt, list entries at their final
-// slots (lane order inside a wave; the order between waves is arbitrary and
-// is removed by the sorts that follow).
-__device__ __forceinline__ void classify_fused(const PlanArgs& A, CoreShared& S, unsigned* he) {
+// histogram `he`, counts and sums into S.cnt, list entries at the slots
+// reserve_pass gives them (tab: two pass tables in LDS).
+__device__ __forceinline__ void classify_fused(const PlanArgs& A, CoreShared& S, unsigned* he,
+                                               unsigned* tab) {
     ClassSums t;
-    const unsigned step = kClassBatch * blockDim.x;
+    constexpr unsigned step = kClassBatch * kCoreThreads;
     AgentBatch b;
     load_agents(A, threadIdx.x, A.n, b);
-    for (unsigned base = 0; base < A.n; base += step) {
+    unsigned pass = 0;
+    for (unsigned base = 0; base < A.n; base += step, ++pass) {
         AgentBatch nb;                               // next pass's loads in flight
         load_agents(A, base + step + threadIdx.x, A.n, nb);
+        u64 key[kClassBatch];
+        unsigned lst[kClassBatch], slot[kClassBatch];
 #pragma unroll
         for (unsigned u = 0; u < kClassBatch; ++u) {
-            const unsigned a = base + u * blockDim.x + threadIdx.x;
-            if (a - lane_id() >= A.n) break;          // wave-uniform: no agent left in this wave
+            const unsigned a = base + u * kCoreThreads + threadIdx.x;
             const AgentClass c = classify(A, a, a < A.n, b.D[u], b.act[u] != 0, b.res[u] != 0);
             if (c.isC) atomicAdd(&S.histw[c.bucket], (u64)b.s[u]);
             if (c.isE) atomicAdd(&he[c.bucket], b.s[u]);
-            unsigned oE, oL, oC;
-            wave_reserve_lists(c, &S.cnt, oE, oL, oC);
-            if (c.isE) A.listE[oE] = c.key;
-            if (c.isL) A.listL[oL] = c.key;
-            if (c.isC) A.listC[(u64)c.kl * A.n + oC] = c.key;
+            key[u] = c.key;
+            lst[u] = list_of(c);
             t.add(c, b.act[u] != 0, b.res[u] != 0, b.s[u]);
         }
+        reserve_pass<false>(lst, slot, tab + (pass & 1) * kPassTab, &S.cnt, nullptr);
+#pragma unroll
+        for (unsigned u = 0; u < kClassBatch; ++u)
+            if (lst[u] != kNoList) list_ptr(A, lst[u])[slot[u]] = key[u];
         b = nb;
     }
     flush_sums(t, &S.cnt);
@@ -827,7 +885,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
             he_lds[b] = 0;
         }
         __syncthreads();
-        classify_fused(A, S, he_lds);
+        classify_fused(A, S, he_lds, he_lds + kDistBuckets);
         __syncthreads();
     }
     // the histograms and counters: this workgroup's LDS when it classified the
@@ -1130,7 +1188,7 @@ __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
 // kClassBatch * 1024 agents, gathers its counts and sums in LDS and reaches
 // the global counters with one atomic per counter; its list entries go to the
 // ranges those atomics reserve.  Every workgroup then publishes its writes
-// (agent-scope fence) and counts itself done; the one that counts last
+// (device-scope release) and counts itself done; the one that counts last
 // acquires them all and runs the plan core, so no workgroup ever waits for
 // another and the core starts without a second launch.  It resets the count
 // for the next step.  (Same-address atomics across workgroups serialize, so
@@ -1140,73 +1198,70 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
     __shared__ CoreShared S;
     const unsigned first = blockIdx.x * (kClassBatch * kCoreThreads) + threadIdx.x;
     if (A.phase && blockIdx.x == 0 && threadIdx.x == 0) A.phase[0] = wall_clock64();
+    AgentBatch b;
+    load_agents(A, first, A.n, b);                   // in flight while LDS is cleared
     unsigned* he = reinterpret_cast<unsigned*>(lds);  // evictable units per bucket (this workgroup)
+    unsigned* tab = he + kDistBuckets;                // reserve_pass's table
     if (threadIdx.x == 0) S.cnt = PlanCounters{};
-    for (unsigned b = threadIdx.x; b < kDistBuckets; b += kCoreThreads) {
-        S.histw[b] = 0;
-        he[b] = 0;
+    for (unsigned k = threadIdx.x; k < kDistBuckets; k += kCoreThreads) {
+        S.histw[k] = 0;
+        he[k] = 0;
     }
     __syncthreads();
-    AgentBatch b;
-    load_agents(A, first, A.n, b);
-    AgentClass c[kClassBatch];
-    unsigned oE[kClassBatch], oL[kClassBatch], oC[kClassBatch];
+    u64 key[kClassBatch];
+    unsigned lst[kClassBatch], slot[kClassBatch];
     ClassSums t;
 #pragma unroll
     for (unsigned u = 0; u < kClassBatch; ++u) {
         const unsigned a = first + u * kCoreThreads;
-        c[u] = classify(A, a, a < A.n, b.D[u], b.act[u] != 0, b.res[u] != 0);
+        const AgentClass c = classify(A, a, a < A.n, b.D[u], b.act[u] != 0, b.res[u] != 0);
         // candidate and evictable units per distance bucket: LDS first
         // (distances concentrate on few buckets, where global atomics would
         // serialize), one global atomic per non-empty bucket and workgroup
         // below
-        if (c[u].isC) atomicAdd(&S.histw[c[u].bucket], (u64)b.s[u]);
-        if (c[u].isE) atomicAdd(&he[c[u].bucket], b.s[u]);
-        wave_reserve_lists(c[u], &S.cnt, oE[u], oL[u], oC[u]);
-        t.add(c[u], b.act[u] != 0, b.res[u] != 0, b.s[u]);
+        if (c.isC) atomicAdd(&S.histw[c.bucket], (u64)b.s[u]);
+        if (c.isE) atomicAdd(&he[c.bucket], b.s[u]);
+        key[u] = c.key;
+        lst[u] = list_of(c);
+        t.add(c, b.act[u] != 0, b.res[u] != 0, b.s[u]);
     }
-    flush_sums(t, &S.cnt);
-    __syncthreads();
-    if (threadIdx.x < 64) {
-        // the workgroup's list ranges and sums: one lane per global counter, so
-        // each kind is one vector atomic and the wave waits for one round trip
-        PlanCounters* g = A.cnt;
+    flush_sums(t, &S.cnt);                           // complete at reserve_pass's first barrier
+    reserve_pass<true>(lst, slot, tab, &S.cnt, A.cnt);
+    if (threadIdx.x < 5) {                           // the workgroup's unit sums, one lane each
         const PlanCounters& lc = S.cnt;
+        PlanCounters* g = A.cnt;
         const unsigned l = threadIdx.x;
-        unsigned* ctr = l < kCandLists ? &g->n_C[l] : l == kCandLists ? &g->n_E : &g->n_L;
-        const unsigned val = l < kCandLists ? lc.n_C[l] : l == kCandLists ? lc.n_E : lc.n_L;
-        unsigned base = 0;
-        if (l < kCandLists + 2 && val) base = atomicAdd(ctr, val);
-        u64* sctr = &g->sum_active;
-        u64 sval = lc.sum_active;
-        if (l == 1) { sctr = &g->sum_resident; sval = lc.sum_resident; }
-        if (l == 2) { sctr = &g->sum_demand; sval = lc.sum_demand; }
-        if (l == 3) { sctr = &g->sum_evictable; sval = lc.sum_evictable; }
-        if (l == 4) { sctr = &g->sum_cand; sval = lc.sum_cand; }
-        if (l < 5 && sval) atomicAdd(sctr, sval);
-        if (l < kCandLists) S.cbase[l] = base;
-        if (l == kCandLists) S.uscal[0] = base;
-        if (l == kCandLists + 1) S.uscal[1] = base;
+        const u64 v = l == 0 ? lc.sum_active : l == 1 ? lc.sum_resident : l == 2 ? lc.sum_demand
+                    : l == 3 ? lc.sum_evictable : lc.sum_cand;
+        u64* dst = l == 0 ? &g->sum_active : l == 1 ? &g->sum_resident : l == 2 ? &g->sum_demand
+                 : l == 3 ? &g->sum_evictable : &g->sum_cand;
+        if (v) atomicAdd(dst, v);
     }
-    __syncthreads();
 #pragma unroll
-    for (unsigned u = 0; u < kClassBatch; ++u) {
-        if (c[u].isE) A.listE[S.uscal[0] + oE[u]] = c[u].key;
-        if (c[u].isL) A.listL[S.uscal[1] + oL[u]] = c[u].key;
-        if (c[u].isC) A.listC[(u64)c[u].kl * A.n + S.cbase[c[u].kl] + oC[u]] = c[u].key;
-    }
+    for (unsigned u = 0; u < kClassBatch; ++u)
+        if (lst[u] != kNoList) list_ptr(A, lst[u])[slot[u]] = key[u];
     for (unsigned k = threadIdx.x; k < kDistBuckets; k += kCoreThreads) {
         if (S.histw[k]) atomicAdd(&A.hist_w[k], S.histw[k]);
         if (he[k]) atomicAdd(&A.hist_e[k], he[k]);
     }
-    __threadfence();                                 // release this workgroup's writes
+    // Every wave has issued its list entries and atomics before the barrier;
+    // one thread's device-scope release then covers them (the L2 write-back
+    // it issues completes behind the requests the compute unit issued before
+    // it), and it counts the workgroup done.  The last workgroup's thread
+    // acquires every workgroup's writes the same way before the barrier that
+    // lets its workgroup read them.
     __syncthreads();
-    if (threadIdx.x == 0) S.uscal[3] = atomicAdd(A.done, 1u) == gridDim.x - 1;
+    if (threadIdx.x == 0) {
+        __threadfence();
+        const bool last = atomicAdd(A.done, 1u) == gridDim.x - 1;
+        if (last) {
+            __threadfence();
+            *A.done = 0;
+        }
+        S.uscal[3] = last;
+    }
     __syncthreads();
     if (!S.uscal[3]) return;                         // workgroup-uniform
-    __threadfence();                                 // acquire every workgroup's writes
-    if (threadIdx.x == 0) *A.done = 0;
-    __syncthreads();
     plan_core<false>(A, lds, S);
 }
 
