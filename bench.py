@@ -971,9 +971,9 @@ def main():
             "host_inputs": dict(lat_host, inputs="host memory (numpy arrays; the call copies "
                                 "them into pinned memory the plan kernel reads over the host "
                                 "link)"),
-            "core_phases_us": dict(zip(("classify", "demand_and_evictable_sorts",
-                                        "candidate_select", "candidate_sort", "acceptance",
-                                        "lists", "free_units"), phases)),
+            "core_phases_us": dict(zip(("classify", "cuts_and_sorts", "demand_victims",
+                                        "candidate_prefix", "acceptance", "lists",
+                                        "free_units"), phases)),
             "gpu_kernels_us": 1e3 * plan_gpu_ms / nps,
             "host_enqueue_us": host[0] / nps, "host_wait_us": host[1] / nps,
             "host_readback_us": host[2] / nps,

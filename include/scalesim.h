@@ -152,9 +152,11 @@ typedef struct {                    /* cumulative since create or ss_reset_stats
     double   plan_gpu_ms;                  /* plan kernels, from the first workgroup's
                                               entry to the end of the block-table update,
                                               by the kernels' own wall-clock stamps       */
-    double   plan_phase_us[7];             /* plan phases (classify, demand and evictable
-                                              sorts, candidate select, candidate sort,
-                                              acceptance, lists, free units); classify runs
+    double   plan_phase_us[7];             /* plan phases (classify; the histogram cuts
+                                              and the sorts of the evictable, demand and
+                                              candidate sets with their unit prefixes;
+                                              demand victims; candidate prefix;
+                                              acceptance; lists; free units); classify runs
                                               from the plan kernel's entry (its first
                                               workgroup when N > 12288)                     */
     double   plan_host_us[3];              /* ss_plan_step on the host: queueing the plan,

@@ -293,7 +293,7 @@ struct CoreShared {
 
 // Exclusive block scan of one value per thread; returns the prefix and sets
 // *total (same on every thread).
-__device__ u64 block_excl_scan(u64 v, CoreShared& S, u64* total) {
+__device__ __forceinline__ u64 block_excl_scan(u64 v, CoreShared& S, u64* total) {
     const unsigned w = threadIdx.x >> 6, l = lane_id();
     const unsigned nw = blockDim.x >> 6;
     const u64 inc = wave_incl_scan(v);
@@ -319,7 +319,7 @@ __device__ u64 block_excl_scan(u64 v, CoreShared& S, u64* total) {
 // element per thread: fewer instructions when most threads would idle).
 constexpr unsigned kPrefixRun = 4;
 template <class F>
-__device__ void block_prefix(unsigned n, F f, u64* out, CoreShared& S) {
+__device__ __forceinline__ void block_prefix(unsigned n, F f, u64* out, CoreShared& S) {
     u64 carry = 0;
     if (threadIdx.x == 0) out[0] = 0;
     if (n <= blockDim.x) {
@@ -352,20 +352,21 @@ __device__ void block_prefix(unsigned n, F f, u64* out, CoreShared& S) {
 }
 
 // Keys src[i] (i < n) with keep(key) appended to buf[*counter ...] (slots at
-// or beyond cap are counted but not written).  Each thread loads kGatherLoads
-// keys per round, and the next round's loads are issued before this round's
-// keys are placed; each wave reserves the slots of a whole round with one LDS
-// atomic.  The order of the appended keys is arbitrary.
+// or beyond cap are counted but not written), each stored or'ed with tag.
+// Each thread loads kGatherLoads keys per round, and the next round's loads
+// are issued before this round's keys are placed; each wave reserves the
+// slots of a whole round with one LDS atomic.  The order of the appended keys
+// is arbitrary.
 constexpr unsigned kGatherLoads = 8;
 template <class Keep>
 __device__ __forceinline__ void gather_keys(const u64* src, unsigned n, Keep keep, u64* buf,
-                                            unsigned cap, unsigned* counter) {
+                                            unsigned cap, unsigned* counter, u64 tag = 0) {
     if (n <= blockDim.x) {
         const unsigned i = threadIdx.x;
         const u64 k = i < n ? src[i] : ~0ull;
         const bool take = k != ~0ull && keep(k);
         const unsigned pos = wave_reserve(take, counter);
-        if (take && pos < cap) buf[pos] = k;
+        if (take && pos < cap) buf[pos] = k | tag;
         return;
     }
     const unsigned step = kGatherLoads * blockDim.x;
@@ -396,7 +397,7 @@ __device__ __forceinline__ void gather_keys(const u64* src, unsigned n, Keep kee
 #pragma unroll
             for (unsigned u = 0; u < kGatherLoads; ++u) {
                 const unsigned pos = off + mbcnt(mask[u]);
-                if (((mask[u] >> lane_id()) & 1) && pos < cap) buf[pos] = k[u];
+                if (((mask[u] >> lane_id()) & 1) && pos < cap) buf[pos] = k[u] | tag;
                 off += (unsigned)__popcll(mask[u]);
             }
         }
@@ -566,20 +567,24 @@ __device__ __forceinline__ void merge_sort_lds_e(u64* lds, unsigned npad) {
 
 // Keys per lane by list size (measured on one 1024-thread workgroup: longer
 // register runs save merge rounds until the register stage's exchanges cost
-// more than the rounds they save).
-__device__ void merge_sort_lds(u64* lds, unsigned npad) {
+// more than the rounds they save).  Inlined where the plan's sorts run (its
+// LDS accesses then stay LDS instructions); the rare separate sorts share one
+// out-of-line copy (merge_sort_lds), whose accesses are flat.
+__device__ __forceinline__ void merge_sort_lds_inl(u64* lds, unsigned npad) {
     if (npad <= 512) merge_sort_lds_e<1>(lds, npad);
     else if (npad <= 2048) merge_sort_lds_e<2>(lds, npad);
     else if (npad == 4096) merge_sort_lds_e<4>(lds, npad);
     else merge_sort_lds_e<8>(lds, npad);
 }
 
+__device__ __noinline__ void merge_sort_lds(u64* lds, unsigned npad) { merge_sort_lds_inl(lds, npad); }
+
 // The keys that gather(buf, cap, counter) appends (its calls of gather_keys
 // with one LDS counter), sorted ascending into dst[0..m); returns m.  They are
 // gathered into LDS and sorted there when they fit; otherwise they are
 // gathered again, into dst (room for pow2ceil(N) keys), and sorted there.
 template <class Gather>
-__device__ unsigned gather_sorted(Gather gather, u64* dst, u64* lds, CoreShared& S) {
+__device__ __forceinline__ unsigned gather_sorted(Gather gather, u64* dst, u64* lds, CoreShared& S) {
     if (threadIdx.x == 0) S.uscal[7] = 0;
     __syncthreads();
     gather(lds, (unsigned)kLdsKeys, &S.uscal[7]);
@@ -610,8 +615,8 @@ __device__ unsigned gather_sorted(Gather gather, u64* dst, u64* lds, CoreShared&
 // Sort the keys src[i] < kstar (there are exactly m of them) ascending into
 // dst[0..m).  dst has room for pow2ceil(N) keys and doubles as the sort buffer
 // when m exceeds the LDS budget.
-__device__ void select_sort(const u64* src, unsigned n_src, u64 kstar, unsigned m,
-                            u64* dst, u64* lds, CoreShared& S) {
+__device__ __forceinline__ void select_sort(const u64* src, unsigned n_src, u64 kstar, unsigned m,
+                                            u64* dst, u64* lds, CoreShared& S) {
     if (m == 0) return;
     const unsigned npad = pow2ceil(m);
     u64* buf = (npad <= (unsigned)kLdsKeys) ? lds : dst;
@@ -627,6 +632,35 @@ __device__ void select_sort(const u64* src, unsigned n_src, u64 kstar, unsigned 
         for (unsigned i = threadIdx.x; i < m; i += blockDim.x) dst[i] = lds[i];
         __syncthreads();
     }
+}
+
+// The three key sets a plan sorts (evictable residents T, demand loads L,
+// candidates C) as one array: a tag above the key bits makes T sort first,
+// then L, then C, so one merge sort replaces three (each sort's rounds are
+// barrier- and latency-bound on one workgroup, so three small sorts cost
+// about three times one sort of their union).  Keys are below
+// 2^(32 + idbits), so the tags fit when idbits <= kTagShift - 32.
+constexpr unsigned kTagShift = 62;
+constexpr u64 kTagL = 1ull << kTagShift, kTagC = 2ull << kTagShift;
+constexpr u64 kKeyBits = kTagL - 1;
+constexpr unsigned kJointKeys = 1024 * kRegKeys;   // largest joint sort (LDS: twice this)
+static_assert(2 * kJointKeys <= (unsigned)kLdsKeys, "joint sort and its merge scratch fit");
+
+// Sorts lds[0..n) (tagged keys) and writes each set, untagged and ascending,
+// to its array: sortE[0..nT), sortL[0..nL), sortC[0..n - nT - nL).
+__device__ __forceinline__ void joint_sort_out(u64* lds, unsigned n, unsigned nT, unsigned nL,
+                                               u64* sortE, u64* sortL, u64* sortC) {
+    if (n == 0) return;
+    const unsigned npad = pow2ceil(n);
+    for (unsigned i = n + threadIdx.x; i < npad; i += kCoreThreads) lds[i] = ~0ull;
+    __syncthreads();
+    merge_sort_lds_inl(lds, npad);
+    for (unsigned i = threadIdx.x; i < n; i += kCoreThreads) {
+        const u64 k = lds[i] & kKeyBits;
+        u64* dst = i < nT ? sortE + i : i < nT + nL ? sortL + (i - nT) : sortC + (i - nT - nL);
+        *dst = k;
+    }
+    __syncthreads();
 }
 
 // ---------------------------------------------------------------------------
@@ -952,15 +986,49 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         b_E = reach ? (unsigned)reach - 1 : 0;       // none reaches R: every evictable resident
     }
 
-    // demand loads by id (their distance is 0, so key order is id order)
-    select_sort(A.listL, nL, ~0ull, nL, A.sortL, lds, S);
-    // the evictable residents of buckets >= b_E, ascending; eviction order is
-    // descending key = the reversed array
-    const unsigned nT = b_E >= kDistBuckets ? 0u : gather_sorted(
-        [&](u64* buf, unsigned cap, unsigned* counter) {
-            gather_keys(A.listE, nE, [&](u64 k) { return dist_bucket((unsigned)(k >> idb)) >= b_E; },
-                        buf, cap, counter);
-        }, A.sortE, lds, S);
+    // The sorted sets: the evictable residents of buckets >= b_E (ascending;
+    // eviction order is descending key = the reversed array), the demand loads
+    // by id (their distance is 0, so key order is id order) and the candidates
+    // of buckets < b_cut, from the sub-lists whose distance range starts below
+    // b_cut.  Jointly in LDS when they fit (their counts are known once they
+    // are gathered), else one by one with the global-memory fallbacks.
+    auto keepT = [&](u64 k) { return dist_bucket((unsigned)(k >> idb)) >= b_E; };
+    auto keepC = [&](u64 k) { return dist_bucket((unsigned)(k >> idb)) < b_cut; };
+    auto gatherC = [&](u64* buf, unsigned cap, unsigned* counter, u64 tag) {
+        for (unsigned k = 0; k < kCandLists; ++k)
+            if (cand_list_start(k) < b_cut && c.n_C[k])
+                gather_keys(A.listC + (u64)k * A.n, c.n_C[k], keepC, buf, cap, counter, tag);
+    };
+    unsigned nT = 0, m = 0;
+    bool joint = idb + 32 <= kTagShift;              // kernel-uniform
+    if (joint) {
+        if (tid == 0) {
+            S.uscal[6] = 0;
+            S.uscal[7] = 0;
+        }
+        __syncthreads();
+        if (b_E < kDistBuckets) gather_keys(A.listE, nE, keepT, lds, kJointKeys, &S.uscal[7]);
+        __syncthreads();
+        nT = S.uscal[7];
+        if (nT + nL <= kJointKeys) {                 // block-uniform
+            for (unsigned i = tid; i < nL; i += kCoreThreads) lds[nT + i] = A.listL[i] | kTagL;
+            gatherC(lds + nT + nL, kJointKeys - nT - nL, &S.uscal[6], kTagC);
+        }
+        __syncthreads();
+        m = S.uscal[6];
+        if (nT + nL + m <= kJointKeys) joint_sort_out(lds, nT + nL + m, nT, nL, A.sortE, A.sortL, A.sortC);
+        else joint = false;
+    }
+    if (!joint) {
+        select_sort(A.listL, nL, ~0ull, nL, A.sortL, lds, S);
+        nT = b_E >= kDistBuckets ? 0u : gather_sorted(
+            [&](u64* buf, unsigned cap, unsigned* counter) {
+                gather_keys(A.listE, nE, keepT, buf, cap, counter);
+            }, A.sortE, lds, S);
+        m = gather_sorted(
+            [&](u64* buf, unsigned cap, unsigned* counter) { gatherC(buf, cap, counter, 0); },
+            A.sortC, lds, S);
+    }
     const u64* sortE = A.sortE;
     block_prefix(nT, [&](unsigned i) { return (u64)units[sortE[nT - 1 - i] & idmask]; },
                  A.prefE, S);
@@ -984,16 +1052,6 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     const unsigned n_d = S.uscal[2];
     const u64 free1 = free_before + A.prefE[n_d] - c.sum_demand;
 
-    // the candidates of buckets < b_cut, from the sub-lists whose distance
-    // range starts below b_cut, sorted by key
-    const unsigned m = gather_sorted(
-        [&](u64* buf, unsigned cap, unsigned* counter) {
-            for (unsigned k = 0; k < kCandLists; ++k)
-                if (cand_list_start(k) < b_cut && c.n_C[k])
-                    gather_keys(A.listC + (u64)k * A.n, c.n_C[k],
-                                [&](u64 key) { return dist_bucket((unsigned)(key >> idb)) < b_cut; },
-                                buf, cap, counter);
-        }, A.sortC, lds, S);
     stamp(3);
     const u64* sortC = A.sortC;
     block_prefix(m, [&](unsigned i) { return (u64)units[sortC[i] & idmask]; }, A.prefC, S);

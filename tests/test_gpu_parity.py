@@ -376,6 +376,26 @@ def test_cut_sets_beyond_lds():
                label="cut sets beyond LDS")
 
 
+@pytest.mark.parametrize("n,cap", [(8000, 4000), (8292, 4100), (16000, 8000)])
+def test_joint_sort_sizes(n, cap):
+    # Step 0 fills the pool with agents that never run again; at step 1, 100
+    # other agents run (demand loads) and the rest (at most cap of them, so
+    # that step 2 fits) are one step away (candidates), so the plan sorts the
+    # whole pool (T = cap keys), the 100 demand loads and n - cap - 100
+    # candidates.  Their union takes the plan core's joint LDS sort up to 8,192
+    # keys (8,000: padded to 8,192) and the separate sorts beyond (8,192 + 100;
+    # 16,000).
+    active = np.zeros((4, n), np.uint8)
+    active[0, :cap] = 1
+    active[1, cap:cap + 100] = 1
+    active[2, cap + 100:] = 1
+    dist = W.exact_distances(active)
+    pool = W.PoolSpec("syn", cap, [16], np.ones(n, np.uint32))
+    tr = W.Trace(f"joint{n}", n, 4, [pool], active, dist, dist.copy(), {})
+    run_parity(tr, theta=S, slot_units=8192, ring_slots=2, sample_units=4000,
+               label=f"joint sort {n} agents")
+
+
 @pytest.mark.parametrize("n_agents", [40000, 50000])
 @pytest.mark.parametrize("theta,budget", [(S, None), (3, None), (S, 300)])
 def test_many_agents_variable_sizes(n_agents, theta, budget):
