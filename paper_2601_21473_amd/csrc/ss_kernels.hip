@@ -873,8 +873,9 @@ __device__ __forceinline__ void publish_plan(const PlanArgs& A) {
 
 // The plan core: one workgroup of kCoreThreads threads; `lds` holds kLdsKeys
 // keys.  Inlined into both kernels below so that its LDS accesses stay LDS
-// instructions.  kFused: the core classifies the agents itself (k_plan_core);
-// otherwise it runs in the last classifying workgroup of k_classify_core.
+// instructions.  kFused: its workgroup classified the agents (k_plan_core;
+// histograms and counters in LDS); otherwise it runs in the last classifying
+// workgroup of k_classify_core (histograms and counters in global memory).
 // After publishing the plan it updates the block table.
 //
 // Only the keys that can take part in the plan are sorted.  Write need for the
@@ -907,21 +908,10 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     auto stamp = [&](int k) {
         if (A.phase && tid == 0) A.phase[k] = wall_clock64();
     };
-    if (kFused) stamp(0);                           // else stamped at the classifying kernel's entry
     const u64 idmask = (1ull << A.idbits) - 1;
     const unsigned idb = A.idbits;
     const unsigned* units = A.units;
     unsigned* he_lds = reinterpret_cast<unsigned*>(lds);
-    if (kFused) {
-        if (tid == 0) S.cnt = PlanCounters{};
-        for (unsigned b = tid; b < kDistBuckets; b += blockDim.x) {
-            S.histw[b] = 0;
-            he_lds[b] = 0;
-        }
-        __syncthreads();
-        classify_fused(A, S, he_lds, he_lds + kDistBuckets);
-        __syncthreads();
-    }
     // the histograms and counters: this workgroup's LDS when it classified the
     // agents itself, else the global sums of all classifying workgroups (the
     // counters copied into LDS)
@@ -1235,10 +1225,36 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     }
 }
 
+typedef const __attribute__((address_space(4))) PlanArgs PlanArgsK;
+
+// The kernel's arguments read afresh from the kernel-argument segment,
+// through a pointer the compiler cannot trace back to earlier loads: the plan
+// core takes its arguments from it after the classification, otherwise the
+// compiler keeps the argument block that the classification's loads merged
+// live across the whole core, spilled to lanes of a vector register and
+// reloaded as a unit (thousands of v_readlane).
+__device__ __forceinline__ const PlanArgs& fresh_args() {
+    u64 bits = (u64)__builtin_amdgcn_kernarg_segment_ptr();
+    asm volatile("" : "+s"(bits));
+    bits = ((u64)(unsigned)__builtin_amdgcn_readfirstlane((int)(bits >> 32)) << 32) |
+           (unsigned)__builtin_amdgcn_readfirstlane((int)bits);
+    return *(const PlanArgs*)(PlanArgsK*)bits;      // constant segment: scalar loads
+}
+
 __global__ void __launch_bounds__(kCoreThreads) k_plan_core(PlanArgs A) {
     __shared__ u64 lds[kLdsKeys];
     __shared__ CoreShared S;
-    plan_core<true>(A, lds, S);
+    if (A.phase && threadIdx.x == 0) A.phase[0] = wall_clock64();
+    unsigned* he = reinterpret_cast<unsigned*>(lds);  // evictable units per bucket
+    if (threadIdx.x == 0) S.cnt = PlanCounters{};
+    for (unsigned b = threadIdx.x; b < kDistBuckets; b += kCoreThreads) {
+        S.histw[b] = 0;
+        he[b] = 0;
+    }
+    __syncthreads();
+    classify_fused(A, S, he, he + kDistBuckets);
+    __syncthreads();
+    plan_core<true>(fresh_args(), lds, S);
 }
 
 // Classification over many workgroups, then the plan core in the workgroup
@@ -1320,7 +1336,7 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
     }
     __syncthreads();
     if (!S.uscal[3]) return;                         // workgroup-uniform
-    plan_core<false>(A, lds, S);
+    plan_core<false>(fresh_args(), lds, S);
 }
 
 // ---------------------------------------------------------------------------
