@@ -479,13 +479,17 @@ constexpr unsigned kRegKeys = 8;
 // run pair finds how many of the outputs before it come from the left run,
 // then it merges its kE outputs sequentially with the two run heads in
 // registers.  Ties take the left run first, so the padding keys (all equal)
-// keep a consistent order.
+// keep a consistent order.  Only the first n keys are real (n <= npad): when
+// lds[n..npad) and lds[npad + n..2 npad) hold padding, every round's outputs
+// from n on are padding too (the real keys of a pair of runs precede its
+// padding, and only the pair holding key n - 1 has both), so the waves and
+// threads whose keys or outputs all lie there do nothing.
 template <unsigned kE>
-__device__ __forceinline__ void merge_sort_lds_e(u64* lds, unsigned npad) {
+__device__ __forceinline__ void merge_sort_lds_e(u64* lds, unsigned npad, unsigned n) {
     constexpr unsigned W = 64 * kE;                  // keys per wave run
     const unsigned t = threadIdx.x, l = lane_id();
     const unsigned base = (t >> 6) * W;
-    if (base < npad) {                               // wave-uniform: the wave holds keys
+    if (base < n) {                                  // wave-uniform: the wave holds real keys
         u64 x[kE];
 #pragma unroll
         for (unsigned r = 0; r < kE; ++r) {
@@ -529,7 +533,7 @@ __device__ __forceinline__ void merge_sort_lds_e(u64* lds, unsigned npad) {
     u64* dst = lds + npad;
     for (unsigned L = W; L < npad; L <<= 1) {
         const unsigned o = t * kE;                   // first output of this thread
-        if (o < npad) {
+        if (o < n) {
             const unsigned b0 = o & ~(2 * L - 1);
             const unsigned d = o - b0;               // outputs of the pair before o
             const u64* A = src + b0;
@@ -560,7 +564,7 @@ __device__ __forceinline__ void merge_sort_lds_e(u64* lds, unsigned npad) {
         dst = tmp;
     }
     if (src != lds) {
-        for (unsigned i = t; i < npad; i += blockDim.x) lds[i] = src[i];
+        for (unsigned i = t; i < n; i += blockDim.x) lds[i] = src[i];
         __syncthreads();
     }
 }
@@ -570,14 +574,17 @@ __device__ __forceinline__ void merge_sort_lds_e(u64* lds, unsigned npad) {
 // more than the rounds they save).  Inlined where the plan's sorts run (its
 // LDS accesses then stay LDS instructions); the rare separate sorts share one
 // out-of-line copy (merge_sort_lds), whose accesses are flat.
-__device__ __forceinline__ void merge_sort_lds_inl(u64* lds, unsigned npad) {
-    if (npad <= 512) merge_sort_lds_e<1>(lds, npad);
-    else if (npad <= 2048) merge_sort_lds_e<2>(lds, npad);
-    else if (npad == 4096) merge_sort_lds_e<4>(lds, npad);
-    else merge_sort_lds_e<8>(lds, npad);
+__device__ __forceinline__ void merge_sort_lds_inl(u64* lds, unsigned npad, unsigned n) {
+    if (npad <= 512) merge_sort_lds_e<1>(lds, npad, n);
+    else if (npad <= 2048) merge_sort_lds_e<2>(lds, npad, n);
+    else if (npad == 4096) merge_sort_lds_e<4>(lds, npad, n);
+    else merge_sort_lds_e<8>(lds, npad, n);
 }
 
-__device__ __noinline__ void merge_sort_lds(u64* lds, unsigned npad) { merge_sort_lds_inl(lds, npad); }
+// (all npad keys treated as real: the callers pad only the first half)
+__device__ __noinline__ void merge_sort_lds(u64* lds, unsigned npad) {
+    merge_sort_lds_inl(lds, npad, npad);
+}
 
 // The keys that gather(buf, cap, counter) appends (its calls of gather_keys
 // with one LDS counter), sorted ascending into dst[0..m); returns m.  They are
@@ -634,6 +641,10 @@ __device__ __forceinline__ void select_sort(const u64* src, unsigned n_src, u64 
     }
 }
 
+// Occupancy words per thread that the free-unit scan holds in registers
+// (pools of up to 1024 * 16 * 32 = 524,288 units; larger pools loop).
+constexpr unsigned kOccRegs = 16;
+
 // The three key sets a plan sorts (evictable residents T, demand loads L,
 // candidates C) as one array: a tag above the key bits makes T sort first,
 // then L, then C, so one merge sort replaces three (each sort's rounds are
@@ -652,9 +663,12 @@ __device__ __forceinline__ void joint_sort_out(u64* lds, unsigned n, unsigned nT
                                                u64* sortE, u64* sortL, u64* sortC) {
     if (n == 0) return;
     const unsigned npad = pow2ceil(n);
-    for (unsigned i = n + threadIdx.x; i < npad; i += kCoreThreads) lds[i] = ~0ull;
+    for (unsigned i = n + threadIdx.x; i < npad; i += kCoreThreads) {
+        lds[i] = ~0ull;                              // padding, and the same range of
+        lds[npad + i] = ~0ull;                       // the merge rounds' second buffer
+    }
     __syncthreads();
-    merge_sort_lds_inl(lds, npad);
+    merge_sort_lds_inl(lds, npad, n);
     for (unsigned i = threadIdx.x; i < n; i += kCoreThreads) {
         const u64 k = lds[i] & kKeyBits;
         u64* dst = i < nT ? sortE + i : i < nT + nL ? sortL + (i - nT) : sortC + (i - nT - nL);
@@ -1050,19 +1064,20 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     // acceptance: S_i <= budget and S_i <= free1 + (units of the remaining
     // evictable residents with distance strictly larger than d_i)
     if (tid == 0) S.uscal[3] = m;
-    // the evictable keys, and their unit prefix when it fits too, in LDS for
-    // the searches below (the sort buffer is free)
-    const u64* keysE = sortE;
-    const u64* pref = A.prefE;
-    if (nT <= (unsigned)kLdsKeys) {
-        const bool both = 2 * nT + 1 <= (unsigned)kLdsKeys;
-        for (unsigned i = tid; i < nT; i += blockDim.x) lds[i] = sortE[i];
-        if (both) for (unsigned i = tid; i <= nT; i += blockDim.x) lds[nT + i] = A.prefE[i];
-        keysE = lds;
-        if (both) pref = lds + nT;
+    // the evictable keys and their unit prefix in LDS for the searches below
+    // when both fit (the joint sort left the keys there; the sort buffer is
+    // free otherwise)
+    const bool in_lds = 2 * nT + 1 <= (unsigned)kLdsKeys;   // block-uniform
+    if (in_lds) {
+        if (!joint) for (unsigned i = tid; i < nT; i += blockDim.x) lds[i] = sortE[i];
+        for (unsigned i = tid; i <= nT; i += blockDim.x) lds[nT + i] = A.prefE[i];
     }
+    const u64* keysE = in_lds ? lds : sortE;
+    const u64* pref = in_lds ? lds + nT : A.prefE;
     __syncthreads();
-    {
+    // (the search runs on LDS or on global memory; each instance sees which,
+    // so the LDS one uses LDS instructions)
+    auto accept = [&](const u64* keysE, const u64* pref) __attribute__((always_inline)) {
         // kAccept candidates per thread at once: their binary searches run in
         // lockstep (ceil(log2(nT + 1)) steps), so the loads of one overlap the
         // others'
@@ -1103,18 +1118,20 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
                     atomicMin(&S.uscal[3], i);
             }
         }
-    }
+    };
+    if (in_lds) accept(lds, lds + nT);
+    else accept(sortE, A.prefE);
     __syncthreads();
     stamp(5);
     const unsigned n_p = S.uscal[3];
     if (tid == 0) {
         unsigned n_v = n_d;
         if (n_p > 0 && A.prefC[n_p] > free1) {
-            const u64 target = A.prefE[n_d] + (A.prefC[n_p] - free1);
+            const u64 target = pref[n_d] + (A.prefC[n_p] - free1);
             unsigned lo = n_d + 1, hi = nT;
             while (lo < hi) {
                 const unsigned mid = (lo + hi) >> 1;
-                if (A.prefE[mid] >= target) hi = mid; else lo = mid + 1;
+                if (pref[mid] >= target) hi = mid; else lo = mid + 1;
             }
             n_v = lo < nT ? lo : nT;
         }
@@ -1123,7 +1140,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     __syncthreads();
     const unsigned n_v = S.uscal[4];
     const unsigned n_l = nL + n_p;
-    const u64 units_out = A.prefE[n_v];
+    const u64 units_out = pref[n_v];
     const u64 units_in = c.sum_demand + A.prefC[n_p];
 
     // plan lists, load offsets, residency (victims and loads are disjoint)
@@ -1138,7 +1155,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     // them without a mask): with at most one victim per thread, from the same
     // loads in one pass
     auto victim = [&](unsigned i, u64* wunits) {
-        const unsigned v = (unsigned)(sortE[nT - 1 - i] & idmask);
+        const unsigned v = (unsigned)(keysE[nT - 1 - i] & idmask);
         const unsigned char w = (!A.dirty || A.dirty[v]) ? 1 : 0;
         A.victims[i] = v;
         A.victims_host[i] = v;
@@ -1159,7 +1176,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         u64 wv;
         for (unsigned i = tid; i < n_v; i += blockDim.x) victim(i, &wv);
         block_prefix(n_v, [&](unsigned i) {
-            const unsigned v = (unsigned)(sortE[nT - 1 - i] & idmask);
+            const unsigned v = (unsigned)(keysE[nT - 1 - i] & idmask);
             return (!A.dirty || A.dirty[v]) ? (u64)units[v] : 0ull;
         }, A.woff, S);
     }
@@ -1171,9 +1188,33 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     // word).  The block-table update then only frees the released units that
     // no load takes.
     const u64 n_free_used = units_in < free_before ? units_in : free_before;
-    if (n_free_used > 0) {
+    const unsigned occ_per = (A.occ_words + blockDim.x - 1) / blockDim.x;
+    if (n_free_used > 0 && occ_per <= kOccRegs) {
+        // each thread's words in registers, all loads in flight at once
+        const unsigned w0 = tid * occ_per;
+        unsigned word[kOccRegs];
+#pragma unroll
+        for (unsigned k = 0; k < kOccRegs; ++k)
+            word[k] = k < occ_per && w0 + k < A.occ_words ? A.occ[w0 + k] : ~0u;
+        u64 cnt = 0;
+#pragma unroll
+        for (unsigned k = 0; k < kOccRegs; ++k) cnt += __popc(~word[k]);
+        u64 tot;
+        u64 pos = block_excl_scan(cnt, S, &tot);
+#pragma unroll
+        for (unsigned k = 0; k < kOccRegs; ++k) {
+            unsigned bits = ~word[k], used = 0;
+            while (bits && pos < n_free_used) {
+                const unsigned b = __ffs(bits) - 1;
+                bits &= bits - 1;
+                used |= 1u << b;
+                A.free_old[pos++] = (int)((w0 + k) * 32u + b);
+            }
+            if (used) A.occ[w0 + k] = word[k] | used;
+        }
+    } else if (n_free_used > 0) {
         const unsigned W = A.occ_words;
-        const unsigned per = (W + blockDim.x - 1) / blockDim.x;
+        const unsigned per = occ_per;
         const unsigned w0 = tid * per;
         const unsigned w1 = min(W, w0 + per);
         u64 cnt = 0;

@@ -427,6 +427,29 @@ InputKind input_kind(const void* ptr, u64 bytes, int device) {
     return device_range_ok(ptr, bytes, device) ? kInDevice : kInBad;
 }
 
+// The host's unit offsets of the current plan's lists (victims and loads in
+// unit order, the written-back victims' units, and per victim the last
+// written-back victim at or before it), for the copies of ss_evict_pack and
+// ss_prefetch_unpack.  Computed by ss_evict_pack rather than ss_plan_step, so
+// the plan call returns the plan without this bookkeeping.
+void host_offsets(ss_pool* p) {
+    const PlanResult& r = p->res;
+    p->voff.resize(r.n_victims + 1);
+    p->loff.resize(r.n_loads + 1);
+    p->voff[0] = 0;
+    for (unsigned i = 0; i < r.n_victims; ++i) p->voff[i + 1] = p->voff[i] + p->s[p->h_victims[i]];
+    p->loff[0] = 0;
+    for (unsigned i = 0; i < r.n_loads; ++i) p->loff[i + 1] = p->loff[i] + p->s[p->h_loads[i]];
+    p->woff.resize(r.n_victims + 1);
+    p->last_written.resize(r.n_victims);
+    p->woff[0] = 0;
+    for (unsigned i = 0; i < r.n_victims; ++i) {
+        const bool w = p->h_vwritten[i] != 0;
+        p->woff[i + 1] = p->woff[i] + (w ? p->s[p->h_victims[i]] : 0);
+        p->last_written[i] = w ? (long long)i : (i ? p->last_written[i - 1] : -1);
+    }
+}
+
 ss_status check_usable(ss_pool* p) {
     if (!p) return set_err(SS_ERR_ARG, "pool is NULL");
     if (p->poisoned) return set_err(SS_ERR_POISONED, "pool is poisoned by an earlier HIP failure");
@@ -892,20 +915,6 @@ ss_status ss_plan_step(ss_pool* p, const uint32_t* distances, const uint8_t* act
                        (unsigned long long)p->U);
     }
     p->res = r;
-    p->voff.resize(r.n_victims + 1);
-    p->loff.resize(r.n_loads + 1);
-    p->voff[0] = 0;
-    for (unsigned i = 0; i < r.n_victims; ++i) p->voff[i + 1] = p->voff[i] + p->s[p->h_victims[i]];
-    p->loff[0] = 0;
-    for (unsigned i = 0; i < r.n_loads; ++i) p->loff[i + 1] = p->loff[i] + p->s[p->h_loads[i]];
-    p->woff.resize(r.n_victims + 1);
-    p->last_written.resize(r.n_victims);
-    p->woff[0] = 0;
-    for (unsigned i = 0; i < r.n_victims; ++i) {
-        const bool w = p->h_vwritten[i] != 0;
-        p->woff[i + 1] = p->woff[i] + (w ? p->s[p->h_victims[i]] : 0);
-        p->last_written[i] = w ? (long long)i : (i ? p->last_written[i - 1] : -1);
-    }
 
     ss_plan& pl = p->plan;
     pl.n_victims = r.n_victims;
@@ -946,6 +955,7 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
     if (st) return st;
     if (p->state != kPlanned) return set_err(SS_ERR_ORDER, "ss_evict_pack must follow ss_plan_step");
     DeviceGuard g(p->device);
+    host_offsets(p);
     hipStream_t caller = static_cast<hipStream_t>(stream);
     const u64 total = p->res.units_written;
     const u64 ups = p->units_per_slot;
