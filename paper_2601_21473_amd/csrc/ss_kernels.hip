@@ -645,6 +645,34 @@ __device__ __forceinline__ void select_sort(const u64* src, unsigned n_src, u64 
 // (pools of up to 1024 * 16 * 32 = 524,288 units; larger pools loop).
 constexpr unsigned kOccRegs = 16;
 
+// The plan's first n_free_used free units in ascending order into free_old,
+// each marked in use in the occupancy bitmap (thread t owns words
+// [t * per, (t + 1) * per), per <= kR: all of them are loaded at once).
+template <unsigned kR>
+__device__ __forceinline__ void free_scan_regs(const PlanArgs& A, u64 n_free_used, unsigned per,
+                                               CoreShared& S) {
+    const unsigned w0 = threadIdx.x * per;
+    unsigned word[kR];
+#pragma unroll
+    for (unsigned k = 0; k < kR; ++k) word[k] = k < per && w0 + k < A.occ_words ? A.occ[w0 + k] : ~0u;
+    u64 cnt = 0;
+#pragma unroll
+    for (unsigned k = 0; k < kR; ++k) cnt += __popc(~word[k]);
+    u64 tot;
+    u64 pos = block_excl_scan(cnt, S, &tot);
+#pragma unroll
+    for (unsigned k = 0; k < kR; ++k) {
+        unsigned bits = ~word[k], used = 0;
+        while (bits && pos < n_free_used) {
+            const unsigned b = __ffs(bits) - 1;
+            bits &= bits - 1;
+            used |= 1u << b;
+            A.free_old[pos++] = (int)((w0 + k) * 32u + b);
+        }
+        if (used) A.occ[w0 + k] = word[k] | used;
+    }
+}
+
 // The three key sets a plan sorts (evictable residents T, demand loads L,
 // candidates C) as one array: a tag above the key bits makes T sort first,
 // then L, then C, so one merge sort replaces three (each sort's rounds are
@@ -962,10 +990,30 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     const long long need = (long long)c.sum_demand - (long long)free_before;
     const unsigned nE = c.n_E, nL = c.n_L;
 
-    // the cuts (see above), from one scan of each histogram
-    u64 tot_c, tot_e;
-    const u64 hcb = block_excl_scan(hc0 + hc1, S, &tot_c);     // HCbefore(b0)
-    const u64 heb = block_excl_scan(he0 + he1, S, &tot_e);     // HEbefore(b0)
+    // the cuts (see above): one scan of both histograms (packed into one word
+    // when their totals fit 32 bits), then the first bucket that fails and the
+    // first that does not reach R, each the minimum of a per-wave candidate
+    // (lanes hold ascending buckets) by one LDS atomic per wave
+    if (tid == 0) {
+        S.uscal[0] = kDistBuckets;
+        S.uscal[1] = kDistBuckets;
+    }
+    u64 hcb, heb, tot_c, tot_e;                      // HCbefore(b0), HEbefore(b0), totals
+    if (c.sum_cand < (1ull << 32) && c.sum_evictable < (1ull << 32)) {   // block-uniform
+        u64 tot;
+        const u64 x = block_excl_scan(((hc0 + hc1) << 32) | (he0 + he1), S, &tot);
+        hcb = x >> 32;
+        heb = x & 0xFFFFFFFFull;
+        tot_c = tot >> 32;
+        tot_e = tot & 0xFFFFFFFFull;
+    } else {
+        hcb = block_excl_scan(hc0 + hc1, S, &tot_c);
+        heb = block_excl_scan(he0 + he1, S, &tot_e);
+    }
+    auto wave_first = [&](unsigned b, unsigned* dst) {
+        const u64 m = __ballot(b < kDistBuckets);
+        if (m && lane_id() == (unsigned)__ffsll((long long)m) - 1) atomicMin(dst, b);
+    };
     const long long f1ub = need > 0 ? (long long)A.smax - 1 : -need;
     auto fails = [&](u64 hc_before, u64 he_before) {
         long long lim = (long long)(tot_e - he_before) - need;  // HEsuf(b) - need
@@ -973,21 +1021,25 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         const u64 cap = A.budget < (u64)lim ? A.budget : (u64)lim;
         return hc_before >= cap;                                // hc_before + 1 > cap
     };
-    // the buckets that do not fail form the prefix [0, b_cut): count them and
-    // sum their candidate units in one reduction (count in the low 12 bits)
-    const u64 keep0 = fails(hcb, heb) ? 0 : ((hc0 << 12) | 1);
-    const u64 keep1 = fails(hcb + hc0, heb + he0) ? 0 : ((hc1 << 12) | 1);
-    u64 kept;
-    (void)block_excl_scan(keep0 + keep1, S, &kept);
-    const unsigned b_cut = (unsigned)(kept & 4095u);
-    const u64 cmax = A.budget < (kept >> 12) ? A.budget : (kept >> 12);
+    // the buckets that do not fail form the prefix [0, b_cut)
+    wave_first(fails(hcb, heb) ? b0 : fails(hcb + hc0, heb + he0) ? b0 + 1 : kDistBuckets,
+               &S.uscal[0]);
+    __syncthreads();
+    const unsigned b_cut = S.uscal[0];
+    if (b_cut < kDistBuckets && tid == b_cut / 2) S.wsum[0] = (b_cut & 1) ? hcb + hc0 : hcb;
+    __syncthreads();
+    const u64 hc_cut = b_cut < kDistBuckets ? S.wsum[0] : tot_c;       // HCbefore(b_cut)
+    const u64 cmax = A.budget < hc_cut ? A.budget : hc_cut;
     const long long R = need + (long long)cmax;
     unsigned b_E = kDistBuckets;                     // R <= 0: no victims
     if (R > 0) {
+        // the buckets whose HEsuf reaches R form a prefix [0, b_E]
         const u64 r = (u64)R;
-        u64 reach;
-        (void)block_excl_scan((u64)(tot_e - heb >= r) + (u64)(tot_e - heb - he0 >= r), S, &reach);
-        b_E = reach ? (unsigned)reach - 1 : 0;       // none reaches R: every evictable resident
+        wave_first(tot_e - heb < r ? b0 : tot_e - heb - he0 < r ? b0 + 1 : kDistBuckets,
+                   &S.uscal[1]);
+        __syncthreads();
+        const unsigned fr = S.uscal[1];
+        b_E = fr ? fr - 1 : 0;                       // none reaches R: every evictable resident
     }
 
     // The sorted sets: the evictable residents of buckets >= b_E (ascending;
@@ -1189,29 +1241,10 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     // no load takes.
     const u64 n_free_used = units_in < free_before ? units_in : free_before;
     const unsigned occ_per = (A.occ_words + blockDim.x - 1) / blockDim.x;
-    if (n_free_used > 0 && occ_per <= kOccRegs) {
-        // each thread's words in registers, all loads in flight at once
-        const unsigned w0 = tid * occ_per;
-        unsigned word[kOccRegs];
-#pragma unroll
-        for (unsigned k = 0; k < kOccRegs; ++k)
-            word[k] = k < occ_per && w0 + k < A.occ_words ? A.occ[w0 + k] : ~0u;
-        u64 cnt = 0;
-#pragma unroll
-        for (unsigned k = 0; k < kOccRegs; ++k) cnt += __popc(~word[k]);
-        u64 tot;
-        u64 pos = block_excl_scan(cnt, S, &tot);
-#pragma unroll
-        for (unsigned k = 0; k < kOccRegs; ++k) {
-            unsigned bits = ~word[k], used = 0;
-            while (bits && pos < n_free_used) {
-                const unsigned b = __ffs(bits) - 1;
-                bits &= bits - 1;
-                used |= 1u << b;
-                A.free_old[pos++] = (int)((w0 + k) * 32u + b);
-            }
-            if (used) A.occ[w0 + k] = word[k] | used;
-        }
+    if (n_free_used > 0 && occ_per <= 2) {
+        free_scan_regs<2>(A, n_free_used, occ_per, S);
+    } else if (n_free_used > 0 && occ_per <= kOccRegs) {
+        free_scan_regs<kOccRegs>(A, n_free_used, occ_per, S);
     } else if (n_free_used > 0) {
         const unsigned W = A.occ_words;
         const unsigned per = occ_per;
