@@ -1086,31 +1086,35 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
             A.sortC, lds, S);
     }
     const u64* sortE = A.sortE;
-    block_prefix(nT, [&](unsigned i) { return (u64)units[sortE[nT - 1 - i] & idmask]; },
+    // (the unit prefixes read the keys from the joint sort's LDS array, where
+    // it ran: evictable keys at [0, nT), demand keys after them, then the
+    // candidates; tags lie above idmask)
+    block_prefix(nT, [&](unsigned i) {
+        return (u64)units[(joint ? lds[nT - 1 - i] : sortE[nT - 1 - i]) & idmask]; },
                  A.prefE, S);
-    block_prefix(nL, [&](unsigned i) { return (u64)units[A.sortL[i] & idmask]; }, A.loff, S);
+    block_prefix(nL, [&](unsigned i) {
+        return (u64)units[(joint ? lds[nT + i] : A.sortL[i]) & idmask]; }, A.loff, S);
     stamp(2);
 
-    // demand victims: shortest prefix of the eviction order covering `need`
-    if (tid == 0) {
-        unsigned n_d = 0;
-        if (need > 0) {
-            unsigned lo = 1, hi = nT;                // prefE[nT] >= R >= need holds
-            while (lo < hi) {
-                const unsigned mid = (lo + hi) >> 1;
-                if ((long long)A.prefE[mid] >= need) hi = mid; else lo = mid + 1;
-            }
-            n_d = lo < nT ? lo : nT;
-        }
-        S.uscal[2] = n_d;
+    // demand victims: shortest prefix of the eviction order covering `need`.
+    // prefE is non-decreasing and prefE[nT] >= R >= need, so its length is the
+    // number of prefix values below need (prefE[0] = 0 among them): counted by
+    // the whole block instead of one thread's chain of dependent loads.
+    unsigned n_d = 0;
+    if (need > 0) {                                  // block-uniform
+        u64 below = 0;
+#pragma unroll 4
+        for (unsigned i = tid; i < nT; i += blockDim.x) below += (long long)A.prefE[i] < need;
+        u64 tot;
+        (void)block_excl_scan(below, S, &tot);
+        n_d = (unsigned)tot;
     }
-    __syncthreads();
-    const unsigned n_d = S.uscal[2];
     const u64 free1 = free_before + A.prefE[n_d] - c.sum_demand;
 
     stamp(3);
     const u64* sortC = A.sortC;
-    block_prefix(m, [&](unsigned i) { return (u64)units[sortC[i] & idmask]; }, A.prefC, S);
+    block_prefix(m, [&](unsigned i) {
+        return (u64)units[(joint ? lds[nT + nL + i] : sortC[i]) & idmask]; }, A.prefC, S);
     stamp(4);
 
     // acceptance: S_i <= budget and S_i <= free1 + (units of the remaining
