@@ -907,12 +907,23 @@ def main():
     }
     direct = {k: sum(s[k] for s in stats) for k in
               ("direct_out_launches", "direct_in_launches", "direct_out_bytes", "direct_in_bytes",
-               "direct_out_ms", "direct_in_ms")}
+               "direct_out_ms", "direct_in_ms", "duplex_launches", "duplex_bytes", "duplex_ms")}
     for d in ("out", "in"):
         direct[f"direct_{d}_GBps"] = (direct[f"direct_{d}_bytes"] /
                                       max(direct[f"direct_{d}_ms"], 1e-9) / 1e6)
+    direct["duplex_GBps"] = direct["duplex_bytes"] / max(direct["duplex_ms"], 1e-9) / 1e6
     dom = "pack" if pack_ms >= unpack_ms else "unpack"
-    if pack_ms + unpack_ms >= direct["direct_out_ms"] + direct["direct_in_ms"]:
+    direct_ms = direct["direct_out_ms"] + direct["direct_in_ms"]
+    if direct["duplex_ms"] > max(pack_ms + unpack_ms, direct_ms):
+        # steps small enough to move both directions in one launch straight
+        # over the host link: peak = the measured two-way copy-engine rate
+        n = max(direct["duplex_launches"], 1)
+        peak = probe.get("duplex_GBps") if probe else None
+        ach = direct["duplex_GBps"]
+        roofline = {"bound": "host-link", "kernel": "k_duplex", "achieved": ach, "peak": peak,
+                    "unit": "GB/s", "frac": ach / peak if peak else None, "traffic": None,
+                    "algorithmic_bytes_per_launch": direct["duplex_bytes"] / n}
+    elif pack_ms + unpack_ms >= direct_ms:
         traffic = None
         pmc_path = os.path.join(ROOT, "profiles", f"k_copy_{args.workload}_pmc.json")
         if os.path.exists(pmc_path):

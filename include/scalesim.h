@@ -106,9 +106,12 @@ typedef struct {
                                        units and the pinned host copies (no staging, no
                                        copy commands), which suits small steps where the
                                        latency of each copy dominates; larger steps use the
-                                       staged pipeline.  0 = always staged.  host_backing
-                                       must then be device-accessible pinned memory.
-                                       (The load scheduler ignores it.)                    */
+                                       staged pipeline.  When both directions of a step
+                                       are direct and non-empty they run as one launch
+                                       (each released unit written back, then loaded).
+                                       0 = always staged.  host_backing must then be
+                                       device-accessible pinned memory.  (The load
+                                       scheduler ignores it.)                             */
 } ss_pool_desc;
 
 typedef struct {
@@ -169,6 +172,12 @@ typedef struct {                    /* cumulative since create or ss_reset_stats
                                               copying) the inputs, queueing the stream
                                               waits, queueing the plan kernel and its
                                               events, the rest                             */
+    uint64_t duplex_launches;              /* direct steps whose two directions moved in
+                                              one launch (both non-empty, both within
+                                              direct_bytes)                               */
+    uint64_t duplex_bytes;                 /* their bytes, both directions (not counted
+                                              in direct_out/in above)                     */
+    double   duplex_ms;                    /* event time of those launches                */
 } ss_stats;
 
 /* Create a pool (Appendix A: register a memory module).  Validates every

@@ -91,7 +91,8 @@ class ss_stats(C.Structure):
                 ("direct_out_launches", C.c_uint64), ("direct_in_launches", C.c_uint64),
                 ("direct_out_bytes", C.c_uint64), ("direct_in_bytes", C.c_uint64),
                 ("direct_out_ms", C.c_double), ("direct_in_ms", C.c_double),
-                ("plan_enqueue_us", C.c_double * 4)]
+                ("plan_enqueue_us", C.c_double * 4), ("duplex_launches", C.c_uint64),
+                ("duplex_bytes", C.c_uint64), ("duplex_ms", C.c_double)]
 
 
 class ScaleSimError(RuntimeError):

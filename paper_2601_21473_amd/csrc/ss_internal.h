@@ -81,6 +81,10 @@ struct BtArgs {
     u64 unit_bytes;
     u64* whost;                     // [U] host byte offset of each written-back unit (or null)
     u64* lhost;                     // [U] host byte offset of each loaded unit (or null)
+    u64* rhost;                     // [U] per released position: the host byte offset of
+                                    // its unit when written back, else ~0 (or null)
+    unsigned* wrel;                 // [U] per written-back position: its released position
+                                    // (or null)
 };
 
 struct PlanArgs {
@@ -172,6 +176,27 @@ constexpr int kLdsKeys = 16384;                   // 128 KiB of u64 keys in LDS
 // itself), or classification over many workgroups whose last one runs the core.
 hipError_t launch_plan(const PlanArgs& a, hipStream_t st);
 constexpr unsigned kFuseAgents = 12288;           // plan core classifies up to this many
+// Both directions of a direct step in one launch (see k_duplex).
+struct DuplexArgs {
+    const int* lunits;              // [n_in] unit of each load position
+    const u64* lhost;               // [n_in] host byte offset of each load position's bytes
+    const int* wunits;              // [n_written] unit of each written-back position
+    const u64* whost;               // [n_written] host byte offset it goes to
+    const unsigned* wrel;           // [n_written] its released position
+    const u64* rhost;               // [released] host byte offset if written back, else ~0
+    u64 n_in;                       // load positions (units loaded)
+    u64 n_written;                  // written-back positions (units written back)
+    u64 n_free;                     // load positions < n_free take pre-step free units;
+                                    // position q >= n_free takes released position q - n_free
+    const CopyItem* items;
+    unsigned n_items;               // items per unit
+    unsigned item_groups;           // ceil(n_items / kCopyWavesPerBlock) blocks per position
+    const u64* plane_base;          // [P] device addresses
+    const u64* chunk_bytes;         // [P]
+    char* host;                     // device address of the host copies
+    u64 capacity;                   // U; unit ids outside [0, U) are skipped
+};
+hipError_t launch_duplex(const DuplexArgs& a, hipStream_t st);
 hipError_t launch_pack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_unpack(const CopyArgs& a, hipStream_t st);
 hipError_t launch_zero_u32(unsigned* p, u64 n, hipStream_t st);

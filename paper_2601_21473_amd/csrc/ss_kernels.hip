@@ -774,7 +774,9 @@ __device__ __forceinline__ void bt_release_group(const BtArgs& B, const u64 (&ba
             if (w[g]) {
                 B.wunits[ow[g] + j] = u[g];
                 if (B.whost) B.whost[ow[g] + j] = hoff[g] + (u64)j * B.unit_bytes;
+                if (B.wrel) B.wrel[ow[g] + j] = (unsigned)(o[g] + j);
             }
+            if (B.rhost) B.rhost[o[g] + j] = w[g] ? hoff[g] + (u64)j * B.unit_bytes : ~0ull;
             B.bt[base[g] + j] = -1;
         }
     }
@@ -1576,6 +1578,59 @@ hipError_t launch_probe_copy(void* dst, const void* src, u64 bytes, hipStream_t 
     if (blocks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_probe_copy, dim3((unsigned)blocks), dim3(kCopyThreads), 0, st,
                        static_cast<char*>(dst), static_cast<const char*>(src), bytes);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// direct two-way copies
+// ---------------------------------------------------------------------------
+
+// Both directions of a direct step in one launch, so that the host link
+// carries them at once: position p < n_in is load position p, whose unit
+// first gives its old bytes to the host copy of the victim that released it
+// (when that victim is written back) and then takes the load's bytes from its
+// host copy; the positions after those are the written-back units that no
+// load takes (written back only).  One wave per (position, item) in the pack
+// order.  A unit's write-back and its load are the same wave's, in program
+// order: the load's stores into the unit are issued after the write-back's
+// loads from it have returned (the write-back's stores wait for their data).
+__global__ void __launch_bounds__(kCopyThreads) k_duplex(DuplexArgs A) {
+    const unsigned b = blockIdx.x;
+    const unsigned wid = threadIdx.x >> 6;
+    const u64 p = b / A.item_groups;
+    const unsigned r =
+        __builtin_amdgcn_readfirstlane((b - (unsigned)p * A.item_groups) * kCopyWavesPerBlock + wid);
+    if (r >= A.n_items) return;
+    const CopyItem it = A.items[r];
+    auto chunk = [&](u64 u) {
+        return reinterpret_cast<char*>(A.plane_base[it.plane]) + u * A.chunk_bytes[it.plane] +
+               it.chunk_off;
+    };
+    if (p < A.n_in) {
+        const u64 u = (u64)(unsigned)A.lunits[p];
+        if (u >= A.capacity) return;
+        if (p >= A.n_free) {
+            const u64 h = A.rhost[p - A.n_free];
+            if (h != ~0ull) wave_copy_burst(A.host + h + it.unit_off, chunk(u), it.len);
+        }
+        wave_copy_burst(chunk(u), A.host + A.lhost[p] + it.unit_off, it.len);
+    } else {
+        const u64 w = p - A.n_in;
+        if (w >= A.n_written) return;
+        if ((u64)A.wrel[w] + A.n_free < A.n_in) return;   // its load position wrote it back
+        const u64 u = (u64)(unsigned)A.wunits[w];
+        if (u >= A.capacity) return;
+        wave_copy_burst(A.host + A.whost[w] + it.unit_off, chunk(u), it.len);
+    }
+}
+
+hipError_t launch_duplex(const DuplexArgs& a, hipStream_t st) {
+    const u64 positions = a.n_in + a.n_written;
+    if (positions == 0) return hipSuccess;
+    if (a.item_groups == 0 || a.n_items == 0) return hipErrorInvalidValue;
+    const u64 blocks = positions * a.item_groups;
+    if (blocks > 0x7fffffffull) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_duplex, dim3((unsigned)blocks), dim3(kCopyThreads), 0, st, a);
     return hipGetLastError();
 }
 

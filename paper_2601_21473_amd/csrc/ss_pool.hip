@@ -134,6 +134,8 @@ struct ss_pool {
     u64* d_woff = nullptr;
     u64* d_host_off = nullptr;     // direct mode: [N] host-copy offsets
     u64 *d_whost = nullptr, *d_lhost = nullptr;   // direct mode: [U] per moved unit
+    u64* d_rhost = nullptr;                       // direct mode: [U] per released position
+    unsigned* d_wrel = nullptr;                   // direct mode: [U] per written-back position
     PlanResult* d_res = nullptr;
     BtArgs* d_btargs = nullptr;    // the block-table update's arguments (pool constants)
     // timing mode: two plans' phase stamps in mapped host memory (the kernel
@@ -179,14 +181,16 @@ struct ss_pool {
     unsigned n_pack_step = 0;                     // pack launches of the current step
     bool direct_out = false;                      // this step's eviction went direct
     bool inline_step = false;                     // this step runs on the caller's stream
+    bool duplex_step = false;                     // this step's two directions were one launch
     hipStream_t bt_stream = nullptr;              // stream of the last plan's block-table update
     hipStream_t joined_stream = nullptr;          // caller stream that the last ss_prefetch_unpack
                                                   // made wait for the whole step
     bool joined_valid = false;
 
     // timing (SS_FLAG_TIMING): one pair per launch or per slot's copies
-    std::vector<TimedPair> t_pack, t_unpack, t_d2h, t_h2d, t_dout, t_din;
-    size_t n_t_pack = 0, n_t_unpack = 0, n_t_d2h = 0, n_t_h2d = 0, n_t_dout = 0, n_t_din = 0;
+    std::vector<TimedPair> t_pack, t_unpack, t_d2h, t_h2d, t_dout, t_din, t_dup;
+    size_t n_t_pack = 0, n_t_unpack = 0, n_t_d2h = 0, n_t_h2d = 0, n_t_dout = 0, n_t_din = 0,
+           n_t_dup = 0;
     ss_stats stats{};
 
     // plan of the current step (host)
@@ -288,7 +292,7 @@ void free_pool(ss_pool* p) {
                      p->d_lunits, p->d_free_old, p->d_res, p->d_hist_w, p->d_hist_e,
                      p->d_wunits, p->d_vwritten, p->d_woff, p->d_items, p->d_plane_base,
                      p->d_chunk_bytes, p->d_done, p->d_host_off, p->d_whost, p->d_lhost,
-                     p->d_btargs};
+                     p->d_rhost, p->d_wrel, p->d_btargs};
     for (void* d : dptrs)
         if (d) (void)hipFree(d);
     void* hptrs[] = {p->h_flag, p->h_phase, p->h_res, p->h_victims, p->h_loads, p->h_vwritten,
@@ -301,7 +305,8 @@ void free_pool(ss_pool* p) {
         if (e) (void)hipEventDestroy(e);
     for (hipEvent_t e : p->ev_packed)
         if (e) (void)hipEventDestroy(e);
-    for (auto* v : {&p->t_pack, &p->t_unpack, &p->t_d2h, &p->t_h2d, &p->t_dout, &p->t_din})
+    for (auto* v : {&p->t_pack, &p->t_unpack, &p->t_d2h, &p->t_h2d, &p->t_dout, &p->t_din,
+                    &p->t_dup})
         for (auto& tp : *v) {
             if (tp.a) (void)hipEventDestroy(tp.a);
             if (tp.b) (void)hipEventDestroy(tp.b);
@@ -349,7 +354,10 @@ void collect_timing(ss_pool* p) {
          &p->stats.direct_out_launches);
     fold(p->t_din, p->n_t_din, &p->stats.direct_in_ms, &p->stats.direct_in_bytes,
          &p->stats.direct_in_launches);
+    fold(p->t_dup, p->n_t_dup, &p->stats.duplex_ms, &p->stats.duplex_bytes,
+         &p->stats.duplex_launches);
     p->n_t_pack = p->n_t_unpack = p->n_t_d2h = p->n_t_h2d = p->n_t_dout = p->n_t_din = 0;
+    p->n_t_dup = 0;
 }
 
 // Fold plan slot k (its phase stamps: the kernel's wall clock at its entry,
@@ -508,6 +516,8 @@ BtArgs bt_args(const ss_pool* p) {
     B.unit_bytes = p->unit_bytes;
     B.whost = p->d_whost;
     B.lhost = p->d_lhost;
+    B.rhost = p->d_rhost;
+    B.wrel = p->d_wrel;
     return B;
 }
 
@@ -655,6 +665,8 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
         CREATE_TRY(dalloc(&p->d_host_off, N));
         CREATE_TRY(dalloc(&p->d_whost, U));
         CREATE_TRY(dalloc(&p->d_lhost, U));
+        CREATE_TRY(dalloc(&p->d_rhost, U));
+        CREATE_TRY(dalloc(&p->d_wrel, U));
         CREATE_TRY(hipMemcpy(p->d_host_off, p->host_off.data(), N * sizeof(u64),
                              hipMemcpyHostToDevice));
     }
@@ -968,6 +980,10 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
     const bool direct_in = p->direct_bytes && total_in &&
                            total_in * p->unit_bytes <= p->direct_bytes;
     p->inline_step = p->direct_bytes && (total == 0 || direct) && (total_in == 0 || direct_in);
+    // Both directions direct and non-empty: one launch moves both (k_duplex),
+    // so the link carries them at once instead of one after the other (the
+    // loads mostly reuse the units the victims release).
+    p->duplex_step = p->inline_step && direct && direct_in && p->d_rhost;
     hipStream_t so = p->inline_step ? caller : p->st_out;
     st = collect_plan_timing(p);
     if (st) return st;
@@ -1001,7 +1017,34 @@ ss_status ss_evict_pack(ss_pool* p, void* stream) {
     C.chunk_bytes = p->d_chunk_bytes;
     C.unit_bytes = p->unit_bytes;
     C.capacity = p->U;
-    if (direct) {
+    if (p->duplex_step) {
+        DuplexArgs D{};
+        D.lunits = p->d_lunits;
+        D.lhost = p->d_lhost;
+        D.wunits = p->d_wunits;
+        D.whost = p->d_whost;
+        D.wrel = p->d_wrel;
+        D.rhost = p->d_rhost;
+        D.n_in = total_in;
+        D.n_written = total;
+        D.n_free = p->res.n_free_used;
+        D.items = p->d_items;
+        D.n_items = p->n_items;
+        D.item_groups = C.item_groups;
+        D.plane_base = p->d_plane_base;
+        D.chunk_bytes = p->d_chunk_bytes;
+        D.host = p->host_dev;
+        D.capacity = p->U;
+        TimedPair* tp = nullptr;
+        if (timing) {
+            TRY_HIP(p, timed_pair(p->t_dup, p->n_t_dup++, &tp), true);
+            tp->bytes = (total + total_in) * p->unit_bytes;
+            TRY_HIP(p, hipEventRecord(tp->a, so), true);
+        }
+        TRY_HIP(p, launch_duplex(D, so), true);
+        if (timing) TRY_HIP(p, hipEventRecord(tp->b, so), true);
+        TRY_HIP(p, hipEventRecord(p->ev_packed[0], so), true);
+    } else if (direct) {
         // one launch gathers every written-back unit straight into its host copy
         C.first = 0;
         C.count = total;
@@ -1088,9 +1131,10 @@ ss_status ss_prefetch_unpack(ss_pool* p, void* stream) {
     C.chunk_bytes = p->d_chunk_bytes;
     C.unit_bytes = p->unit_bytes;
     C.capacity = p->U;
-    if (direct) {
+    if (direct && !p->duplex_step) {
         // one launch scatters every load straight from its host copy; units
         // released this step are overwritten only after the packs read them
+        // (a duplex step's loads moved with its write-backs)
         if (total > nF && p->n_pack_step)
             TRY_HIP(p, hipStreamWaitEvent(si, p->ev_packed[p->n_pack_step - 1], 0), true);
         C.first = 0;

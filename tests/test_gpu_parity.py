@@ -63,7 +63,10 @@ def test_tiny_direct(seed, theta):
     st = run_parity(W.make_trace("tiny", seed), theta=theta, slot_units=3, ring_slots=2,
                     direct_bytes=1 << 40, label=f"tiny direct s{seed} t{theta}")
     assert st["pack_launches"] == 0 and st["unpack_launches"] == 0
-    assert st["direct_out_launches"] > 50 and st["direct_in_launches"] > 50
+    # steps that both write back and load move both directions in one launch
+    assert st["duplex_launches"] > 50
+    assert st["direct_out_launches"] + st["duplex_launches"] > 50
+    assert st["direct_in_launches"] + st["duplex_launches"] > 50
     assert st["d2h_bytes"] == 0 and st["h2d_bytes"] == 0
 
 
@@ -83,7 +86,8 @@ def test_direct_and_staged_mixed(name, n_agents, steps, pool_index, limit_units)
     st = run_parity(tr, pool_index=pool_index, theta=S, steps=steps, slot_units=slot_units,
                     ring_slots=2, sample_units=48, direct_bytes=limit_units * spec.unit_bytes,
                     label=f"{name}[{pool_index}] direct<={limit_units}u")
-    assert st["direct_out_launches"] > 0 and st["direct_in_launches"] > 0
+    assert st["direct_out_launches"] + st["duplex_launches"] > 0
+    assert st["direct_in_launches"] + st["duplex_launches"] > 0
     assert st["pack_launches"] > 0 and st["unpack_launches"] > 0
 
 
@@ -292,9 +296,12 @@ def test_write_back_elision_direct(mode):
                     label=f"direct elision {mode}")
     assert st["pack_launches"] == 0 and st["unpack_launches"] == 0
     if mode == "clean":
+        # nothing is written back: loads alone, never the two-way launch
         assert st["direct_out_launches"] == 0 and st["direct_out_bytes"] == 0
+        assert st["duplex_launches"] == 0
     else:
-        assert st["direct_out_launches"] > 0
+        # clean victims' released units are loaded without a write-back
+        assert st["direct_out_launches"] + st["duplex_launches"] > 0
 
 
 def test_two_pools_share_streams():
