@@ -984,7 +984,7 @@ def main():
                                 "link)"),
             "core_phases_us": dict(zip(("classify", "cuts_and_sorts", "demand_victims",
                                         "candidate_prefix", "acceptance", "lists",
-                                        "free_units"), phases)),
+                                        "publish"), phases)),
             "gpu_kernels_us": 1e3 * plan_gpu_ms / nps,
             "host_enqueue_us": host[0] / nps, "host_wait_us": host[1] / nps,
             "host_readback_us": host[2] / nps,

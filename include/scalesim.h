@@ -155,13 +155,16 @@ typedef struct {                    /* cumulative since create or ss_reset_stats
     double   plan_gpu_ms;                  /* plan kernels, from the first workgroup's
                                               entry to the end of the block-table update,
                                               by the kernels' own wall-clock stamps       */
-    double   plan_phase_us[7];             /* plan phases (classify; the histogram cuts
-                                              and the sorts of the evictable, demand and
-                                              candidate sets with their unit prefixes;
-                                              demand victims; candidate prefix;
-                                              acceptance; lists; free units); classify runs
+    double   plan_phase_us[7];             /* plan phases up to the published plan
+                                              (classify; the histogram cuts and the sorts
+                                              of the evictable, demand and candidate sets
+                                              with their unit prefixes; demand victims;
+                                              candidate prefix; acceptance; lists; the
+                                              result and its publication); classify runs
                                               from the plan kernel's entry (its first
-                                              workgroup when N > 12288)                     */
+                                              workgroup when N > 12288).  The free-unit
+                                              pick and the block-table update follow in
+                                              plan_gpu_ms only                             */
     double   plan_host_us[3];              /* ss_plan_step on the host: queueing the plan,
                                               waiting for it, reading it back              */
     uint64_t direct_out_launches, direct_in_launches;  /* directions moved by direct_bytes */

@@ -1240,12 +1240,39 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     }
 
     stamp(6);
-    // pre-step free units in ascending order, as many as the loads can use;
-    // they all go to this step's loads, so the thread that owns their
-    // occupancy word marks them in use there (plain stores: one owner per
-    // word).  The block-table update then only frees the released units that
-    // no load takes.
+    // pre-step free units, as many as the loads can use (the host needs only
+    // their count)
     const u64 n_free_used = units_in < free_before ? units_in : free_before;
+    __syncthreads();
+    if (tid == 0) {
+        PlanResult r = {};
+        r.status = 0;
+        r.n_victims = n_v;
+        r.n_loads = n_l;
+        r.n_demand = nL;
+        r.n_demand_victims = n_d;
+        r.units_out = units_out;
+        r.units_in = units_in;
+        r.free_before = free_before;
+        r.n_free_used = n_free_used;
+        r.units_written = A.woff[n_v];
+        *A.res = r;
+        *A.res_host = r;
+        if (!kFused) *A.cnt = PlanCounters{};
+    }
+    publish_plan(A);
+    stamp(7);
+    // The host has the plan; the workgroup goes on to pick the pre-step free
+    // units (ascending) and to update the block table (waves over victims,
+    // then over loads), off the plan's return path.  The update saves the
+    // step the launches of separate update kernels (queueing those two
+    // kernels behind the multi-workgroup plan kernel cost the host about
+    // 0.1 ms per call).  The free units all go to this step's loads, so the
+    // thread that owns their occupancy word marks them in use there (plain
+    // stores: one owner per word); the update then only frees the released
+    // units that no load takes.  Every list the update reads was written above
+    // by this workgroup; the barriers inside publish_plan and below order
+    // those writes before its reads.
     const unsigned occ_per = (A.occ_words + blockDim.x - 1) / blockDim.x;
     if (n_free_used > 0 && occ_per <= 2) {
         free_scan_regs<2>(A, n_free_used, occ_per, S);
@@ -1274,30 +1301,6 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     }
 
     __syncthreads();
-    stamp(7);
-    if (tid == 0) {
-        PlanResult r = {};
-        r.status = 0;
-        r.n_victims = n_v;
-        r.n_loads = n_l;
-        r.n_demand = nL;
-        r.n_demand_victims = n_d;
-        r.units_out = units_out;
-        r.units_in = units_in;
-        r.free_before = free_before;
-        r.n_free_used = n_free_used;
-        r.units_written = A.woff[n_v];
-        *A.res = r;
-        *A.res_host = r;
-        if (!kFused) *A.cnt = PlanCounters{};
-    }
-    publish_plan(A);
-    // The host has the plan; the workgroup goes on to update the block table
-    // (waves over victims, then over loads), which saves the step the launches
-    // of separate update kernels (queueing those two kernels behind the
-    // multi-workgroup plan kernel cost the host about 0.1 ms per call).  Every
-    // list it reads was written above by this workgroup; the barrier inside
-    // publish_plan ordered those writes before these reads.
     bt_tail(A.bt, n_v, n_l, n_free_used, units_in, units_out);
     if (A.phase) {                                   // kernel-uniform
         __syncthreads();
