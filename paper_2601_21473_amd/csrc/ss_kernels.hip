@@ -744,9 +744,6 @@ __device__ __forceinline__ void classify_fused(const PlanArgs& A, CoreShared& S,
     flush_sums(t, &S.cnt);
 }
 
-// Publish the plan to the host: every thread's host-visible writes are made
-// visible at system scope, then one thread writes the plan's sequence number
-// to the mapped flag word, which the host polls.  Last action of the core.
 // Items (victims or loads) of the block-table update handled together: every
 // lane loads its entries of all of them before it stores any, so a group
 // costs one memory round trip per 64 of its logical units.
@@ -906,13 +903,16 @@ __device__ __attribute__((noinline)) void bt_tail(const BtArgs* Bp, unsigned n_v
     bt_update_block(B, n_v, n_l, nF, units_in, units_out);
 }
 
+// Publish the plan to the host: every thread's host-visible writes are made
+// visible at system scope, then one thread writes the plan's sequence number
+// to the mapped flag word, which the host polls.  The fences only release:
+// nothing after them reads what the host writes (a full fence also
+// invalidates the L2 at system scope, in every wave).
 __device__ __forceinline__ void publish_plan(const PlanArgs& A) {
-    __threadfence_system();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
     __syncthreads();
-    if (threadIdx.x == 0) {
-        __threadfence_system();
-        __hip_atomic_store(A.flag_host, A.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-    }
+    if (threadIdx.x == 0)
+        __hip_atomic_store(A.flag_host, A.seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 // The plan core: one workgroup of kCoreThreads threads; `lds` holds kLdsKeys
