@@ -1409,10 +1409,10 @@ __global__ void __launch_bounds__(kCoreThreads) k_classify_core(PlanArgs A) {
     // lets its workgroup read them.
     __syncthreads();
     if (threadIdx.x == 0) {
-        __threadfence();
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         const bool last = atomicAdd(A.done, 1u) == gridDim.x - 1;
         if (last) {
-            __threadfence();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             *A.done = 0;
         }
         S.uscal[3] = last;
