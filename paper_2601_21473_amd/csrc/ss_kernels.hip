@@ -203,8 +203,8 @@ __device__ __forceinline__ u64* list_ptr(const PlanArgs& A, unsigned k) {
 
 // Slots of one pass's agents in their lists (the whole workgroup, one agent
 // per thread and u).  No atomic sits in the waves' path: each wave ranks its
-// lanes within every list (ballot, mbcnt) and stores its per-list counts in
-// tab[list][wave, u]; after a barrier wave k scans list k's 64 counts (DPP)
+// lanes within their lists (ballots, mbcnt) and stores its per-list counts
+// in tab[list][wave, u]; after a barrier wave k scans list k's 64 counts (DPP)
 // and adds the list's base, which is this workgroup's running count of the
 // list (kGlobal false) or the range that one device-wide atomic reserves for
 // the workgroup's whole list (kGlobal true: one pass per workgroup); after a
@@ -217,27 +217,47 @@ __device__ __forceinline__ void reserve_pass(const unsigned (&lst)[kClassBatch],
                                              unsigned (&slot)[kClassBatch], unsigned* tab,
                                              PlanCounters* local, PlanCounters* global) {
     const unsigned w = threadIdx.x >> 6, l = lane_id();
-    // this wave's column of the table: zero, then the count of every list
-    // present in the wave (in order behind the zeros: one wave's LDS accesses
-    // complete in order)
-    if (l < kLists * kClassBatch)
-        tab[(l / kClassBatch) * kPassSlots + w * kClassBatch + l % kClassBatch] = 0;
+    static_assert(kLists <= 15, "list ids and kNoList's low bits fit four bits");
     unsigned rank[kClassBatch];
 #pragma unroll
     for (unsigned u = 0; u < kClassBatch; ++u) {
-        // one round per distinct list among the wave's lanes (usually one to
-        // three), instead of one ballot per list: every instruction of this
-        // single-workgroup path is on the plan's critical path
-        u64 rest = __ballot(lst[u] != kNoList);
-        unsigned r = 0;
-        while (rest) {                               // wave-uniform
-            const unsigned k = (unsigned)__builtin_amdgcn_readlane((int)lst[u], (int)__builtin_ctzll(rest));
-            const u64 m = __ballot(lst[u] == k);
-            r = lst[u] == k ? mbcnt(m) : r;
-            if (l == 0) tab[k * kPassSlots + w * kClassBatch + u] = (unsigned)__popcll(m);
+        // The first two lists of the wave by one ballot each (in a single
+        // workgroup's classification most waves hold one or two); if lanes
+        // remain, a multi-split by the four bits of the list id: four
+        // ballots, then the lanes of list k are those whose bits match k's.
+        // The many-workgroup classification (large agent counts, whose waves
+        // mostly hold three or more lists) goes to the multi-split directly.
+        // Selects throughout, no branches per lane.
+        const u64 valid = __ballot(lst[u] != kNoList);
+        u64 rest = valid;
+        unsigned r = 0, k0 = kNoList, k1 = kNoList, c0 = 0, c1 = 0;
+        if (!kGlobal && rest) {                      // wave-uniform
+            k0 = (unsigned)__builtin_amdgcn_readlane((int)lst[u], (int)__builtin_ctzll(rest));
+            const u64 m = __ballot(lst[u] == k0);
+            r = lst[u] == k0 ? mbcnt(m) : r;
+            c0 = (unsigned)__popcll(m);
             rest &= ~m;
         }
+        if (!kGlobal && rest) {
+            k1 = (unsigned)__builtin_amdgcn_readlane((int)lst[u], (int)__builtin_ctzll(rest));
+            const u64 m = __ballot(lst[u] == k1);
+            r = lst[u] == k1 ? mbcnt(m) : r;
+            c1 = (unsigned)__popcll(m);
+            rest &= ~m;
+        }
+        unsigned cnt = l == k0 ? c0 : l == k1 ? c1 : 0u;
+        if (rest) {
+            const u64 m0 = __ballot(lst[u] & 1u), m1 = __ballot(lst[u] & 2u);
+            const u64 m2 = __ballot(lst[u] & 4u), m3 = __ballot(lst[u] & 8u);
+            auto lanes_of = [&](unsigned k) {
+                return valid & ((k & 1u) ? m0 : ~m0) & ((k & 2u) ? m1 : ~m1) &
+                       ((k & 4u) ? m2 : ~m2) & ((k & 8u) ? m3 : ~m3);
+            };
+            r = mbcnt(lanes_of(lst[u]));
+            cnt = (unsigned)__popcll(lanes_of(l));
+        }
         rank[u] = r;
+        if (l < kLists) tab[l * kPassSlots + w * kClassBatch + u] = cnt;
     }
     __syncthreads();
     if (w < kLists) {                                // wave-uniform
@@ -1182,21 +1202,20 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     __syncthreads();
     stamp(5);
     const unsigned n_p = S.uscal[3];
-    if (tid == 0) {
-        unsigned n_v = n_d;
-        if (n_p > 0 && A.prefC[n_p] > free1) {
-            const u64 target = pref[n_d] + (A.prefC[n_p] - free1);
-            unsigned lo = n_d + 1, hi = nT;
-            while (lo < hi) {
-                const unsigned mid = (lo + hi) >> 1;
-                if (pref[mid] >= target) hi = mid; else lo = mid + 1;
-            }
-            n_v = lo < nT ? lo : nT;
-        }
-        S.uscal[4] = n_v;
+    // victims: the demand victims, extended while the accepted loads need
+    // room: to the first eviction index past n_d whose prefix reaches the
+    // target, i.e. n_d + 1 plus the prefix values below it (counted by the
+    // whole block), at most nT
+    unsigned n_v = n_d;
+    if (n_p > 0 && A.prefC[n_p] > free1) {           // block-uniform
+        const u64 target = pref[n_d] + (A.prefC[n_p] - free1);
+        u64 below = 0;
+#pragma unroll 4
+        for (unsigned i = n_d + 1 + tid; i < nT; i += blockDim.x) below += pref[i] < target;
+        u64 tot;
+        (void)block_excl_scan(below, S, &tot);
+        n_v = min(nT, n_d + 1 + (unsigned)tot);
     }
-    __syncthreads();
-    const unsigned n_v = S.uscal[4];
     const unsigned n_l = nL + n_p;
     const u64 units_out = pref[n_v];
     const u64 units_in = c.sum_demand + A.prefC[n_p];
