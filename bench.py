@@ -982,8 +982,8 @@ def main():
             "host_inputs": dict(lat_host, inputs="host memory (numpy arrays; the call copies "
                                 "them into pinned memory the plan kernel reads over the host "
                                 "link)"),
-            "core_phases_us": dict(zip(("classify", "cuts_and_sorts", "demand_victims",
-                                        "candidate_prefix", "acceptance", "lists",
+            "core_phases_us": dict(zip(("classify", "cuts_sorts_prefixes", "demand_victims",
+                                        "acceptance_setup", "acceptance", "lists",
                                         "publish"), phases)),
             "gpu_kernels_us": 1e3 * plan_gpu_ms / nps,
             "host_enqueue_us": host[0] / nps, "host_wait_us": host[1] / nps,

@@ -159,8 +159,9 @@ typedef struct {                    /* cumulative since create or ss_reset_stats
                                               (classify; the histogram cuts and the sorts
                                               of the evictable, demand and candidate sets
                                               with their unit prefixes; demand victims;
-                                              candidate prefix; acceptance; lists; the
-                                              result and its publication); classify runs
+                                              the acceptance's LDS copy of the evictable
+                                              prefix; acceptance; lists; the result and
+                                              its publication); classify runs
                                               from the plan kernel's entry (its first
                                               workgroup when N > 12288).  The free-unit
                                               pick and the block-table update follow in

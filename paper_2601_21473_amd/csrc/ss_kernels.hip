@@ -332,22 +332,21 @@ __device__ __forceinline__ u64 block_excl_scan(u64 v, CoreShared& S, u64* total)
     return r;
 }
 
-// out[0] = 0, out[i+1] = out[i] + f(i) for i < n.
+// out(i, f(0) + ... + f(i)) for i < n: the inclusive prefix of every element.
 // Lists longer than the block: each thread takes kPrefixRun consecutive
 // elements per round, so the f(i) of a round (often gathers) are in flight
 // together and a block scan covers 4096 elements (shorter lists keep one
 // element per thread: fewer instructions when most threads would idle).
 constexpr unsigned kPrefixRun = 4;
-template <class F>
-__device__ __forceinline__ void block_prefix(unsigned n, F f, u64* out, CoreShared& S) {
+template <class F, class Out>
+__device__ __forceinline__ void block_prefix_to(unsigned n, F f, Out out, CoreShared& S) {
     u64 carry = 0;
-    if (threadIdx.x == 0) out[0] = 0;
     if (n <= blockDim.x) {
         const unsigned i = threadIdx.x;
         const u64 v = (i < n) ? f(i) : 0;
         u64 tot;
         const u64 ex = block_excl_scan(v, S, &tot);
-        if (i < n) out[i + 1] = ex + v;
+        if (i < n) out(i, ex + v);
         __syncthreads();
         return;
     }
@@ -364,11 +363,18 @@ __device__ __forceinline__ void block_prefix(unsigned n, F f, u64* out, CoreShar
 #pragma unroll
         for (unsigned u = 0; u < kPrefixRun; ++u) {
             run += v[u];
-            if (i0 + u < n) out[i0 + u + 1] = run;
+            if (i0 + u < n) out(i0 + u, run);
         }
         carry += tot;
     }
     __syncthreads();
+}
+
+// out[0] = 0, out[i+1] = out[i] + f(i) for i < n.
+template <class F>
+__device__ __forceinline__ void block_prefix(unsigned n, F f, u64* out, CoreShared& S) {
+    if (threadIdx.x == 0) out[0] = 0;
+    block_prefix_to(n, f, [&](unsigned i, u64 v) { out[i + 1] = v; }, S);
 }
 
 // Keys src[i] (i < n) with keep(key) appended to buf[*counter ...] (slots at
@@ -1062,7 +1068,12 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
         __syncthreads();
         const unsigned fr = S.uscal[1];
         b_E = fr ? fr - 1 : 0;                       // none reaches R: every evictable resident
+        // units of the evictable residents of buckets >= b_E (the set sorted
+        // below): HEsuf(b_E), from the thread that holds bucket b_E
+        if (tid == b_E / 2) S.scal[0] = tot_e - ((b_E & 1) ? heb + he0 : heb);
+        __syncthreads();
     }
+    const u64 units_T = b_E < kDistBuckets ? S.scal[0] : 0;
 
     // The sorted sets: the evictable residents of buckets >= b_E (ascending;
     // eviction order is descending key = the reversed array), the demand loads
@@ -1108,14 +1119,33 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
             A.sortC, lds, S);
     }
     const u64* sortE = A.sortE;
-    // (the unit prefixes read the keys from the joint sort's LDS array, where
-    // it ran: evictable keys at [0, nT), demand keys after them, then the
-    // candidates; tags lie above idmask)
-    block_prefix(nT, [&](unsigned i) {
-        return (u64)units[(joint ? lds[nT - 1 - i] : sortE[nT - 1 - i]) & idmask]; },
-                 A.prefE, S);
-    block_prefix(nL, [&](unsigned i) {
-        return (u64)units[(joint ? lds[nT + i] : A.sortL[i]) & idmask]; }, A.loff, S);
+    const u64* sortC = A.sortC;
+    // The three unit prefixes in one pass over the evictable keys in eviction
+    // order (descending), then the demand keys, then the candidates: prefE
+    // over the first, loff and prefC over the others, each from 0 (the bases
+    // are the units of the evictable set, HEsuf(b_E), and of the demand loads,
+    // sum_demand).  The keys come from the joint sort's LDS array where it ran
+    // (evictable keys at [0, nT), demand keys after them, then the candidates;
+    // tags lie above idmask).
+    {
+        const unsigned nTL = nT + nL;
+        const u64 baseL = units_T, baseC = units_T + c.sum_demand;
+        if (tid == 0) {
+            A.prefE[0] = 0;
+            A.loff[0] = 0;
+            A.prefC[0] = 0;
+        }
+        block_prefix_to(nTL + m, [&](unsigned i) {
+            u64 k;
+            if (joint) k = lds[i < nT ? nT - 1 - i : i];
+            else k = i < nT ? sortE[nT - 1 - i] : i < nTL ? A.sortL[i - nT] : sortC[i - nTL];
+            return (u64)units[k & idmask];
+        }, [&](unsigned i, u64 v) {
+            if (i < nT) A.prefE[i + 1] = v;
+            else if (i < nTL) A.loff[i - nT + 1] = v - baseL;
+            else A.prefC[i - nTL + 1] = v - baseC;
+        }, S);
+    }
     stamp(2);
 
     // demand victims: shortest prefix of the eviction order covering `need`.
@@ -1134,10 +1164,6 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     const u64 free1 = free_before + A.prefE[n_d] - c.sum_demand;
 
     stamp(3);
-    const u64* sortC = A.sortC;
-    block_prefix(m, [&](unsigned i) {
-        return (u64)units[(joint ? lds[nT + nL + i] : sortC[i]) & idmask]; }, A.prefC, S);
-    stamp(4);
 
     // acceptance: S_i <= budget and S_i <= free1 + (units of the remaining
     // evictable residents with distance strictly larger than d_i)
@@ -1153,6 +1179,7 @@ __device__ __forceinline__ void plan_core(const PlanArgs& A, u64* lds, CoreShare
     const u64* keysE = in_lds ? lds : sortE;
     const u64* pref = in_lds ? lds + nT : A.prefE;
     __syncthreads();
+    stamp(4);
     // (the search runs on LDS or on global memory; each instance sees which,
     // so the LDS one uses LDS instructions)
     auto accept = [&](const u64* keysE, const u64* pref) __attribute__((always_inline)) {

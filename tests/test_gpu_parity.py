@@ -403,6 +403,22 @@ def test_joint_sort_sizes(n, cap):
                label=f"joint sort {n} agents")
 
 
+@pytest.mark.parametrize("capacity", [65536, 65600, 524320])
+def test_free_unit_scan_pool_sizes(capacity):
+    # The plan picks the pre-step free units from the occupancy bitmap with
+    # each thread holding ceil(words / 1024) words: up to 2 in registers (pools
+    # up to 65,536 units), up to 16 (524,288 units), a loop beyond.  2,000
+    # agents of about capacity / 600 units each, 30 of them run per step, so
+    # every step evicts and the free units left by earlier steps are reused.
+    rng = np.random.default_rng(capacity)
+    per = capacity // 600
+    units = rng.integers(per // 2, per + per // 2, size=2000).astype(np.uint32)
+    tr = synthetic_trace(2000, capacity, 10, 30, seed=capacity, units=units, chunk_bytes=(16,),
+                         noisy=True)
+    run_parity(tr, theta=S, slot_units=65536, ring_slots=2, sample_units=4000,
+               label=f"free-unit scan, {capacity} units")
+
+
 @pytest.mark.parametrize("n_agents", [40000, 50000])
 @pytest.mark.parametrize("theta,budget", [(S, None), (3, None), (S, 300)])
 def test_many_agents_variable_sizes(n_agents, theta, budget):
