@@ -7,13 +7,13 @@
 //                candidates, stream compaction of each class (wave64 ballot
 //                + mbcnt ranks, one DPP scan per list over the waves' counts),
 //                and the unit sums the plan needs;
-//   plan core    one workgroup of 1024 threads: register/LDS merge sorts,
-//                the distance-histogram cut (weighted radix select as the
-//                fallback) of the candidate prefix that can possibly fit,
-//                prefix sums, the prefetch acceptance rule in closed form,
-//                the victim count, the free-unit list, and the plan written
-//                to a mapped host mirror, published by a sequence number
-//                written last.
+//   plan core    one workgroup of 1024 threads: the distance-histogram
+//                cuts of the evictable and candidate sets that can take part
+//                in the plan, one register/LDS merge sort of both (and of the
+//                demand loads), prefix sums, the prefetch acceptance rule in
+//                closed form, the victim count, and the plan written to a
+//                mapped host mirror, published by a sequence number written
+//                last; then the pick of the pre-step free units.
 //   k_plan_core      the plan core, classifying the agents itself
 //                    (N <= kFuseAgents = 12,288);
 //   k_classify_core  classification over N / 4096 workgroups, the last of
@@ -24,7 +24,9 @@
 //   k_copy<pack>  gathers (pack) or scatters (unpack) whole units between the
 //                pool's planes and a contiguous staging slot, one wave per
 //                piece of at most 32 KiB moved as one burst of 16-byte
-//                non-temporal accesses.
+//                non-temporal accesses;
+//   k_duplex     both directions of a small step in one launch, straight
+//                between the pool's units and the pinned host copies.
 //
 // Nothing here is a dense contraction; all work is integer indexing and byte
 // movement, so there is no MFMA.
