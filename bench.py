@@ -285,6 +285,9 @@ def parse():
     ap.add_argument("--null-stream", action="store_true",
                     help="queue the plan and the step on the null stream instead of a stream "
                          "of the caller's own")
+    ap.add_argument("--blocking-wait", action="store_true",
+                    help="the pools' waits (ss_sync) block instead of polling "
+                         "(SS_FLAG_POLL_WAIT off)")
     ap.add_argument("--direct-mib", type=float, default=4,
                     help="directions of a step that move at most this many MiB go by kernel "
                          "straight between units and host copies (0 = always staged)")
@@ -728,7 +731,8 @@ def main():
         host_slots = None if args.host_copies == 0 else args.host_copies
         mem = PoolMemory(spec, args.staging_mib << 20, args.ring, host_slots=host_slots)
         mems.append(mem)
-        pools.append(mem.make_pool(timing=True, direct_bytes=int(args.direct_mib * (1 << 20))))
+        pools.append(mem.make_pool(timing=True, direct_bytes=int(args.direct_mib * (1 << 20)),
+                                   poll_wait=not args.blocking_wait))
     probe = {} if args.no_probe else probes(binding, mems[0].host)
     N = trace.n_agents
     d_np = np.ascontiguousarray(trace.dist, dtype=np.uint32)
@@ -833,7 +837,9 @@ def main():
     moved = out_b + in_b
     stats = [p.stats() for p in pools]
 
-    # plan latency: each plan issued with the device idle; wall time of the
+    # plan latency: each plan issued with the device idle (after the pools'
+    # wait, which polls unless --blocking-wait: a launch after a blocking wait
+    # on long work costs the host 2-3 times as much); wall time of the
     # Python call (counts only) and the library's own host time of the C call
     # (stats are read only after a plan, so that nothing is submitted between
     # the wait for the previous step and the measured call).  First with the
@@ -1015,6 +1021,8 @@ def main():
                    "write_back": "none (clean evictions)" if args.clean_evict else "every eviction",
                    "direct_limit_bytes": int(args.direct_mib * (1 << 20)),
                    "caller_stream": "null stream" if args.null_stream else "own non-blocking stream",
+                   "caller_wait": ("ss_sync blocks" if args.blocking_wait else
+                                   "ss_sync polls (SS_FLAG_POLL_WAIT)"),
                    "host_copies": ("one per agent" if args.host_copies == 0 else
                                    f"{args.host_copies} shared round-robin"),
                    "bytes_out": out_b, "bytes_in": in_b},

@@ -81,6 +81,13 @@ typedef int32_t ss_status;
 #define SS_NO_DISTANCE     0xFFFFFFFFu  /* "never activated again"; never < threshold */
 
 #define SS_FLAG_TIMING     1u       /* record HIP events around every copy launch   */
+#define SS_FLAG_POLL_WAIT  2u       /* ss_sync and ss_get_stats poll the pool's
+                                       streams and events instead of blocking: the
+                                       calling thread spins while the device works,
+                                       and the next call's launches cost their warm
+                                       host time (after a blocking wait on long work
+                                       a launch and its event record take 2-3 times
+                                       as long)                                    */
 
 typedef struct {
     uint32_t        n_agents;       /* N >= 1, N < 2^31                                    */
@@ -472,7 +479,8 @@ ss_status ss_loader_pending(ss_loader* loader, uint32_t* queued, uint32_t* runni
 ss_status ss_loader_sync(ss_loader* loader);
 ss_status ss_loader_get_stats(ss_loader* loader, ss_loader_stats* out);
 
-/* Block until all work the pool has queued (plan, copies, kernels) is done. */
+/* Wait until all work the pool has queued (plan, copies, kernels) is done
+ * (blocking, or polling under SS_FLAG_POLL_WAIT). */
 ss_status ss_sync(ss_pool* pool);
 
 /* Plumbing for callers without a framework allocator: thin wrappers over the

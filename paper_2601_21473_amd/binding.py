@@ -27,6 +27,7 @@ SS_ERR_POISONED = -6
 SS_NO_BUDGET = (1 << 64) - 1
 SS_NO_DISTANCE = 0xFFFFFFFF
 SS_FLAG_TIMING = 1
+SS_FLAG_POLL_WAIT = 2
 
 EXPORTS = ["ss_pool_create", "ss_pool_destroy", "ss_plan_step", "ss_evict_pack",
            "ss_prefetch_unpack", "ss_block_table", "ss_block_table_host", "ss_block_table_host_all", "ss_resident_host",
@@ -226,14 +227,15 @@ class Pool:
 
     def __init__(self, *, capacity_units, chunk_bytes, agent_units, plane_base, host_backing,
                  host_bytes, dev_staging, staging_bytes, ring_slots, host_off=None, device=0,
-                 timing=False, direct_bytes=0):
+                 timing=False, direct_bytes=0, poll_wait=False):
         L = load()
         d, self._keep = make_desc(capacity_units=capacity_units, chunk_bytes=chunk_bytes,
                                   agent_units=agent_units, plane_base=plane_base,
                                   host_backing=host_backing, host_bytes=host_bytes,
                                   dev_staging=dev_staging, staging_bytes=staging_bytes,
                                   ring_slots=ring_slots, host_off=host_off, device=device,
-                                  flags=SS_FLAG_TIMING if timing else 0,
+                                  flags=(SS_FLAG_TIMING if timing else 0)
+                                  | (SS_FLAG_POLL_WAIT if poll_wait else 0),
                                   direct_bytes=direct_bytes)
         self._chunk = self._keep[0]
         self._units = self._keep[1]

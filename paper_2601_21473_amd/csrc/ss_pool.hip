@@ -464,6 +464,28 @@ ss_status check_usable(ss_pool* p) {
     return SS_OK;
 }
 
+// The pool's waits: blocking, or under SS_FLAG_POLL_WAIT a loop of queries
+// (the thread stays busy and the runtime's state stays in its caches, so the
+// launches of the next call cost their warm host time).  A query that finds
+// the work pending leaves that status as the thread's last error: cleared.
+template <class Query>
+hipError_t poll_until_done(Query query) {
+    hipError_t e;
+    while ((e = query()) == hipErrorNotReady) __builtin_ia32_pause();
+    (void)hipGetLastError();
+    return e;
+}
+
+hipError_t wait_stream(const ss_pool* p, hipStream_t s) {
+    if (!(p->flags & SS_FLAG_POLL_WAIT)) return hipStreamSynchronize(s);
+    return poll_until_done([s] { return hipStreamQuery(s); });
+}
+
+hipError_t wait_event(const ss_pool* p, hipEvent_t ev) {
+    if (!(p->flags & SS_FLAG_POLL_WAIT)) return hipEventSynchronize(ev);
+    return poll_until_done([ev] { return hipEventQuery(ev); });
+}
+
 // Fold the previous step's copy events and the previous plan's event time and
 // phase stamps into the stats (timing mode; called before this step's pack).
 // The previous step's loads completed before this plan's kernel ran, and so
@@ -471,7 +493,7 @@ ss_status check_usable(ss_pool* p) {
 // plan is folded at the next step, or by ss_get_stats.
 ss_status collect_plan_timing(ss_pool* p) {
     if (!(p->flags & SS_FLAG_TIMING)) return SS_OK;
-    TRY_HIP(p, hipEventSynchronize(p->ev_out_done), true);
+    TRY_HIP(p, wait_event(p, p->ev_out_done), true);
     collect_timing(p);
     fold_plan(p, (int)((p->plan_seq + 1) & 1));      // the previous plan's slot
     return SS_OK;
@@ -480,9 +502,8 @@ ss_status collect_plan_timing(ss_pool* p) {
 // Everything pending, the current plan included (its kernel is waited for).
 ss_status collect_all_timing(ss_pool* p) {
     if (!(p->flags & SS_FLAG_TIMING)) return SS_OK;
-    TRY_HIP(p, hipEventSynchronize(p->ev_planned), true);
-    TRY_HIP(p, hipEventSynchronize(p->ev_out_done), true);
-    TRY_HIP(p, hipEventSynchronize(p->ev_in_done), true);
+    for (hipEvent_t e : {p->ev_planned, p->ev_out_done, p->ev_in_done})
+        TRY_HIP(p, wait_event(p, e), true);
     collect_timing(p);
     fold_plan(p, 0);
     fold_plan(p, 1);
@@ -540,7 +561,7 @@ ss_status ss_pool_create(const ss_pool_desc* d, ss_pool** out) {
     if (!d->host_backing) return set_err(SS_ERR_ARG, "host_backing is required");
     if (!d->dev_staging) return set_err(SS_ERR_ARG, "dev_staging is required");
     if (d->ring_slots == 0) return set_err(SS_ERR_ARG, "ring_slots must be >= 1");
-    if (d->flags & ~SS_FLAG_TIMING) return set_err(SS_ERR_ARG, "unknown flag bits");
+    if (d->flags & ~(SS_FLAG_TIMING | SS_FLAG_POLL_WAIT)) return set_err(SS_ERR_ARG, "unknown flag bits");
     u64 unit_bytes = 0;
     for (uint32_t c = 0; c < d->n_planes; ++c) {
         const u64 cb = d->chunk_bytes[c];
@@ -1318,10 +1339,10 @@ ss_status ss_sync(ss_pool* p) {
     if (st) return st;
     DeviceGuard g(p->device);
     for (hipStream_t s : {p->st_out, p->st_in})
-        TRY_HIP(p, hipStreamSynchronize(s), true);
+        TRY_HIP(p, wait_stream(p, s), true);
     // work of a step that ran on a caller's stream
     for (hipEvent_t e : {p->ev_planned, p->ev_out_done, p->ev_in_done})
-        TRY_HIP(p, hipEventSynchronize(e), true);
+        TRY_HIP(p, wait_event(p, e), true);
     return SS_OK;
 }
 

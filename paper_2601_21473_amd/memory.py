@@ -107,7 +107,8 @@ class PoolMemory:
                     staging_bytes=self.staging.nbytes, ring_slots=self.ring_slots,
                     device=self.device)
 
-    def make_pool(self, timing: bool = False, direct_bytes: int = 0) -> binding.Pool:
+    def make_pool(self, timing: bool = False, direct_bytes: int = 0,
+                  poll_wait: bool = False) -> binding.Pool:
         s = self.spec
         return binding.Pool(capacity_units=s.capacity_units, chunk_bytes=s.chunk_bytes,
                             agent_units=s.agent_units,
@@ -115,7 +116,8 @@ class PoolMemory:
                             host_backing=self.host.ptr, host_bytes=self.host.nbytes,
                             host_off=self.host_off, dev_staging=self.staging.ptr,
                             staging_bytes=self.staging.nbytes, ring_slots=self.ring_slots,
-                            device=self.device, timing=timing, direct_bytes=direct_bytes)
+                            device=self.device, timing=timing, direct_bytes=direct_bytes,
+                            poll_wait=poll_wait)
 
     def host_copy(self, agent: int) -> np.ndarray:
         """View of an agent's host copy (unit-major, planes in order)."""

@@ -94,7 +94,7 @@ def _desc(**kw):
     ("host_backing", None, "host_backing"),
     ("dev_staging", None, "dev_staging"),
     ("ring_slots", 0, "ring_slots"),
-    ("flags", 2, "flag"),
+    ("flags", 4, "flag"),
     ("host_bytes", 4 * 96 - 16, "exceeds host_bytes"),
     ("staging_bytes", 95, "too small"),
 ])

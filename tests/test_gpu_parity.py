@@ -124,8 +124,9 @@ def test_bench_configuration_sampled(name, steps, watched):
     # 448 planes in a second pool planned with the same inputs; 512 KiB units
     # in one 160 GB pool for the 50,000-agent workload), 8 GiB of staging per
     # pool in four slots per direction, a 4 MiB direct limit, 128 host copies
-    # per pool shared round-robin by the agents and a stream of the caller's
-    # own; the host waits for the pool only every tenth step.  Plans match the
+    # per pool shared round-robin by the agents, a stream of the caller's own
+    # and the pools' polled waits; the host waits for the pool only every
+    # tenth step.  Plans match the
     # oracle at every step; block tables and residency every tenth step and
     # after the last.  Bytes are checked where one step fixes them, on sampled
     # units every tenth step: a victim whose host copy no other agent moving
@@ -156,7 +157,7 @@ def test_bench_configuration_sampled(name, steps, watched):
         units = spec.agent_units.astype(np.int64)
         ctx.append(dict(spec=spec, ub=ub, mem=mem, units=units,
                         row=np.concatenate([[0], np.cumsum(units)]),
-                        pool=mem.make_pool(timing=True, direct_bytes=4 << 20),
+                        pool=mem.make_pool(timing=True, direct_bytes=4 << 20, poll_wait=True),
                         opool=OraclePool(spec.capacity_units, spec.agent_units, ub)))
     dev = upload_trace(tr)
     stream = B.Stream()
