@@ -599,9 +599,10 @@ __device__ __forceinline__ void merge_sort_lds_e(u64* lds, unsigned npad, unsign
 
 // Keys per lane by list size (measured on one 1024-thread workgroup: longer
 // register runs save merge rounds until the register stage's exchanges cost
-// more than the rounds they save).  Inlined where the plan's sorts run (its
-// LDS accesses then stay LDS instructions); the rare separate sorts share one
-// out-of-line copy (merge_sort_lds), whose accesses are flat.
+// more than the rounds they save).  Inlined wherever a plan sorts (its LDS
+// accesses then stay LDS instructions, and the plan kernels make no calls: a
+// call would give them a stack in scratch memory for the callee's saved
+// registers, and a longer register allocation).
 __device__ __forceinline__ void merge_sort_lds_inl(u64* lds, unsigned npad, unsigned n) {
     if (npad <= 512) merge_sort_lds_e<1>(lds, npad, n);
     else if (npad <= 2048) merge_sort_lds_e<2>(lds, npad, n);
@@ -610,7 +611,7 @@ __device__ __forceinline__ void merge_sort_lds_inl(u64* lds, unsigned npad, unsi
 }
 
 // (all npad keys treated as real: the callers pad only the first half)
-__device__ __noinline__ void merge_sort_lds(u64* lds, unsigned npad) {
+__device__ __forceinline__ void merge_sort_lds(u64* lds, unsigned npad) {
     merge_sort_lds_inl(lds, npad, npad);
 }
 
@@ -922,10 +923,10 @@ __device__ __forceinline__ void bt_update_block(const BtArgs& B, unsigned n_v, u
     }
 }
 
-// The plan core's tail, compiled apart (not inlined) so that its
-// registers do not weigh on the core's own allocation; its arguments come from
-// the pool's device copy, not from the kernel's.
-__device__ __attribute__((noinline)) void bt_tail(const BtArgs* Bp, unsigned n_v, unsigned n_l,
+// The plan core's tail; its arguments come from the pool's device copy, not
+// from the kernel's.  Inlined like the rest of the plan (no call, so no stack
+// in scratch memory).
+__device__ __forceinline__ void bt_tail(const BtArgs* Bp, unsigned n_v, unsigned n_l,
                                                   u64 nF, u64 units_in, u64 units_out) {
     const BtArgs B = *Bp;
     bt_update_block(B, n_v, n_l, nF, units_in, units_out);
