@@ -376,15 +376,10 @@ void fold_plan(ss_pool* p, int k) {
 
 }  // namespace
 
-namespace ss {
-// True if [ptr, ptr + bytes) lies inside one allocation of device memory on
-// `device` (or managed memory).
-bool device_range_ok(const void* ptr, u64 bytes, int device) {
-    hipPointerAttribute_t attr;
-    if (hipPointerGetAttributes(&attr, ptr) != hipSuccess) {
-        (void)hipGetLastError();
-        return false;
-    }
+namespace {
+// device_range_ok for a pointer whose attributes are already known.
+bool device_range_attr_ok(const hipPointerAttribute_t& attr, const void* ptr, u64 bytes,
+                          int device) {
     if (attr.type == hipMemoryTypeManaged) return true;
     if (attr.type != hipMemoryTypeDevice || attr.device != device) return false;
     hipDeviceptr_t base = nullptr;
@@ -396,7 +391,19 @@ bool device_range_ok(const void* ptr, u64 bytes, int device) {
     const u64 off = reinterpret_cast<uintptr_t>(ptr) - reinterpret_cast<uintptr_t>(base);
     return off <= size && bytes <= size - off;
 }
+}  // namespace
 
+namespace ss {
+// True if [ptr, ptr + bytes) lies inside one allocation of device memory on
+// `device` (or managed memory).
+bool device_range_ok(const void* ptr, u64 bytes, int device) {
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, ptr) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    return device_range_attr_ok(attr, ptr, bytes, device);
+}
 
 // True if host_ptr is pinned (page-locked) host memory; when the runtime
 // reports the allocation's extent, [host_ptr, host_ptr + bytes) must fit in it.
@@ -432,7 +439,7 @@ InputKind input_kind(const void* ptr, u64 bytes, int device) {
         return kInHost;                              // memory the runtime does not know: pageable
     }
     if (attr.type == hipMemoryTypeHost || attr.type == hipMemoryTypeUnregistered) return kInHost;
-    return device_range_ok(ptr, bytes, device) ? kInDevice : kInBad;
+    return device_range_attr_ok(attr, ptr, bytes, device) ? kInDevice : kInBad;
 }
 
 // The host's unit offsets of the current plan's lists (victims and loads in
