@@ -69,20 +69,35 @@ def launch_units(kind, blocks, n_items, n_planes):
     return blocks // n_items * waves
 
 
-def summarize_pmc(fetch_csv, write_csv, workload, out_json, commands):
+def whole_slot_grid(kind, spec, staging_bytes, ring):
+    """Threads of a copy launch over one whole staging slot of pool ``spec``
+    (each half of the staging buffer is cut into ``ring`` slots of whole
+    units): the inverse of launch_units."""
+    ups = (staging_bytes // 2 // ring) // spec.unit_bytes
+    n_items = sum((c + COPY_ITEM_BYTES - 1) // COPY_ITEM_BYTES for c in spec.chunk_bytes)
+    waves = COPY_BLOCK // 64
+    if kind == "pack" or n_items != len(spec.chunk_bytes):
+        blocks = ups * ((n_items + waves - 1) // waves)
+    else:
+        blocks = (ups + waves - 1) // waves * n_items
+    return blocks * COPY_BLOCK
+
+
+def summarize_pmc(fetch_csv, write_csv, workload, out_json, commands,
+                  staging_bytes=8192 << 20, ring=4):
     """HBM traffic of the copy kernels from two rocprofv3 --pmc runs
     (FETCH_SIZE, WRITE_SIZE in KiB per dispatch), each scaled by the ratio of
     known bytes to the same counter on the probe's plain copy of PROBE_BYTES.
-    Counted over the launches that cover a whole staging slot (largest grid),
-    whose unit count follows from the grid: pack launches item_groups blocks
-    per unit, unpack n_items blocks per 8 units."""
+    Counted over the launches that cover a whole staging slot of a pool,
+    recognised by their grid (whole_slot_grid; the pools of one workload
+    must differ in it), whose unit count follows from the grid: pack
+    launches item_groups blocks per unit, unpack n_items blocks per 8 units.
+    With several pools, each kernel's ratio is over all of their whole-slot
+    launches, with each pool's figures under "pools"."""
     import csv
     import collections
     import workloads as W
-    spec = W.make_trace(workload, 0).pools[0]
-    n_items = sum((c + COPY_ITEM_BYTES - 1) // COPY_ITEM_BYTES for c in spec.chunk_bytes)
-    waves = COPY_BLOCK // 64
-    groups = (n_items + waves - 1) // waves
+    pools = W.make_trace(workload, 0).pools
     vals = {}
     for path, counter in ((fetch_csv, "FETCH_SIZE"), (write_csv, "WRITE_SIZE")):
         per = collections.defaultdict(list)
@@ -95,24 +110,35 @@ def summarize_pmc(fetch_csv, write_csv, workload, out_json, commands):
     out = {"workload": workload, "kernel_source_sha256_16": kernel_source_hash(),
            "commands": commands, "probe_scale_factor": factor, "kernels": {}}
     for name, short in PMC_KERNELS.items():
-        f = vals["FETCH_SIZE"].get(name, [])
-        w = vals["WRITE_SIZE"].get(name, [])
-        if not f or not w:
-            continue
-        grid = max(g for _, g in f)
-        f = [v for v, g in f if g == grid]
-        w = [v for v, g in w if g == grid]
-        blocks = grid // COPY_BLOCK
-        units = launch_units(short, blocks, n_items, len(spec.chunk_bytes))
-        alg = 2 * units * spec.unit_bytes
-        fetch_b = np.mean(f) * 1024 * factor["FETCH_SIZE"]
-        write_b = np.mean(w) * 1024 * factor["WRITE_SIZE"]
-        out["kernels"][short] = {
-            "dispatches": len(f), "grid_threads": grid, "units_per_launch": units,
-            "hbm_read_bytes_per_launch": fetch_b, "hbm_write_bytes_per_launch": write_b,
-            "hbm_bytes_per_launch": fetch_b + write_b,
-            "algorithmic_bytes_per_launch": float(alg),
-            "traffic_over_algorithmic": (fetch_b + write_b) / float(alg)}
+        grids = [whole_slot_grid(short, spec, staging_bytes, ring) for spec in pools]
+        if len(set(grids)) != len(grids):
+            raise ValueError(f"{workload}: pools with the same whole-slot {short} grid")
+        per_pool = {}
+        for spec, grid in zip(pools, grids):
+            f = [v for v, g in vals["FETCH_SIZE"].get(name, []) if g == grid]
+            w = [v for v, g in vals["WRITE_SIZE"].get(name, []) if g == grid]
+            if not f or not w:
+                continue
+            n_items = sum((c + COPY_ITEM_BYTES - 1) // COPY_ITEM_BYTES for c in spec.chunk_bytes)
+            units = launch_units(short, grid // COPY_BLOCK, n_items, len(spec.chunk_bytes))
+            alg = 2 * units * spec.unit_bytes
+            fetch_b = np.mean(f) * 1024 * factor["FETCH_SIZE"]
+            write_b = np.mean(w) * 1024 * factor["WRITE_SIZE"]
+            per_pool[spec.name] = {
+                "dispatches": len(f), "grid_threads": grid, "units_per_launch": units,
+                "hbm_read_bytes_per_launch": fetch_b, "hbm_write_bytes_per_launch": write_b,
+                "hbm_bytes_per_launch": fetch_b + write_b,
+                "algorithmic_bytes_per_launch": float(alg),
+                "traffic_over_algorithmic": (fetch_b + write_b) / float(alg)}
+        if len(pools) == 1:
+            if per_pool:
+                out["kernels"][short] = per_pool[pools[0].name]
+        elif per_pool:
+            hbm = sum(p["hbm_bytes_per_launch"] * p["dispatches"] for p in per_pool.values())
+            alg = sum(p["algorithmic_bytes_per_launch"] * p["dispatches"] for p in per_pool.values())
+            out["kernels"][short] = {
+                "dispatches": sum(p["dispatches"] for p in per_pool.values()),
+                "traffic_over_algorithmic": hbm / alg, "pools": per_pool}
     json.dump(out, open(out_json, "w"), indent=1)
     return out
 
@@ -693,7 +719,9 @@ def main():
         return
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(*args.summarize_pmc[:2], args.workload,
-                                       args.summarize_pmc[2], args.pmc_commands), indent=1))
+                                       args.summarize_pmc[2], args.pmc_commands,
+                                       staging_bytes=args.staging_mib << 20, ring=args.ring),
+                         indent=1))
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (--gpus {args.gpus} requested): the library "

@@ -176,3 +176,54 @@ def test_summarize_copies(tmp_path):
     assert "| host to device | 1 | 25000.0 | nan | 25.0 | 2.00 | 80.0 | 100.0 | 0.800 |" in md
     # both: 3.5 GB over the union [100, 130.5] = 30.5 ms = 114.8 GB/s
     assert "3.50 GB over 30.5 ms" in md and "= 114.8 GB/s" in md and "(0.956)" in md
+
+
+def test_whole_slot_grids_by_layout():
+    # 1 GiB slots (8 GiB of staging, four slots per direction): 512 round-robin
+    # units (pack 8 workgroups per unit, unpack 64 workgroups per 8 units),
+    # 2,048 diffusion units (2 workgroups per unit both ways) and 12 LoRA
+    # adapter slots of 80 MiB (2,560 items: 320 workgroups per unit both ways)
+    import bench
+    import workloads as W
+    kv, lora = W.make_trace("zipf_lora", 0).pools
+    rr = W.make_trace("roundrobin", 0).pools[0]
+    for kind in ("pack", "unpack"):
+        assert bench.whole_slot_grid(kind, rr, 8192 << 20, 4) == 4096 * bench.COPY_BLOCK
+        assert bench.whole_slot_grid(kind, kv, 8192 << 20, 4) == 4096 * bench.COPY_BLOCK
+        assert bench.whole_slot_grid(kind, lora, 8192 << 20, 4) == 12 * 320 * bench.COPY_BLOCK
+    assert bench.whole_slot_grid("unpack", rr, 8192 << 20, 8) == 2048 * bench.COPY_BLOCK
+
+
+def test_summarize_pmc_two_pools(tmp_path):
+    # The LoRA workload's KV pool (whole-slot grid 4,096 workgroups) and
+    # adapter pool (3,840): each pool's launches are told apart by their grid;
+    # the kernel's ratio is over both pools' launches (bytes-weighted), each
+    # pool's own under "pools".
+    import bench
+    pack, unpack = list(bench.PMC_KERNELS)
+    kib = bench.PROBE_BYTES / 1024
+    kv_kib = 512 * (2 << 20) / 1024
+    lora_kib = 12 * 83886080 / 1024
+    g_kv, g_lora = 4096 * bench.COPY_BLOCK, 3840 * bench.COPY_BLOCK
+    hdr = ["Kernel_Name", "Counter_Name", "Counter_Value", "Grid_Size"]
+    fetch, write = [(bench.PROBE_KERNEL, "FETCH_SIZE", kib, 1 << 20)], \
+        [(bench.PROBE_KERNEL, "WRITE_SIZE", kib, 1 << 20)]
+    for k in (pack, unpack):
+        fetch += [(k, "FETCH_SIZE", kv_kib, g_kv), (k, "FETCH_SIZE", kv_kib, g_kv),
+                  (k, "FETCH_SIZE", 1.02 * lora_kib, g_lora), (k, "FETCH_SIZE", 3.0, 1024)]
+        write += [(k, "WRITE_SIZE", kv_kib, g_kv), (k, "WRITE_SIZE", kv_kib, g_kv),
+                  (k, "WRITE_SIZE", 1.02 * lora_kib, g_lora), (k, "WRITE_SIZE", 3.0, 1024)]
+    _write_csv(tmp_path / "f.csv", hdr, fetch)
+    _write_csv(tmp_path / "w.csv", hdr, write)
+    out = bench.summarize_pmc(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "zipf_lora",
+                              str(tmp_path / "pmc.json"), ["cmd"])
+    for short in ("pack", "unpack"):
+        k = out["kernels"][short]
+        assert k["dispatches"] == 3
+        assert k["pools"]["kv"]["units_per_launch"] == 512
+        assert k["pools"]["lora"]["units_per_launch"] == 12
+        assert abs(k["pools"]["kv"]["traffic_over_algorithmic"] - 1.0) < 1e-12
+        assert abs(k["pools"]["lora"]["traffic_over_algorithmic"] - 1.02) < 1e-12
+        a_kv, a_lora = 2 * 2 * kv_kib * 1024, 2 * lora_kib * 1024
+        want = (a_kv + 1.02 * a_lora) / (a_kv + a_lora)
+        assert abs(k["traffic_over_algorithmic"] - want) < 1e-12
