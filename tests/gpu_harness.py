@@ -139,8 +139,8 @@ def run_parity(trace, pool_index=0, theta=S, budget=None, steps=None, check_byte
         o = opool.plan_step(trace.dist[t], trace.active[t], theta, budget,
                             None if dirty is None else dirty[t])
         assert g["units_written"] == o.units_written, (label, t)
-        assert g["victim_written"].astype(bool).tolist() == \
-            [int(v) in set(o.written.tolist()) for v in o.victims], (label, t)
+        assert np.array_equal(g["victim_written"].astype(bool),
+                              np.isin(o.victims, o.written)), (label, t)
         if check_bytes and dirty is not None:
             # a written-back victim's host copy must be rewritten by this step
             for v in o.written:

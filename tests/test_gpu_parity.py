@@ -21,7 +21,8 @@ and byte movement.  Cases:
     and a limit that sends some steps' directions direct and others staged;
   * edge cases: one-unit ring slots, no prefetch, budgets, an agent count
     that is not a multiple of the wave or block size, lists larger than the
-    plan kernel's LDS sort buffer, empty steps, overcommit and call order."""
+    plan kernel's LDS sort buffer, 2^20 agents, empty steps, overcommit and
+    call order."""
 import numpy as np
 import pytest
 
@@ -433,6 +434,18 @@ def test_many_agents_variable_sizes(n_agents, theta, budget):
                          units=units, chunk_bytes=(16,), noisy=True)
     run_parity(tr, theta=theta, budget=budget, slot_units=8192, ring_slots=2, sample_units=3000,
                label=f"{n_agents} agents t{theta} b{budget}")
+
+
+@pytest.mark.parametrize("theta,budget", [(S, None), (3, 5000)])
+def test_million_agents(theta, budget):
+    # The largest agent count of the tests: 2^20 one-unit agents (20 id bits,
+    # 256 classifying workgroups) sharing a 65,536-unit pool, 30,000 of them
+    # active per step with noisy distances, so that steps evict and load
+    # 20,000-38,000 agents: evictable and candidate sets far beyond the plan
+    # kernel's LDS sorts (its global-memory sorts), budgets and thresholds.
+    tr = synthetic_trace(1 << 20, 65536, 6, 30000, seed=21, chunk_bytes=(16,), noisy=True)
+    run_parity(tr, theta=theta, budget=budget, slot_units=65536, ring_slots=2, sample_units=4000,
+               label=f"2^20 agents t{theta} b{budget}")
 
 
 @pytest.mark.parametrize("direct", [0, 1 << 20])

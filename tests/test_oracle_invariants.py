@@ -169,7 +169,8 @@ def test_checker_flags_a_prefetch_that_replaced_a_nearer_agent():
 
 def test_checker_flags_victims_beyond_need():
     pool, plan, D, act, before = _prefetch_step()
-    extra = [int(a) for a in np.flatnonzero(before & ~act) if a not in set(plan.victims.tolist())]
+    victims = set(plan.victims.tolist())
+    extra = [int(a) for a in np.flatnonzero(before & ~act) if a not in victims]
     bad = copy.copy(plan)
     bad.victims = np.concatenate([plan.victims, extra[:1]])
     with pytest.raises(AssertionError, match="I6: victims beyond what the loads need"):
